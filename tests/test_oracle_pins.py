@@ -1,0 +1,318 @@
+"""Pins for the CPU oracle: facts fixed by the paper and by mathematics.
+
+Each test compares the oracle (sequential float64 recurrence) with something
+that is not the oracle: the matrix form written entry by entry, closed forms,
+library solvers, invariants.  A dropped term, a wrong sign or index, or a
+transposed operand in the oracle fails at least one of them.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+
+import oracle
+import oracle.chunked as chunked
+from paper_2405_21060_amd.inputs import (
+    Problem, WORKLOADS, bf16_bits_to_f32, f32_to_bf16_bits, make_inputs)
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rand_problem(rng, b=2, T=37, H=4, P=3, N=5, G=2, init=True):
+    x = rng.standard_normal((b, T, H, P))
+    dt = np.log1p(np.exp(rng.standard_normal((b, T, H)) - 1.0))
+    A_log = rng.uniform(-1.0, 1.5, H)
+    B = rng.standard_normal((b, T, G, N))
+    C = rng.standard_normal((b, T, G, N))
+    D = rng.standard_normal(H)
+    h0 = rng.standard_normal((b, H, P, N)) if init else None
+    return x, dt, A_log, B, C, D, h0
+
+
+def matrix_form(x, dt, A_log, B, C, D, h0):
+    """Section 3 eq. (ssm-matrix), entry by entry:
+    M_ji = C_j^T (A_j ... A_{i+1}) B_i with scalar A_k = exp(dt_k * A), so
+    y_j = sum_{i<=j} M_ji (dt_i x_i) + D x_j + C_j^T (A_j ... A_0) h0
+    (the initial state precedes token 0 and is decayed by it).
+    Products are taken as explicit products, not via cumulative sums."""
+    b, T, H, P = x.shape
+    G = B.shape[2]
+    y = np.zeros_like(x)
+    fin = np.zeros((b, H, P, B.shape[3]))
+    for bb in range(b):
+        for h in range(H):
+            g = h // (H // G)
+            Ak = np.exp(dt[bb, :, h] * (-np.exp(A_log[h])))
+            prod = lambda j, i: float(np.prod(Ak[i + 1:j + 1]))  # A_j...A_{i+1}
+            M = np.zeros((T, T))
+            for j in range(T):
+                for i in range(j + 1):
+                    M[j, i] = (C[bb, j, g] @ B[bb, i, g]) * prod(j, i)
+            xin = dt[bb, :, h, None] * x[bb, :, h]
+            y[bb, :, h] = M @ xin + D[h] * x[bb, :, h]
+            if h0 is not None:
+                for j in range(T):
+                    y[bb, j, h] += float(np.prod(Ak[:j + 1])) * (h0[bb, h] @ C[bb, j, g])
+            # final state: h_{T-1} = sum_i (A_{T-1}...A_{i+1}) B_i xin_i (+ decayed h0)
+            for i in range(T):
+                fin[bb, h] += prod(T - 1, i) * np.outer(xin[i], B[bb, i, g])
+            if h0 is not None:
+                fin[bb, h] += float(np.prod(Ak)) * h0[bb, h]
+    return y, fin
+
+
+def test_matrix_form_bruteforce():
+    rng = np.random.default_rng(11)
+    args = rand_problem(rng)
+    y, fin = oracle.forward(*args)
+    y_ref, fin_ref = matrix_form(*args)
+    assert np.abs(y - y_ref).max() <= 1e-12 * max(1.0, np.abs(y_ref).max())
+    assert np.abs(fin - fin_ref).max() <= 1e-12 * max(1.0, np.abs(fin_ref).max())
+
+
+def test_zero_decay_is_causal_linear_attention():
+    """a = 0 (A = -exp(-inf) = 0): L is the causal mask, so (Section 4,
+    linear attention) Y = C . cumsum_s (B_s (dt_s x_s)^T)."""
+    rng = np.random.default_rng(2)
+    x, dt, _, B, C, _, _ = rand_problem(rng, b=1, T=50, H=2, G=1, init=False)
+    A_log = np.full(2, -np.inf)
+    y, fin = oracle.forward(x, dt, A_log, B, C)
+    xin = dt[..., None] * x                                  # (b,T,H,P)
+    kv = np.cumsum(np.einsum("btn,bthp->bthnp", B[:, :, 0], xin), axis=1)
+    y_ref = np.einsum("btn,bthnp->bthp", C[:, :, 0], kv)
+    assert np.allclose(y, y_ref, rtol=1e-12, atol=1e-12)
+    assert np.allclose(fin[0], np.swapaxes(kv[0, -1], -1, -2), rtol=1e-12, atol=1e-12)
+
+
+def test_full_decay_is_memoryless():
+    """exp(a) == 0 (a = -exp(7) ~ -1097 underflows): the 1-SS mask is the
+    identity, so y_t = dt_t (C_t . B_t) x_t + D x_t."""
+    rng = np.random.default_rng(3)
+    x, _, _, B, C, D, _ = rand_problem(rng, b=1, T=30, H=2, G=1, init=False)
+    dt = np.ones((1, 30, 2))
+    y, _ = oracle.forward(x, dt, np.full(2, 7.0), B, C, D)
+    cb = np.einsum("btn,btn->bt", C[:, :, 0], B[:, :, 0])
+    y_ref = cb[:, :, None, None] * x + D[None, None, :, None] * x
+    assert np.allclose(y, y_ref, rtol=1e-13, atol=1e-13)
+
+
+def test_constant_decay_geometric_series():
+    """N = P = 1, B = C = 1, x = 1, constant dt: a constant-decay (LTI,
+    RetNet-like) scan whose output is a geometric series,
+    y_t = dt (1 - g^(t+1)) / (1 - g), g = exp(dt A)."""
+    T, dtv, A_log = 200, 0.05, math.log(3.0)
+    g = math.exp(-dtv * 3.0)
+    ones = np.ones((1, T, 1, 1))
+    y, fin = oracle.forward(ones, np.full((1, T, 1), dtv), np.array([A_log]),
+                            ones, ones)
+    t = np.arange(T)
+    y_ref = dtv * (1 - g ** (t + 1)) / (1 - g)
+    assert np.allclose(y[0, :, 0, 0], y_ref, rtol=1e-13)
+    assert np.isclose(fin[0, 0, 0, 0], y_ref[-1], rtol=1e-13)
+
+
+def test_scalar_scan_is_bidiagonal_solve():
+    """N = P = 1: the scan h_t = alpha_t h_{t-1} + u_t is the solve of the
+    2-banded system (I - subdiag(alpha)) h = u (Appendix C remark on the
+    inverse of a 1-SS matrix); solved here by LAPACK's banded solver."""
+    rng = np.random.default_rng(5)
+    T = 300
+    dt = rng.uniform(0.01, 0.5, (1, T, 1))
+    x = rng.standard_normal((1, T, 1, 1))
+    A_log = np.array([0.3])
+    ones = np.ones((1, T, 1, 1))
+    y, _ = oracle.forward(x, dt, A_log, ones, ones)
+    alpha = np.exp(dt[0, :, 0] * -np.exp(A_log[0]))
+    u = dt[0, :, 0] * x[0, :, 0, 0]
+    ab = np.zeros((2, T))
+    ab[0] = 1.0
+    ab[1, :-1] = -alpha[1:]
+    h = scipy.linalg.solve_banded((1, 0), ab, u)
+    assert np.allclose(y[0, :, 0, 0], h, rtol=1e-12, atol=1e-14)
+
+
+def test_zero_input_pure_decay_of_initial_state():
+    """x = 0: only the left factors act on the initial state,
+    y_t = exp(sum_{k<=t} a_k) C_t^T h0 and h_final = exp(sum_k a_k) h0."""
+    rng = np.random.default_rng(6)
+    _, dt, A_log, B, C, D, h0 = rand_problem(rng, b=2, T=25, H=3, G=1)
+    x = np.zeros((2, 25, 3, 3))
+    y, fin = oracle.forward(x, dt, A_log, B, C, D, h0)
+    a = dt * -np.exp(A_log)[None, None, :]
+    dec = np.exp(np.cumsum(a, axis=1))                    # (b,T,H)
+    y_ref = dec[..., None] * np.einsum("bhpn,btn->bthp", h0, C[:, :, 0])
+    assert np.allclose(y, y_ref, rtol=1e-12, atol=1e-15)
+    assert np.allclose(fin, dec[:, -1, :, None, None] * h0, rtol=1e-12)
+
+
+def test_offdiagonal_blocks_have_rank_at_most_N():
+    """Semiseparable structure (Section 3, definition of N-semiseparable and
+    the SSS rank lemma): every submatrix below the diagonal of the impulse
+    response matrix M has rank <= N."""
+    rng = np.random.default_rng(7)
+    T, N = 24, 3
+    dt = rng.uniform(0.05, 0.3, (1, T, 1))
+    B = rng.standard_normal((1, T, 1, N))
+    C = rng.standard_normal((1, T, 1, N))
+    M = np.zeros((T, T))
+    for i in range(T):
+        e = np.zeros((1, T, 1, 1))
+        e[0, i] = 1.0 / dt[0, i, 0]       # unit discretised input at token i
+        y, _ = oracle.forward(e, dt, np.array([0.0]), B, C)
+        M[:, i] = y[0, :, 0, 0]
+    assert np.allclose(np.triu(M, 1), 0.0)
+    for k in range(N + 1, T - N):
+        sv = np.linalg.svd(M[k:, :k], compute_uv=False)
+        assert (sv > 1e-10 * sv[0]).sum() <= N
+
+
+def test_split_and_state_passing_equals_full_run():
+    """Running [0,k) then [k,T) from the first part's final state equals one
+    run: the state passing of context parallelism (Section 8) and of the
+    state-passing scan mode (Appendix B)."""
+    rng = np.random.default_rng(8)
+    x, dt, A_log, B, C, D, h0 = rand_problem(rng, b=2, T=60, H=4, G=2)
+    y, fin = oracle.forward(x, dt, A_log, B, C, D, h0)
+    k = 23
+    y1, f1 = oracle.forward(x[:, :k], dt[:, :k], A_log, B[:, :k], C[:, :k], D, h0)
+    y2, f2 = oracle.forward(x[:, k:], dt[:, k:], A_log, B[:, k:], C[:, k:], D, f1)
+    assert np.allclose(np.concatenate([y1, y2], axis=1), y, rtol=1e-12, atol=1e-13)
+    assert np.allclose(f2, fin, rtol=1e-12, atol=1e-13)
+
+
+def test_packed_varlen_equals_separate_runs():
+    """Section 8.3: a packed row with sequence boundaries equals running every
+    sequence on its own, each from its own initial state."""
+    rng = np.random.default_rng(9)
+    lens = [5, 1, 17, 9, 1, 31]
+    T = sum(lens)
+    x, dt, A_log, B, C, D, _ = rand_problem(rng, b=1, T=T, H=3, G=1, init=False)
+    h0 = rng.standard_normal((len(lens), 3, 3, 5))
+    seq = np.repeat(np.arange(len(lens)), lens).astype(np.int32)[None]
+    y, fin = oracle.forward(x, dt, A_log, B, C, D, h0, seq)
+    s = 0
+    for q, L in enumerate(lens):
+        sl = slice(s, s + L)
+        yq, fq = oracle.forward(x[:, sl], dt[:, sl], A_log, B[:, sl], C[:, sl], D, h0[q:q + 1])
+        assert np.allclose(y[:, sl], yq, rtol=1e-13, atol=1e-14)
+        assert np.allclose(fin[q], fq[0], rtol=1e-13, atol=1e-14)
+        s += L
+
+
+def test_linearity_in_x_and_separable_D():
+    rng = np.random.default_rng(10)
+    x1, dt, A_log, B, C, D, _ = rand_problem(rng, init=False)
+    x2 = rng.standard_normal(x1.shape)
+    ya, _ = oracle.forward(2.0 * x1 - 3.0 * x2, dt, A_log, B, C)
+    y1, _ = oracle.forward(x1, dt, A_log, B, C)
+    y2, _ = oracle.forward(x2, dt, A_log, B, C)
+    assert np.allclose(ya, 2.0 * y1 - 3.0 * y2, rtol=1e-11, atol=1e-12)
+    yD, _ = oracle.forward(x1, dt, A_log, B, C, D)
+    assert np.allclose(yD - y1, D[None, None, :, None] * x1, rtol=1e-12, atol=1e-13)
+
+
+def test_grouped_heads_use_contiguous_groups():
+    """Grouped-input SSM (Section 7): head h reads B, C of group h // (H/G).
+    Compared with one single-group run per head on that group's B, C; and
+    G identical groups equal one shared group."""
+    rng = np.random.default_rng(12)
+    x, dt, A_log, B, C, D, h0 = rand_problem(rng, b=1, T=20, H=6, G=3)
+    y, fin = oracle.forward(x, dt, A_log, B, C, D, h0)
+    for h in range(6):
+        g = h // 2
+        sl = slice(h, h + 1)
+        yh, fh = oracle.forward(x[:, :, sl], dt[:, :, sl], A_log[sl], B[:, :, g:g + 1],
+                                C[:, :, g:g + 1], D[sl], h0[:, sl])
+        assert np.allclose(y[:, :, sl], yh, rtol=1e-13, atol=1e-14)
+        assert np.allclose(fin[:, sl], fh, rtol=1e-13, atol=1e-14)
+    Brep = np.repeat(B[:, :, :1], 3, axis=2)
+    Crep = np.repeat(C[:, :, :1], 3, axis=2)
+    y3, _ = oracle.forward(x, dt, A_log, Brep, Crep, D, h0)
+    y1, _ = oracle.forward(x, dt, A_log, B[:, :, :1], C[:, :, :1], D, h0)
+    assert np.array_equal(y3, y1)
+
+
+def test_golden_block_decomposition_T9_Q3():
+    """The paper's T=9, Q=3 worked example: each off-diagonal block equals
+    left * center * right^T with the printed A_{u:v} index pattern."""
+    rng = np.random.default_rng(13)
+    T = 9
+    a = rng.uniform(0.3, 0.99, T)     # scalar A_k
+    c = rng.standard_normal(T)
+    bvec = rng.standard_normal(T)
+    Auv = lambda u, v: float(np.prod(a[v + 1:u + 1]))   # A_u ... A_{v+1}
+    M = np.array([[c[j] * Auv(j, i) * bvec[i] if i <= j else 0.0 for i in range(T)]
+                  for j in range(T)])
+    lines = [l for l in open(os.path.join(GOLDEN, "block_decomposition_T9_Q3.txt"))
+             if l.startswith("block")]
+    assert len(lines) == 3
+    for line in lines:
+        head, left, center, right = [p.split() for p in line.split("|")]
+        j, i = int(head[1]), int(head[2])
+        pair = lambda s: tuple(int(v) for v in s.split(":"))
+        lf = np.array([c[3 * j + r] * Auv(*pair(e)) for r, e in enumerate(left)])
+        cf = Auv(*pair(center[0]))
+        rf = np.array([bvec[3 * i + r] * Auv(*pair(e)) for r, e in enumerate(right)])
+        blk = M[3 * j:3 * j + 3, 3 * i:3 * i + 3]
+        assert np.allclose(np.outer(lf, rf) * cf, blk, rtol=1e-14)
+    # and the sequential oracle computes y = M x for this example (N = P = 1)
+    x = rng.standard_normal(T)
+    dt = np.ones((1, T, 1))
+    A_log = np.array([0.0])        # A = -1: exp(dt*A_k) must equal a_k, so fold
+    dt = (-np.log(a))[None, :, None]   # dt_k = -log a_k gives exp(-dt_k) = a_k
+    y, _ = oracle.forward((x / dt[0, :, 0])[None, :, None, None], dt, A_log,
+                          bvec[None, :, None, None], c[None, :, None, None])
+    assert np.allclose(y[0, :, 0, 0], M @ x, rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("Q", [4, 8, 16, 64])
+def test_chunked_reference_matches_oracle(Q):
+    """The block decomposition (Section 6) equals the recurrence for any chunk
+    size, including an uneven last chunk (T % Q != 0)."""
+    rng = np.random.default_rng(14)
+    args = rand_problem(rng, b=2, T=45, H=4, G=2)
+    y, fin = oracle.forward(*args)
+    yc, fc, im = chunked.forward(*args, chunk_size=Q)
+    assert np.abs(yc - y).max() <= 1e-11 * np.abs(y).max()
+    assert np.abs(fc - fin).max() <= 1e-11 * np.abs(fin).max()
+
+
+@pytest.mark.parametrize("Q", [8, 16, 64])
+def test_chunked_reference_varlen_matches_oracle(Q):
+    rng = np.random.default_rng(15)
+    lens = [3, 16, 1, 1, 20, 8, 30, 1]
+    T = sum(lens)
+    x, dt, A_log, B, C, D, _ = rand_problem(rng, b=1, T=T, H=4, G=2, init=False)
+    h0 = rng.standard_normal((len(lens), 4, 3, 5))
+    seq = np.repeat(np.arange(len(lens)), lens).astype(np.int32)[None]
+    y, fin = oracle.forward(x, dt, A_log, B, C, D, h0, seq)
+    yc, fc, _ = chunked.forward(x, dt, A_log, B, C, D, h0, seq, chunk_size=Q)
+    assert np.abs(yc - y).max() <= 1e-11 * np.abs(y).max()
+    assert np.abs(fc - fin).max() <= 1e-11 * np.abs(fin).max()
+
+
+def test_bf16_round_to_nearest_even():
+    v = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, -2.5, 1 + 2 ** -7 + 2 ** -9], np.float32)
+    bits = f32_to_bf16_bits(v)
+    assert list(bits) == [0x3F80, 0x3F80, 0x3F82, 0xC020, 0x3F81]
+    assert np.array_equal(bf16_bits_to_f32(bits)[[0, 3]], np.array([1.0, -2.5], np.float32))
+
+
+def test_inputs_are_deterministic_and_in_range():
+    p = Problem(2, 300, 6, 16, 32, 2, 64, "bf16")
+    a = make_inputs(p, 3)
+    b = make_inputs(p, 3)
+    for n in ("x", "dt", "A_log", "B", "C", "D"):
+        assert np.array_equal(getattr(a, n), getattr(b, n))
+    c = make_inputs(p, 4)
+    assert not np.array_equal(a.x, c.x)
+    A = -np.exp(a.A_log)
+    assert np.all(A <= -1.0) and np.all(A >= -16.0 - 1e-5)
+    assert np.all(a.as_f64("dt") > 0)
+    v = make_inputs(WORKLOADS["varlen_g8"].__class__(1, 32768, 2, 4, 4, 1, 256, "bf16",
+                                                      varlen=True, init_states=True), 0)
+    lens = np.bincount(v.seq_idx[0])
+    assert lens.sum() == 32768 and np.all(lens[:-1] >= 256) and np.all(lens <= 4096)
+    assert v.initial_states.shape == (v.nseq, 2, 4, 4)
