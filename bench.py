@@ -1,0 +1,176 @@
+"""Benchmark of the SSD layer forward on one MI355X.
+
+One step = one ``ssd_forward`` call (every step of the block decomposition)
+over one batch of seeded synthetic input already resident in HBM.  Inputs
+rotate among three independent copies so that the 256 MB last-level cache
+cannot serve a step from the previous one.  Prints one JSON line.
+
+Default workload: Mamba-2-2.7B-like layer, batch 4 x seqlen 4096, 80 heads of
+64, state 128, one group, chunk 256, bf16 inputs with float32 accumulation.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+PEAK_BF16_FLOPS = 2.5e15
+PEAK_F32_MFMA_FLOPS = 157.3e12
+PEAK_HBM_BPS = 8.0e12
+
+
+def algorithmic_counts(p, nseq):
+    """FLOPs (block-decomposition cost model of Section 6 with the Gram C B^T
+    counted once per group, in two conventions) and compulsory HBM bytes."""
+    b, T, H, P, N, G, Q = p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups, p.chunk_size
+    tok = b * T
+    f_full = tok * (2 * Q * N * G + H * (2 * Q * P + 4 * N * P))
+    f_causal = tok * ((Q + 1) * N * G + H * ((Q + 1) * P + 4 * N * P))
+    act = 2 if p.dtype == "bf16" else 4
+    units = nseq if p.varlen else b
+    state_bytes = units * H * P * N * 4
+    byts = act * (2 * tok * H * P + tok * H + 2 * tok * G * N) + state_bytes
+    if p.init_states:
+        byts += state_bytes
+    if p.varlen:
+        byts += 4 * tok
+    byts += 4 * 2 * H  # A_log, D
+    return f_full, f_causal, byts
+
+
+def cpu_baseline(inp, budget_s=20.0):
+    """The oracle (untuned) on the host cores, on a bounded sample of the
+    workload: all tokens, a subset of heads sized to ~budget_s of CPU time."""
+    import numpy as np
+
+    import oracle
+
+    p = inp.problem
+    threads = oracle.default_threads()
+    # calibrate on one head
+    t0 = time.perf_counter()
+    oracle.forward_inputs(inp, heads=[0], nthreads=1)
+    one = time.perf_counter() - t0
+    nheads = int(max(1, min(p.nheads, budget_s * threads / max(one, 1e-6) / 1.5)))
+    heads = list(np.linspace(0, p.nheads - 1, nheads).astype(int))
+    t0 = time.perf_counter()
+    oracle.forward_inputs(inp, heads=heads, nthreads=threads)
+    el = time.perf_counter() - t0
+    tok_per_s = p.batch * p.seqlen * (len(heads) / p.nheads) / el
+    return {"value": tok_per_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "all %d tokens x %d of %d heads (float64 sequential recurrence, "
+                      "OpenMP over heads), %.1f s; rate scaled to all heads"
+                      % (p.batch * p.seqlen, len(heads), p.nheads, el)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mamba2_2p7b")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copies", type=int, default=3)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (--gpus 1); the sequence/head "
+              "sharding across GPUs is designed but not built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2405_21060_amd import ssd
+    from paper_2405_21060_amd.inputs import WORKLOADS, make_inputs
+    from tests.ssd_harness import to_device
+
+    p = WORKLOADS[args.workload]
+    inp = make_inputs(p, args.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    copies = [to_device(inp) for _ in range(max(1, args.copies))]
+    outs = [torch.empty_like(c["x"]) for c in copies]
+    units = inp.nseq if p.varlen else p.batch
+    fins = [torch.empty((units, p.nheads, p.headdim, p.dstate), dtype=torch.float32, device=dev)
+            for _ in copies]
+    prob = ssd.make_problem(p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups,
+                            p.chunk_size, ssd.SSD_DTYPE_BF16 if p.dtype == "bf16" else ssd.SSD_DTYPE_F32,
+                            inp.nseq if p.varlen else 0)
+    wsb = ssd.ssd_workspace_bytes(prob)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i):
+        c = copies[i % len(copies)]
+        ptr = lambda t: None if t is None else t.data_ptr()
+        rc = ssd.ssd_forward(prob, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]),
+                             ptr(c["C"]), ptr(c["D"]), ptr(c["initial_states"]), ptr(c["seq_idx"]),
+                             ptr(outs[i % len(copies)]), ptr(fins[i % len(copies)]), ws.data_ptr(),
+                             wsb, stream.cuda_stream)
+        if rc != 0:
+            raise ssd.SsdError(rc, "ssd_forward")
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(args.steps):
+        step(i)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+
+    f_full, f_causal, byts = algorithmic_counts(p, inp.nseq)
+    sec = ms * 1e-3
+    tokens = p.batch * p.seqlen
+    peak_flops = PEAK_BF16_FLOPS if p.dtype == "bf16" else PEAK_F32_MFMA_FLOPS
+    t_hbm, t_mfma = byts / PEAK_HBM_BPS, f_full / peak_flops
+    if t_hbm >= t_mfma:
+        roof = {"bound": "hbm", "achieved": byts / sec / 1e9, "peak": PEAK_HBM_BPS / 1e9,
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": f_full / sec / 1e12, "peak": peak_flops / 1e12,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    line = {
+        "metric": "SSD fwd tokens/s (2.7B-layer shape, 1 GPU)",
+        "value": tokens / sec,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": p.dtype,
+        "data": "synthetic (seeded; shapes and distributions of the Mamba-2 layer)",
+        "config": {"workload": args.workload, "batch": p.batch, "seqlen": p.seqlen,
+                   "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate,
+                   "ngroups": p.ngroups, "chunk_size": p.chunk_size,
+                   "nseq": inp.nseq if p.varlen else None},
+        "tflops_full_block": f_full / sec / 1e12,
+        "tflops_causal": f_causal / sec / 1e12,
+        "pct_mfma_peak_full_block": 100.0 * f_full / sec / peak_flops,
+        "pct_mfma_peak_causal": 100.0 * f_causal / sec / peak_flops,
+        "hbm_gbps_compulsory": byts / sec / 1e9,
+        "roofline": roof,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(inp)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

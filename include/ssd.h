@@ -1,0 +1,112 @@
+/*
+ * ssd.h -- C ABI of the MI355X (gfx950) SSD layer forward.
+ *
+ * Computes y = SSM(A, B, C)(x) for the scalar-transition selective SSM of the
+ * SSD layer (Section 5 of "Transformers are SSMs"), by the chunked block
+ * decomposition of its 1-semiseparable matrix (Section 6): per chunk of Q
+ * tokens, the diagonal block in its quadratic (masked-attention) form, the
+ * chunk-final states (right factors), a scan of the states over chunks (centre
+ * factors, the scalar SSM scan of Appendix B) and the state-to-output term
+ * (left factors).  The problem statement follows the paper's
+ *   Y, final_state = ssd(X, A, B, C, block_len, initial_states)
+ * with discretisation exp(dt*A) / dt*x, a per-head skip D, grouped B/C heads
+ * (Section 7) and packed variable-length rows (Section 8.3) added.
+ *
+ * Per head h (group g = h / (H/G)), with A_h = -exp(A_log[h]) and state S (P x N):
+ *     S_t = exp(dt_t A_h) S_{t-1} + (dt_t x_t) B_t^T,    y_t = S_t C_t + D_h x_t,
+ * S_{-1} = initial state (zero when none).  With seq_idx the state entering
+ * the first token of every sequence is that sequence's initial state.
+ *
+ * Layouts (row-major, contiguous, element strides implied by the shape):
+ *   x, y            (batch, seqlen, nheads, headdim)      dtype
+ *   dt              (batch, seqlen, nheads)               dtype, already positive
+ *                                                         (softplus applied by the caller)
+ *   A_log           (nheads)                              float32
+ *   B, C            (batch, seqlen, ngroups, dstate)      dtype
+ *   D               (nheads)                              float32, may be NULL (= 0)
+ *   seq_idx         (1, seqlen)                           int32, may be NULL
+ *   initial_states  (batch, nheads, headdim, dstate)      float32, may be NULL (= 0);
+ *                   (nseq, nheads, headdim, dstate) when seq_idx is given
+ *   final_states    same shape as initial_states          float32, may be NULL (not written)
+ * "dtype" is SSD_DTYPE_F32 (float) or SSD_DTYPE_BF16 (bfloat16 bits).  All
+ * arithmetic accumulates in float32; y is rounded to dtype (nearest even).
+ *
+ * seq_idx contract (not checked on the device): non-decreasing, starting at 0,
+ * consecutive ids, last value nseq - 1; batch must be 1.
+ *
+ * Ownership: every pointer is device memory owned by the caller; the library
+ * allocates nothing on the call path.  `workspace` is caller-provided device
+ * memory of at least ssd_workspace_bytes() bytes; its contents on entry do not
+ * matter and on exit are unspecified.  The call is asynchronous on `stream`
+ * (a hipStream_t; NULL = the null stream); it keeps no global mutable state, so
+ * concurrent calls with distinct workspaces are safe.  Results are
+ * deterministic (no floating-point atomics).
+ *
+ * Errors: functions return SSD_OK (0) or a negative ssd_status.  On error no
+ * device work has been enqueued, except SSD_ERR_LAUNCH (a launch failed after
+ * earlier kernels of the call were enqueued).
+ */
+#ifndef SSD_H_
+#define SSD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SSD_DTYPE_F32 = 0,
+    SSD_DTYPE_BF16 = 1
+} ssd_dtype;
+
+typedef enum {
+    SSD_OK = 0,
+    SSD_ERR_NULL_ARG = -1,         /* a required pointer is NULL                     */
+    SSD_ERR_BAD_SHAPE = -2,        /* a dimension < 1, or nheads % ngroups != 0,
+                                      or nseq < 1 with seq_idx                        */
+    SSD_ERR_BAD_CHUNK = -3,        /* chunk_size not in {32, 64, 128, 256}           */
+    SSD_ERR_BAD_DTYPE = -4,        /* dtype not an ssd_dtype                         */
+    SSD_ERR_UNSUPPORTED_DIMS = -5, /* headdim not a multiple of 16 in [16, 128], or
+                                      dstate not a multiple of 16 in [16, 256]       */
+    SSD_ERR_SEQIDX_BATCH = -6,     /* seq_idx given with batch != 1                  */
+    SSD_ERR_WORKSPACE = -7,        /* workspace NULL or smaller than required        */
+    SSD_ERR_LAUNCH = -8,           /* a kernel launch failed                         */
+    SSD_ERR_TOO_LARGE = -9         /* a tensor exceeds the supported index range     */
+} ssd_status;
+
+typedef struct {
+    int64_t batch;       /* b                                        */
+    int64_t seqlen;      /* T (any length >= 1; the last chunk may be partial) */
+    int64_t nheads;      /* H                                        */
+    int64_t headdim;     /* P                                        */
+    int64_t dstate;      /* N                                        */
+    int64_t ngroups;     /* G, divides H                             */
+    int64_t chunk_size;  /* Q, the block length of the decomposition */
+    int64_t nseq;        /* number of sequences; read only when seq_idx != NULL */
+    int32_t dtype;       /* ssd_dtype of x, dt, B, C, y              */
+} ssd_problem;
+
+/* Workspace size in bytes for `prob` (Section 6 intermediates: chunk cumsums,
+ * chunk states).  Returns SSD_OK and writes *bytes, or a validation error. */
+int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes);
+
+/* The SSD forward (Section 6 algorithm; definition above).  `D`,
+ * `initial_states`, `seq_idx` and `final_states` may be NULL.  `stream` is a
+ * hipStream_t. */
+int ssd_forward(const ssd_problem* prob,
+                const void* x, const void* dt, const float* A_log,
+                const void* B, const void* C, const float* D,
+                const float* initial_states, const int32_t* seq_idx,
+                void* y, float* final_states,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* ssd_error_string(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSD_H_ */

@@ -1,0 +1,152 @@
+// C ABI of the SSD forward: validation, workspace planning, launch.
+// Everything here runs on the host; no HIP call is made before the arguments
+// have been validated, so an error return never leaves work on the stream.
+#include "ssd.h"
+
+#include <hip/hip_runtime.h>
+
+#include "ssd_internal.h"
+
+namespace ssd {
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Shape {
+    int64_t b, T, H, P, N, G, Q, nC, nseq;
+    bool bf16;
+};
+
+// 2^31 - 1: every per-tensor element count must stay below it, and every
+// kernel grid dimension far below it.
+constexpr int64_t kMaxElems = 0x7fffffffLL;
+
+int validate(const ssd_problem* prob, bool has_seq_idx, Shape* s)
+{
+    if (!prob) return SSD_ERR_NULL_ARG;
+    if (prob->dtype != SSD_DTYPE_F32 && prob->dtype != SSD_DTYPE_BF16) return SSD_ERR_BAD_DTYPE;
+    if (prob->batch < 1 || prob->seqlen < 1 || prob->nheads < 1 || prob->headdim < 1 ||
+        prob->dstate < 1 || prob->ngroups < 1 || prob->nheads % prob->ngroups != 0)
+        return SSD_ERR_BAD_SHAPE;
+    const int64_t Q = prob->chunk_size;
+    if (Q != 32 && Q != 64 && Q != 128 && Q != 256) return SSD_ERR_BAD_CHUNK;
+    if (prob->headdim % 16 != 0 || prob->headdim > 128 || prob->dstate % 16 != 0 ||
+        prob->dstate > 256)
+        return SSD_ERR_UNSUPPORTED_DIMS;
+    if (has_seq_idx) {
+        if (prob->batch != 1) return SSD_ERR_SEQIDX_BATCH;
+        if (prob->nseq < 1 || prob->nseq > prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    }
+    s->b = prob->batch;
+    s->T = prob->seqlen;
+    s->H = prob->nheads;
+    s->P = prob->headdim;
+    s->N = prob->dstate;
+    s->G = prob->ngroups;
+    s->Q = Q;
+    s->nC = (s->T + Q - 1) / Q;
+    s->nseq = has_seq_idx ? prob->nseq : s->b;
+    s->bf16 = prob->dtype == SSD_DTYPE_BF16;
+    // index-range limits (grid y/z are H and b; flat element counts in int64
+    // arithmetic everywhere, but keep each tensor addressable by 31 bits of
+    // 16-byte vectors and the grid inside HIP's limits)
+    if (s->H > 65535 || s->b > 65535 || s->nC > 0x7fffffff) return SSD_ERR_TOO_LARGE;
+    const double elems_x = static_cast<double>(s->b) * s->T * s->H * s->P;
+    const double elems_st = static_cast<double>(s->b) * s->nC * s->H * s->P * s->N;
+    if (elems_x > 16.0 * kMaxElems || elems_st > 16.0 * kMaxElems) return SSD_ERR_TOO_LARGE;
+    return SSD_OK;
+}
+
+}  // namespace
+
+WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int64_t G,
+                                 int64_t Q, int64_t nC)
+{
+    WorkspaceLayout w;
+    size_t off = 0;
+    w.cs = off;
+    off = align_up(off + sizeof(float) * static_cast<size_t>(b * H * nC * Q));
+    w.info = off;
+    off = align_up(off + sizeof(int4) * static_cast<size_t>(b * H * nC));
+    w.gram = off;
+    off = align_up(off + sizeof(float) * static_cast<size_t>(b * G * nC) * static_cast<size_t>(Q * Q));
+    w.states = off;
+    off = align_up(off + sizeof(float) * static_cast<size_t>(b * nC * H) * static_cast<size_t>(P * N));
+    w.total = off;
+    return w;
+}
+
+}  // namespace ssd
+
+extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
+{
+    if (!bytes) return SSD_ERR_NULL_ARG;
+    ssd::Shape s;
+    const int rc = ssd::validate(prob, /*has_seq_idx=*/false, &s);  // size does not depend on it
+    if (rc != SSD_OK) return rc;
+    *bytes = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC).total;
+    return SSD_OK;
+}
+
+extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* dt,
+                           const float* A_log, const void* B, const void* C, const float* D,
+                           const float* initial_states, const int32_t* seq_idx, void* y,
+                           float* final_states, void* workspace, size_t workspace_bytes,
+                           void* stream)
+{
+    ssd::Shape s;
+    int rc = ssd::validate(prob, seq_idx != nullptr, &s);
+    if (rc != SSD_OK) return rc;
+    if (!x || !dt || !A_log || !B || !C || !y) return SSD_ERR_NULL_ARG;
+    const ssd::WorkspaceLayout w = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC);
+    if (!workspace || workspace_bytes < w.total) return SSD_ERR_WORKSPACE;
+
+    ssd::Params p;
+    p.b = s.b;
+    p.T = s.T;
+    p.H = s.H;
+    p.P = s.P;
+    p.N = s.N;
+    p.G = s.G;
+    p.Q = s.Q;
+    p.nC = s.nC;
+    p.nseq = s.nseq;
+    p.x = x;
+    p.dt = dt;
+    p.A_log = A_log;
+    p.B = B;
+    p.C = C;
+    p.D = D;
+    p.init = initial_states;
+    p.seq_idx = seq_idx;
+    p.y = y;
+    p.fin = final_states;
+    char* ws = static_cast<char*>(workspace);
+    p.cs = reinterpret_cast<float*>(ws + w.cs);
+    p.info = reinterpret_cast<int4*>(ws + w.info);
+    p.gram = reinterpret_cast<float*>(ws + w.gram);
+    p.states = reinterpret_cast<float*>(ws + w.states);
+    const hipError_t err = ssd::launch_unfused(p, s.bf16, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
+extern "C" const char* ssd_error_string(int code)
+{
+    switch (code) {
+    case SSD_OK: return "success";
+    case SSD_ERR_NULL_ARG: return "a required pointer is NULL";
+    case SSD_ERR_BAD_SHAPE: return "invalid shape (dimension < 1, nheads % ngroups != 0, or bad nseq)";
+    case SSD_ERR_BAD_CHUNK: return "chunk_size must be 32, 64, 128 or 256";
+    case SSD_ERR_BAD_DTYPE: return "dtype must be SSD_DTYPE_F32 or SSD_DTYPE_BF16";
+    case SSD_ERR_UNSUPPORTED_DIMS:
+        return "headdim must be a multiple of 16 in [16,128] and dstate a multiple of 16 in [16,256]";
+    case SSD_ERR_SEQIDX_BATCH: return "seq_idx requires batch == 1";
+    case SSD_ERR_WORKSPACE: return "workspace missing or smaller than ssd_workspace_bytes()";
+    case SSD_ERR_LAUNCH: return "kernel launch failed";
+    case SSD_ERR_TOO_LARGE: return "problem exceeds the supported index range";
+    default: return "unknown ssd status";
+    }
+}

@@ -1,0 +1,163 @@
+"""Python binding of the C ABI in ``include/ssd.h`` (argument marshalling only).
+
+Every step of the forward runs in the HIP kernels of ``libssd_hip.so``; this
+module only turns torch tensors into device pointers and the current HIP stream
+into a ``hipStream_t``.  There is no CPU fallback: if the library is missing
+or cannot be loaded, every call raises.
+
+Names mirror the ABI: :func:`ssd_workspace_bytes`, :func:`ssd_forward`,
+:func:`ssd_error_string`; :func:`forward` is the tensor-level convenience
+wrapper returning ``(y, final_states)`` like the paper's
+``ssd(X, A, B, C, block_len, initial_states)``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libssd_hip.so")
+
+SSD_DTYPE_F32 = 0
+SSD_DTYPE_BF16 = 1
+SSD_OK = 0
+SSD_ERR_NULL_ARG = -1
+SSD_ERR_BAD_SHAPE = -2
+SSD_ERR_BAD_CHUNK = -3
+SSD_ERR_BAD_DTYPE = -4
+SSD_ERR_UNSUPPORTED_DIMS = -5
+SSD_ERR_SEQIDX_BATCH = -6
+SSD_ERR_WORKSPACE = -7
+SSD_ERR_LAUNCH = -8
+SSD_ERR_TOO_LARGE = -9
+
+EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_error_string")
+
+
+class SsdProblem(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int64),
+        ("seqlen", ctypes.c_int64),
+        ("nheads", ctypes.c_int64),
+        ("headdim", ctypes.c_int64),
+        ("dstate", ctypes.c_int64),
+        ("ngroups", ctypes.c_int64),
+        ("chunk_size", ctypes.c_int64),
+        ("nseq", ctypes.c_int64),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class SsdError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__("%s failed: %s (%d)" % (where, ssd_error_string(code), code))
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load ``libssd_hip.so`` (built by ``paper_2405_21060_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            "HIP library %s is missing: build it with `python -m paper_2405_21060_amd.build` "
+            "(there is no CPU fallback)" % path)
+    lib = ctypes.CDLL(path)
+    vp = ctypes.c_void_p
+    lib.ssd_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_workspace_bytes.argtypes = [ctypes.POINTER(SsdProblem), ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_forward.restype = ctypes.c_int
+    lib.ssd_forward.argtypes = [ctypes.POINTER(SsdProblem)] + [vp] * 10 + [vp, ctypes.c_size_t, vp]
+    lib.ssd_error_string.restype = ctypes.c_char_p
+    lib.ssd_error_string.argtypes = [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+def make_problem(batch, seqlen, nheads, headdim, dstate, ngroups, chunk_size, dtype, nseq=0):
+    return SsdProblem(batch, seqlen, nheads, headdim, dstate, ngroups, chunk_size, nseq, dtype)
+
+
+def ssd_workspace_bytes(prob: SsdProblem) -> int:
+    out = ctypes.c_size_t(0)
+    rc = load_library().ssd_workspace_bytes(ctypes.byref(prob), ctypes.byref(out))
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_workspace_bytes")
+    return int(out.value)
+
+
+def ssd_error_string(code: int) -> str:
+    return load_library().ssd_error_string(int(code)).decode()
+
+
+def ssd_forward(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx, y,
+                final_states, workspace, workspace_bytes: int, stream) -> int:
+    """Raw ABI call on integer device addresses (0 = NULL); returns the status."""
+    return load_library().ssd_forward(
+        ctypes.byref(prob), x, dt, A_log, B, C, D or None, initial_states or None,
+        seq_idx or None, y, final_states or None, workspace, int(workspace_bytes),
+        stream or None)
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def forward(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=None,
+            seq_idx=None, nseq: Optional[int] = None, return_final_states: bool = True,
+            workspace=None, out=None, final_out=None) -> Tuple[object, object]:
+    """SSD forward on device tensors; returns ``(y, final_states or None)``.
+
+    x (b,T,H,P), dt (b,T,H), B/C (b,T,G,N): float32 or bfloat16, all the same
+    dtype, contiguous, on one HIP device.  A_log, D (H): float32.
+    initial_states (b|nseq,H,P,N) float32.  seq_idx (1,T) int32 with nseq
+    sequences.  Launches on torch's current stream of x's device.
+    """
+    import torch
+
+    dev = x.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    if x.dtype == torch.bfloat16:
+        dtype = SSD_DTYPE_BF16
+    elif x.dtype == torch.float32:
+        dtype = SSD_DTYPE_F32
+    else:
+        raise TypeError("x must be float32 or bfloat16")
+    for name, t in (("dt", dt), ("B", B), ("C", C)):
+        if t.dtype != x.dtype:
+            raise TypeError("%s must have x's dtype" % name)
+    for name, t in (("A_log", A_log), ("D", D), ("initial_states", initial_states)):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("%s must be float32" % name)
+    if seq_idx is not None and seq_idx.dtype != torch.int32:
+        raise TypeError("seq_idx must be int32")
+    for t in (x, dt, A_log, B, C, D, initial_states, seq_idx):
+        if t is not None and (t.device != dev or not t.is_contiguous()):
+            raise ValueError("all tensors must be contiguous and on x's device")
+    b, T, H, P = x.shape
+    G, N = B.shape[2], B.shape[3]
+    if seq_idx is not None and nseq is None:
+        nseq = int(seq_idx[0, -1].item()) + 1
+    prob = make_problem(b, T, H, P, N, G, chunk_size, dtype, nseq or 0)
+    wsb = ssd_workspace_bytes(prob)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    y = out if out is not None else torch.empty_like(x)
+    units = nseq if seq_idx is not None else b
+    fin = None
+    if return_final_states:
+        fin = final_out if final_out is not None else torch.empty(
+            (units, H, P, N), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = ssd_forward(prob, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),
+                     _ptr(initial_states), _ptr(seq_idx), _ptr(y), _ptr(fin),
+                     _ptr(workspace), wsb, stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_forward")
+    return y, fin

@@ -1,0 +1,101 @@
+"""Host-side checks of the C ABI: the library loads, exports what the header
+declares, and rejects invalid arguments before touching the device."""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2405_21060_amd import ssd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssd.h")
+
+# Fake, never dereferenced addresses: every call below fails validation first.
+FAKE = 0x10000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\s*\*)\s*(ssd_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ssd.load_library()
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(ssd.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", ssd.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s+(\w+)$", out, re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def prob(**kw):
+    base = dict(batch=4, seqlen=4096, nheads=80, headdim=64, dstate=128, ngroups=1,
+                chunk_size=256, dtype=ssd.SSD_DTYPE_BF16, nseq=0)
+    base.update(kw)
+    return ssd.make_problem(base["batch"], base["seqlen"], base["nheads"], base["headdim"],
+                            base["dstate"], base["ngroups"], base["chunk_size"], base["dtype"],
+                            base["nseq"])
+
+
+def fwd(p, ws_bytes=1 << 40, seq_idx=0, x=FAKE):
+    return ssd.ssd_forward(p, x, FAKE, FAKE, FAKE, FAKE, 0, 0, seq_idx, FAKE, 0, FAKE,
+                           ws_bytes, 0)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), ssd.SSD_ERR_BAD_DTYPE),
+    (dict(nheads=80, ngroups=3), ssd.SSD_ERR_BAD_SHAPE),
+    (dict(seqlen=0), ssd.SSD_ERR_BAD_SHAPE),
+    (dict(batch=-1), ssd.SSD_ERR_BAD_SHAPE),
+    (dict(chunk_size=48), ssd.SSD_ERR_BAD_CHUNK),
+    (dict(chunk_size=512), ssd.SSD_ERR_BAD_CHUNK),
+    (dict(headdim=24), ssd.SSD_ERR_UNSUPPORTED_DIMS),
+    (dict(headdim=256), ssd.SSD_ERR_UNSUPPORTED_DIMS),
+    (dict(dstate=512), ssd.SSD_ERR_UNSUPPORTED_DIMS),
+    (dict(dstate=8), ssd.SSD_ERR_UNSUPPORTED_DIMS),
+    (dict(nheads=70000, ngroups=1), ssd.SSD_ERR_TOO_LARGE),
+])
+def test_validation_errors(lib, kw, code):
+    p = prob(**kw)
+    with pytest.raises(ssd.SsdError) as e:
+        ssd.ssd_workspace_bytes(p)
+    assert e.value.code == code
+    assert fwd(p) == code
+
+
+def test_seq_idx_rules(lib):
+    assert fwd(prob(batch=2, nseq=3), seq_idx=FAKE) == ssd.SSD_ERR_SEQIDX_BATCH
+    assert fwd(prob(batch=1, nseq=0), seq_idx=FAKE) == ssd.SSD_ERR_BAD_SHAPE
+    assert fwd(prob(batch=1, seqlen=10, nseq=11), seq_idx=FAKE) == ssd.SSD_ERR_BAD_SHAPE
+
+
+def test_null_and_workspace_errors(lib):
+    p = prob()
+    assert fwd(p, x=0) == ssd.SSD_ERR_NULL_ARG
+    need = ssd.ssd_workspace_bytes(p)
+    assert fwd(p, ws_bytes=need - 1) == ssd.SSD_ERR_WORKSPACE
+    assert lib.ssd_workspace_bytes(None, None) == ssd.SSD_ERR_NULL_ARG
+
+
+def test_workspace_grows_with_problem(lib):
+    small = ssd.ssd_workspace_bytes(prob(batch=1, seqlen=256))
+    large = ssd.ssd_workspace_bytes(prob())
+    assert 0 < small < large
+    assert ssd.ssd_workspace_bytes(prob(seqlen=4097)) > large  # partial chunk counted
+
+
+def test_error_strings(lib):
+    for code in range(0, -10, -1):
+        s = ssd.ssd_error_string(code)
+        assert s and s != "unknown ssd status"
+    assert ssd.ssd_error_string(-100) == "unknown ssd status"

@@ -1,0 +1,133 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Tolerance (per output tensor, max |gpu - oracle| / max |oracle|): 1e-4 for
+float32 inputs, 2e-2 for bfloat16 inputs with float32 accumulation.  Full-size
+workloads are checked on sampled heads (the oracle computes only those heads;
+heads are independent given their group's B and C).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2405_21060_amd.inputs import WORKLOADS, Problem, make_inputs
+from tests.ssd_harness import TOL, announce, rel_err, run_gpu, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    from paper_2405_21060_amd import ssd
+
+    ssd.load_library()  # raises loudly when the HIP library is missing
+
+
+def check(inp, chunk_size=None, heads=None, use_init=True, tag=""):
+    p = inp.problem
+    announce("%s %s seed-shape b%d T%d H%d P%d N%d G%d Q%s varlen=%s" % (
+        tag, p.dtype, p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups,
+        chunk_size or p.chunk_size, p.varlen))
+    y, fin = run_gpu(inp, chunk_size=chunk_size, use_init=use_init)
+    if not use_init:
+        inp.initial_states = None
+    y_ref, fin_ref = oracle.forward_inputs(inp, heads=heads)
+    y_gpu = to_f64(y)
+    fin_gpu = fin.cpu().numpy().astype(np.float64)
+    if heads is not None:
+        y_gpu = y_gpu[:, :, heads]
+        fin_gpu = fin_gpu[:, heads]
+    ey, ef = rel_err(y_gpu, y_ref), rel_err(fin_gpu, fin_ref)
+    announce("  rel err y %.3e final %.3e (tol %.0e)" % (ey, ef, TOL[p.dtype]))
+    assert np.all(np.isfinite(y_gpu)) and np.all(np.isfinite(fin_gpu))
+    assert ey <= TOL[p.dtype], ey
+    assert ef <= TOL[p.dtype], ef
+    return y, fin
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_tiny_f32(seed):
+    check(make_inputs(WORKLOADS["tiny_f32"], seed), tag="tiny_f32")
+
+
+@pytest.mark.parametrize("Q", [32, 64, 128, 256])
+def test_chunk_sizes_ragged_bf16(Q):
+    # several chunks and tiles, ragged last chunk (1000 % Q != 0), G = 2
+    p = Problem(2, 1000, 4, 64, 128, 2, Q, "bf16", init_states=True)
+    check(make_inputs(p, 5), tag="ragged")
+
+
+@pytest.mark.parametrize("Q", [32, 64, 256])
+def test_chunk_sizes_ragged_f32(Q):
+    p = Problem(1, 777, 3, 32, 48, 3, Q, "f32", init_states=True)
+    check(make_inputs(p, 6), tag="ragged_f32")
+
+
+@pytest.mark.parametrize("dims", [(16, 16), (64, 64), (64, 256), (128, 128), (32, 16)])
+def test_state_and_head_dims(dims):
+    P, N = dims
+    p = Problem(1, 600, 2, P, N, 1, 128, "bf16", init_states=True)
+    check(make_inputs(p, 7), tag="dims")
+
+
+def test_single_token_and_short_sequences():
+    for T in (1, 2, 17, 255, 256, 257):
+        p = Problem(2, T, 3, 16, 32, 1, 256, "f32", init_states=True)
+        check(make_inputs(p, T), tag="T=%d" % T)
+
+
+def test_varlen_small_with_edge_boundaries():
+    # boundaries at a chunk edge (64), at a chunk's last token (127 -> 128),
+    # length-1 sequences, several sequences inside one chunk
+    lens = [64, 63, 1, 1, 70, 5, 3, 200, 1, 40]
+    T = sum(lens)
+    p = Problem(1, T, 4, 32, 64, 2, 64, "f32", varlen=True, init_states=True)
+    inp = make_inputs(p, 8)
+    inp.seq_idx = np.repeat(np.arange(len(lens), dtype=np.int32), lens).reshape(1, T)
+    inp.nseq = len(lens)
+    inp.initial_states = np.random.default_rng(1).standard_normal(
+        (len(lens), 4, 32, 64)).astype(np.float32)
+    check(inp, tag="varlen_edges_f32")
+    check(inp, use_init=False, tag="varlen_edges_noinit")
+
+
+def test_varlen_bf16_small():
+    p = Problem(1, 3000, 8, 64, 128, 4, 256, "bf16", varlen=True, len_lo=1, len_hi=700,
+                init_states=True)
+    check(make_inputs(p, 9), tag="varlen_bf16_small")
+
+
+def test_deterministic_repeat():
+    import torch
+
+    inp = make_inputs(Problem(2, 1024, 8, 64, 128, 1, 256, "bf16"), 3)
+    y1, f1 = run_gpu(inp)
+    y2, f2 = run_gpu(inp)
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    assert torch.equal(f1, f2)
+
+
+def test_chunk_size_independence_large():
+    """Chunk-size independence at a size beyond the oracle's comfort: the
+    block decomposition is exact for any block length (Section 6)."""
+    inp = make_inputs(Problem(2, 4096, 16, 64, 128, 1, 256, "bf16"), 4)
+    ys = [to_f64(run_gpu(inp, chunk_size=Q)[0]) for Q in (64, 128, 256)]
+    for y in ys[:-1]:
+        assert rel_err(y, ys[-1]) <= TOL["bf16"]
+
+
+# Full-size workloads: every head of the GPU result is produced; the oracle
+# checks a sample of heads (first, last, and a middle one per group span).
+FULL = ["mamba2_130m", "mamba2_2p7b", "varlen_g8", "sweep_T512_N128",
+        "sweep_T65536_N128", "sweep_T16384_N64", "sweep_T16384_N256"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_sampled_heads(name):
+    p = WORKLOADS[name]
+    inp = make_inputs(p, 0)
+    heads = sorted({0, p.nheads // 2 + 1, p.nheads - 1})
+    check(inp, heads=heads, tag=name)
