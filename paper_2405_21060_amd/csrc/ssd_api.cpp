@@ -5,6 +5,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
+
 #include "ssd_internal.h"
 
 namespace ssd {
@@ -62,6 +64,20 @@ int validate(const ssd_problem* prob, bool has_seq_idx, Shape* s)
 
 }  // namespace
 
+// Heads per workgroup of the fused path: a divisor of the heads per group
+// (a workgroup's heads share B and C).  SSD_HEADS_PER_WG overrides the default
+// (tuning knob; ignored unless it divides the heads per group).
+int64_t heads_per_workgroup(int64_t heads_per_group)
+{
+    if (const char* env = std::getenv("SSD_HEADS_PER_WG")) {
+        const long v = std::strtol(env, nullptr, 10);
+        if (v >= 1 && heads_per_group % v == 0) return v;
+    }
+    for (int64_t hg : {4, 2, 1})
+        if (heads_per_group % hg == 0) return hg;
+    return 1;
+}
+
 WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int64_t G,
                                  int64_t Q, int64_t nC)
 {
@@ -87,7 +103,12 @@ extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
     ssd::Shape s;
     const int rc = ssd::validate(prob, /*has_seq_idx=*/false, &s);  // size does not depend on it
     if (rc != SSD_OK) return rc;
-    *bytes = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC).total;
+    size_t need = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC).total;
+    if (ssd::fused_supported(s.P, s.N, s.Q, s.bf16, false)) {
+        const size_t f = ssd::fused_layout(s.b, s.H, s.N, s.G, s.nC).total;
+        if (f > need) need = f;
+    }
+    *bytes = need;
     return SSD_OK;
 }
 
@@ -101,8 +122,43 @@ extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* d
     int rc = ssd::validate(prob, seq_idx != nullptr, &s);
     if (rc != SSD_OK) return rc;
     if (!x || !dt || !A_log || !B || !C || !y) return SSD_ERR_NULL_ARG;
+    size_t need = 0;
+    if (ssd_workspace_bytes(prob, &need) != SSD_OK || !workspace || workspace_bytes < need)
+        return SSD_ERR_WORKSPACE;
+    const char* path = std::getenv("SSD_PATH");  // debug knob: "unfused" forces the step-by-step kernels
+    const bool force_unfused = path && path[0] == 'u';
+    if (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16, seq_idx != nullptr)) {
+        const ssd::FusedLayout fw = ssd::fused_layout(s.b, s.H, s.N, s.G, s.nC);
+        ssd::FusedParams f;
+        f.b = s.b;
+        f.T = s.T;
+        f.H = s.H;
+        f.P = s.P;
+        f.N = s.N;
+        f.G = s.G;
+        f.nC = s.nC;
+        f.HG = ssd::heads_per_workgroup(s.H / s.G);
+        f.x = x;
+        f.dt = dt;
+        f.A_log = A_log;
+        f.B = B;
+        f.C = C;
+        f.D = D;
+        f.init = initial_states;
+        f.y = y;
+        f.fin = final_states;
+        char* base = static_cast<char*>(workspace);
+        f.cs2 = reinterpret_cast<float*>(base + fw.cs2);
+        f.dtT = reinterpret_cast<float*>(base + fw.dtT);
+        f.gram = reinterpret_cast<uint16_t*>(base + fw.gram);
+        f.BT = reinterpret_cast<uint16_t*>(base + fw.BT);
+        f.ring = reinterpret_cast<float*>(base + fw.ring);
+        f.flags = reinterpret_cast<int*>(base + fw.flags);
+        f.ticket = reinterpret_cast<int*>(base + fw.ticket);
+        const hipError_t err = ssd::launch_fused(f, static_cast<hipStream_t>(stream));
+        return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+    }
     const ssd::WorkspaceLayout w = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC);
-    if (!workspace || workspace_bytes < w.total) return SSD_ERR_WORKSPACE;
 
     ssd::Params p;
     p.b = s.b;

@@ -38,4 +38,35 @@ WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int
 // Enqueue the whole forward on `stream`; returns the first launch error.
 hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream);
 
+// Fused path (bf16, P = 64, N in {64, 128}, Q = 256, no packed rows).
+struct FusedParams {
+    int64_t b, T, H, P, N, G, nC, HG;
+    const void* x;
+    const void* dt;
+    const float* A_log;
+    const void* B;
+    const void* C;
+    const float* D;
+    const float* init;
+    void* y;
+    float* fin;
+    // workspace
+    float* cs2;       // (b, H, nC, Q)   chunk-local cumsum of dt*A, log2 units
+    float* dtT;       // (b, H, nC, Q)   dt, head-major
+    uint16_t* gram;   // (b, G, nC, tiles, 64 lanes, 4) causal Gram tiles, bf16, per-lane layout
+    uint16_t* BT;     // (b, G, nC, N, Q) B^T per chunk, bf16
+    float* ring;      // (b, H, 2, P, N) chunk-state ring
+    int* flags;       // (b, H, nC)      state-published flags
+    int* ticket;      // [0] work ticket, [1] wait-timeout error word
+};
+
+struct FusedLayout {
+    size_t cs2, dtT, gram, BT, ring, flags, ticket, total;
+};
+
+int64_t heads_per_workgroup(int64_t heads_per_group);
+bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16, bool varlen);
+FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC);
+hipError_t launch_fused(const FusedParams& p, hipStream_t stream);
+
 }  // namespace ssd
