@@ -104,6 +104,12 @@ __device__ __forceinline__ void st_coherent(float* p, float v)
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Column of token s in row p of the token-major LDS arrays (XT, XW): the
+// 8-token group is XOR-ed with p/8 so that the transposing writes of rows
+// 8 apart fall into different banks.  Groups of 4 and 8 aligned tokens stay
+// contiguous.
+__device__ __forceinline__ int swz(int p, int s) { return s ^ (((p >> 3) & 7) << 3); }
+
 // Causal tile index of (s-tile j, t-tile i), j <= i.
 __device__ __forceinline__ int tile_index(int i, int j) { return i * (i + 1) / 2 + j; }
 
@@ -202,125 +208,139 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
 // ---------------------------------------------------------------------------
 // main
 // ---------------------------------------------------------------------------
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// x of one head lives token-major in LDS: row s = 64 features (128 bytes),
+// its eight 16-byte groups XOR-swizzled by (s & 7) so that the transposing
+// reads of 4 consecutive rows spread over the banks.
+__device__ __forceinline__ int xs_off(int s, int p) { return s * kP + ((((p >> 3) ^ (s & 7)) << 3) | (p & 7)); }
+
+// ds_read_b64_tr_b16 within each 16-lane group: source lane j reads row
+// k0 + j/4, features f0 + 4 (j%4) .. +3; lane i then holds feature f0 + i of
+// rows k0 .. k0+3 -- an MFMA operand fragment (4 contraction slots) of x^T.
+__device__ __forceinline__ uint2 xfrag(const u16* xs, int k0, int f0, int lane)
+{
+    const int j = lane & 15;
+    const u16* a = xs + xs_off(k0 + (j >> 2), f0 + 4 * (j & 3));
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(a)));
+}
+
 template <int N>
 struct MainSmem {
     u16 GR[kTiles * 256];     // Gram tiles of the chunk: [tile][lane][4] bf16
-    u16 XT[kP * kQS];         // x^T (P x Q) of the current head
-    u16 XW[kP * kQS];         // x^T * w (P x Q); after the right factor: bf16 state (P x (N+8))
-    float cs[kQ];             // cs2 of the current head
+    u16 XS[2][kQ * kP];       // x of the current / next head (token-major, swizzled)
+    u16 HB[kP * (N + 8)];     // bf16 state entering the chunk, (P x N)
+    float cs[2][kQ];          // cs2 of the current / next head
+    float dt[2][kQ];
     float vf[kQ];             // dt_s exp2(cs2[tile end] - cs2_s)
     float w[kQ];              // dt_s exp2(cs2[Q-1] - cs2_s)
-    float dt[kQ];
     int ticket;
 };
 
-// One K-step (32 tokens: s-tiles j0, j0+1) of the diagonal block for one
-// 16-token strip: the masked Gram values become the B operand (contraction
-// index permuted to the accumulator layout: slot e<4 -> s = 16 j0 + 4 lg + e,
-// slot e>=4 -> s = 16 (j0+1) + 4 lg + e - 4), x^T rows the A operand.
-// Off-diagonal tiles factor the mask as exp2(cs_t - cs_end(j)) * exp2(cs_end(j) - cs_s),
-// both factors <= 1; the diagonal tile takes exp2(cs_t - cs_s) directly.
-__device__ __forceinline__ void diag_step(const u16* XT, const float* cs, const float* vf,
-                                          const float* dt, uint2 g0, uint2 g1, int j0, int strip,
-                                          int t, float cst, int r, int lg, f32x4_t* y)
+// Masked Gram values of one K-step half (s-tile j, 4 tokens sb..sb+3 of this
+// lane) for the strip whose t-tile is `strip`: the B operand of the diagonal
+// block.  Off-diagonal tiles factor the 1-SS mask as
+// exp2(cs_t - cs_end(j)) * exp2(cs_end(j) - cs_s) (both factors <= 1, the
+// second one folded with dt_s into vf); the diagonal tile takes
+// exp2(cs_t - cs_s) directly, upper triangle zero.
+__device__ __forceinline__ void mask_half(uint2 gp, int j, int strip, int t, float cst, float csend,
+                                          float4 vf4, float4 cs4, float4 dt4, int sb, float* mv)
 {
-    float mv[8];
+    const float gv[4] = {__uint_as_float(gp.x << 16), __uint_as_float(gp.x & 0xFFFF0000u),
+                         __uint_as_float(gp.y << 16), __uint_as_float(gp.y & 0xFFFF0000u)};
+    if (j < strip) {
+        const float u = __builtin_amdgcn_exp2f(cst - csend);
+        mv[0] = gv[0] * (u * vf4.x);
+        mv[1] = gv[1] * (u * vf4.y);
+        mv[2] = gv[2] * (u * vf4.z);
+        mv[3] = gv[3] * (u * vf4.w);
+    } else if (j == strip) {
+        const float csv[4] = {cs4.x, cs4.y, cs4.z, cs4.w}, dtv[4] = {dt4.x, dt4.y, dt4.z, dt4.w};
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-        const int j = j0 + half;
-        const uint2 gp = half ? g1 : g0;
-        const float gv[4] = {__uint_as_float(gp.x << 16), __uint_as_float(gp.x & 0xFFFF0000u),
-                             __uint_as_float(gp.y << 16), __uint_as_float(gp.y & 0xFFFF0000u)};
-        const int sb = 16 * j + 4 * lg;
-        if (j < strip) {
-            const float u = __builtin_amdgcn_exp2f(cst - cs[16 * j + 15]);
-            const float4 vf4 = *reinterpret_cast<const float4*>(&vf[sb]);
-            mv[4 * half + 0] = gv[0] * (u * vf4.x);
-            mv[4 * half + 1] = gv[1] * (u * vf4.y);
-            mv[4 * half + 2] = gv[2] * (u * vf4.z);
-            mv[4 * half + 3] = gv[3] * (u * vf4.w);
-        } else if (j == strip) {
+        for (int v = 0; v < 4; ++v) {
+            // branch-free: the exponent is clamped to <= 0, the upper triangle selected away
+            const float e = __builtin_amdgcn_exp2f(fminf(cst - csv[v], 0.f));
+            mv[v] = (sb + v <= t) ? gv[v] * (e * dtv[v]) : 0.f;
+        }
+    } else {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int s = sb + v;
-                mv[4 * half + v] = (s <= t) ? gv[v] * (__builtin_amdgcn_exp2f(cst - cs[s]) * dt[s]) : 0.f;
-            }
-        } else {
+        for (int v = 0; v < 4; ++v) mv[v] = 0.f;
+    }
+}
+
+// Diagonal block of both strips of a wavefront (t-tiles sA < sB).  K-step m
+// covers s-tiles 2m, 2m+1; its contraction index is permuted to the Gram
+// accumulator layout (slot e<4 -> s = 32m + 4 lg + e, e>=4 -> s = 32m + 16 +
+// 4 lg + e - 4), and the x^T fragments, vf and cumsums of a K-step are read
+// once for both strips.
+__device__ __forceinline__ void diag_block(const u16* xs, const float* cs, const float* vf,
+                                           const float* dt, const u16* GR, int sA, int sB,
+                                           int r, int lg, int lane, f32x4_t* yA, f32x4_t* yB)
+{
+    const int tA = 16 * sA + r, tB = 16 * sB + r;
+    const float csA = cs[tA], csB = cs[tB];
+    const uint2* gA = reinterpret_cast<const uint2*>(GR) + tile_index(sA, 0) * 64 + lane;
+    const uint2* gB = reinterpret_cast<const uint2*>(GR) + tile_index(sB, 0) * 64 + lane;
+    const int nA = sA / 2 + 1, nB = sB / 2 + 1;
+#pragma unroll 1
+    for (int m = 0; m < nB; ++m) {
+        const int j0 = 2 * m;
+        const int sb0 = 32 * m + 4 * lg, sb1 = sb0 + 16;
+        uint4 af[4];
 #pragma unroll
-            for (int v = 0; v < 4; ++v) mv[4 * half + v] = 0.f;
+        for (int pt = 0; pt < 4; ++pt) {
+            const uint2 lo = xfrag(xs, sb0, 16 * pt, lane);
+            const uint2 hi = xfrag(xs, sb1, 16 * pt, lane);
+            af[pt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+        const float4 vf0 = *reinterpret_cast<const float4*>(&vf[sb0]);
+        const float4 vf1 = *reinterpret_cast<const float4*>(&vf[sb1]);
+        const float4 cs0 = *reinterpret_cast<const float4*>(&cs[sb0]);
+        const float4 cs1 = *reinterpret_cast<const float4*>(&cs[sb1]);
+        const float4 dt0 = *reinterpret_cast<const float4*>(&dt[sb0]);
+        const float4 dt1 = *reinterpret_cast<const float4*>(&dt[sb1]);
+        const float ce0 = cs[16 * j0 + 15], ce1 = cs[16 * j0 + 31];
+        {   // strip B (always active)
+            const uint2 g0 = gB[j0 * 64];
+            const uint2 g1 = (j0 + 1 <= sB) ? gB[(j0 + 1) * 64] : make_uint2(0, 0);
+            float mv[8];
+            mask_half(g0, j0, sB, tB, csB, ce0, vf0, cs0, dt0, sb0, mv);
+            mask_half(g1, j0 + 1, sB, tB, csB, ce1, vf1, cs1, dt1, sb1, mv + 4);
+            const bf16x8_t bop = pack8(mv);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) yB[pt] = mfma(as_bf16x8(af[pt]), bop, yB[pt]);
+        }
+        if (m < nA) {   // strip A (its first nA K-steps)
+            const uint2 g0 = gA[j0 * 64];
+            const uint2 g1 = (j0 + 1 <= sA) ? gA[(j0 + 1) * 64] : make_uint2(0, 0);
+            float mv[8];
+            mask_half(g0, j0, sA, tA, csA, ce0, vf0, cs0, dt0, sb0, mv);
+            mask_half(g1, j0 + 1, sA, tA, csA, ce1, vf1, cs1, dt1, sb1, mv + 4);
+            const bf16x8_t bop = pack8(mv);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) yA[pt] = mfma(as_bf16x8(af[pt]), bop, yA[pt]);
         }
     }
-    const bf16x8_t bop = pack8(mv);
-    const int sa = 16 * j0 + 4 * lg;
-#pragma unroll
-    for (int pt = 0; pt < 4; ++pt) {
-        const u16* row = XT + (16 * pt + r) * kQS;
-        const uint2 lo = *reinterpret_cast<const uint2*>(row + sa);
-        const uint2 hi = *reinterpret_cast<const uint2*>(row + sa + 16);
-        y[pt] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, y[pt]);
-    }
 }
 
-// All K-steps of the diagonal block for one strip (Gram tiles from LDS).
-__device__ __forceinline__ void strip_diag(const u16* XT, const float* cs, const float* vf,
-                                           const float* dt, const u16* GR, int strip,
-                                           int r, int lg, int lane, f32x4_t* y)
-{
-    const int t = 16 * strip + r;
-    const float cst = cs[t];
-    const uint2* gt = reinterpret_cast<const uint2*>(GR) + tile_index(strip, 0) * 64 + lane;
-    const int nsteps = strip / 2 + 1;
-#pragma unroll 2
-    for (int m = 0; m < nsteps; ++m) {
-        const int j0 = 2 * m;
-        const uint2 g0 = gt[j0 * 64];
-        const uint2 g1 = (j0 + 1 <= strip) ? gt[(j0 + 1) * 64] : make_uint2(0, 0);
-        diag_step(XT, cs, vf, dt, g0, g1, j0, strip, t, cst, r, lg, y);
-    }
-}
-
-// x of one head: XV vectors of 8 bf16 per thread (token s, features p0..p0+7)
-#define SSD_LOAD_X(hh)                                                                          \
-    _Pragma("unroll") for (int k_ = 0; k_ < XV; ++k_) {                                         \
-        const int vi_ = tid + kMainThreads * k_;                                                \
-        const int s_ = vi_ >> 3, p0_ = (vi_ & 7) * 8;                                           \
-        xr[k_] = make_uint4(0, 0, 0, 0);                                                        \
-        if (s_ < L)                                                                             \
-            xr[k_] = *reinterpret_cast<const uint4*>(xp + ((b * p.T + c0 + s_) * p.H + (hh)) * kP + p0_); \
-    }
-// x^T and (x * w)^T of one head into LDS (needs sm.w of that head)
-#define SSD_STORE_X()                                                                           \
-    _Pragma("unroll") for (int k_ = 0; k_ < XV; ++k_) {                                         \
-        const int vi_ = tid + kMainThreads * k_;                                                \
-        const int s_ = vi_ >> 3, p0_ = (vi_ & 7) * 8;                                           \
-        const U16x8 v_ = __builtin_bit_cast(U16x8, xr[k_]);                                     \
-        const float ws_ = sm.w[s_];                                                             \
-        u16* xt_ = sm.XT + p0_ * kQS + s_;                                                      \
-        u16* xw_ = sm.XW + p0_ * kQS + s_;                                                      \
-        _Pragma("unroll") for (int e_ = 0; e_ < 8; ++e_) {                                      \
-            xt_[e_ * kQS] = v_.v[e_];                                                           \
-            xw_[e_ * kQS] = to_bf16(bf(v_.v[e_]) * ws_);                                        \
-        }                                                                                       \
-    }
-#define SSD_LOAD_SCALARS(hh)                                                                    \
-    if (tid < kQ) {                                                                             \
-        const int64_t row_ = ((static_cast<int64_t>(b) * p.H + (hh)) * p.nC + c) * kQ;          \
-        csr = p.cs2[row_ + tid];                                                                \
-        dtr = p.dtT[row_ + tid];                                                                \
-    }
-// scalars of one head into LDS, then the per-token weights (two barriers)
-#define SSD_STORE_SCALARS()                                                                     \
+#define SSD_DMA_HEAD(hh, q)                                                                     \
     {                                                                                           \
-        if (tid < kQ) {                                                                         \
-            sm.cs[tid] = csr;                                                                   \
-            sm.dt[tid] = dtr;                                                                   \
+        const u16* xb_ = xchunk + static_cast<int64_t>(hh) * kP;                                \
+        _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) {                                      \
+            const int blk_ = 4 * wave + i_;                                                     \
+            const int s_ = 8 * blk_ + (lane >> 3);                                              \
+            const int grp_ = (lane & 7) ^ (s_ & 7);                                             \
+            const unsigned sc_ = static_cast<unsigned>(s_ < L ? s_ : L - 1);                    \
+            __builtin_amdgcn_global_load_lds(xb_ + (sc_ * xrow + 8u * grp_),                    \
+                                             (lds_void*)(&sm.XS[q][blk_ * 512]), 16, 0, 0);     \
         }                                                                                       \
-        __syncthreads();                                                                        \
-        if (tid < kQ) {                                                                         \
-            sm.vf[tid] = dtr * exp2f(sm.cs[tid | 15] - csr);                                    \
-            sm.w[tid] = dtr * exp2f(sm.cs[kQ - 1] - csr);                                       \
-        }                                                                                       \
-        __syncthreads();                                                                        \
+        const int64_t row_ = ((static_cast<int64_t>(b) * p.H + (hh)) * p.nC + c) * kQ;          \
+        if (wave == 0)                                                                          \
+            __builtin_amdgcn_global_load_lds(p.cs2 + row_ + 4 * lane, (lds_void*)(&sm.cs[q][0]), 16, 0, 0); \
+        if (wave == 1)                                                                          \
+            __builtin_amdgcn_global_load_lds(p.dtT + row_ + 4 * lane, (lds_void*)(&sm.dt[q][0]), 16, 0, 0); \
     }
 
 template <int N>
@@ -330,13 +350,15 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     constexpr int PTW = 4 * NT / kWaves;  // p-tiles per wavefront in the right factor (one n-tile each)
     constexpr int KN = N / 32;            // K-steps over n
     constexpr int HBS = N + 8;            // LDS row stride of the bf16 state
-    constexpr int XV = kP * kQ / 8 / kMainThreads;   // x vectors (8 bf16) per thread
     static_assert(PTW == 2 || PTW == 4, "N = 64 or 128");
-    static_assert(kMainThreads >= kQ, "a thread per token of the chunk");
-    static_assert(kP * HBS <= kP * kQS, "state fits in the XW region");
+    static_assert(kMainThreads >= kQ && kP == 64 && kQ * kP * 2 == 32 * 1024 * 1, "x buffer = 32 KiB");
+    static_assert(kQ * kP / 512 == 4 * kWaves, "x DMA: 4 blocks of 8 tokens per wavefront");
+    static_assert((kTiles * 256 * 2) % 1024 == 0, "Gram DMA in 1 KiB blocks");
     __shared__ __attribute__((aligned(16))) MainSmem<N> sm;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
+    // wavefront index, provably uniform (branches on it stay scalar)
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     if (tid == 0) sm.ticket = atomicAdd(p.ticket, 1);
     __syncthreads();
     const int work = sm.ticket;
@@ -363,69 +385,97 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     const int ntw = (PTW == 4) ? wave : (wave & 3);
     const int pt0 = (PTW == 4) ? 0 : 2 * (wave >> 2);
 
-    // ---- Gram tiles of the chunk into LDS (shared by the HG heads) -----------
+    const u16* xchunk = xp + (static_cast<int64_t>(b) * p.T + c0) * p.H * kP;    // token c0, head 0
+    const unsigned xrow = static_cast<unsigned>(p.H * kP);                        // elements per token
+    const u16* cchunk = Cp + ((static_cast<int64_t>(b) * p.T + c0) * p.G + g) * N;  // token c0, group g
+    const unsigned crow = static_cast<unsigned>(p.G * N);
+
+    // Asynchronous global -> LDS loads (no registers): x of head hh into buffer
+    // q, 4 blocks of 8 tokens per wavefront; lane l of a block fetches the
+    // 16 bytes that land at block + 16 l, i.e. physical group l%8 of token
+    // row l/8.  Rows past a partial chunk's end load the last valid row: such
+    // tokens only ever meet zero weights (dt = 0 there, zero Gram rows and
+    // columns) or are never stored.
+
+    // ---- prologue: Gram tiles (shared by the HG heads), head h0, B^T and C fragments
     {
-        const uint4* gsrc = reinterpret_cast<const uint4*>(
-            p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256);
-        uint4* gdst = reinterpret_cast<uint4*>(sm.GR);
-        for (int i = tid; i < kTiles * 256 / 8; i += kMainThreads) gdst[i] = gsrc[i];
+        const u16* gsrc = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
+        constexpr int kBlocks = kTiles * 256 * 2 / 1024;
+        for (int blk = wave; blk < kBlocks; blk += kWaves)
+            __builtin_amdgcn_global_load_lds(gsrc + blk * 512 + 8 * lane, (lds_void*)(&sm.GR[blk * 512]), 16, 0, 0);
     }
+    SSD_DMA_HEAD(h0, 0);
     const u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
-    uint4 xr[XV];
-    float csr = 0.f, dtr = 0.f;
-    SSD_LOAD_X(h0);
-    SSD_LOAD_SCALARS(h0);
-    SSD_STORE_SCALARS();
-    SSD_STORE_X();
+    wait_vmem();
     __syncthreads();
 
     for (int hk = 0; hk < p.HG; ++hk) {
         const int h = h0 + hk;
-        // B^T fragments of this wavefront's n-tile (L2), used after the diagonal block
+        const int q = hk & 1;
+        const u16* xs = sm.XS[q];
+        const float* cs = sm.cs[q];
+        const float* dt = sm.dt[q];
+        // B^T fragments of this wavefront's n-tile (L2), issued before the next head's
+        // DMA so that waiting for them never waits for the DMA (in-order counter)
         bf16x8_t btf[kQ / 32];
 #pragma unroll
         for (int m = 0; m < kQ / 32; ++m)
             btf[m] = as_bf16x8(*reinterpret_cast<const uint4*>(
-                bt + static_cast<int64_t>(16 * ntw + r) * kQ + 32 * m + 8 * lg));
-        if (hk + 1 < p.HG) {   // prefetch the next head while this one computes
-            SSD_LOAD_X(h + 1);
-            SSD_LOAD_SCALARS(h + 1);
-        }
+                bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 32u * m + 8u * lg)));
+        if (hk + 1 < p.HG) SSD_DMA_HEAD(h + 1, q ^ 1);   // lands while this head computes
 
-        // ---- diagonal block: Y^T[p][t] for the four strips ----------------------
+        // per-token weights of this head
+        if (tid < kQ) {
+            const float cst = cs[tid], d = dt[tid];
+            sm.vf[tid] = d * exp2f(cs[tid | 15] - cst);
+            sm.w[tid] = d * exp2f(cs[kQ - 1] - cst);
+        }
+        __syncthreads();
+
+        // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
         f32x4_t y[2][4];
 #pragma unroll
         for (int k4 = 0; k4 < 2; ++k4)
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
-#pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4)
-            strip_diag(sm.XT, sm.cs, sm.vf, sm.dt, sm.GR, strip[k4], r, lg, lane, y[k4]);
+        diag_block(xs, cs, sm.vf, dt, sm.GR, strip[0], strip[1], r, lg, lane, y[0], y[1]);
 
-        // ---- right factor: S[p][n], this wavefront's p-tiles x its n-tile ----------
+        // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
         f32x4_t sacc[PTW];
 #pragma unroll
         for (int i = 0; i < PTW; ++i) sacc[i] = zero4();
 #pragma unroll
         for (int m = 0; m < kQ / 32; ++m) {
+            const int s0 = 32 * m + 8 * lg;
+            const float4 w0 = *reinterpret_cast<const float4*>(&sm.w[s0]);
+            const float4 w1 = *reinterpret_cast<const float4*>(&sm.w[s0 + 4]);
+            const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            const uint4 braw = __builtin_bit_cast(uint4, btf[m]);
+            const u32 bw[4] = {braw.x, braw.y, braw.z, braw.w};
+            float bf8[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                bf8[2 * e] = __uint_as_float(bw[e] << 16) * wv[2 * e];
+                bf8[2 * e + 1] = __uint_as_float(bw[e] & 0xFFFF0000u) * wv[2 * e + 1];
+            }
+            const bf16x8_t bop = pack8(bf8);
 #pragma unroll
             for (int i = 0; i < PTW; ++i) {
-                const bf16x8_t a = as_bf16x8(*reinterpret_cast<const uint4*>(&sm.XW[(16 * (pt0 + i) + r) * kQS + 32 * m + 8 * lg]));
-                sacc[i] = mfma(a, btf[m], sacc[i]);
+                const uint2 lo = xfrag(xs, s0, 16 * (pt0 + i), lane);
+                const uint2 hi = xfrag(xs, s0 + 4, 16 * (pt0 + i), lane);
+                sacc[i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[i]);
             }
         }
 
-        // C fragments of the strips (L2), used by the left factor after the state exchange
+        // C fragments of the strips (L2); rows past a partial chunk are never stored
         bf16x8_t cf[2][KN];
 #pragma unroll
         for (int k4 = 0; k4 < 2; ++k4) {
             const int t = 16 * strip[k4] + r;
+            const unsigned tc = static_cast<unsigned>(t < L ? t : L - 1);
 #pragma unroll
-            for (int k = 0; k < KN; ++k) {
-                uint4 v = make_uint4(0, 0, 0, 0);
-                if (t < L) v = *reinterpret_cast<const uint4*>(Cp + ((b * p.T + c0 + t) * p.G + g) * N + 32 * k + 8 * lg);
-                cf[k4][k] = as_bf16x8(v);
-            }
+            for (int k = 0; k < KN; ++k)
+                cf[k4][k] = as_bf16x8(*reinterpret_cast<const uint4*>(cchunk + (tc * crow + 32u * k + 8u * lg)));
         }
 
         // ---- centre factor: state entering the chunk, state leaving it ----------
@@ -444,7 +494,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                 }
             }
         }
-        __syncthreads();   // flag seen; every wavefront is done reading XW
+        __syncthreads();   // flag seen by tid 0
         f32x4_t hprev[PTW];
         if (has_prev) {
             const int slot = (c + 1) & 1;
@@ -454,23 +504,27 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                 hprev[i] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ring_rs, off, 0, 16));
             }
         } else if (p.init) {
-            const float* hi = p.init + (static_cast<int64_t>(b) * p.H + h) * PN;
+            // (P, N) layout of the caller's initial state: lane offset + uniform row offsets
+            const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<float*>(p.init + (static_cast<int64_t>(b) * p.H + h) * PN), 0,
+                static_cast<int>(PN * sizeof(float)), 0x00020000);
+            const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
 #pragma unroll
             for (int i = 0; i < PTW; ++i)
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    hprev[i][v] = hi[(16 * (pt0 + i) + 4 * lg + v) * N + 16 * ntw + r];
+                    hprev[i][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                        irs, lo, (16 * i + v) * N * static_cast<int>(sizeof(float)), 0));
         } else {
 #pragma unroll
             for (int i = 0; i < PTW; ++i) hprev[i] = zero4();
         }
-        const float decay = exp2f(sm.cs[kQ - 1]);
-        u16* HB = sm.XW;
+        const float decay = exp2f(cs[kQ - 1]);
 #pragma unroll
         for (int i = 0; i < PTW; ++i) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                HB[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
+                sm.HB[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
                 sacc[i][v] = decay * hprev[i][v] + sacc[i][v];
             }
         }
@@ -482,70 +536,78 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(uint4_t, sacc[i]), ring_rs, off, 0, 16);
             }
         } else if (p.fin) {
-            float* fo = p.fin + (static_cast<int64_t>(b) * p.H + h) * PN;
+            const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
+                p.fin + (static_cast<int64_t>(b) * p.H + h) * PN, 0,
+                static_cast<int>(PN * sizeof(float)), 0x00020000);
+            const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
 #pragma unroll
             for (int i = 0; i < PTW; ++i)
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    fo[(16 * (pt0 + i) + 4 * lg + v) * N + 16 * ntw + r] = sacc[i][v];
+                for (int v = 0; v < 4; ++v) {
+                    // extract the element first: bit-casting a vector element in place is
+                    // mis-lowered (component 0 stored for every v)
+                    const float val = sacc[i][v];
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), frs, lo,
+                                                          (16 * i + v) * N * static_cast<int>(sizeof(float)), 0);
+                }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        wait_vmem();
+        wait_vmem();       // state stores complete (and the next head's DMA has landed)
         __syncthreads();
         if (tid == 0 && has_next)
             __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-        // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T), strip by strip -------
+        // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
+        {
+            f32x4_t tq[2][4];
 #pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4) {
-            f32x4_t tq[4];
+            for (int k4 = 0; k4 < 2; ++k4)
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt) tq[pt] = zero4();
+                for (int pt = 0; pt < 4; ++pt) tq[k4][pt] = zero4();
 #pragma unroll
             for (int k = 0; k < KN; ++k) {
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
-                    const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&HB[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
-                    tq[pt] = mfma(aop, cf[k4][k], tq[pt]);
+                    const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&sm.HB[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
+                    tq[0][pt] = mfma(aop, cf[0][k], tq[0][pt]);
+                    tq[1][pt] = mfma(aop, cf[1][k], tq[1][pt]);
                 }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            const float ev = exp2f(sm.cs[16 * strip[k4] + r]);
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt)
+            for (int k4 = 0; k4 < 2; ++k4) {
+                const float ev = exp2f(cs[16 * strip[k4] + r]);
 #pragma unroll
-                for (int v = 0; v < 4; ++v) y[k4][pt][v] += ev * tq[pt][v];
+                for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) y[k4][pt][v] += ev * tq[k4][pt][v];
+            }
         }
 
         // ---- skip term and store -------------------------------------------------
         {
             const float Dh = p.D ? p.D[h] : 0.f;
+            u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
 #pragma unroll
             for (int k4 = 0; k4 < 2; ++k4) {
                 const int t = 16 * strip[k4] + r;
-                if (t < L) {
 #pragma unroll
-                    for (int pt = 0; pt < 4; ++pt) {
-                        u16 o[4];
+                for (int pt = 0; pt < 4; ++pt) {
+                    const uint2 xv = *reinterpret_cast<const uint2*>(xs + xs_off(t, 16 * pt + 4 * lg));
+                    const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
+                                         __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
+                    u16 o[4];
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const int pp = 16 * pt + 4 * lg + v;
-                            o[v] = to_bf16(y[k4][pt][v] + Dh * bf(sm.XT[pp * kQS + t]));
-                        }
-                        uint2 packed;
-                        packed.x = static_cast<u32>(o[0]) | (static_cast<u32>(o[1]) << 16);
-                        packed.y = static_cast<u32>(o[2]) | (static_cast<u32>(o[3]) << 16);
-                        *reinterpret_cast<uint2*>(yp + ((b * p.T + c0 + t) * p.H + h) * kP + 16 * pt + 4 * lg) = packed;
-                    }
+                    for (int v = 0; v < 4; ++v) o[v] = to_bf16(y[k4][pt][v] + Dh * xf[v]);
+                    uint2 packed;
+                    packed.x = static_cast<u32>(o[0]) | (static_cast<u32>(o[1]) << 16);
+                    packed.y = static_cast<u32>(o[2]) | (static_cast<u32>(o[3]) << 16);
+                    if (t < L) *reinterpret_cast<uint2*>(ychunk + (static_cast<unsigned>(t) * xrow + 16u * pt + 4u * lg)) = packed;
                 }
             }
         }
-        __syncthreads();   // XT, XW and the scalars are rewritten for the next head
-        if (hk + 1 < p.HG) {
-            SSD_STORE_SCALARS();
-            SSD_STORE_X();
-            __syncthreads();
-        }
+        __syncthreads();   // this head's LDS buffers may be refilled from here on
     }
 }
 
