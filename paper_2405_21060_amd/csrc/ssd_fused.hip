@@ -415,13 +415,6 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         const u16* xs = sm.XS[q];
         const float* cs = sm.cs[q];
         const float* dt = sm.dt[q];
-        // B^T fragments of this wavefront's n-tile (L2), issued before the next head's
-        // DMA so that waiting for them never waits for the DMA (in-order counter)
-        bf16x8_t btf[kQ / 32];
-#pragma unroll
-        for (int m = 0; m < kQ / 32; ++m)
-            btf[m] = as_bf16x8(*reinterpret_cast<const uint4*>(
-                bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 32u * m + 8u * lg)));
         if (hk + 1 < p.HG) SSD_DMA_HEAD(h + 1, q ^ 1);   // lands while this head computes
 
         // per-token weights of this head
@@ -440,6 +433,14 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
         diag_block(xs, cs, sm.vf, dt, sm.GR, strip[0], strip[1], r, lg, lane, y[0], y[1]);
 
+        // B^T fragments of this wavefront's n-tile (L2; the same for every head).  Loaded
+        // here, not earlier: the vector-memory counter is in order, and loads issued
+        // right after the previous head's output stores would wait for those stores.
+        bf16x8_t btf[kQ / 32];
+#pragma unroll
+        for (int m = 0; m < kQ / 32; ++m)
+            btf[m] = as_bf16x8(*reinterpret_cast<const uint4*>(
+                bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 32u * m + 8u * lg)));
         // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
         f32x4_t sacc[PTW];
 #pragma unroll
@@ -585,16 +586,17 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             }
         }
 
-        // ---- skip term and store -------------------------------------------------
+        // ---- skip term; y staged in place over this head's x, then full-row stores
         {
             const float Dh = p.D ? p.D[h] : 0.f;
-            u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
+            u16* xw = sm.XS[q];
 #pragma unroll
             for (int k4 = 0; k4 < 2; ++k4) {
                 const int t = 16 * strip[k4] + r;
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
-                    const uint2 xv = *reinterpret_cast<const uint2*>(xs + xs_off(t, 16 * pt + 4 * lg));
+                    uint2* cell = reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg));
+                    const uint2 xv = *cell;
                     const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
                                          __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
                     u16 o[4];
@@ -603,8 +605,18 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                     uint2 packed;
                     packed.x = static_cast<u32>(o[0]) | (static_cast<u32>(o[1]) << 16);
                     packed.y = static_cast<u32>(o[2]) | (static_cast<u32>(o[3]) << 16);
-                    if (t < L) *reinterpret_cast<uint2*>(ychunk + (static_cast<unsigned>(t) * xrow + 16u * pt + 4u * lg)) = packed;
+                    *cell = packed;   // same cell this lane just read: in place is safe
                 }
+            }
+            __syncthreads();
+            u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
+#pragma unroll
+            for (int k = 0; k < kQ * kP / 8 / kMainThreads; ++k) {
+                const int ci = tid + kMainThreads * k;      // 16-byte piece: token ci/8, group ci%8
+                const int t = ci >> 3, grp = ci & 7;
+                const uint4 v = *reinterpret_cast<const uint4*>(xw + xs_off(t, 8 * grp));
+                // streaming (non-temporal) stores: y is not read again by this kernel
+                if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
             }
         }
         __syncthreads();   // this head's LDS buffers may be refilled from here on
