@@ -46,6 +46,42 @@ def algorithmic_counts(p, nseq):
     return f_full, f_causal, byts
 
 
+def kernel_sources_digest():
+    """Hash of the HIP sources; counter files record the digest they were taken at."""
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2405_21060_amd", "csrc", "*"))):
+        if f.endswith((".hip", ".cpp", ".h")):
+            with open(f, "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def dominant_kernel_name(p):
+    fused = (p.dtype == "bf16" and not p.varlen and p.headdim == 64 and p.chunk_size == 256
+             and p.dstate in (64, 128))
+    return ("k_fused_main<%d>" % p.dstate) if fused else "k_chunk_output"
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the dominant kernel from the FETCH_SIZE / WRITE_SIZE
+    counter runs committed under profiles/, scaled by the plain-copy calibration;
+    None when there is no record for this workload or the kernels have changed
+    since it was taken."""
+    path = os.path.join(ROOT, "profiles", "ssd_fused_%s_traffic.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("kernel_sources_sha256_16") != kernel_sources_digest():
+        return None
+    cal = rec["calibration"]
+    k = rec["per_dispatch_kib"][rec["dominant_kernel"]]
+    return int(1024 * (k["FETCH_SIZE"] * cal["fetch_factor"] + k["WRITE_SIZE"] * cal["write_factor"]))
+
+
 def cpu_baseline(inp, budget_s=20.0):
     """The oracle (untuned) on the host cores, on a bounded sample of the
     workload: all tokens, a subset of heads sized to ~budget_s of CPU time."""
@@ -80,6 +116,11 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="time whole calls only (no events around the dominant kernel)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="time a plain 1 GiB device-to-device copy instead (reference for the "
+                         "FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (--gpus 1); the sequence/head "
@@ -87,6 +128,24 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        print(json.dumps({"copy_bytes_each_way": n, "ms": ms, "gbps_read_plus_write": 2 * n / ms / 1e6}),
+              flush=True)
+        return
 
     from paper_2405_21060_amd import ssd
     from paper_2405_21060_amd.inputs import WORKLOADS, make_inputs
@@ -108,13 +167,24 @@ def main():
     ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
-    def step(i):
+    # events bracketing the dominant (chunk) kernel of every timed step
+    kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, z in kev:  # create the HIP events before their handles are passed down
+        a.record(stream)
+        z.record(stream)
+
+    def step(i, events=None):
         c = copies[i % len(copies)]
         ptr = lambda t: None if t is None else t.data_ptr()
-        rc = ssd.ssd_forward(prob, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]),
-                             ptr(c["C"]), ptr(c["D"]), ptr(c["initial_states"]), ptr(c["seq_idx"]),
-                             ptr(outs[i % len(copies)]), ptr(fins[i % len(copies)]), ws.data_ptr(),
-                             wsb, stream.cuda_stream)
+        args_ = (prob, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]), ptr(c["C"]),
+                 ptr(c["D"]), ptr(c["initial_states"]), ptr(c["seq_idx"]),
+                 ptr(outs[i % len(copies)]), ptr(fins[i % len(copies)]), ws.data_ptr(), wsb,
+                 stream.cuda_stream)
+        if events is None:
+            rc = ssd.ssd_forward(*args_)
+        else:
+            rc = ssd.ssd_forward_timed(*args_, events[0].cuda_event, events[1].cuda_event)
         if rc != 0:
             raise ssd.SsdError(rc, "ssd_forward")
 
@@ -124,24 +194,36 @@ def main():
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
     for i in range(args.steps):
-        step(i)
+        step(i, None if args.no_kernel_events else kev[i])
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
+    kms = None
+    if not args.no_kernel_events:
+        ks = sorted(a.elapsed_time(z) for a, z in kev)
+        kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
+               "p90": ks[(9 * len(ks)) // 10]}
 
     f_full, f_causal, byts = algorithmic_counts(p, inp.nseq)
     sec = ms * 1e-3
     tokens = p.batch * p.seqlen
     peak_flops = PEAK_BF16_FLOPS if p.dtype == "bf16" else PEAK_F32_MFMA_FLOPS
     t_hbm, t_mfma = byts / PEAK_HBM_BPS, f_full / peak_flops
+    # Roofline of the dominant kernel: it consumes every compulsory input and
+    # produces every output, so its algorithmic bytes per launch are the
+    # forward's compulsory bytes (and its FLOPs all but the Gram products).
+    ksec = (kms["mean"] if kms else ms) * 1e-3
     if t_hbm >= t_mfma:
-        roof = {"bound": "hbm", "achieved": byts / sec / 1e9, "peak": PEAK_HBM_BPS / 1e9,
+        roof = {"bound": "hbm", "achieved": byts / ksec / 1e9, "peak": PEAK_HBM_BPS / 1e9,
                 "unit": "GB/s"}
     else:
-        roof = {"bound": "mfma", "achieved": f_full / sec / 1e12, "peak": peak_flops / 1e12,
+        roof = {"bound": "mfma", "achieved": f_full / ksec / 1e12, "peak": peak_flops / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(args.workload)
+    roof["kernel"] = dominant_kernel_name(p) + (" (whole forward: no kernel events)" if kms is None else "")
+    roof["kernel_ms"] = kms
+    roof["algorithmic_bytes"] = byts
     line = {
         "metric": "SSD fwd tokens/s (2.7B-layer shape, 1 GPU)",
         "value": tokens / sec,

@@ -102,6 +102,21 @@ int ssd_forward(const ssd_problem* prob,
                 void* y, float* final_states,
                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* ssd_forward, plus two hipEvent_t (either may be NULL) recorded on `stream`
+ * immediately before and immediately after the launch of the dominant kernel
+ * of the call (the chunk kernel, which evaluates the diagonal blocks, the
+ * chunk states, the state passing and the state-to-output term), so that a
+ * profiler or benchmark can time that kernel alone with hipEventElapsedTime.
+ * Results, errors and ownership are those of ssd_forward; the events are
+ * owned by the caller and must have been created on the stream's device. */
+int ssd_forward_timed(const ssd_problem* prob,
+                      const void* x, const void* dt, const float* A_log,
+                      const void* B, const void* C, const float* D,
+                      const float* initial_states, const int32_t* seq_idx,
+                      void* y, float* final_states,
+                      void* workspace, size_t workspace_bytes, void* stream,
+                      void* event_begin, void* event_end);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);
 

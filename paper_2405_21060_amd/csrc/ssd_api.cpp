@@ -112,11 +112,12 @@ extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
     return SSD_OK;
 }
 
-extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* dt,
-                           const float* A_log, const void* B, const void* C, const float* D,
-                           const float* initial_states, const int32_t* seq_idx, void* y,
-                           float* final_states, void* workspace, size_t workspace_bytes,
-                           void* stream)
+namespace {
+
+int forward_impl(const ssd_problem* prob, const void* x, const void* dt, const float* A_log,
+                 const void* B, const void* C, const float* D, const float* initial_states,
+                 const int32_t* seq_idx, void* y, float* final_states, void* workspace,
+                 size_t workspace_bytes, void* stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
     ssd::Shape s;
     int rc = ssd::validate(prob, seq_idx != nullptr, &s);
@@ -155,7 +156,8 @@ extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* d
         f.ring = reinterpret_cast<float*>(base + fw.ring);
         f.flags = reinterpret_cast<int*>(base + fw.flags);
         f.ticket = reinterpret_cast<int*>(base + fw.ticket);
-        const hipError_t err = ssd::launch_fused(f, static_cast<hipStream_t>(stream));
+        const hipError_t err =
+            ssd::launch_fused(f, static_cast<hipStream_t>(stream), ev_begin, ev_end);
         return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
     }
     const ssd::WorkspaceLayout w = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC);
@@ -185,8 +187,33 @@ extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* d
     p.info = reinterpret_cast<int4*>(ws + w.info);
     p.gram = reinterpret_cast<float*>(ws + w.gram);
     p.states = reinterpret_cast<float*>(ws + w.states);
-    const hipError_t err = ssd::launch_unfused(p, s.bf16, static_cast<hipStream_t>(stream));
+    const hipError_t err =
+        ssd::launch_unfused(p, s.bf16, static_cast<hipStream_t>(stream), ev_begin, ev_end);
     return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* dt,
+                           const float* A_log, const void* B, const void* C, const float* D,
+                           const float* initial_states, const int32_t* seq_idx, void* y,
+                           float* final_states, void* workspace, size_t workspace_bytes,
+                           void* stream)
+{
+    return forward_impl(prob, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
+                        workspace, workspace_bytes, stream, nullptr, nullptr);
+}
+
+extern "C" int ssd_forward_timed(const ssd_problem* prob, const void* x, const void* dt,
+                                 const float* A_log, const void* B, const void* C,
+                                 const float* D, const float* initial_states,
+                                 const int32_t* seq_idx, void* y, float* final_states,
+                                 void* workspace, size_t workspace_bytes, void* stream,
+                                 void* event_begin, void* event_end)
+{
+    return forward_impl(prob, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
+                        workspace, workspace_bytes, stream, static_cast<hipEvent_t>(event_begin),
+                        static_cast<hipEvent_t>(event_end));
 }
 
 extern "C" const char* ssd_error_string(int code)

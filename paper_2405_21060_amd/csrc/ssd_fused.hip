@@ -15,17 +15,24 @@
 //
 // k_fused_main, one workgroup (8 wavefronts) per (chunk, batch, group of HG
 // heads), ordered chunk-major through a ticket counter:
-//   * the chunk's Gram tiles are streamed from L2 in their per-lane layout;
-//     B^T is staged in LDS once, x^T (P x Q) per head;
-//   * right factor (Section 6.2): S = sum_s dt_s exp(cs_end - cs_s) x_s B_s^T on
-//     the matrix cores;
-//   * diagonal block (Section 6.1): Y^T = x^T (L o G)^T dt, the mask applied to
-//     the Gram fragments in registers and fed straight back into the matrix cores
-//     (accumulator layout -> operand layout by permuting the contraction index);
+//   * prologue: the chunk's Gram tiles (shared by the HG heads) are copied to
+//     LDS with asynchronous global->LDS loads; per head, x (Q x P, token-major,
+//     swizzled), cs2 and dt land in a double-buffered LDS slot while the
+//     previous head computes, and MFMA operand fragments of x^T are read from
+//     it with transposing LDS reads (ds_read_b64_tr_b16);
+//   * diagonal block (Section 6.1): Y^T = x^T (L o G)^T dt, the 1-SS mask
+//     applied to the Gram fragments in registers and fed straight back into the
+//     matrix cores (accumulator layout -> operand layout by permuting the
+//     contraction index);
+//   * right factor (Section 6.2): S = sum_s dt_s exp(cs_end - cs_s) x_s B_s^T,
+//     B^T fragments read from L2;
 //   * centre factor (Section 6.2, scalar scan of Appendix B, sequential
 //     chunk-to-chunk state passing): wait for the state entering the chunk,
-//     publish h_c = exp(cs_end) h_{c-1} + S for the next chunk;
-//   * left factor: Y^T += exp(cs_t) (h_{c-1} C_t^T), then + D x, stored bf16.
+//     publish h_c = exp(cs_end) h_{c-1} + S for the next chunk (or write the
+//     final state);
+//   * left factor: Y^T += exp(cs_t) (h_{c-1} C_t^T), then + D x, rounded to
+//     bf16, staged in LDS over the head's x and written as full 128-byte rows
+//     with streaming stores.
 //
 // Cross-workgroup state passing.  States go through a two-slot ring per
 // (batch, head); h_c is written with device-coherent (sc1) stores, the stores
@@ -52,8 +59,6 @@ constexpr int kP = 64;                        // head dimension
 constexpr int kWaves = 8;
 constexpr int kMainThreads = kWaves * 64;
 constexpr int kPrepThreads = 256;
-constexpr int kRowPad = 8;                    // bf16 elements of padding per LDS row
-constexpr int kQS = kQ + kRowPad;             // LDS row stride of token-major rows
 constexpr long long kSpinLimit = 1LL << 22;   // polls (with s_sleep) before giving up
 
 typedef unsigned short u16;
@@ -624,13 +629,18 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
 }
 
 template <int N>
-hipError_t launch_n(const FusedParams& p, hipStream_t stream)
+hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
     const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), kPrepParts);
     hipLaunchKernelGGL(k_fused_prep<N>, g_prep, dim3(kPrepThreads), 0, stream, p);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess && ev_begin) err = hipEventRecord(ev_begin, stream);
+    if (err != hipSuccess) return err;
     const unsigned nwork = static_cast<unsigned>(p.nC * p.b * (p.H / p.HG));
     hipLaunchKernelGGL(k_fused_main<N>, dim3(nwork), dim3(kMainThreads), 0, stream, p);
-    return hipGetLastError();
+    err = hipGetLastError();
+    if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
+    return err;
 }
 
 }  // namespace
@@ -663,9 +673,11 @@ FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC)
     return w;
 }
 
-hipError_t launch_fused(const FusedParams& p, hipStream_t stream)
+hipError_t launch_fused(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin,
+                        hipEvent_t ev_end)
 {
-    return p.N == 64 ? launch_n<64>(p, stream) : launch_n<128>(p, stream);
+    return p.N == 64 ? launch_n<64>(p, stream, ev_begin, ev_end)
+                     : launch_n<128>(p, stream, ev_begin, ev_end);
 }
 
 }  // namespace ssd

@@ -35,8 +35,12 @@ struct WorkspaceLayout {
 WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int64_t G,
                                  int64_t Q, int64_t nC);
 
-// Enqueue the whole forward on `stream`; returns the first launch error.
-hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream);
+// Enqueue the whole forward on `stream`; returns the first launch or record
+// error.  `ev_begin` / `ev_end` (may be null) are recorded on `stream` right
+// before and right after the dominant kernel (the chunk-output kernel here,
+// the chunk kernel of the fused path).
+hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream,
+                          hipEvent_t ev_begin, hipEvent_t ev_end);
 
 // Fused path (bf16, P = 64, N in {64, 128}, Q = 256, no packed rows).
 struct FusedParams {
@@ -67,6 +71,7 @@ struct FusedLayout {
 int64_t heads_per_workgroup(int64_t heads_per_group);
 bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16, bool varlen);
 FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC);
-hipError_t launch_fused(const FusedParams& p, hipStream_t stream);
+hipError_t launch_fused(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin,
+                        hipEvent_t ev_end);
 
 }  // namespace ssd

@@ -418,7 +418,7 @@ __global__ __launch_bounds__(kThreads) void k_chunk_output(Params p)
 }
 
 template <typename T>
-hipError_t launch_all(const Params& p, hipStream_t stream)
+hipError_t launch_all(const Params& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
     const dim3 blk(kThreads);
     const dim3 g_chunk(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.H), static_cast<unsigned>(p.b));
@@ -429,16 +429,24 @@ hipError_t launch_all(const Params& p, hipStream_t stream)
     hipLaunchKernelGGL(k_gram<T>, g_gram, blk, 0, stream, p);
     hipLaunchKernelGGL(k_chunk_state<T>, g_chunk, blk, 0, stream, p);
     hipLaunchKernelGGL(k_state_scan, g_scan, blk, 0, stream, p);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess && ev_begin) err = hipEventRecord(ev_begin, stream);
+    if (err != hipSuccess) return err;
     hipLaunchKernelGGL(k_chunk_output<T>, g_chunk, blk, 0, stream, p);
+    err = hipGetLastError();
+    if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
+    if (err != hipSuccess) return err;
     if (p.seq_idx && p.fin) hipLaunchKernelGGL(k_varlen_final<T>, g_chunk, blk, 0, stream, p);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream)
+hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream, hipEvent_t ev_begin,
+                          hipEvent_t ev_end)
 {
-    return bf16 ? launch_all<uint16_t>(p, stream) : launch_all<float>(p, stream);
+    return bf16 ? launch_all<uint16_t>(p, stream, ev_begin, ev_end)
+                : launch_all<float>(p, stream, ev_begin, ev_end);
 }
 
 }  // namespace ssd

@@ -32,7 +32,7 @@ SSD_ERR_WORKSPACE = -7
 SSD_ERR_LAUNCH = -8
 SSD_ERR_TOO_LARGE = -9
 
-EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_error_string")
+EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_error_string")
 
 
 class SsdProblem(ctypes.Structure):
@@ -73,6 +73,8 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_workspace_bytes.argtypes = [ctypes.POINTER(SsdProblem), ctypes.POINTER(ctypes.c_size_t)]
     lib.ssd_forward.restype = ctypes.c_int
     lib.ssd_forward.argtypes = [ctypes.POINTER(SsdProblem)] + [vp] * 10 + [vp, ctypes.c_size_t, vp]
+    lib.ssd_forward_timed.restype = ctypes.c_int
+    lib.ssd_forward_timed.argtypes = lib.ssd_forward.argtypes + [vp, vp]
     lib.ssd_error_string.restype = ctypes.c_char_p
     lib.ssd_error_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -102,6 +104,17 @@ def ssd_forward(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx
         ctypes.byref(prob), x, dt, A_log, B, C, D or None, initial_states or None,
         seq_idx or None, y, final_states or None, workspace, int(workspace_bytes),
         stream or None)
+
+
+def ssd_forward_timed(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx, y,
+                      final_states, workspace, workspace_bytes: int, stream, event_begin,
+                      event_end) -> int:
+    """``ssd_forward`` that also records two hipEvent_t handles (integers, 0 =
+    none) right before and after the dominant kernel; returns the status."""
+    return load_library().ssd_forward_timed(
+        ctypes.byref(prob), x, dt, A_log, B, C, D or None, initial_states or None,
+        seq_idx or None, y, final_states or None, workspace, int(workspace_bytes),
+        stream or None, event_begin or None, event_end or None)
 
 
 def _ptr(t) -> Optional[int]:

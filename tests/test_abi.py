@@ -94,6 +94,18 @@ def test_workspace_grows_with_problem(lib):
     assert ssd.ssd_workspace_bytes(prob(seqlen=4097)) > large  # partial chunk counted
 
 
+def test_timed_entry_validates_like_forward(lib):
+    def timed(p, ws_bytes=1 << 40, seq_idx=0, x=FAKE):
+        return ssd.ssd_forward_timed(p, x, FAKE, FAKE, FAKE, FAKE, 0, 0, seq_idx, FAKE, 0, FAKE,
+                                     ws_bytes, 0, 0, 0)
+    for kw in (dict(dtype=7), dict(chunk_size=48), dict(dstate=8), dict(seqlen=0)):
+        assert timed(prob(**kw)) == fwd(prob(**kw)) < 0
+    p = prob()
+    assert timed(p, x=0) == ssd.SSD_ERR_NULL_ARG
+    assert timed(p, ws_bytes=ssd.ssd_workspace_bytes(p) - 1) == ssd.SSD_ERR_WORKSPACE
+    assert timed(prob(batch=2, nseq=3), seq_idx=FAKE) == ssd.SSD_ERR_SEQIDX_BATCH
+
+
 def test_error_strings(lib):
     for code in range(0, -10, -1):
         s = ssd.ssd_error_string(code)

@@ -100,6 +100,31 @@ def test_varlen_bf16_small():
     check(make_inputs(p, 9), tag="varlen_bf16_small")
 
 
+@pytest.mark.parametrize("shape", [
+    # (batch, T, H, N, G): ragged last chunk, N = 64, 3 heads per group (1 head per workgroup)
+    (2, 700, 6, 64, 2),
+    # one chunk exactly, 2 heads per group
+    (1, 256, 4, 128, 2),
+    # many chunks, 4 heads per workgroup, several workgroups per (row, chunk)
+    (3, 2000, 16, 128, 1),
+])
+def test_fused_shapes(shape):
+    b, T, H, N, G = shape
+    p = Problem(b, T, H, 64, N, G, 256, "bf16", init_states=True)
+    check(make_inputs(p, 11), tag="fused")
+
+
+def test_general_path_at_fused_shape(monkeypatch):
+    """Both device paths at one shape: the general step-by-step kernels (forced)
+    and the fused ones must each meet the tolerance against the oracle."""
+    p = Problem(2, 1300, 8, 64, 128, 2, 256, "bf16", init_states=True)
+    inp = make_inputs(p, 12)
+    monkeypatch.setenv("SSD_PATH", "unfused")
+    check(inp, tag="general_forced")
+    monkeypatch.delenv("SSD_PATH")
+    check(inp, tag="fused")
+
+
 def test_deterministic_repeat():
     import torch
 
