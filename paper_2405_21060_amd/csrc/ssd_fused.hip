@@ -46,6 +46,8 @@
 // Two ring slots suffice: chunk c+2 overwrites the slot of chunk c only after
 // reading the state of chunk c+1, which chunk c+1 published only after it had
 // read (consumed) the state of chunk c.
+#include <utility>
+
 #include "ssd_device.h"
 #include "ssd_internal.h"
 
@@ -244,89 +246,162 @@ struct MainSmem {
     int ticket;
 };
 
-// Masked Gram values of one K-step half (s-tile j, 4 tokens sb..sb+3 of this
-// lane) for the strip whose t-tile is `strip`: the B operand of the diagonal
-// block.  Off-diagonal tiles factor the 1-SS mask as
-// exp2(cs_t - cs_end(j)) * exp2(cs_end(j) - cs_s) (both factors <= 1, the
-// second one folded with dt_s into vf); the diagonal tile takes
-// exp2(cs_t - cs_s) directly, upper triangle zero.
-__device__ __forceinline__ void mask_half(uint2 gp, int j, int strip, int t, float cst, float csend,
-                                          float4 vf4, float4 cs4, float4 dt4, int sb, float* mv)
+// Transposing read at a precomputed LDS byte address (see x_tr_base).
+__device__ __forceinline__ uint2 tr_read(const char* a)
 {
-    const float gv[4] = {__uint_as_float(gp.x << 16), __uint_as_float(gp.x & 0xFFFF0000u),
-                         __uint_as_float(gp.y << 16), __uint_as_float(gp.y & 0xFFFF0000u)};
-    if (j < strip) {
-        const float u = __builtin_amdgcn_exp2f(cst - csend);
-        mv[0] = gv[0] * (u * vf4.x);
-        mv[1] = gv[1] * (u * vf4.y);
-        mv[2] = gv[2] * (u * vf4.z);
-        mv[3] = gv[3] * (u * vf4.w);
-    } else if (j == strip) {
-        const float csv[4] = {cs4.x, cs4.y, cs4.z, cs4.w}, dtv[4] = {dt4.x, dt4.y, dt4.z, dt4.w};
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(a)));
+}
+
+// Byte offset, within a head's x buffer, of this lane's transposing read of
+// rows 4 lg + (lane%16)/4 (+ 32 m, + 16), features f0 + 4 (lane%4) .. +3.
+// Adding a multiple of 8 to the row leaves the swizzle unchanged, so the reads
+// of every K-step m and of the upper half (+16 rows) are this offset plus the
+// constants 4096 m and 2048.
+__device__ __forceinline__ int x_tr_base(int f0, int lane)
+{
+    const int j = lane & 15, lg = lane >> 4;
+    return 2 * xs_off(4 * lg + (j >> 2), f0 + 4 * (j & 3));
+}
+
+__device__ __forceinline__ void unpack4(uint2 gp, float* g)
+{
+    g[0] = __uint_as_float(gp.x << 16);
+    g[1] = __uint_as_float(gp.x & 0xFFFF0000u);
+    g[2] = __uint_as_float(gp.y << 16);
+    g[3] = __uint_as_float(gp.y & 0xFFFF0000u);
+}
+
+// Off-diagonal s-tile (entirely before the strip): the 1-SS mask factors as
+// exp2(cs_t - cs_end(j)) * exp2(cs_end(j) - cs_s), both factors <= 1, the
+// second folded with dt_s into vf.
+__device__ __forceinline__ void mask_off(uint2 gp, float u, float4 vf4, float* mv)
+{
+    float g[4];
+    unpack4(gp, g);
+    mv[0] = g[0] * (u * vf4.x);
+    mv[1] = g[1] * (u * vf4.y);
+    mv[2] = g[2] * (u * vf4.z);
+    mv[3] = g[3] * (u * vf4.w);
+}
+
+// The strip's own s-tile: exp2(cs_t - cs_s) dt_s directly for s <= t, zero
+// above the diagonal (branch-free: exponent clamped, upper triangle selected away).
+__device__ __forceinline__ void mask_diag(uint2 gp, int t, int sb, float cst, float4 cs4, float4 dt4,
+                                          float* mv)
+{
+    float g[4];
+    unpack4(gp, g);
+    const float csv[4] = {cs4.x, cs4.y, cs4.z, cs4.w}, dtv[4] = {dt4.x, dt4.y, dt4.z, dt4.w};
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            // branch-free: the exponent is clamped to <= 0, the upper triangle selected away
-            const float e = __builtin_amdgcn_exp2f(fminf(cst - csv[v], 0.f));
-            mv[v] = (sb + v <= t) ? gv[v] * (e * dtv[v]) : 0.f;
-        }
-    } else {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) mv[v] = 0.f;
+    for (int v = 0; v < 4; ++v) {
+        const float e = __builtin_amdgcn_exp2f(fminf(cst - csv[v], 0.f));
+        mv[v] = (sb + v <= t) ? g[v] * (e * dtv[v]) : 0.f;
     }
 }
 
-// Diagonal block of both strips of a wavefront (t-tiles sA < sB).  K-step m
-// covers s-tiles 2m, 2m+1; its contraction index is permuted to the Gram
-// accumulator layout (slot e<4 -> s = 32m + 4 lg + e, e>=4 -> s = 32m + 16 +
-// 4 lg + e - 4), and the x^T fragments, vf and cumsums of a K-step are read
-// once for both strips.
-__device__ __forceinline__ void diag_block(const u16* xs, const float* cs, const float* vf,
-                                           const float* dt, const u16* GR, int sA, int sB,
-                                           int r, int lg, int lane, f32x4_t* yA, f32x4_t* yB)
+// One K-step (s-tiles 2m, 2m+1) of strip S: masked Gram operand, 4 MFMAs.
+template <int S, int M>
+__device__ __forceinline__ void strip_step(const uint4* af, const char* gbase, int t, float cst,
+                                           float ce0, float ce1, float4 vf0, float4 vf1,
+                                           const float* cs, const float* dt, int lg, f32x4_t* yv)
 {
+    constexpr int j0 = 2 * M, j1 = 2 * M + 1;
+    float mv[8];
+    const uint2 g0 = *reinterpret_cast<const uint2*>(gbase + j0 * 512);
+    if constexpr (j1 < S) {
+        const uint2 g1 = *reinterpret_cast<const uint2*>(gbase + j1 * 512);
+        mask_off(g0, __builtin_amdgcn_exp2f(cst - ce0), vf0, mv);
+        mask_off(g1, __builtin_amdgcn_exp2f(cst - ce1), vf1, mv + 4);
+    } else if constexpr (j1 == S) {
+        const uint2 g1 = *reinterpret_cast<const uint2*>(gbase + j1 * 512);
+        const int sb1 = 16 * j1 + 4 * lg;
+        mask_off(g0, __builtin_amdgcn_exp2f(cst - ce0), vf0, mv);
+        mask_diag(g1, t, sb1, cst, *reinterpret_cast<const float4*>(cs + sb1),
+                  *reinterpret_cast<const float4*>(dt + sb1), mv + 4);
+    } else {   // j0 == S
+        const int sb0 = 16 * j0 + 4 * lg;
+        mask_diag(g0, t, sb0, cst, *reinterpret_cast<const float4*>(cs + sb0),
+                  *reinterpret_cast<const float4*>(dt + sb0), mv);
+#pragma unroll
+        for (int v = 4; v < 8; ++v) mv[v] = 0.f;
+    }
+    const bf16x8_t bop = pack8(mv);
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) yv[pt] = mfma(as_bf16x8(af[pt]), bop, yv[pt]);
+}
+
+// Diagonal block of wavefront W, whose strips (t-tiles) are W and 15 - W
+// (9 K-steps between them for every W).  K-step m covers s-tiles 2m, 2m+1; its
+// contraction index is permuted to the Gram accumulator layout (slot e<4 ->
+// s = 32m + 4 lg + e, e>=4 -> s = 32m + 16 + 4 lg + e - 4), and the x^T
+// fragments and vf of a K-step are read once for both strips.  Everything
+// about the strips is a compile-time constant, so the body is straight-line
+// code with immediate LDS offsets.
+template <int W>
+__device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const float* cs,
+                                          const float* vf, const float* dt, const u16* GR, int r,
+                                          int lg, int lane, f32x4_t* yA, f32x4_t* yB)
+{
+    constexpr int sA = W, sB = 15 - W;
+    constexpr int nA = sA / 2 + 1, nB = sB / 2 + 1;
     const int tA = 16 * sA + r, tB = 16 * sB + r;
     const float csA = cs[tA], csB = cs[tB];
-    const uint2* gA = reinterpret_cast<const uint2*>(GR) + tile_index(sA, 0) * 64 + lane;
-    const uint2* gB = reinterpret_cast<const uint2*>(GR) + tile_index(sB, 0) * 64 + lane;
-    const int nA = sA / 2 + 1, nB = sB / 2 + 1;
-#pragma unroll 1
-    for (int m = 0; m < nB; ++m) {
-        const int j0 = 2 * m;
-        const int sb0 = 32 * m + 4 * lg, sb1 = sb0 + 16;
+    const char* gA = reinterpret_cast<const char*>(GR) + tile_index(sA, 0) * 512 + 8 * lane;
+    const char* gB = reinterpret_cast<const char*>(GR) + tile_index(sB, 0) * 512 + 8 * lane;
+    const float* vfl = vf + 4 * lg;
+    const char* x0 = xsb + xa[0];
+    const char* x1 = xsb + xa[1];
+    const char* x2 = xsb + xa[2];
+    const char* x3 = xsb + xa[3];
+    // Software pipeline: the LDS operands of K-step m+1 are requested before
+    // the masking and MFMAs of K-step m.
+    struct Step {
         uint4 af[4];
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            const uint2 lo = xfrag(xs, sb0, 16 * pt, lane);
-            const uint2 hi = xfrag(xs, sb1, 16 * pt, lane);
-            af[pt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        }
-        const float4 vf0 = *reinterpret_cast<const float4*>(&vf[sb0]);
-        const float4 vf1 = *reinterpret_cast<const float4*>(&vf[sb1]);
-        const float4 cs0 = *reinterpret_cast<const float4*>(&cs[sb0]);
-        const float4 cs1 = *reinterpret_cast<const float4*>(&cs[sb1]);
-        const float4 dt0 = *reinterpret_cast<const float4*>(&dt[sb0]);
-        const float4 dt1 = *reinterpret_cast<const float4*>(&dt[sb1]);
-        const float ce0 = cs[16 * j0 + 15], ce1 = cs[16 * j0 + 31];
-        {   // strip B (always active)
-            const uint2 g0 = gB[j0 * 64];
-            const uint2 g1 = (j0 + 1 <= sB) ? gB[(j0 + 1) * 64] : make_uint2(0, 0);
-            float mv[8];
-            mask_half(g0, j0, sB, tB, csB, ce0, vf0, cs0, dt0, sb0, mv);
-            mask_half(g1, j0 + 1, sB, tB, csB, ce1, vf1, cs1, dt1, sb1, mv + 4);
-            const bf16x8_t bop = pack8(mv);
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) yB[pt] = mfma(as_bf16x8(af[pt]), bop, yB[pt]);
-        }
-        if (m < nA) {   // strip A (its first nA K-steps)
-            const uint2 g0 = gA[j0 * 64];
-            const uint2 g1 = (j0 + 1 <= sA) ? gA[(j0 + 1) * 64] : make_uint2(0, 0);
-            float mv[8];
-            mask_half(g0, j0, sA, tA, csA, ce0, vf0, cs0, dt0, sb0, mv);
-            mask_half(g1, j0 + 1, sA, tA, csA, ce1, vf1, cs1, dt1, sb1, mv + 4);
-            const bf16x8_t bop = pack8(mv);
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) yA[pt] = mfma(as_bf16x8(af[pt]), bop, yA[pt]);
-        }
+        float4 vf0, vf1;
+        float ce0, ce1;
+    };
+    auto load = [&](int m, Step& d) {
+        const uint2 l0 = tr_read(x0 + 4096 * m), h0 = tr_read(x0 + 4096 * m + 2048);
+        const uint2 l1 = tr_read(x1 + 4096 * m), h1 = tr_read(x1 + 4096 * m + 2048);
+        const uint2 l2 = tr_read(x2 + 4096 * m), h2 = tr_read(x2 + 4096 * m + 2048);
+        const uint2 l3 = tr_read(x3 + 4096 * m), h3 = tr_read(x3 + 4096 * m + 2048);
+        d.af[0] = make_uint4(l0.x, l0.y, h0.x, h0.y);
+        d.af[1] = make_uint4(l1.x, l1.y, h1.x, h1.y);
+        d.af[2] = make_uint4(l2.x, l2.y, h2.x, h2.y);
+        d.af[3] = make_uint4(l3.x, l3.y, h3.x, h3.y);
+        d.vf0 = *reinterpret_cast<const float4*>(vfl + 32 * m);
+        d.vf1 = *reinterpret_cast<const float4*>(vfl + 32 * m + 16);
+        d.ce0 = cs[32 * m + 15];
+        d.ce1 = cs[32 * m + 31];
+    };
+    Step cur;
+    load(0, cur);
+    [&]<int... Ms>(std::integer_sequence<int, Ms...>) {
+        ([&] {
+            constexpr int m = Ms;
+            Step nxt;
+            if constexpr (m + 1 < nB) load(m + 1, nxt);
+            strip_step<sB, m>(cur.af, gB, tB, csB, cur.ce0, cur.ce1, cur.vf0, cur.vf1, cs, dt, lg, yB);
+            if constexpr (m < nA)
+                strip_step<sA, m>(cur.af, gA, tA, csA, cur.ce0, cur.ce1, cur.vf0, cur.vf1, cs, dt, lg, yA);
+            if constexpr (m + 1 < nB) cur = nxt;
+        }(), ...);
+    }(std::make_integer_sequence<int, nB>{});
+}
+
+__device__ __forceinline__ void diag_block(int wave, const char* xsb, const int* xa, const float* cs,
+                                           const float* vf, const float* dt, const u16* GR, int r,
+                                           int lg, int lane, f32x4_t* yA, f32x4_t* yB)
+{
+    switch (wave) {
+    case 0: diag_wave<0>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 1: diag_wave<1>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 2: diag_wave<2>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 3: diag_wave<3>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 4: diag_wave<4>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 5: diag_wave<5>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 6: diag_wave<6>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    default: diag_wave<7>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
     }
 }
 
@@ -410,9 +485,37 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             __builtin_amdgcn_global_load_lds(gsrc + blk * 512 + 8 * lane, (lds_void*)(&sm.GR[blk * 512]), 16, 0, 0);
     }
     SSD_DMA_HEAD(h0, 0);
-    const u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
+    // Operands shared by the HG heads, kept in registers for the whole work item:
+    // B^T fragments of this wavefront's n-tile for the right factor, in the
+    // diagonal block's contraction order (slots 0-3: tokens 32m + 4 lg + e,
+    // slots 4-7: 32m + 16 + 4 lg + e - 4) so that the x^T reads are the same,
+    // and the C fragments of the two strips for the left factor (rows past a
+    // partial chunk's end are clamped; they are never stored).
+    uint2 btf[kQ / 32][2];
+    {
+        const u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
+        const u16* btr = bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 4u * lg);
+#pragma unroll
+        for (int m = 0; m < kQ / 32; ++m) {
+            btf[m][0] = *reinterpret_cast<const uint2*>(btr + 32 * m);
+            btf[m][1] = *reinterpret_cast<const uint2*>(btr + 32 * m + 16);
+        }
+    }
+    bf16x8_t cf[2][KN];
+#pragma unroll
+    for (int k4 = 0; k4 < 2; ++k4) {
+        const int t = 16 * strip[k4] + r;
+        const unsigned tc = static_cast<unsigned>(t < L ? t : L - 1);
+#pragma unroll
+        for (int k = 0; k < KN; ++k)
+            cf[k4][k] = as_bf16x8(*reinterpret_cast<const uint4*>(cchunk + (tc * crow + 32u * k + 8u * lg)));
+    }
     wait_vmem();
     __syncthreads();
+
+    int xa[4];   // byte offsets of this lane's transposing x reads, per p-tile
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) xa[pt] = x_tr_base(16 * pt, lane);
 
     for (int hk = 0; hk < p.HG; ++hk) {
         const int h = h0 + hk;
@@ -436,52 +539,35 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         for (int k4 = 0; k4 < 2; ++k4)
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
-        diag_block(xs, cs, sm.vf, dt, sm.GR, strip[0], strip[1], r, lg, lane, y[0], y[1]);
+        diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, sm.vf, dt, sm.GR, r, lg, lane, y[0], y[1]);
 
-        // B^T fragments of this wavefront's n-tile (L2; the same for every head).  Loaded
-        // here, not earlier: the vector-memory counter is in order, and loads issued
-        // right after the previous head's output stores would wait for those stores.
-        bf16x8_t btf[kQ / 32];
-#pragma unroll
-        for (int m = 0; m < kQ / 32; ++m)
-            btf[m] = as_bf16x8(*reinterpret_cast<const uint4*>(
-                bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 32u * m + 8u * lg)));
         // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
         f32x4_t sacc[PTW];
 #pragma unroll
         for (int i = 0; i < PTW; ++i) sacc[i] = zero4();
+        {
+            const char* xsb = reinterpret_cast<const char*>(xs);
+            const float* wl = sm.w + 4 * lg;
 #pragma unroll
-        for (int m = 0; m < kQ / 32; ++m) {
-            const int s0 = 32 * m + 8 * lg;
-            const float4 w0 = *reinterpret_cast<const float4*>(&sm.w[s0]);
-            const float4 w1 = *reinterpret_cast<const float4*>(&sm.w[s0 + 4]);
-            const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-            const uint4 braw = __builtin_bit_cast(uint4, btf[m]);
-            const u32 bw[4] = {braw.x, braw.y, braw.z, braw.w};
-            float bf8[8];
+            for (int m = 0; m < kQ / 32; ++m) {
+                const float4 w0 = *reinterpret_cast<const float4*>(wl + 32 * m);
+                const float4 w1 = *reinterpret_cast<const float4*>(wl + 32 * m + 16);
+                const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+                const u32 bw[4] = {btf[m][0].x, btf[m][0].y, btf[m][1].x, btf[m][1].y};
+                float bf8[8];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                bf8[2 * e] = __uint_as_float(bw[e] << 16) * wv[2 * e];
-                bf8[2 * e + 1] = __uint_as_float(bw[e] & 0xFFFF0000u) * wv[2 * e + 1];
+                for (int e = 0; e < 4; ++e) {
+                    bf8[2 * e] = __uint_as_float(bw[e] << 16) * wv[2 * e];
+                    bf8[2 * e + 1] = __uint_as_float(bw[e] & 0xFFFF0000u) * wv[2 * e + 1];
+                }
+                const bf16x8_t bop = pack8(bf8);
+#pragma unroll
+                for (int i = 0; i < PTW; ++i) {
+                    const char* xb = xsb + xa[pt0 + i] + 4096 * m;
+                    const uint2 lo = tr_read(xb), hi = tr_read(xb + 2048);
+                    sacc[i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[i]);
+                }
             }
-            const bf16x8_t bop = pack8(bf8);
-#pragma unroll
-            for (int i = 0; i < PTW; ++i) {
-                const uint2 lo = xfrag(xs, s0, 16 * (pt0 + i), lane);
-                const uint2 hi = xfrag(xs, s0 + 4, 16 * (pt0 + i), lane);
-                sacc[i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[i]);
-            }
-        }
-
-        // C fragments of the strips (L2); rows past a partial chunk are never stored
-        bf16x8_t cf[2][KN];
-#pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4) {
-            const int t = 16 * strip[k4] + r;
-            const unsigned tc = static_cast<unsigned>(t < L ? t : L - 1);
-#pragma unroll
-            for (int k = 0; k < KN; ++k)
-                cf[k4][k] = as_bf16x8(*reinterpret_cast<const uint4*>(cchunk + (tc * crow + 32u * k + 8u * lg)));
         }
 
         // ---- centre factor: state entering the chunk, state leaving it ----------
@@ -557,12 +643,9 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                                                           (16 * i + v) * N * static_cast<int>(sizeof(float)), 0);
                 }
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        wait_vmem();       // state stores complete (and the next head's DMA has landed)
-        __syncthreads();
-        if (tid == 0 && has_next)
-            __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // The state stores drain while the left factor runs; the flag is set after
+        // the epilogue's barrier, once every wavefront has waited for its stores.
+        __syncthreads();   // bf16 state in LDS complete
 
         // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
         {
@@ -613,7 +696,12 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                     *cell = packed;   // same cell this lane just read: in place is safe
                 }
             }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            wait_vmem();   // state stores complete (and the next head's DMA has landed)
             __syncthreads();
+            if (tid == 0 && has_next)
+                __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
 #pragma unroll
             for (int k = 0; k < kQ * kP / 8 / kMainThreads; ++k) {
