@@ -73,12 +73,17 @@ struct U16x8 {
 
 __device__ __forceinline__ float bf(u16 u) { return __uint_as_float(static_cast<u32>(u) << 16); }
 
-__device__ __forceinline__ u16 to_bf16(float f)
+// Two floats -> packed bf16 pair (hardware conversion, round to nearest even).
+__device__ __forceinline__ u32 pack_bf16x2(float lo, float hi)
 {
-    u32 u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return static_cast<u16>(u >> 16);
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    bf16x2_t v;
+    v[0] = static_cast<__bf16>(lo);
+    v[1] = static_cast<__bf16>(hi);
+    return __builtin_bit_cast(u32, v);
 }
+
+__device__ __forceinline__ u16 to_bf16(float f) { return static_cast<u16>(pack_bf16x2(f, 0.f)); }
 
 __device__ __forceinline__ bf16x8_t pack8(const float* f)
 {
@@ -100,6 +105,20 @@ __device__ __forceinline__ f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c)
 
 // Drain this wavefront's outstanding vector-memory operations.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Workgroup barrier for LDS data only.  __syncthreads() also waits for every
+// outstanding global -> LDS copy (vmcnt(0)), which would expose the latency of
+// copies issued ahead for a later head; here those copies are waited for
+// explicitly (wait_vmem) where their data is first needed.  The wavefront-scope
+// fences keep the compiler from moving memory accesses across the barrier;
+// lgkmcnt(0) completes this wavefront's LDS accesses before it.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 __device__ __forceinline__ float ld_coherent(const float* p)
 {
@@ -206,8 +225,8 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
             acc = mfma(as_bf16x8(va), as_bf16x8(vb), acc);
         }
         uint2 packed;
-        packed.x = static_cast<u32>(to_bf16(acc[0])) | (static_cast<u32>(to_bf16(acc[1])) << 16);
-        packed.y = static_cast<u32>(to_bf16(acc[2])) | (static_cast<u32>(to_bf16(acc[3])) << 16);
+        packed.x = pack_bf16x2(acc[0], acc[1]);
+        packed.y = pack_bf16x2(acc[2], acc[3]);
         *reinterpret_cast<uint2*>(gram + (static_cast<int64_t>(ti) * 64 + lane) * 4) = packed;
     }
 }
@@ -234,11 +253,12 @@ __device__ __forceinline__ uint2 xfrag(const u16* xs, int k0, int f0, int lane)
     return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(a)));
 }
 
+// LDS of the chunk kernel.  The Gram tiles and the bf16 state are separate
+// __shared__ objects (declared in the kernel) so that the compiler can tell
+// that copies into them never alias the reads of this struct's buffers.
 template <int N>
 struct MainSmem {
-    u16 GR[kTiles * 256];     // Gram tiles of the chunk: [tile][lane][4] bf16
     u16 XS[2][kQ * kP];       // x of the current / next head (token-major, swizzled)
-    u16 HB[kP * (N + 8)];     // bf16 state entering the chunk, (P x N)
     float cs[2][kQ];          // cs2 of the current / next head
     float dt[2][kQ];
     float vf[kQ];             // dt_s exp2(cs2[tile end] - cs2_s)
@@ -405,23 +425,128 @@ __device__ __forceinline__ void diag_block(int wave, const char* xsb, const int*
     }
 }
 
-#define SSD_DMA_HEAD(hh, q)                                                                     \
-    {                                                                                           \
-        const u16* xb_ = xchunk + static_cast<int64_t>(hh) * kP;                                \
-        _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) {                                      \
-            const int blk_ = 4 * wave + i_;                                                     \
-            const int s_ = 8 * blk_ + (lane >> 3);                                              \
-            const int grp_ = (lane & 7) ^ (s_ & 7);                                             \
-            const unsigned sc_ = static_cast<unsigned>(s_ < L ? s_ : L - 1);                    \
-            __builtin_amdgcn_global_load_lds(xb_ + (sc_ * xrow + 8u * grp_),                    \
-                                             (lds_void*)(&sm.XS[q][blk_ * 512]), 16, 0, 0);     \
-        }                                                                                       \
-        const int64_t row_ = ((static_cast<int64_t>(b) * p.H + (hh)) * p.nC + c) * kQ;          \
-        if (wave == 0)                                                                          \
-            __builtin_amdgcn_global_load_lds(p.cs2 + row_ + 4 * lane, (lds_void*)(&sm.cs[q][0]), 16, 0, 0); \
-        if (wave == 1)                                                                          \
-            __builtin_amdgcn_global_load_lds(p.dtT + row_ + 4 * lane, (lds_void*)(&sm.dt[q][0]), 16, 0, 0); \
+// One work item of the chunk kernel: (chunk, batch row, group of HG heads).
+struct Item {
+    int c, b, h0, g, L;
+    int64_t c0;
+    const u16* xchunk;   // x at token c0, head 0
+    const u16* cchunk;   // C at token c0, group g
+    bool has_prev, has_next;
+};
+
+__device__ __forceinline__ Item decode_item(const FusedParams& p, int work, int per_c, int nHG, int N)
+{
+    Item it;
+    it.c = work / per_c;
+    it.b = (work % per_c) / nHG;
+    it.h0 = (work % nHG) * static_cast<int>(p.HG);
+    it.g = it.h0 / static_cast<int>(p.H / p.G);
+    it.c0 = static_cast<int64_t>(it.c) * kQ;
+    it.L = static_cast<int>(kQ < p.T - it.c0 ? kQ : p.T - it.c0);
+    it.xchunk = static_cast<const u16*>(p.x) + (static_cast<int64_t>(it.b) * p.T + it.c0) * p.H * kP;
+    it.cchunk = static_cast<const u16*>(p.C) + ((static_cast<int64_t>(it.b) * p.T + it.c0) * p.G + it.g) * N;
+    it.has_prev = it.c > 0;
+    it.has_next = it.c + 1 < p.nC;
+    return it;
+}
+
+// Per-lane byte offsets of the asynchronous global -> LDS copies, fixed for the
+// whole kernel.  The copies are buffer loads with these offsets in VGPRs and the
+// head / tile offsets in SGPRs: an offset register of an outstanding copy is
+// never overwritten, so no later instruction has to wait for the copy to finish.
+struct DmaOffsets {
+    int x[4];   // x: token row s = 8 (4 wave + i) + lane/8, physical 16-byte group lane%8
+    int l16;    // 16 lane
+};
+
+__device__ __forceinline__ DmaOffsets dma_offsets(const FusedParams& p, int wave, int lane)
+{
+    DmaOffsets o;
+    const int xrow_bytes = static_cast<int>(p.H * kP * 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int s = 8 * (4 * wave + i) + (lane >> 3);
+        const int grp = (lane & 7) ^ (s & 7);   // logical group stored at physical slot lane%8
+        o.x[i] = s * xrow_bytes + 16 * grp;
+        asm volatile("" : "+v"(o.x[i]));       // keep in a register for the whole kernel
     }
+    o.l16 = 16 * lane;
+    asm volatile("" : "+v"(o.l16));
+    return o;
+}
+
+// Asynchronous copies of head hh of an item into LDS buffer q: x as 4 blocks of
+// 8 tokens per wavefront (lane l of a block fetches the 16 bytes that land at
+// block + 16 l), and the head's cs2 / dt rows.  The x buffer descriptor ends at
+// the end of the batch row, so rows past a partial last chunk read as zeros
+// (such tokens have dt = 0 and zero Gram rows and columns, and are never stored).
+template <int N>
+__device__ __forceinline__ void dma_head(MainSmem<N>& sm, const FusedParams& p, const Item& it, int hh,
+                                         int q, int wave, const DmaOffsets& o)
+{
+    const int64_t xbytes = (p.T - it.c0) * p.H * kP * 2;
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<u16*>(it.xchunk), 0, static_cast<int>(xbytes < 0x7FFFFFFF ? xbytes : 0x7FFFFFFF), 0x00020000);
+    const int hoff = hh * kP * 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)(&sm.XS[q][(4 * wave + i) * 512]), 16, o.x[i],
+                                                 hoff, 0, 0);
+    const int64_t row = ((static_cast<int64_t>(it.b) * p.H + hh) * p.nC + it.c) * kQ;
+    if (wave == 0) {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(p.cs2 + row, 0, kQ * 4, 0x00020000);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(&sm.cs[q][0]), 16, o.l16, 0, 0, 0);
+    }
+    if (wave == 1) {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(p.dtT + row, 0, kQ * 4, 0x00020000);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(&sm.dt[q][0]), 16, o.l16, 0, 0, 0);
+    }
+}
+
+// The chunk's causal Gram tiles (shared by the item's heads) into LDS.
+__device__ __forceinline__ void dma_gram(u16* gr, const FusedParams& p, const Item& it, int wave,
+                                         const DmaOffsets& o)
+{
+    constexpr int kBlocks = kTiles * 256 * 2 / 1024;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        p.gram + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * kTiles * 256, 0, kBlocks * 1024,
+        0x00020000);
+    for (int blk = wave; blk < kBlocks; blk += kWaves)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(&gr[blk * 512]), 16, o.l16, blk * 1024, 0, 0);
+}
+
+// B^T fragments of n-tile ntw for the right factor, in the diagonal block's
+// contraction order (slots 0-3: tokens 32m + 4 lg + e, slots 4-7:
+// 32m + 16 + 4 lg + e - 4), so that both share the x^T reads.
+template <int N>
+__device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, int ntw, int r, int lg,
+                                        uint2 (&btf)[kQ / 32][2])
+{
+    const u16* bt = p.BT + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * N * kQ;
+    const u16* btr = bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 4u * lg);
+#pragma unroll
+    for (int m = 0; m < kQ / 32; ++m) {
+        btf[m][0] = *reinterpret_cast<const uint2*>(btr + 32 * m);
+        btf[m][1] = *reinterpret_cast<const uint2*>(btr + 32 * m + 16);
+    }
+}
+
+// C fragments of the two strips for the left factor (rows past a partial
+// chunk's end are clamped; they are never stored).
+template <int N>
+__device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, const int* strip, int r, int lg,
+                                       bf16x8_t (&cf)[2][N / 32])
+{
+    const unsigned crow = static_cast<unsigned>(p.G * N);
+#pragma unroll
+    for (int k4 = 0; k4 < 2; ++k4) {
+        const int t = 16 * strip[k4] + r;
+        const unsigned tc = static_cast<unsigned>(t < it.L ? t : it.L - 1);
+#pragma unroll
+        for (int k = 0; k < N / 32; ++k)
+            cf[k4][k] = as_bf16x8(*reinterpret_cast<const uint4*>(it.cchunk + (tc * crow + 32u * k + 8u * lg)));
+    }
+}
 
 template <int N>
 __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
@@ -435,27 +560,18 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     static_assert(kQ * kP / 512 == 4 * kWaves, "x DMA: 4 blocks of 8 tokens per wavefront");
     static_assert((kTiles * 256 * 2) % 1024 == 0, "Gram DMA in 1 KiB blocks");
     __shared__ __attribute__((aligned(16))) MainSmem<N> sm;
+    __shared__ __attribute__((aligned(16))) u16 s_gr[kTiles * 256];   // Gram tiles: [tile][lane][4] bf16
+    __shared__ __attribute__((aligned(16))) u16 s_hb[kP * HBS];       // bf16 state entering the chunk (P x N)
 
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
     // wavefront index, provably uniform (branches on it stay scalar)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if (tid == 0) sm.ticket = atomicAdd(p.ticket, 1);
-    __syncthreads();
-    const int work = sm.ticket;
     const int nHG = static_cast<int>(p.H / p.HG);
     const int per_c = static_cast<int>(p.b) * nHG;
-    const int c = work / per_c;
-    const int b = (work % per_c) / nHG;
-    const int hg = work % nHG;
-    const int h0 = hg * static_cast<int>(p.HG);
-    const int g = h0 / static_cast<int>(p.H / p.G);
-    const int64_t c0 = static_cast<int64_t>(c) * kQ;
-    const int L = static_cast<int>(kQ < p.T - c0 ? kQ : p.T - c0);
-    const u16* xp = static_cast<const u16*>(p.x);
-    const u16* Cp = static_cast<const u16*>(p.C);
+    const int nwork = static_cast<int>(p.nC) * per_c;
     u16* yp = static_cast<u16*>(p.y);
     const int64_t PN = static_cast<int64_t>(kP) * N;
-    const bool has_prev = c > 0, has_next = c + 1 < p.nC;
+    const unsigned xrow = static_cast<unsigned>(p.H * kP);   // elements per token
 
     // strips (16-token t-tiles) of this wavefront: balanced causal work (9 K-steps)
     int strip[2];
@@ -464,66 +580,68 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     // state tiles of this wavefront in the right factor: n-tile ntw, p-tiles pt0..pt0+PTW-1
     const int ntw = (PTW == 4) ? wave : (wave & 3);
     const int pt0 = (PTW == 4) ? 0 : 2 * (wave >> 2);
-
-    const u16* xchunk = xp + (static_cast<int64_t>(b) * p.T + c0) * p.H * kP;    // token c0, head 0
-    const unsigned xrow = static_cast<unsigned>(p.H * kP);                        // elements per token
-    const u16* cchunk = Cp + ((static_cast<int64_t>(b) * p.T + c0) * p.G + g) * N;  // token c0, group g
-    const unsigned crow = static_cast<unsigned>(p.G * N);
-
-    // Asynchronous global -> LDS loads (no registers): x of head hh into buffer
-    // q, 4 blocks of 8 tokens per wavefront; lane l of a block fetches the
-    // 16 bytes that land at block + 16 l, i.e. physical group l%8 of token
-    // row l/8.  Rows past a partial chunk's end load the last valid row: such
-    // tokens only ever meet zero weights (dt = 0 there, zero Gram rows and
-    // columns) or are never stored.
-
-    // ---- prologue: Gram tiles (shared by the HG heads), head h0, B^T and C fragments
-    {
-        const u16* gsrc = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
-        constexpr int kBlocks = kTiles * 256 * 2 / 1024;
-        for (int blk = wave; blk < kBlocks; blk += kWaves)
-            __builtin_amdgcn_global_load_lds(gsrc + blk * 512 + 8 * lane, (lds_void*)(&sm.GR[blk * 512]), 16, 0, 0);
-    }
-    SSD_DMA_HEAD(h0, 0);
-    // Operands shared by the HG heads, kept in registers for the whole work item:
-    // B^T fragments of this wavefront's n-tile for the right factor, in the
-    // diagonal block's contraction order (slots 0-3: tokens 32m + 4 lg + e,
-    // slots 4-7: 32m + 16 + 4 lg + e - 4) so that the x^T reads are the same,
-    // and the C fragments of the two strips for the left factor (rows past a
-    // partial chunk's end are clamped; they are never stored).
-    uint2 btf[kQ / 32][2];
-    {
-        const u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
-        const u16* btr = bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 4u * lg);
-#pragma unroll
-        for (int m = 0; m < kQ / 32; ++m) {
-            btf[m][0] = *reinterpret_cast<const uint2*>(btr + 32 * m);
-            btf[m][1] = *reinterpret_cast<const uint2*>(btr + 32 * m + 16);
-        }
-    }
-    bf16x8_t cf[2][KN];
-#pragma unroll
-    for (int k4 = 0; k4 < 2; ++k4) {
-        const int t = 16 * strip[k4] + r;
-        const unsigned tc = static_cast<unsigned>(t < L ? t : L - 1);
-#pragma unroll
-        for (int k = 0; k < KN; ++k)
-            cf[k4][k] = as_bf16x8(*reinterpret_cast<const uint4*>(cchunk + (tc * crow + 32u * k + 8u * lg)));
-    }
-    wait_vmem();
-    __syncthreads();
-
+    const DmaOffsets dmo = dma_offsets(p, wave, lane);
     int xa[4];   // byte offsets of this lane's transposing x reads, per p-tile
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) xa[pt] = x_tr_base(16 * pt, lane);
 
+    // Persistent workgroups: work items are taken from a ticket counter in
+    // chunk-major order, so an item only ever waits for an item already taken
+    // by a running (or finished) workgroup.  The operands of the next item are
+    // prefetched during the last head of the current one.
+    if (tid == 0) sm.ticket = atomicAdd(p.ticket, 1);
+    __syncthreads();
+    int work = sm.ticket;
+    if (work >= nwork) return;
+    {
+        const Item it = decode_item(p, work, per_c, nHG, N);
+        dma_gram(s_gr, p, it, wave, dmo);
+        dma_head(sm, p, it, it.h0, 0, wave, dmo);
+    }
+    wait_vmem();
+    __syncthreads();
+
+    int q = 0;   // LDS buffer of the current head
+    bool first_item = true;
+    for (;;) {
+    const Item it = decode_item(p, work, per_c, nHG, N);
+    int next = nwork;
+    // register operands shared by the item's heads (see load_bt / load_c)
+    uint2 btf[kQ / 32][2];
+    bf16x8_t cf[2][KN];
     for (int hk = 0; hk < p.HG; ++hk) {
-        const int h = h0 + hk;
-        const int q = hk & 1;
+        const int h = it.h0 + hk;
+        const bool last = hk + 1 == p.HG;
+        const int b = it.b, c = it.c, L = it.L;
+        const int64_t c0 = it.c0;
+        const bool has_prev = it.has_prev, has_next = it.has_next;
         const u16* xs = sm.XS[q];
         const float* cs = sm.cs[q];
         const float* dt = sm.dt[q];
-        if (hk + 1 < p.HG) SSD_DMA_HEAD(h + 1, q ^ 1);   // lands while this head computes
+        const float Dh = p.D ? p.D[h] : 0.f;   // issued early: used in the epilogue
+        // x of the next head (of this item, or of the next item once known) lands while
+        // this head computes
+        if (!last)
+            dma_head(sm, p, it, h + 1, q ^ 1, wave, dmo);
+        else if (hk > 0 && next < nwork)
+            dma_head(sm, p, decode_item(p, next, per_c, nHG, N), 0, q ^ 1, wave, dmo);
+        if (hk == 0 && tid == 0)
+            sm.ticket = atomicAdd(p.ticket, 1);   // reserve the next work item now
+
+        if (hk == 0) {
+            if (!first_item) {
+                // the Gram tiles prefetched during the previous item must have landed
+                // (all but the 4 copies just issued for the next head, when there were any)
+                if (p.HG > 1)
+                    __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4)
+                else
+                    wait_vmem();
+            }
+            // issued after that wait so that it does not wait for them; first needed
+            // by the right factor, after the diagonal block
+            load_bt<N>(p, it, ntw, r, lg, btf);
+            load_c<N>(p, it, strip, r, lg, cf);
+        }
 
         // per-token weights of this head
         if (tid < kQ) {
@@ -531,7 +649,12 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             sm.vf[tid] = d * exp2f(cs[tid | 15] - cst);
             sm.w[tid] = d * exp2f(cs[kQ - 1] - cst);
         }
-        __syncthreads();
+        lds_barrier();
+        if (hk == 0) {
+            next = sm.ticket;
+            if (last && next < nwork)   // one head per item: its successor's x only now
+                dma_head(sm, p, decode_item(p, next, per_c, nHG, N), 0, q ^ 1, wave, dmo);
+        }
 
         // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
         f32x4_t y[2][4];
@@ -539,7 +662,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         for (int k4 = 0; k4 < 2; ++k4)
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
-        diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, sm.vf, dt, sm.GR, r, lg, lane, y[0], y[1]);
+        diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, sm.vf, dt, s_gr, r, lg, lane, y[0], y[1]);
 
         // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
         f32x4_t sacc[PTW];
@@ -570,6 +693,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             }
         }
 
+
         // ---- centre factor: state entering the chunk, state leaving it ----------
         float* ring_h = p.ring + (static_cast<int64_t>(b) * p.H + h) * 2 * PN;
         const __amdgpu_buffer_rsrc_t ring_rs =
@@ -586,7 +710,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                 }
             }
         }
-        __syncthreads();   // flag seen by tid 0
+        lds_barrier();   // flag seen by tid 0
         f32x4_t hprev[PTW];
         if (has_prev) {
             const int slot = (c + 1) & 1;
@@ -616,7 +740,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         for (int i = 0; i < PTW; ++i) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                sm.HB[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
+                s_hb[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
                 sacc[i][v] = decay * hprev[i][v] + sacc[i][v];
             }
         }
@@ -645,7 +769,8 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         }
         // The state stores drain while the left factor runs; the flag is set after
         // the epilogue's barrier, once every wavefront has waited for its stores.
-        __syncthreads();   // bf16 state in LDS complete
+        lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
+        const bool gram_ahead = last && next < nwork;
 
         // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
         {
@@ -658,7 +783,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             for (int k = 0; k < KN; ++k) {
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
-                    const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&sm.HB[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
+                    const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&s_hb[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
                     tq[0][pt] = mfma(aop, cf[0][k], tq[0][pt]);
                     tq[1][pt] = mfma(aop, cf[1][k], tq[1][pt]);
                 }
@@ -674,9 +799,9 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
             }
         }
 
+
         // ---- skip term; y staged in place over this head's x, then full-row stores
         {
-            const float Dh = p.D ? p.D[h] : 0.f;
             u16* xw = sm.XS[q];
 #pragma unroll
             for (int k4 = 0; k4 < 2; ++k4) {
@@ -687,32 +812,48 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
                     const uint2 xv = *cell;
                     const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
                                          __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
-                    u16 o[4];
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) o[v] = to_bf16(y[k4][pt][v] + Dh * xf[v]);
                     uint2 packed;
-                    packed.x = static_cast<u32>(o[0]) | (static_cast<u32>(o[1]) << 16);
-                    packed.y = static_cast<u32>(o[2]) | (static_cast<u32>(o[3]) << 16);
+                    packed.x = pack_bf16x2(y[k4][pt][0] + Dh * xf[0], y[k4][pt][1] + Dh * xf[1]);
+                    packed.y = pack_bf16x2(y[k4][pt][2] + Dh * xf[2], y[k4][pt][3] + Dh * xf[3]);
                     *cell = packed;   // same cell this lane just read: in place is safe
                 }
             }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-            wait_vmem();   // state stores complete (and the next head's DMA has landed)
-            __syncthreads();
+            // The next item's Gram tiles (its heads' x arrives head by head), issued
+            // once this head's x cells have been read: only the Gram buffer, a
+            // separate LDS object, is written by these copies.
+            if (gram_ahead) dma_gram(s_gr, p, decode_item(p, next, per_c, nHG, N), wave, dmo);
+            // state stores complete (and the next head's x has landed); the Gram copies
+            // issued after them (at most 9 per wavefront, at least 8) may stay in flight
+            if (gram_ahead)
+                __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8)
+            else
+                wait_vmem();
+            lds_barrier();
             if (tid == 0 && has_next)
                 __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
+            constexpr int kPieces = kQ * kP / 8 / kMainThreads;   // 16-byte pieces per thread
+            uint4 v[kPieces];
 #pragma unroll
-            for (int k = 0; k < kQ * kP / 8 / kMainThreads; ++k) {
-                const int ci = tid + kMainThreads * k;      // 16-byte piece: token ci/8, group ci%8
+            for (int k = 0; k < kPieces; ++k) {
+                const int ci = tid + kMainThreads * k;      // piece: token ci/8, group ci%8
+                v[k] = *reinterpret_cast<const uint4*>(xw + xs_off(ci >> 3, 8 * (ci & 7)));
+            }
+#pragma unroll
+            for (int k = 0; k < kPieces; ++k) {
+                const int ci = tid + kMainThreads * k;
                 const int t = ci >> 3, grp = ci & 7;
-                const uint4 v = *reinterpret_cast<const uint4*>(xw + xs_off(t, 8 * grp));
                 // streaming (non-temporal) stores: y is not read again by this kernel
-                if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
+                if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
             }
         }
-        __syncthreads();   // this head's LDS buffers may be refilled from here on
+        lds_barrier();   // this head's LDS buffers may be refilled from here on
+        q ^= 1;
+    }
+    if (next >= nwork) break;
+    work = next;
+    first_item = false;
     }
 }
 
@@ -724,8 +865,14 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     hipError_t err = hipGetLastError();
     if (err == hipSuccess && ev_begin) err = hipEventRecord(ev_begin, stream);
     if (err != hipSuccess) return err;
-    const unsigned nwork = static_cast<unsigned>(p.nC * p.b * (p.H / p.HG));
-    hipLaunchKernelGGL(k_fused_main<N>, dim3(nwork), dim3(kMainThreads), 0, stream, p);
+    const int64_t nwork = p.nC * p.b * (p.H / p.HG);
+    int dev = 0, cus = 0;
+    err = hipGetDevice(&dev);
+    if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    // one persistent workgroup per compute unit (the LDS footprint allows one)
+    const unsigned grid = static_cast<unsigned>(nwork < cus ? nwork : cus);
+    hipLaunchKernelGGL(k_fused_main<N>, dim3(grid), dim3(kMainThreads), 0, stream, p);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;
