@@ -46,6 +46,7 @@
 // Two ring slots suffice: chunk c+2 overwrites the slot of chunk c only after
 // reading the state of chunk c+1, which chunk c+1 published only after it had
 // read (consumed) the state of chunk c.
+#include <cstdlib>
 #include <utility>
 
 #include "ssd_device.h"
@@ -142,7 +143,7 @@ __device__ __forceinline__ int tile_index(int i, int j) { return i * (i + 1) / 2
 // ---------------------------------------------------------------------------
 // prep
 // ---------------------------------------------------------------------------
-constexpr int kPrepParts = 8;   // workgroups per (batch, chunk, group)
+constexpr int kPrepParts = 32;  // workgroups per (batch, chunk, group)
 
 template <int N>
 __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
@@ -168,6 +169,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
         }
     }
 
+    // Rows past a partial chunk's end are read clamped to the last row (every load
+    // is unconditional, so they all stay in flight together) and then zeroed.
+
     // step 1 for the heads of this part: one wavefront per head, 4 tokens per lane
     for (int hh = part * 4 + wave; hh < hpg; hh += kPrepParts * 4) {
         const int h = g * hpg + hh;
@@ -176,7 +180,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int t = 4 * lane + k;
-            d[k] = (t < L) ? bf(dtp[(b * p.T + c0 + t) * p.H + h]) : 0.f;
+            const int tc = t < L ? t : L - 1;
+            const float v = bf(dtp[(b * p.T + c0 + tc) * p.H + h]);
+            d[k] = (t < L) ? v : 0.f;
             a[k] = d[k] * A2;
         }
         a[1] += a[0];
@@ -195,35 +201,46 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
     }
 
     // B^T of the chunk, rows n of this part: lanes walk n (coalesced row reads of B)
+    const u16* Bchunk = Bp + ((b * p.T + c0) * p.G + g) * N;
+    const int64_t brow = p.G * N;
     u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
     constexpr int kBtItems = N * (kQ / 8) / kPrepParts;
     for (int idx = tid; idx < kBtItems; idx += kPrepThreads) {
         const int gi = part * kBtItems + idx;
         const int n = gi % N, so = gi / N;
-        U16x8 v;
+        u16 raw[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int s = 8 * so + e;
-            v.v[e] = (s < L) ? Bp[((b * p.T + c0 + s) * p.G + g) * N + n] : static_cast<u16>(0);
+            raw[e] = Bchunk[(s < L ? s : L - 1) * brow + n];
         }
+        U16x8 v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v.v[e] = (8 * so + e < L) ? raw[e] : static_cast<u16>(0);
         *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
     }
 
     // Gram tiles G^T[s][t] = sum_n B_s[n] C_t[n] (bf16), accumulator layout per lane
+    const u16* Cchunk = Cp + ((b * p.T + c0) * p.G + g) * N;
     u16* gram = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
     for (int ti = part * 4 + wave; ti < kTiles; ti += kPrepParts * 4) {
         int i = 0;
         while ((i + 1) * (i + 2) / 2 <= ti) ++i;
         const int j = ti - i * (i + 1) / 2;
         const int s = 16 * j + r, t = 16 * i + r;
+        const u16* bs = Bchunk + (s < L ? s : L - 1) * brow + 8 * lg;
+        const u16* ct = Cchunk + (t < L ? t : L - 1) * brow + 8 * lg;
+        uint4 va[N / 32], vb[N / 32];
+#pragma unroll
+        for (int k = 0; k < N / 32; ++k) {
+            va[k] = *reinterpret_cast<const uint4*>(bs + 32 * k);
+            vb[k] = *reinterpret_cast<const uint4*>(ct + 32 * k);
+        }
+        const uint4 z = make_uint4(0, 0, 0, 0);
         f32x4_t acc = zero4();
 #pragma unroll
-        for (int k0 = 0; k0 < N; k0 += 32) {
-            uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
-            if (s < L) va = *reinterpret_cast<const uint4*>(Bp + ((b * p.T + c0 + s) * p.G + g) * N + k0 + 8 * lg);
-            if (t < L) vb = *reinterpret_cast<const uint4*>(Cp + ((b * p.T + c0 + t) * p.G + g) * N + k0 + 8 * lg);
-            acc = mfma(as_bf16x8(va), as_bf16x8(vb), acc);
-        }
+        for (int k = 0; k < N / 32; ++k)
+            acc = mfma(as_bf16x8(s < L ? va[k] : z), as_bf16x8(t < L ? vb[k] : z), acc);
         uint2 packed;
         packed.x = pack_bf16x2(acc[0], acc[1]);
         packed.y = pack_bf16x2(acc[2], acc[3]);
@@ -623,8 +640,10 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         // this head computes
         if (!last)
             dma_head(sm, p, it, h + 1, q ^ 1, wave, dmo);
-        else if (hk > 0 && next < nwork)
-            dma_head(sm, p, decode_item(p, next, per_c, nHG, N), 0, q ^ 1, wave, dmo);
+        else if (hk > 0 && next < nwork) {
+            const Item nit = decode_item(p, next, per_c, nHG, N);
+            dma_head(sm, p, nit, nit.h0, q ^ 1, wave, dmo);
+        }
         if (hk == 0 && tid == 0)
             sm.ticket = atomicAdd(p.ticket, 1);   // reserve the next work item now
 
@@ -653,7 +672,10 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
         if (hk == 0) {
             next = sm.ticket;
             if (last && next < nwork)   // one head per item: its successor's x only now
-                dma_head(sm, p, decode_item(p, next, per_c, nHG, N), 0, q ^ 1, wave, dmo);
+            {
+                const Item nit = decode_item(p, next, per_c, nHG, N);
+                dma_head(sm, p, nit, nit.h0, q ^ 1, wave, dmo);
+            }
         }
 
         // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
@@ -870,9 +892,14 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     err = hipGetDevice(&dev);
     if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    // one persistent workgroup per compute unit (the LDS footprint allows one)
-    const unsigned grid = static_cast<unsigned>(nwork < cus ? nwork : cus);
-    hipLaunchKernelGGL(k_fused_main<N>, dim3(grid), dim3(kMainThreads), 0, stream, p);
+    // one persistent workgroup per compute unit (the LDS footprint allows one);
+    // SSD_MAX_WORKGROUPS caps it (a test knob: few workgroups, many items each)
+    int64_t grid = nwork < cus ? nwork : cus;
+    if (const char* cap = std::getenv("SSD_MAX_WORKGROUPS")) {
+        const long v = std::strtol(cap, nullptr, 10);
+        if (v >= 1 && v < grid) grid = v;
+    }
+    hipLaunchKernelGGL(k_fused_main<N>, dim3(static_cast<unsigned>(grid)), dim3(kMainThreads), 0, stream, p);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;

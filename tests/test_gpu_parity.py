@@ -114,6 +114,16 @@ def test_fused_shapes(shape):
     check(make_inputs(p, 11), tag="fused")
 
 
+@pytest.mark.parametrize("hg", ["1", "2", "4"])
+def test_fused_persistent_items(monkeypatch, hg):
+    """Few persistent workgroups, so that each one runs many work items in a row
+    (prefetching the next item's operands); every head is checked."""
+    monkeypatch.setenv("SSD_MAX_WORKGROUPS", "3")
+    monkeypatch.setenv("SSD_HEADS_PER_WG", hg)
+    p = Problem(2, 1500, 8, 64, 128, 1, 256, "bf16", init_states=True)
+    check(make_inputs(p, 13), tag="persistent_hg" + hg)
+
+
 def test_general_path_at_fused_shape(monkeypatch):
     """Both device paths at one shape: the general step-by-step kernels (forced)
     and the fused ones must each meet the tolerance against the oracle."""
@@ -154,5 +164,7 @@ FULL = ["mamba2_130m", "mamba2_2p7b", "varlen_g8", "sweep_T512_N128",
 def test_full_size_sampled_heads(name):
     p = WORKLOADS[name]
     inp = make_inputs(p, 0)
-    heads = sorted({0, p.nheads // 2 + 1, p.nheads - 1})
+    # first, second and last head, and the first and second head of a work item in
+    # the middle (items are groups of up to 4 consecutive heads)
+    heads = sorted({0, 1, p.nheads // 2, p.nheads // 2 + 1, p.nheads - 1})
     check(inp, heads=heads, tag=name)
