@@ -467,10 +467,37 @@ __device__ __forceinline__ Item decode_item(const FusedParams& p, int work, int 
     return it;
 }
 
-// Per-lane byte offsets of the asynchronous global -> LDS copies, fixed for the
-// whole kernel.  The copies are buffer loads with these offsets in VGPRs and the
-// head / tile offsets in SGPRs: an offset register of an outstanding copy is
-// never overwritten, so no later instruction has to wait for the copy to finish.
+// Asynchronous global -> LDS copies (buffer_load ... lds, 16 bytes per lane,
+// landing at the LDS address in M0 + 16 lane).  They are issued through inline
+// assembly so that the compiler, which cannot tell which LDS bytes such a copy
+// writes, does not make every later LDS access wait for it; every read of
+// copied data is preceded by an explicit wait (s_waitcnt vmcnt) and a barrier.
+// A copy adds to the vector-memory counter like any load, so the compiler's
+// own waits for its loads stay correct (they can only wait longer).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer descriptor (raw, no stride) over `bytes` bytes from `base`; reads past
+// the end return zeros.  The base is uniform across the wavefront.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int64_t bytes)
+{
+    const unsigned long long a = reinterpret_cast<unsigned long long>(base);
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane(static_cast<int>(a & 0xFFFFFFFFull));
+    r[1] = __builtin_amdgcn_readfirstlane(static_cast<int>((a >> 32) & 0xFFFFull));
+    r[2] = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes < 0x7FFFFFFF ? bytes : 0x7FFFFFFF));
+    r[3] = 0x00020000;
+    return r;
+}
+
+__device__ __forceinline__ void copy16_to_lds(i32x4 rsrc, const void* lds_dst, int voffset, int soffset)
+{
+    const unsigned m0 =
+        __builtin_amdgcn_readfirstlane(static_cast<unsigned>(reinterpret_cast<uintptr_t>(lds_dst)));
+    asm volatile("buffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :: "v"(voffset), "s"(rsrc), "s"(soffset), "{m0}"(m0) : "memory");
+}
+
+// Per-lane byte offsets of the copies, fixed for the whole kernel.
 struct DmaOffsets {
     int x[4];   // x: token row s = 8 (4 wave + i) + lane/8, physical 16-byte group lane%8
     int l16;    // 16 lane
@@ -485,39 +512,27 @@ __device__ __forceinline__ DmaOffsets dma_offsets(const FusedParams& p, int wave
         const int s = 8 * (4 * wave + i) + (lane >> 3);
         const int grp = (lane & 7) ^ (s & 7);   // logical group stored at physical slot lane%8
         o.x[i] = s * xrow_bytes + 16 * grp;
-        asm volatile("" : "+v"(o.x[i]));       // keep in a register for the whole kernel
     }
     o.l16 = 16 * lane;
-    asm volatile("" : "+v"(o.l16));
     return o;
 }
 
-// Asynchronous copies of head hh of an item into LDS buffer q: x as 4 blocks of
-// 8 tokens per wavefront (lane l of a block fetches the 16 bytes that land at
-// block + 16 l), and the head's cs2 / dt rows.  The x buffer descriptor ends at
-// the end of the batch row, so rows past a partial last chunk read as zeros
-// (such tokens have dt = 0 and zero Gram rows and columns, and are never stored).
-template <int N>
-__device__ __forceinline__ void dma_head(MainSmem<N>& sm, const FusedParams& p, const Item& it, int hh,
-                                         int q, int wave, const DmaOffsets& o)
+// Copies of head hh of an item into the LDS buffers xdst / csdst / dtdst: x as
+// 4 blocks of 8 tokens per wavefront (lane l of a block fetches the 16 bytes
+// that land at block + 16 l), and the head's cs2 / dt rows.  The x descriptor
+// ends at the end of the batch row, so rows past a partial last chunk read as
+// zeros (such tokens have dt = 0 and zero Gram rows and columns, and are never
+// stored).
+__device__ __forceinline__ void dma_head(const FusedParams& p, const Item& it, int hh, u16* xdst, float* csdst,
+                                         float* dtdst, int wave, const DmaOffsets& o)
 {
-    const int64_t xbytes = (p.T - it.c0) * p.H * kP * 2;
-    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<u16*>(it.xchunk), 0, static_cast<int>(xbytes < 0x7FFFFFFF ? xbytes : 0x7FFFFFFF), 0x00020000);
+    const i32x4 xrs = buffer_rsrc(it.xchunk, (p.T - it.c0) * p.H * kP * 2);
     const int hoff = hh * kP * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)(&sm.XS[q][(4 * wave + i) * 512]), 16, o.x[i],
-                                                 hoff, 0, 0);
+    for (int i = 0; i < 4; ++i) copy16_to_lds(xrs, xdst + (4 * wave + i) * 512, o.x[i], hoff);
     const int64_t row = ((static_cast<int64_t>(it.b) * p.H + hh) * p.nC + it.c) * kQ;
-    if (wave == 0) {
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(p.cs2 + row, 0, kQ * 4, 0x00020000);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(&sm.cs[q][0]), 16, o.l16, 0, 0, 0);
-    }
-    if (wave == 1) {
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(p.dtT + row, 0, kQ * 4, 0x00020000);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(&sm.dt[q][0]), 16, o.l16, 0, 0, 0);
-    }
+    if (wave == 0) copy16_to_lds(buffer_rsrc(p.cs2 + row, kQ * 4), csdst, o.l16, 0);
+    if (wave == 1) copy16_to_lds(buffer_rsrc(p.dtT + row, kQ * 4), dtdst, o.l16, 0);
 }
 
 // The chunk's causal Gram tiles (shared by the item's heads) into LDS.
@@ -525,11 +540,9 @@ __device__ __forceinline__ void dma_gram(u16* gr, const FusedParams& p, const It
                                          const DmaOffsets& o)
 {
     constexpr int kBlocks = kTiles * 256 * 2 / 1024;
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        p.gram + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * kTiles * 256, 0, kBlocks * 1024,
-        0x00020000);
-    for (int blk = wave; blk < kBlocks; blk += kWaves)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(&gr[blk * 512]), 16, o.l16, blk * 1024, 0, 0);
+    const i32x4 rs = buffer_rsrc(p.gram + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * kTiles * 256,
+                                 kBlocks * 1024);
+    for (int blk = wave; blk < kBlocks; blk += kWaves) copy16_to_lds(rs, gr + blk * 512, o.l16, blk * 1024);
 }
 
 // B^T fragments of n-tile ntw for the right factor, in the diagonal block's
@@ -565,6 +578,273 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
     }
 }
 
+// One head of a work item.  Every LDS buffer is a separate __restrict__
+// parameter: the compiler then knows that the asynchronous copies into the
+// next head's buffers (and the next item's Gram tiles) never alias the buffers
+// read here, and does not make those reads wait for the copies.
+template <int N>
+__device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
+                                          int per_c, int nHG,
+                                          uint2 (&btf)[kQ / 32][2], bf16x8_t (&cf)[2][N / 32],
+                                          u16* __restrict__ xs, u16* __restrict__ xs_n,
+                                          float* __restrict__ cs, float* __restrict__ cs_n,
+                                          float* __restrict__ dt, float* __restrict__ dt_n,
+                                          float* __restrict__ vf, float* __restrict__ w,
+                                          u16* __restrict__ gr, u16* __restrict__ hb, int* __restrict__ tk)
+{
+    constexpr int NT = N / 16;
+    constexpr int PTW = 4 * NT / kWaves;
+    constexpr int KN = N / 32;
+    constexpr int HBS = N + 8;
+    // per-wavefront constants (loop-invariant; the compiler keeps them out of the loops)
+    const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // provably uniform
+    // strips (16-token t-tiles) of this wavefront: balanced causal work (9 K-steps)
+    const int strip[2] = {wave, kNQ - 1 - wave};
+    // state tiles of this wavefront in the right factor: n-tile ntw, p-tiles pt0..pt0+PTW-1
+    const int ntw = (PTW == 4) ? wave : (wave & 3);
+    const int pt0 = (PTW == 4) ? 0 : 2 * (wave >> 2);
+    int xa[4];   // byte offsets of this lane's transposing x reads, per p-tile
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) xa[pt] = x_tr_base(16 * pt, lane);
+    const DmaOffsets dmo = dma_offsets(p, wave, lane);
+    u16* yp = static_cast<u16*>(p.y);
+    const int64_t PN = static_cast<int64_t>(kP) * N;
+    const unsigned xrow = static_cast<unsigned>(p.H * kP);
+
+    const int h = it.h0 + hk;
+    const bool last = hk + 1 == p.HG;
+    const int b = it.b, c = it.c, L = it.L;
+    const int64_t c0 = it.c0;
+    const bool has_prev = it.has_prev, has_next = it.has_next;
+    const float Dh = p.D ? p.D[h] : 0.f;   // issued early: used in the epilogue
+    // x of the next head (of this item, or of the next item once known) lands while
+    // this head computes
+    if (!last)
+        dma_head(p, it, h + 1, xs_n, cs_n, dt_n, wave, dmo);
+    else if (hk > 0 && next < nwork) {
+        const Item nit = decode_item(p, next, per_c, nHG, N);
+        dma_head(p, nit, nit.h0, xs_n, cs_n, dt_n, wave, dmo);
+    }
+    // Reserve the next work item now; the result is shared through LDS at this
+    // head's state barrier, late enough that waiting for the atomic costs nothing.
+    int tk_reg = 0;
+    if (hk == 0 && tid == 0) tk_reg = atomicAdd(p.ticket, 1);
+
+    // per-token weights of this head
+    if (tid < kQ) {
+        const float cst = cs[tid], d = dt[tid];
+        vf[tid] = d * exp2f(cs[tid | 15] - cst);
+        w[tid] = d * exp2f(cs[kQ - 1] - cst);
+    }
+    lds_barrier();
+
+    // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
+    f32x4_t y[2][4];
+#pragma unroll
+    for (int k4 = 0; k4 < 2; ++k4)
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
+    diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, gr, r, lg, lane, y[0], y[1]);
+
+    // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
+    f32x4_t sacc[PTW];
+#pragma unroll
+    for (int i = 0; i < PTW; ++i) sacc[i] = zero4();
+    // Opaque to the optimiser, so that it does not hoist the unpacking of B^T out
+    // of the head loop (64 more registers, and a wait for the loads at the start
+    // of every item).
+#pragma unroll
+    for (int m = 0; m < kQ / 32; ++m) asm volatile("" : "+v"(btf[m][0]), "+v"(btf[m][1]));
+    {
+        const char* xsb = reinterpret_cast<const char*>(xs);
+        const float* wl = w + 4 * lg;
+#pragma unroll
+        for (int m = 0; m < kQ / 32; ++m) {
+            const float4 w0 = *reinterpret_cast<const float4*>(wl + 32 * m);
+            const float4 w1 = *reinterpret_cast<const float4*>(wl + 32 * m + 16);
+            const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            const u32 bw[4] = {btf[m][0].x, btf[m][0].y, btf[m][1].x, btf[m][1].y};
+            float bf8[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                bf8[2 * e] = __uint_as_float(bw[e] << 16) * wv[2 * e];
+                bf8[2 * e + 1] = __uint_as_float(bw[e] & 0xFFFF0000u) * wv[2 * e + 1];
+            }
+            const bf16x8_t bop = pack8(bf8);
+#pragma unroll
+            for (int i = 0; i < PTW; ++i) {
+                const char* xb = xsb + xa[pt0 + i] + 4096 * m;
+                const uint2 lo = tr_read(xb), hi = tr_read(xb + 2048);
+                sacc[i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[i]);
+            }
+        }
+    }
+
+
+    // ---- centre factor: state entering the chunk, state leaving it ----------
+    float* ring_h = p.ring + (static_cast<int64_t>(b) * p.H + h) * 2 * PN;
+    const __amdgpu_buffer_rsrc_t ring_rs =
+        __builtin_amdgcn_make_buffer_rsrc(ring_h, 0, static_cast<int>(2 * PN * sizeof(float)), 0x00020000);
+    const int frag_base = wave * PTW * 64 + lane;   // private ring layout: [wave][frag][lane][4]
+    if (has_prev && tid == 0) {
+        const int* flag = p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + (c - 1);
+        long long spins = 0;
+        while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+            __builtin_amdgcn_s_sleep(2);
+            if (++spins > kSpinLimit) {
+                __hip_atomic_store(p.ticket + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+        }
+    }
+    lds_barrier();   // flag seen by tid 0
+    f32x4_t hprev[PTW];
+    if (has_prev) {
+        const int slot = (c + 1) & 1;
+#pragma unroll
+        for (int i = 0; i < PTW; ++i) {
+            const int off = static_cast<int>((slot * PN + (frag_base + i * 64) * 4) * sizeof(float));
+            hprev[i] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ring_rs, off, 0, 16));
+        }
+    } else if (p.init) {
+        // (P, N) layout of the caller's initial state: lane offset + uniform row offsets
+        const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(p.init + (static_cast<int64_t>(b) * p.H + h) * PN), 0,
+            static_cast<int>(PN * sizeof(float)), 0x00020000);
+        const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
+#pragma unroll
+        for (int i = 0; i < PTW; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                hprev[i][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    irs, lo, (16 * i + v) * N * static_cast<int>(sizeof(float)), 0));
+    } else {
+#pragma unroll
+        for (int i = 0; i < PTW; ++i) hprev[i] = zero4();
+    }
+    const float decay = exp2f(cs[kQ - 1]);
+#pragma unroll
+    for (int i = 0; i < PTW; ++i) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            hb[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
+            sacc[i][v] = decay * hprev[i][v] + sacc[i][v];
+        }
+    }
+    if (has_next) {
+        const int slot = c & 1;
+#pragma unroll
+        for (int i = 0; i < PTW; ++i) {
+            const int off = static_cast<int>((slot * PN + (frag_base + i * 64) * 4) * sizeof(float));
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(uint4_t, sacc[i]), ring_rs, off, 0, 16);
+        }
+    } else if (p.fin) {
+        const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
+            p.fin + (static_cast<int64_t>(b) * p.H + h) * PN, 0,
+            static_cast<int>(PN * sizeof(float)), 0x00020000);
+        const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
+#pragma unroll
+        for (int i = 0; i < PTW; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                // extract the element first: bit-casting a vector element in place is
+                // mis-lowered (component 0 stored for every v)
+                const float val = sacc[i][v];
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), frs, lo,
+                                                      (16 * i + v) * N * static_cast<int>(sizeof(float)), 0);
+            }
+    }
+    // The state stores drain while the left factor runs; the flag is set after
+    // the epilogue's barrier, once every wavefront has waited for its stores.
+    if (hk == 0 && tid == 0) *tk = tk_reg;
+    lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
+    if (hk == 0) next = *tk;
+    // The next item's Gram tiles (and, with one head per item, its first head's
+    // x): only the bf16 state and this head's x are read from here on.
+    const bool gram_ahead = last && next < nwork;
+    if (gram_ahead) {
+        const Item nit = decode_item(p, next, per_c, nHG, N);
+        dma_gram(gr, p, nit, wave, dmo);
+        if (hk == 0) dma_head(p, nit, nit.h0, xs_n, cs_n, dt_n, wave, dmo);
+    }
+
+    // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
+    {
+        f32x4_t tq[2][4];
+#pragma unroll
+        for (int k4 = 0; k4 < 2; ++k4)
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) tq[k4][pt] = zero4();
+#pragma unroll
+        for (int k = 0; k < KN; ++k) {
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+                const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&hb[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
+                tq[0][pt] = mfma(aop, cf[0][k], tq[0][pt]);
+                tq[1][pt] = mfma(aop, cf[1][k], tq[1][pt]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int k4 = 0; k4 < 2; ++k4) {
+            const float ev = exp2f(cs[16 * strip[k4] + r]);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) y[k4][pt][v] += ev * tq[k4][pt][v];
+        }
+    }
+
+
+    // ---- skip term; y staged in place over this head's x, then full-row stores
+    {
+        u16* xw = xs;
+#pragma unroll
+        for (int k4 = 0; k4 < 2; ++k4) {
+            const int t = 16 * strip[k4] + r;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+                uint2* cell = reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg));
+                const uint2 xv = *cell;
+                const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
+                                     __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
+                uint2 packed;
+                packed.x = pack_bf16x2(y[k4][pt][0] + Dh * xf[0], y[k4][pt][1] + Dh * xf[1]);
+                packed.y = pack_bf16x2(y[k4][pt][2] + Dh * xf[2], y[k4][pt][3] + Dh * xf[3]);
+                *cell = packed;   // same cell this lane just read: in place is safe
+            }
+        }
+        // state stores complete (and the next head's x has landed); the Gram copies
+        // issued after them (at most 9 per wavefront, at least 8) may stay in flight
+        if (gram_ahead)
+            __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8)
+        else
+            wait_vmem();
+        lds_barrier();
+        if (tid == 0 && has_next)
+            __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
+        constexpr int kPieces = kQ * kP / 8 / kMainThreads;   // 16-byte pieces per thread
+        uint4 v[kPieces];
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) {
+            const int ci = tid + kMainThreads * k;      // piece: token ci/8, group ci%8
+            v[k] = *reinterpret_cast<const uint4*>(xw + xs_off(ci >> 3, 8 * (ci & 7)));
+        }
+        if (gram_ahead) wait_vmem();   // the next item's Gram tiles have landed
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) {
+            const int ci = tid + kMainThreads * k;
+            const int t = ci >> 3, grp = ci & 7;
+            // streaming (non-temporal) stores: y is not read again by this kernel
+            if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
+        }
+    }
+    lds_barrier();   // this head's LDS buffers may be refilled from here on
+}
+
 template <int N>
 __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
 {
@@ -586,21 +866,9 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     const int nHG = static_cast<int>(p.H / p.HG);
     const int per_c = static_cast<int>(p.b) * nHG;
     const int nwork = static_cast<int>(p.nC) * per_c;
-    u16* yp = static_cast<u16*>(p.y);
-    const int64_t PN = static_cast<int64_t>(kP) * N;
-    const unsigned xrow = static_cast<unsigned>(p.H * kP);   // elements per token
-
-    // strips (16-token t-tiles) of this wavefront: balanced causal work (9 K-steps)
-    int strip[2];
-    strip[0] = wave;
-    strip[1] = kNQ - 1 - wave;
-    // state tiles of this wavefront in the right factor: n-tile ntw, p-tiles pt0..pt0+PTW-1
-    const int ntw = (PTW == 4) ? wave : (wave & 3);
-    const int pt0 = (PTW == 4) ? 0 : 2 * (wave >> 2);
     const DmaOffsets dmo = dma_offsets(p, wave, lane);
-    int xa[4];   // byte offsets of this lane's transposing x reads, per p-tile
-#pragma unroll
-    for (int pt = 0; pt < 4; ++pt) xa[pt] = x_tr_base(16 * pt, lane);
+    const int ntw = (PTW == 4) ? wave : (wave & 3);
+    const int strip[2] = {wave, kNQ - 1 - wave};
 
     // Persistent workgroups: work items are taken from a ticket counter in
     // chunk-major order, so an item only ever waits for an item already taken
@@ -613,269 +881,28 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     {
         const Item it = decode_item(p, work, per_c, nHG, N);
         dma_gram(s_gr, p, it, wave, dmo);
-        dma_head(sm, p, it, it.h0, 0, wave, dmo);
+        dma_head(p, it, it.h0, sm.XS[0], sm.cs[0], sm.dt[0], wave, dmo);
     }
     wait_vmem();
     __syncthreads();
 
     int q = 0;   // LDS buffer of the current head
-    bool first_item = true;
     for (;;) {
     const Item it = decode_item(p, work, per_c, nHG, N);
     int next = nwork;
-    // register operands shared by the item's heads (see load_bt / load_c)
+    // register operands shared by the item's heads (see load_bt / load_c); first
+    // needed by the right factor, after the first head's diagonal block
     uint2 btf[kQ / 32][2];
     bf16x8_t cf[2][KN];
+    load_bt<N>(p, it, ntw, r, lg, btf);
+    load_c<N>(p, it, strip, r, lg, cf);
     for (int hk = 0; hk < p.HG; ++hk) {
-        const int h = it.h0 + hk;
-        const bool last = hk + 1 == p.HG;
-        const int b = it.b, c = it.c, L = it.L;
-        const int64_t c0 = it.c0;
-        const bool has_prev = it.has_prev, has_next = it.has_next;
-        const u16* xs = sm.XS[q];
-        const float* cs = sm.cs[q];
-        const float* dt = sm.dt[q];
-        const float Dh = p.D ? p.D[h] : 0.f;   // issued early: used in the epilogue
-        // x of the next head (of this item, or of the next item once known) lands while
-        // this head computes
-        if (!last)
-            dma_head(sm, p, it, h + 1, q ^ 1, wave, dmo);
-        else if (hk > 0 && next < nwork) {
-            const Item nit = decode_item(p, next, per_c, nHG, N);
-            dma_head(sm, p, nit, nit.h0, q ^ 1, wave, dmo);
-        }
-        if (hk == 0 && tid == 0)
-            sm.ticket = atomicAdd(p.ticket, 1);   // reserve the next work item now
-
-        if (hk == 0) {
-            if (!first_item) {
-                // the Gram tiles prefetched during the previous item must have landed
-                // (all but the 4 copies just issued for the next head, when there were any)
-                if (p.HG > 1)
-                    __builtin_amdgcn_s_waitcnt(0x0F74);   // vmcnt(4)
-                else
-                    wait_vmem();
-            }
-            // issued after that wait so that it does not wait for them; first needed
-            // by the right factor, after the diagonal block
-            load_bt<N>(p, it, ntw, r, lg, btf);
-            load_c<N>(p, it, strip, r, lg, cf);
-        }
-
-        // per-token weights of this head
-        if (tid < kQ) {
-            const float cst = cs[tid], d = dt[tid];
-            sm.vf[tid] = d * exp2f(cs[tid | 15] - cst);
-            sm.w[tid] = d * exp2f(cs[kQ - 1] - cst);
-        }
-        lds_barrier();
-        if (hk == 0) {
-            next = sm.ticket;
-            if (last && next < nwork)   // one head per item: its successor's x only now
-            {
-                const Item nit = decode_item(p, next, per_c, nHG, N);
-                dma_head(sm, p, nit, nit.h0, q ^ 1, wave, dmo);
-            }
-        }
-
-        // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
-        f32x4_t y[2][4];
-#pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4)
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
-        diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, sm.vf, dt, s_gr, r, lg, lane, y[0], y[1]);
-
-        // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
-        f32x4_t sacc[PTW];
-#pragma unroll
-        for (int i = 0; i < PTW; ++i) sacc[i] = zero4();
-        {
-            const char* xsb = reinterpret_cast<const char*>(xs);
-            const float* wl = sm.w + 4 * lg;
-#pragma unroll
-            for (int m = 0; m < kQ / 32; ++m) {
-                const float4 w0 = *reinterpret_cast<const float4*>(wl + 32 * m);
-                const float4 w1 = *reinterpret_cast<const float4*>(wl + 32 * m + 16);
-                const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-                const u32 bw[4] = {btf[m][0].x, btf[m][0].y, btf[m][1].x, btf[m][1].y};
-                float bf8[8];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    bf8[2 * e] = __uint_as_float(bw[e] << 16) * wv[2 * e];
-                    bf8[2 * e + 1] = __uint_as_float(bw[e] & 0xFFFF0000u) * wv[2 * e + 1];
-                }
-                const bf16x8_t bop = pack8(bf8);
-#pragma unroll
-                for (int i = 0; i < PTW; ++i) {
-                    const char* xb = xsb + xa[pt0 + i] + 4096 * m;
-                    const uint2 lo = tr_read(xb), hi = tr_read(xb + 2048);
-                    sacc[i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[i]);
-                }
-            }
-        }
-
-
-        // ---- centre factor: state entering the chunk, state leaving it ----------
-        float* ring_h = p.ring + (static_cast<int64_t>(b) * p.H + h) * 2 * PN;
-        const __amdgpu_buffer_rsrc_t ring_rs =
-            __builtin_amdgcn_make_buffer_rsrc(ring_h, 0, static_cast<int>(2 * PN * sizeof(float)), 0x00020000);
-        const int frag_base = wave * PTW * 64 + lane;   // private ring layout: [wave][frag][lane][4]
-        if (has_prev && tid == 0) {
-            const int* flag = p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + (c - 1);
-            long long spins = 0;
-            while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-                __builtin_amdgcn_s_sleep(2);
-                if (++spins > kSpinLimit) {
-                    __hip_atomic_store(p.ticket + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-            }
-        }
-        lds_barrier();   // flag seen by tid 0
-        f32x4_t hprev[PTW];
-        if (has_prev) {
-            const int slot = (c + 1) & 1;
-#pragma unroll
-            for (int i = 0; i < PTW; ++i) {
-                const int off = static_cast<int>((slot * PN + (frag_base + i * 64) * 4) * sizeof(float));
-                hprev[i] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ring_rs, off, 0, 16));
-            }
-        } else if (p.init) {
-            // (P, N) layout of the caller's initial state: lane offset + uniform row offsets
-            const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
-                const_cast<float*>(p.init + (static_cast<int64_t>(b) * p.H + h) * PN), 0,
-                static_cast<int>(PN * sizeof(float)), 0x00020000);
-            const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
-#pragma unroll
-            for (int i = 0; i < PTW; ++i)
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    hprev[i][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                        irs, lo, (16 * i + v) * N * static_cast<int>(sizeof(float)), 0));
-        } else {
-#pragma unroll
-            for (int i = 0; i < PTW; ++i) hprev[i] = zero4();
-        }
-        const float decay = exp2f(cs[kQ - 1]);
-#pragma unroll
-        for (int i = 0; i < PTW; ++i) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                s_hb[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
-                sacc[i][v] = decay * hprev[i][v] + sacc[i][v];
-            }
-        }
-        if (has_next) {
-            const int slot = c & 1;
-#pragma unroll
-            for (int i = 0; i < PTW; ++i) {
-                const int off = static_cast<int>((slot * PN + (frag_base + i * 64) * 4) * sizeof(float));
-                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(uint4_t, sacc[i]), ring_rs, off, 0, 16);
-            }
-        } else if (p.fin) {
-            const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
-                p.fin + (static_cast<int64_t>(b) * p.H + h) * PN, 0,
-                static_cast<int>(PN * sizeof(float)), 0x00020000);
-            const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
-#pragma unroll
-            for (int i = 0; i < PTW; ++i)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    // extract the element first: bit-casting a vector element in place is
-                    // mis-lowered (component 0 stored for every v)
-                    const float val = sacc[i][v];
-                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), frs, lo,
-                                                          (16 * i + v) * N * static_cast<int>(sizeof(float)), 0);
-                }
-        }
-        // The state stores drain while the left factor runs; the flag is set after
-        // the epilogue's barrier, once every wavefront has waited for its stores.
-        lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
-        const bool gram_ahead = last && next < nwork;
-
-        // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
-        {
-            f32x4_t tq[2][4];
-#pragma unroll
-            for (int k4 = 0; k4 < 2; ++k4)
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt) tq[k4][pt] = zero4();
-#pragma unroll
-            for (int k = 0; k < KN; ++k) {
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt) {
-                    const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&s_hb[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
-                    tq[0][pt] = mfma(aop, cf[0][k], tq[0][pt]);
-                    tq[1][pt] = mfma(aop, cf[1][k], tq[1][pt]);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-#pragma unroll
-            for (int k4 = 0; k4 < 2; ++k4) {
-                const float ev = exp2f(cs[16 * strip[k4] + r]);
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) y[k4][pt][v] += ev * tq[k4][pt][v];
-            }
-        }
-
-
-        // ---- skip term; y staged in place over this head's x, then full-row stores
-        {
-            u16* xw = sm.XS[q];
-#pragma unroll
-            for (int k4 = 0; k4 < 2; ++k4) {
-                const int t = 16 * strip[k4] + r;
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt) {
-                    uint2* cell = reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg));
-                    const uint2 xv = *cell;
-                    const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
-                                         __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
-                    uint2 packed;
-                    packed.x = pack_bf16x2(y[k4][pt][0] + Dh * xf[0], y[k4][pt][1] + Dh * xf[1]);
-                    packed.y = pack_bf16x2(y[k4][pt][2] + Dh * xf[2], y[k4][pt][3] + Dh * xf[3]);
-                    *cell = packed;   // same cell this lane just read: in place is safe
-                }
-            }
-            // The next item's Gram tiles (its heads' x arrives head by head), issued
-            // once this head's x cells have been read: only the Gram buffer, a
-            // separate LDS object, is written by these copies.
-            if (gram_ahead) dma_gram(s_gr, p, decode_item(p, next, per_c, nHG, N), wave, dmo);
-            // state stores complete (and the next head's x has landed); the Gram copies
-            // issued after them (at most 9 per wavefront, at least 8) may stay in flight
-            if (gram_ahead)
-                __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8)
-            else
-                wait_vmem();
-            lds_barrier();
-            if (tid == 0 && has_next)
-                __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
-            constexpr int kPieces = kQ * kP / 8 / kMainThreads;   // 16-byte pieces per thread
-            uint4 v[kPieces];
-#pragma unroll
-            for (int k = 0; k < kPieces; ++k) {
-                const int ci = tid + kMainThreads * k;      // piece: token ci/8, group ci%8
-                v[k] = *reinterpret_cast<const uint4*>(xw + xs_off(ci >> 3, 8 * (ci & 7)));
-            }
-#pragma unroll
-            for (int k = 0; k < kPieces; ++k) {
-                const int ci = tid + kMainThreads * k;
-                const int t = ci >> 3, grp = ci & 7;
-                // streaming (non-temporal) stores: y is not read again by this kernel
-                if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
-            }
-        }
-        lds_barrier();   // this head's LDS buffers may be refilled from here on
+        head_step<N>(p, it, hk, next, nwork, per_c, nHG, btf, cf, sm.XS[q], sm.XS[q ^ 1],
+                     sm.cs[q], sm.cs[q ^ 1], sm.dt[q], sm.dt[q ^ 1], sm.vf, sm.w, s_gr, s_hb, &sm.ticket);
         q ^= 1;
     }
     if (next >= nwork) break;
     work = next;
-    first_item = false;
     }
 }
 
