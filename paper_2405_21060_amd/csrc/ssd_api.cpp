@@ -149,8 +149,6 @@ int forward_impl(const ssd_problem* prob, const void* x, const void* dt, const f
         f.y = y;
         f.fin = final_states;
         char* base = static_cast<char*>(workspace);
-        f.cs2 = reinterpret_cast<float*>(base + fw.cs2);
-        f.dtT = reinterpret_cast<float*>(base + fw.dtT);
         f.gram = reinterpret_cast<uint16_t*>(base + fw.gram);
         f.BT = reinterpret_cast<uint16_t*>(base + fw.BT);
         f.ring = reinterpret_cast<float*>(base + fw.ring);

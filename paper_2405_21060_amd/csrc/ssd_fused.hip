@@ -3,29 +3,28 @@
 //
 // Two launches per call.
 //
-// k_fused_prep, one workgroup per (batch, chunk, group):
-//   * step 1 for every head of the group: a = dt*A, chunk-local inclusive
-//     cumsum in log2 units (cs2), written per (batch, head, chunk) together
-//     with dt itself, both as float32 rows of Q (coalesced for the main kernel);
+// k_fused_prep, four workgroups per (batch, chunk, group):
 //   * B^T of the chunk (N x Q, bf16), the operand layout the chunk-state
 //     contraction needs (contraction over tokens);
 //   * the Gram matrix C B^T of the chunk (Section 5, eq. ssm-quad: G = C B^T),
 //     only its causal 16x16 tiles, stored in the exact per-lane accumulator
 //     layout in which the main kernel's wavefronts hold them.
 //
-// k_fused_main, one workgroup (8 wavefronts) per (chunk, batch, group of HG
-// heads), ordered chunk-major through a ticket counter:
-//   * prologue: the chunk's Gram tiles (shared by the HG heads) are copied to
-//     LDS with asynchronous global->LDS loads; per head, x (Q x P, token-major,
-//     swizzled), cs2 and dt land in a double-buffered LDS slot while the
-//     previous head computes, and MFMA operand fragments of x^T are read from
-//     it with transposing LDS reads (ds_read_b64_tr_b16);
+// k_fused_main, persistent workgroups (8 wavefronts, one per compute unit)
+// taking work items (chunk, batch, group of HG heads) from a ticket counter in
+// chunk-major order:
+//   * per item: the chunk's Gram tiles (shared by the HG heads) are copied to
+//     LDS asynchronously, B^T and C fragments loaded into registers; per head,
+//     x (Q x P, token-major, swizzled) lands in a double-buffered LDS slot while
+//     the previous head computes, and MFMA operand fragments of x^T are read
+//     from it with transposing LDS reads (ds_read_b64_tr_b16);
+//   * step 1: a = dt*A and its chunk-local inclusive cumsum in log2 units, one
+//     token per thread, with the per-token weights of the next two steps;
 //   * diagonal block (Section 6.1): Y^T = x^T (L o G)^T dt, the 1-SS mask
 //     applied to the Gram fragments in registers and fed straight back into the
 //     matrix cores (accumulator layout -> operand layout by permuting the
 //     contraction index);
-//   * right factor (Section 6.2): S = sum_s dt_s exp(cs_end - cs_s) x_s B_s^T,
-//     B^T fragments read from L2;
+//   * right factor (Section 6.2): S = sum_s dt_s exp(cs_end - cs_s) x_s B_s^T;
 //   * centre factor (Section 6.2, scalar scan of Appendix B, sequential
 //     chunk-to-chunk state passing): wait for the state entering the chunk,
 //     publish h_c = exp(cs_end) h_{c-1} + S for the next chunk (or write the
@@ -61,7 +60,7 @@ constexpr int kTiles = kNQ * (kNQ + 1) / 2;   // causal 16x16 tiles (s-tile <= t
 constexpr int kP = 64;                        // head dimension
 constexpr int kWaves = 8;
 constexpr int kMainThreads = kWaves * 64;
-constexpr int kPrepThreads = 256;
+constexpr int kPrepThreads = 512;
 constexpr long long kSpinLimit = 1LL << 22;   // polls (with s_sleep) before giving up
 
 typedef unsigned short u16;
@@ -143,23 +142,39 @@ __device__ __forceinline__ int tile_index(int i, int j) { return i * (i + 1) / 2
 // ---------------------------------------------------------------------------
 // prep
 // ---------------------------------------------------------------------------
-constexpr int kPrepParts = 32;  // workgroups per (batch, chunk, group)
 
+constexpr int kGramParts = 4;   // Gram / B^T workgroups per (batch, chunk, group)
+
+// LDS of the prep kernel: the chunk's B rows and the 64 C rows of a part's
+// t-tiles (row stride N + 8 so that the 16 rows an MFMA operand reads start in
+// different banks), or the dt block of the cumsum workgroups.
+template <int N>
+struct PrepSmem {
+    u16 B[kQ * (N + 8)];
+    u16 C[64 * (N + 8)];
+};
+
+// Gram workgroup (chunk c, batch b / group g, part z < 4): B rows (and the C
+// rows it needs) of the chunk into LDS; the causal Gram tiles of t-tile rows
+// {z, 7 - z, 8 + z, 15 - z} on MFMA (34 tiles, two wavefronts per row); a
+// quarter of B^T from LDS; z == 0 also zeroes the flags of (b, c, g) and, once,
+// the ticket counter.
 template <int N>
 __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
 {
+    constexpr int RS = N + 8;
+    __shared__ __attribute__((aligned(16))) PrepSmem<N> sm;
     const int c = blockIdx.x;
     const int b = static_cast<int>(blockIdx.y / p.G), g = static_cast<int>(blockIdx.y % p.G);
     const int part = blockIdx.z;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t c0 = static_cast<int64_t>(c) * kQ;
     const int L = static_cast<int>(kQ < p.T - c0 ? kQ : p.T - c0);
     const int hpg = static_cast<int>(p.H / p.G);
-    const u16* dtp = static_cast<const u16*>(p.dt);
-    const u16* Bp = static_cast<const u16*>(p.B);
-    const u16* Cp = static_cast<const u16*>(p.C);
 
-    // flags of this (batch, chunk) and group, and the ticket counter
+
+    // ---- flags of this (batch, chunk) and group, and the ticket counter
     if (part == 0) {
         for (int hh = tid; hh < hpg; hh += kPrepThreads)
             p.flags[(static_cast<int64_t>(b) * p.H + g * hpg + hh) * p.nC + c] = 0;
@@ -168,83 +183,62 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
             p.ticket[1] = 0;  // error word: set when a state wait times out
         }
     }
+    // t-tile rows of this part (balanced: 34 tiles)
+    const int rows[4] = {part, 7 - part, 8 + part, kNQ - 1 - part};
 
-    // Rows past a partial chunk's end are read clamped to the last row (every load
-    // is unconditional, so they all stay in flight together) and then zeroed.
-
-    // step 1 for the heads of this part: one wavefront per head, 4 tokens per lane
-    for (int hh = part * 4 + wave; hh < hpg; hh += kPrepParts * 4) {
-        const int h = g * hpg + hh;
-        const float A2 = -expf(p.A_log[h]) * kLog2e;
-        float d[4], a[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int t = 4 * lane + k;
-            const int tc = t < L ? t : L - 1;
-            const float v = bf(dtp[(b * p.T + c0 + tc) * p.H + h]);
-            d[k] = (t < L) ? v : 0.f;
-            a[k] = d[k] * A2;
-        }
-        a[1] += a[0];
-        a[2] += a[1];
-        a[3] += a[2];
-        float incl = a[3];
-#pragma unroll
-        for (int s = 1; s < 64; s <<= 1) {
-            const float o = __shfl_up(incl, s, 64);
-            if (lane >= s) incl += o;
-        }
-        const float excl = incl - a[3];
-        const int64_t row = ((static_cast<int64_t>(b) * p.H + h) * p.nC + c) * kQ + 4 * lane;
-        *reinterpret_cast<float4*>(p.cs2 + row) = make_float4(a[0] + excl, a[1] + excl, a[2] + excl, a[3] + excl);
-        *reinterpret_cast<float4*>(p.dtT + row) = make_float4(d[0], d[1], d[2], d[3]);
-    }
-
-    // B^T of the chunk, rows n of this part: lanes walk n (coalesced row reads of B)
-    const u16* Bchunk = Bp + ((b * p.T + c0) * p.G + g) * N;
+    // ---- B rows of the chunk and C rows of this part's t-tiles into LDS (rows
+    // past a partial chunk: zeros).  C row tile rows[k] lands at LDS row 16 k.
+    const u16* Bchunk = static_cast<const u16*>(p.B) + ((b * p.T + c0) * p.G + g) * N;
+    const u16* Cchunk = static_cast<const u16*>(p.C) + ((b * p.T + c0) * p.G + g) * N;
     const int64_t brow = p.G * N;
-    u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
-    constexpr int kBtItems = N * (kQ / 8) / kPrepParts;
-    for (int idx = tid; idx < kBtItems; idx += kPrepThreads) {
-        const int gi = part * kBtItems + idx;
-        const int n = gi % N, so = gi / N;
-        u16 raw[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int s = 8 * so + e;
-            raw[e] = Bchunk[(s < L ? s : L - 1) * brow + n];
-        }
-        U16x8 v;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v.v[e] = (8 * so + e < L) ? raw[e] : static_cast<u16>(0);
-        *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
+    for (int i = tid; i < kQ * N / 8; i += kPrepThreads) {
+        const int s = i / (N / 8), col = 8 * (i % (N / 8));
+        uint4 vb = *reinterpret_cast<const uint4*>(Bchunk + (s < L ? s : L - 1) * brow + col);
+        if (s >= L) vb = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&sm.B[s * RS + col]) = vb;
     }
+    for (int i = tid; i < 64 * N / 8; i += kPrepThreads) {
+        const int lr = i / (N / 8), col = 8 * (i % (N / 8));
+        const int t = 16 * rows[lr >> 4] + (lr & 15);
+        uint4 vc = *reinterpret_cast<const uint4*>(Cchunk + (t < L ? t : L - 1) * brow + col);
+        if (t >= L) vc = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&sm.C[lr * RS + col]) = vc;
+    }
+    __syncthreads();
 
-    // Gram tiles G^T[s][t] = sum_n B_s[n] C_t[n] (bf16), accumulator layout per lane
-    const u16* Cchunk = Cp + ((b * p.T + c0) * p.G + g) * N;
+    // ---- Gram tiles G^T[s][t] = sum_n B_s[n] C_t[n] (bf16), accumulator layout per lane.
+    // Wavefront w: row rows[w / 2], s-tiles j = w%2, w%2 + 2, ...
     u16* gram = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
-    for (int ti = part * 4 + wave; ti < kTiles; ti += kPrepParts * 4) {
-        int i = 0;
-        while ((i + 1) * (i + 2) / 2 <= ti) ++i;
-        const int j = ti - i * (i + 1) / 2;
-        const int s = 16 * j + r, t = 16 * i + r;
-        const u16* bs = Bchunk + (s < L ? s : L - 1) * brow + 8 * lg;
-        const u16* ct = Cchunk + (t < L ? t : L - 1) * brow + 8 * lg;
-        uint4 va[N / 32], vb[N / 32];
-#pragma unroll
-        for (int k = 0; k < N / 32; ++k) {
-            va[k] = *reinterpret_cast<const uint4*>(bs + 32 * k);
-            vb[k] = *reinterpret_cast<const uint4*>(ct + 32 * k);
-        }
-        const uint4 z = make_uint4(0, 0, 0, 0);
-        f32x4_t acc = zero4();
+    {
+        const int i = rows[wave >> 1];
+        uint4 cfr[N / 32];
 #pragma unroll
         for (int k = 0; k < N / 32; ++k)
-            acc = mfma(as_bf16x8(s < L ? va[k] : z), as_bf16x8(t < L ? vb[k] : z), acc);
-        uint2 packed;
-        packed.x = pack_bf16x2(acc[0], acc[1]);
-        packed.y = pack_bf16x2(acc[2], acc[3]);
-        *reinterpret_cast<uint2*>(gram + (static_cast<int64_t>(ti) * 64 + lane) * 4) = packed;
+            cfr[k] = *reinterpret_cast<const uint4*>(&sm.C[(16 * (wave >> 1) + r) * RS + 32 * k + 8 * lg]);
+#pragma unroll 1
+        for (int j = wave & 1; j <= i; j += 2) {
+            f32x4_t acc = zero4();
+#pragma unroll
+            for (int k = 0; k < N / 32; ++k) {
+                const uint4 va = *reinterpret_cast<const uint4*>(&sm.B[(16 * j + r) * RS + 32 * k + 8 * lg]);
+                acc = mfma(as_bf16x8(va), as_bf16x8(cfr[k]), acc);
+            }
+            uint2 packed;
+            packed.x = pack_bf16x2(acc[0], acc[1]);
+            packed.y = pack_bf16x2(acc[2], acc[3]);
+            *reinterpret_cast<uint2*>(gram + (static_cast<int64_t>(tile_index(i, j)) * 64 + lane) * 4) = packed;
+        }
+    }
+
+    // ---- this part's quarter of B^T from LDS: item (n, 8 tokens), 16-byte stores along s
+    u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
+    constexpr int kBtItems = N * (kQ / 8) / kGramParts;
+    for (int i = part * kBtItems + tid; i < (part + 1) * kBtItems; i += kPrepThreads) {
+        const int n = i % N, so = i / N;
+        U16x8 v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v.v[e] = sm.B[(8 * so + e) * RS + n];
+        *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
     }
 }
 
@@ -276,10 +270,11 @@ __device__ __forceinline__ uint2 xfrag(const u16* xs, int k0, int f0, int lane)
 template <int N>
 struct MainSmem {
     u16 XS[2][kQ * kP];       // x of the current / next head (token-major, swizzled)
-    float cs[2][kQ];          // cs2 of the current / next head
+    float cs[2][kQ];          // chunk-local cumsum of dt A (log2 units) of the current / next head
     float dt[2][kQ];
-    float vf[kQ];             // dt_s exp2(cs2[tile end] - cs2_s)
-    float w[kQ];              // dt_s exp2(cs2[Q-1] - cs2_s)
+    float wtot[4];            // per-wavefront totals of the cumsum
+    float vf[kQ];             // dt_s exp2(cs[tile end] - cs_s)
+    float w[kQ];              // dt_s exp2(cs[Q-1] - cs_s)
     int ticket;
 };
 
@@ -517,22 +512,25 @@ __device__ __forceinline__ DmaOffsets dma_offsets(const FusedParams& p, int wave
     return o;
 }
 
-// Copies of head hh of an item into the LDS buffers xdst / csdst / dtdst: x as
-// 4 blocks of 8 tokens per wavefront (lane l of a block fetches the 16 bytes
-// that land at block + 16 l), and the head's cs2 / dt rows.  The x descriptor
-// ends at the end of the batch row, so rows past a partial last chunk read as
-// zeros (such tokens have dt = 0 and zero Gram rows and columns, and are never
-// stored).
-__device__ __forceinline__ void dma_head(const FusedParams& p, const Item& it, int hh, u16* xdst, float* csdst,
-                                         float* dtdst, int wave, const DmaOffsets& o)
+// Copy of head hh's x (an item's chunk) into the LDS buffer xdst: 4 blocks of
+// 8 tokens per wavefront (lane l of a block fetches the 16 bytes that land at
+// block + 16 l).  The descriptor ends at the end of the batch row, so rows
+// past a partial last chunk read as zeros (such tokens have dt = 0 and zero
+// Gram rows and columns, and are never stored).
+__device__ __forceinline__ void dma_head(const FusedParams& p, const Item& it, int hh, u16* xdst, int wave,
+                                         const DmaOffsets& o)
 {
     const i32x4 xrs = buffer_rsrc(it.xchunk, (p.T - it.c0) * p.H * kP * 2);
     const int hoff = hh * kP * 2;
 #pragma unroll
     for (int i = 0; i < 4; ++i) copy16_to_lds(xrs, xdst + (4 * wave + i) * 512, o.x[i], hoff);
-    const int64_t row = ((static_cast<int64_t>(it.b) * p.H + hh) * p.nC + it.c) * kQ;
-    if (wave == 0) copy16_to_lds(buffer_rsrc(p.cs2 + row, kQ * 4), csdst, o.l16, 0);
-    if (wave == 1) copy16_to_lds(buffer_rsrc(p.dtT + row, kQ * 4), dtdst, o.l16, 0);
+}
+
+// dt of token `tid` (clamped to the chunk) of head hh of an item, raw bf16.
+__device__ __forceinline__ u16 load_dt(const FusedParams& p, const Item& it, int hh, int tid)
+{
+    const int t = tid < it.L ? tid : it.L - 1;
+    return static_cast<const u16*>(p.dt)[(it.b * p.T + it.c0 + t) * p.H + hh];
 }
 
 // The chunk's causal Gram tiles (shared by the item's heads) into LDS.
@@ -586,11 +584,11 @@ template <int N>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
                                           uint2 (&btf)[kQ / 32][2], bf16x8_t (&cf)[2][N / 32],
-                                          u16* __restrict__ xs, u16* __restrict__ xs_n,
-                                          float* __restrict__ cs, float* __restrict__ cs_n,
-                                          float* __restrict__ dt, float* __restrict__ dt_n,
-                                          float* __restrict__ vf, float* __restrict__ w,
-                                          u16* __restrict__ gr, u16* __restrict__ hb, int* __restrict__ tk)
+                                          u16& dtr, u16* __restrict__ xs, u16* __restrict__ xs_n,
+                                          float* __restrict__ cs, float* __restrict__ dt,
+                                          float* __restrict__ wt, float* __restrict__ vf, float* __restrict__ w,
+                                          u16* __restrict__ gr, u16* __restrict__ hb, int* __restrict__ tk,
+                                          const float* __restrict__ A_logp, const float* __restrict__ Dp)
 {
     constexpr int NT = N / 16;
     constexpr int PTW = 4 * NT / kWaves;
@@ -617,25 +615,48 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     const int b = it.b, c = it.c, L = it.L;
     const int64_t c0 = it.c0;
     const bool has_prev = it.has_prev, has_next = it.has_next;
-    const float Dh = p.D ? p.D[h] : 0.f;   // issued early: used in the epilogue
-    // x of the next head (of this item, or of the next item once known) lands while
-    // this head computes
-    if (!last)
-        dma_head(p, it, h + 1, xs_n, cs_n, dt_n, wave, dmo);
-    else if (hk > 0 && next < nwork) {
+    const float Dh = Dp ? Dp[h] : 0.f;   // scalar loads (read-only kernel arguments)
+    // x (and this thread's dt) of the next head -- of this item, or of the next
+    // item once known -- arrive while this head computes
+    u16 dtr_next = 0;
+    if (!last) {
+        dma_head(p, it, h + 1, xs_n, wave, dmo);
+        if (tid < kQ) dtr_next = load_dt(p, it, h + 1, tid);
+    } else if (hk > 0 && next < nwork) {
         const Item nit = decode_item(p, next, per_c, nHG, N);
-        dma_head(p, nit, nit.h0, xs_n, cs_n, dt_n, wave, dmo);
+        dma_head(p, nit, nit.h0, xs_n, wave, dmo);
+        if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
     }
-    // Reserve the next work item now; the result is shared through LDS at this
-    // head's state barrier, late enough that waiting for the atomic costs nothing.
-    int tk_reg = 0;
-    if (hk == 0 && tid == 0) tk_reg = atomicAdd(p.ticket, 1);
 
-    // per-token weights of this head
+    // ---- step 1: chunk-local inclusive cumsum of a = dt A (log2 units), one token
+    // per thread (wavefront scans, then the wavefront totals through LDS), and the
+    // per-token weights of the diagonal block and the right factor
+    float d = 0.f, incl = 0.f;
     if (tid < kQ) {
-        const float cst = cs[tid], d = dt[tid];
-        vf[tid] = d * exp2f(cs[tid | 15] - cst);
-        w[tid] = d * exp2f(cs[kQ - 1] - cst);
+        d = tid < L ? bf(dtr) : 0.f;
+        incl = d * (-expf(A_logp[h]) * kLog2e);
+#pragma unroll
+        for (int sh = 1; sh < 64; sh <<= 1) {
+            const float o = __shfl_up(incl, sh, 64);
+            if (lane >= sh) incl += o;
+        }
+        if (lane == 63) wt[wave] = incl;
+    }
+    lds_barrier();
+    if (tid < kQ) {
+        float pre = 0.f, tot = 0.f;
+#pragma unroll
+        for (int k = 0; k < kQ / 64; ++k) {
+            const float v = wt[k];
+            tot += v;
+            if (k < wave) pre += v;
+        }
+        const float cst = incl + pre;
+        const float cend = __shfl(cst, lane | 15, 64);   // end of this token's 16-token tile
+        cs[tid] = cst;
+        dt[tid] = d;
+        vf[tid] = d * exp2f(cend - cst);
+        w[tid] = d * exp2f(tot - cst);
     }
     lds_barrier();
 
@@ -687,6 +708,10 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     const __amdgpu_buffer_rsrc_t ring_rs =
         __builtin_amdgcn_make_buffer_rsrc(ring_h, 0, static_cast<int>(2 * PN * sizeof(float)), 0x00020000);
     const int frag_base = wave * PTW * 64 + lane;   // private ring layout: [wave][frag][lane][4]
+    // The first head reserves the next work item here: the wait for the atomic's
+    // result merges with the state wait below, and the result is shared through
+    // LDS at the state barrier.
+    if (hk == 0 && tid == 0) *tk = atomicAdd(p.ticket, 1);
     if (has_prev && tid == 0) {
         const int* flag = p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + (c - 1);
         long long spins = 0;
@@ -757,7 +782,6 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
     // The state stores drain while the left factor runs; the flag is set after
     // the epilogue's barrier, once every wavefront has waited for its stores.
-    if (hk == 0 && tid == 0) *tk = tk_reg;
     lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
     if (hk == 0) next = *tk;
     // The next item's Gram tiles (and, with one head per item, its first head's
@@ -766,7 +790,10 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     if (gram_ahead) {
         const Item nit = decode_item(p, next, per_c, nHG, N);
         dma_gram(gr, p, nit, wave, dmo);
-        if (hk == 0) dma_head(p, nit, nit.h0, xs_n, cs_n, dt_n, wave, dmo);
+        if (hk == 0) {   // one head per item: its successor's x and dt only now
+            dma_head(p, nit, nit.h0, xs_n, wave, dmo);
+            if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
+        }
     }
 
     // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
@@ -843,10 +870,14 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         }
     }
     lds_barrier();   // this head's LDS buffers may be refilled from here on
+    dtr = dtr_next;  // here, where the load has long completed (the epilogue waited for it)
 }
 
+// A_log and D come as separate read-only arguments so that their per-head values
+// are scalar loads (a vector load would wait behind the outstanding copies).
 template <int N>
-__global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
+__global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, const float* __restrict__ A_logp,
+                                                                const float* __restrict__ Dp)
 {
     constexpr int NT = N / 16;            // n-tiles of the state
     constexpr int PTW = 4 * NT / kWaves;  // p-tiles per wavefront in the right factor (one n-tile each)
@@ -874,6 +905,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     // chunk-major order, so an item only ever waits for an item already taken
     // by a running (or finished) workgroup.  The operands of the next item are
     // prefetched during the last head of the current one.
+    u16 dtr = 0;    // this thread's dt of the current head (token tid), raw bf16
     if (tid == 0) sm.ticket = atomicAdd(p.ticket, 1);
     __syncthreads();
     int work = sm.ticket;
@@ -881,12 +913,13 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     {
         const Item it = decode_item(p, work, per_c, nHG, N);
         dma_gram(s_gr, p, it, wave, dmo);
-        dma_head(p, it, it.h0, sm.XS[0], sm.cs[0], sm.dt[0], wave, dmo);
+        dma_head(p, it, it.h0, sm.XS[0], wave, dmo);
+        if (tid < kQ) dtr = load_dt(p, it, it.h0, tid);
     }
     wait_vmem();
     __syncthreads();
 
-    int q = 0;   // LDS buffer of the current head
+    int q = 0;      // LDS buffer of the current head
     for (;;) {
     const Item it = decode_item(p, work, per_c, nHG, N);
     int next = nwork;
@@ -897,8 +930,8 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
     load_bt<N>(p, it, ntw, r, lg, btf);
     load_c<N>(p, it, strip, r, lg, cf);
     for (int hk = 0; hk < p.HG; ++hk) {
-        head_step<N>(p, it, hk, next, nwork, per_c, nHG, btf, cf, sm.XS[q], sm.XS[q ^ 1],
-                     sm.cs[q], sm.cs[q ^ 1], sm.dt[q], sm.dt[q ^ 1], sm.vf, sm.w, s_gr, s_hb, &sm.ticket);
+        head_step<N>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
+                     sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp);
         q ^= 1;
     }
     if (next >= nwork) break;
@@ -909,7 +942,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p)
 template <int N>
 hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
-    const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), kPrepParts);
+    const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), kGramParts);
     hipLaunchKernelGGL(k_fused_prep<N>, g_prep, dim3(kPrepThreads), 0, stream, p);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess && ev_begin) err = hipEventRecord(ev_begin, stream);
@@ -926,7 +959,8 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
         const long v = std::strtol(cap, nullptr, 10);
         if (v >= 1 && v < grid) grid = v;
     }
-    hipLaunchKernelGGL(k_fused_main<N>, dim3(static_cast<unsigned>(grid)), dim3(kMainThreads), 0, stream, p);
+    hipLaunchKernelGGL(k_fused_main<N>, dim3(static_cast<unsigned>(grid)), dim3(kMainThreads), 0, stream, p,
+                       p.A_log, p.D);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;
@@ -944,10 +978,6 @@ FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC)
     auto al = [](size_t v) { return (v + 255) / 256 * 256; };
     FusedLayout w;
     size_t off = 0;
-    w.cs2 = off;
-    off = al(off + sizeof(float) * static_cast<size_t>(b * H * nC * kQ));
-    w.dtT = off;
-    off = al(off + sizeof(float) * static_cast<size_t>(b * H * nC * kQ));
     w.gram = off;
     off = al(off + sizeof(u16) * static_cast<size_t>(b * G * nC) * kTiles * 256);
     w.BT = off;

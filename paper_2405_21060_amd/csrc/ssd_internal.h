@@ -55,8 +55,6 @@ struct FusedParams {
     void* y;
     float* fin;
     // workspace
-    float* cs2;       // (b, H, nC, Q)   chunk-local cumsum of dt*A, log2 units
-    float* dtT;       // (b, H, nC, Q)   dt, head-major
     uint16_t* gram;   // (b, G, nC, tiles, 64 lanes, 4) causal Gram tiles, bf16, per-lane layout
     uint16_t* BT;     // (b, G, nC, N, Q) B^T per chunk, bf16
     float* ring;      // (b, H, 2, P, N) chunk-state ring
@@ -65,7 +63,7 @@ struct FusedParams {
 };
 
 struct FusedLayout {
-    size_t cs2, dtT, gram, BT, ring, flags, ticket, total;
+    size_t gram, BT, ring, flags, ticket, total;
 };
 
 int64_t heads_per_workgroup(int64_t heads_per_group);
