@@ -191,18 +191,35 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
     const u16* Bchunk = static_cast<const u16*>(p.B) + ((b * p.T + c0) * p.G + g) * N;
     const u16* Cchunk = static_cast<const u16*>(p.C) + ((b * p.T + c0) * p.G + g) * N;
     const int64_t brow = p.G * N;
-    for (int i = tid; i < kQ * N / 8; i += kPrepThreads) {
+    // all loads are issued before any LDS store, so that they are in flight together
+    constexpr int kBPer = kQ * N / 8 / kPrepThreads, kCPer = 64 * N / 8 / kPrepThreads;
+    static_assert(kBPer * kPrepThreads == kQ * N / 8 && kCPer * kPrepThreads == 64 * N / 8, "even split");
+    uint4 vb[kBPer], vc[kCPer];
+#pragma unroll
+    for (int k = 0; k < kBPer; ++k) {
+        const int i = tid + kPrepThreads * k;
         const int s = i / (N / 8), col = 8 * (i % (N / 8));
-        uint4 vb = *reinterpret_cast<const uint4*>(Bchunk + (s < L ? s : L - 1) * brow + col);
-        if (s >= L) vb = make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(&sm.B[s * RS + col]) = vb;
+        vb[k] = *reinterpret_cast<const uint4*>(Bchunk + (s < L ? s : L - 1) * brow + col);
     }
-    for (int i = tid; i < 64 * N / 8; i += kPrepThreads) {
+#pragma unroll
+    for (int k = 0; k < kCPer; ++k) {
+        const int i = tid + kPrepThreads * k;
         const int lr = i / (N / 8), col = 8 * (i % (N / 8));
         const int t = 16 * rows[lr >> 4] + (lr & 15);
-        uint4 vc = *reinterpret_cast<const uint4*>(Cchunk + (t < L ? t : L - 1) * brow + col);
-        if (t >= L) vc = make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(&sm.C[lr * RS + col]) = vc;
+        vc[k] = *reinterpret_cast<const uint4*>(Cchunk + (t < L ? t : L - 1) * brow + col);
+    }
+#pragma unroll
+    for (int k = 0; k < kBPer; ++k) {
+        const int i = tid + kPrepThreads * k;
+        const int s = i / (N / 8), col = 8 * (i % (N / 8));
+        *reinterpret_cast<uint4*>(&sm.B[s * RS + col]) = (s < L) ? vb[k] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kCPer; ++k) {
+        const int i = tid + kPrepThreads * k;
+        const int lr = i / (N / 8), col = 8 * (i % (N / 8));
+        const int t = 16 * rows[lr >> 4] + (lr & 15);
+        *reinterpret_cast<uint4*>(&sm.C[lr * RS + col]) = (t < L) ? vc[k] : make_uint4(0, 0, 0, 0);
     }
     __syncthreads();
 
