@@ -107,6 +107,61 @@ def cpu_baseline(inp, budget_s=20.0):
                       % (p.batch * p.seqlen, len(heads), p.nheads, el)}
 
 
+def decode_bench(args, torch, ssd):
+    """Decode step of the 2.7B-layer shape (H80 P64 N128 G1, bf16) at batch
+    --decode-batch: one step = one token for every sequence, state updated in
+    place.  Bound by HBM: the state is read and written every step (at batch
+    256 it is 671 MB, beyond the 256 MB last-level cache)."""
+    import numpy as np
+
+    b, H, P, N, G = args.decode_batch, 80, 64, 128, 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = torch.Generator(device="cpu").manual_seed(args.seed)
+    x = torch.randn((b, H, P), generator=g).to(torch.bfloat16).to(dev)
+    dt = (torch.rand((b, H), generator=g) * 0.1 + 1e-3).to(torch.bfloat16).to(dev)
+    A_log = (torch.rand((H,), generator=g) * np.log(16.0)).to(dev)
+    B = (torch.randn((b, G, N), generator=g) / np.sqrt(N)).to(torch.bfloat16).to(dev)
+    C = (torch.randn((b, G, N), generator=g) / np.sqrt(N)).to(torch.bfloat16).to(dev)
+    D = torch.randn((H,), generator=g).to(dev)
+    state = torch.randn((b, H, P, N), generator=g).to(dev)
+    y = torch.empty_like(x)
+    stream = torch.cuda.current_stream(dev)
+    prob = ssd.make_problem(b, 1, H, P, N, G, 256, ssd.SSD_DTYPE_BF16, 0)
+    ptr = lambda t: t.data_ptr()
+
+    def step():
+        rc = ssd.ssd_decode_step(prob, ptr(x), ptr(dt), ptr(A_log), ptr(B), ptr(C), ptr(D), ptr(state),
+                                 ptr(y), stream.cuda_stream)
+        if rc != 0:
+            raise ssd.SsdError(rc, "ssd_decode_step")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    sec = ms * 1e-3
+    state_bytes = b * H * P * N * 4
+    byts = 2 * state_bytes + 2 * (2 * b * H * P + b * H + 2 * b * G * N) + 8 * H
+    print(json.dumps({
+        "metric": "SSD decode step tokens/s (2.7B-layer shape, 1 GPU)",
+        "value": b / sec, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "decode_2p7b", "batch": b, "nheads": H, "headdim": P, "dstate": N,
+                   "ngroups": G},
+        "roofline": {"bound": "hbm", "achieved": byts / sec / 1e9, "peak": PEAK_HBM_BPS / 1e9,
+                     "unit": "GB/s", "frac": byts / sec / PEAK_HBM_BPS, "traffic": None,
+                     "kernel": "k_decode_step", "algorithmic_bytes": byts},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -118,6 +173,9 @@ def main():
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="time whole calls only (no events around the dominant kernel)")
+    ap.add_argument("--decode", action="store_true",
+                    help="time the decode step instead (one token per sequence, batch --decode-batch)")
+    ap.add_argument("--decode-batch", type=int, default=256)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -150,6 +208,9 @@ def main():
     from paper_2405_21060_amd import ssd
     from paper_2405_21060_amd.inputs import WORKLOADS, make_inputs
     from tests.ssd_harness import to_device
+
+    if args.decode:
+        return decode_bench(args, torch, ssd)
 
     p = WORKLOADS[args.workload]
     inp = make_inputs(p, args.seed)

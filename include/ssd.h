@@ -117,6 +117,27 @@ int ssd_forward_timed(const ssd_problem* prob,
                       void* workspace, size_t workspace_bytes, void* stream,
                       void* event_begin, void* event_end);
 
+/* One decode step (one new token per sequence) of the same layer, in the
+ * recurrent form of eq. s6 with scalar A (the per-token inference cost of
+ * Section 6.3): per batch row and head h (group g = h / (H/G)),
+ *     S <- exp(dt A_h) S + (dt x) B^T,    y = S C + D_h x.
+ * `prob` gives batch, nheads, headdim, dstate, ngroups and dtype (seqlen,
+ * chunk_size and nseq are ignored; the limits on headdim and dstate are those
+ * of ssd_forward).  Layouts (row-major, contiguous):
+ *   x, y    (batch, nheads, headdim)            dtype
+ *   dt      (batch, nheads)                     dtype, already positive
+ *   A_log   (nheads) float32;  D (nheads) float32, may be NULL (= 0)
+ *   B, C    (batch, ngroups, dstate)            dtype
+ *   state   (batch, nheads, headdim, dstate)    float32, read and updated in
+ *           place, 16-byte aligned (else SSD_ERR_UNSUPPORTED_DIMS)
+ * A state carried through a sequence of decode steps equals the final state
+ * of ssd_forward over the same tokens.  Asynchronous on `stream`; needs no
+ * workspace; errors as for ssd_forward. */
+int ssd_decode_step(const ssd_problem* prob,
+                    const void* x, const void* dt, const float* A_log,
+                    const void* B, const void* C, const float* D,
+                    float* state, void* y, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);
 

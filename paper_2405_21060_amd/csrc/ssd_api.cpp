@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
 #include <cstdlib>
 
 #include "ssd_internal.h"
@@ -63,6 +64,8 @@ int validate(const ssd_problem* prob, bool has_seq_idx, Shape* s)
 }
 
 }  // namespace
+
+constexpr int64_t kMaxElemsPublic = kMaxElems;
 
 // Heads per workgroup of the fused path: a divisor of the heads per group
 // (a workgroup's heads share B and C).  SSD_HEADS_PER_WG overrides the default
@@ -212,6 +215,41 @@ extern "C" int ssd_forward_timed(const ssd_problem* prob, const void* x, const v
     return forward_impl(prob, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
                         workspace, workspace_bytes, stream, static_cast<hipEvent_t>(event_begin),
                         static_cast<hipEvent_t>(event_end));
+}
+
+extern "C" int ssd_decode_step(const ssd_problem* prob, const void* x, const void* dt,
+                               const float* A_log, const void* B, const void* C, const float* D,
+                               float* state, void* y, void* stream)
+{
+    if (!prob) return SSD_ERR_NULL_ARG;
+    if (prob->dtype != SSD_DTYPE_F32 && prob->dtype != SSD_DTYPE_BF16) return SSD_ERR_BAD_DTYPE;
+    if (prob->batch < 1 || prob->nheads < 1 || prob->headdim < 1 || prob->dstate < 1 ||
+        prob->ngroups < 1 || prob->nheads % prob->ngroups != 0)
+        return SSD_ERR_BAD_SHAPE;
+    if (prob->headdim % 16 != 0 || prob->headdim > 128 || prob->dstate % 16 != 0 ||
+        prob->dstate > 256 || reinterpret_cast<uintptr_t>(state) % 16 != 0)
+        return SSD_ERR_UNSUPPORTED_DIMS;
+    if (!x || !dt || !A_log || !B || !C || !state || !y) return SSD_ERR_NULL_ARG;
+    if (prob->batch > 65535 || prob->nheads > 65535 ||
+        static_cast<double>(prob->batch) * prob->nheads * prob->headdim * prob->dstate > 16.0 * ssd::kMaxElemsPublic)
+        return SSD_ERR_TOO_LARGE;
+    ssd::DecodeParams p;
+    p.b = prob->batch;
+    p.H = prob->nheads;
+    p.P = prob->headdim;
+    p.N = prob->dstate;
+    p.G = prob->ngroups;
+    p.x = x;
+    p.dt = dt;
+    p.A_log = A_log;
+    p.B = B;
+    p.C = C;
+    p.D = D;
+    p.state = state;
+    p.y = y;
+    const hipError_t err =
+        ssd::launch_decode(p, prob->dtype == SSD_DTYPE_BF16, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
 extern "C" const char* ssd_error_string(int code)

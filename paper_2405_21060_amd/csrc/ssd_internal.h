@@ -72,4 +72,19 @@ FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC)
 hipError_t launch_fused(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin,
                         hipEvent_t ev_end);
 
+// Decode step (one token per sequence, state updated in place).
+struct DecodeParams {
+    int64_t b, H, P, N, G;
+    const void* x;      // (b, H, P)
+    const void* dt;     // (b, H)
+    const float* A_log;
+    const void* B;      // (b, G, N)
+    const void* C;      // (b, G, N)
+    const float* D;     // (H) or null
+    float* state;       // (b, H, P, N)
+    void* y;            // (b, H, P)
+};
+
+hipError_t launch_decode(const DecodeParams& p, bool bf16, hipStream_t stream);
+
 }  // namespace ssd

@@ -32,7 +32,8 @@ SSD_ERR_WORKSPACE = -7
 SSD_ERR_LAUNCH = -8
 SSD_ERR_TOO_LARGE = -9
 
-EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_error_string")
+EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
+            "ssd_error_string")
 
 
 class SsdProblem(ctypes.Structure):
@@ -75,6 +76,8 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_forward.argtypes = [ctypes.POINTER(SsdProblem)] + [vp] * 10 + [vp, ctypes.c_size_t, vp]
     lib.ssd_forward_timed.restype = ctypes.c_int
     lib.ssd_forward_timed.argtypes = lib.ssd_forward.argtypes + [vp, vp]
+    lib.ssd_decode_step.restype = ctypes.c_int
+    lib.ssd_decode_step.argtypes = [ctypes.POINTER(SsdProblem)] + [vp] * 9
     lib.ssd_error_string.restype = ctypes.c_char_p
     lib.ssd_error_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -174,3 +177,47 @@ def forward(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=No
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_forward")
     return y, fin
+
+
+def ssd_decode_step(prob: SsdProblem, x, dt, A_log, B, C, D, state, y, stream) -> int:
+    """Raw ABI call on integer device addresses (0 = NULL); returns the status."""
+    return load_library().ssd_decode_step(
+        ctypes.byref(prob), x, dt, A_log, B, C, D or None, state, y, stream or None)
+
+
+def decode_step(x, dt, A_log, B, C, state, D=None, out=None):
+    """One decode step on device tensors: updates ``state`` in place, returns y.
+
+    x (b,H,P), dt (b,H), B/C (b,G,N): float32 or bfloat16, the same dtype,
+    contiguous, on one HIP device.  A_log, D (H): float32.  state (b,H,P,N)
+    float32.  Launches on torch's current stream of x's device.
+    """
+    import torch
+
+    dev = x.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    if x.dtype == torch.bfloat16:
+        dtype = SSD_DTYPE_BF16
+    elif x.dtype == torch.float32:
+        dtype = SSD_DTYPE_F32
+    else:
+        raise TypeError("x must be float32 or bfloat16")
+    for name, t in (("dt", dt), ("B", B), ("C", C)):
+        if t.dtype != x.dtype:
+            raise TypeError("%s must have x's dtype" % name)
+    for name, t in (("A_log", A_log), ("D", D), ("state", state)):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("%s must be float32" % name)
+    for t in (x, dt, A_log, B, C, D, state):
+        if t is not None and (t.device != dev or not t.is_contiguous()):
+            raise ValueError("all tensors must be contiguous and on x's device")
+    b, H, P = x.shape
+    G, N = B.shape[1], B.shape[2]
+    prob = make_problem(b, 1, H, P, N, G, 256, dtype, 0)
+    y = out if out is not None else torch.empty_like(x)
+    rc = ssd_decode_step(prob, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),
+                         _ptr(state), _ptr(y), torch.cuda.current_stream(dev).cuda_stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_decode_step")
+    return y

@@ -106,6 +106,21 @@ def test_timed_entry_validates_like_forward(lib):
     assert timed(prob(batch=2, nseq=3), seq_idx=FAKE) == ssd.SSD_ERR_SEQIDX_BATCH
 
 
+def test_decode_step_validation(lib):
+    def dec(p, state=FAKE, x=FAKE):
+        return ssd.ssd_decode_step(p, x, FAKE, FAKE, FAKE, FAKE, 0, state, FAKE, 0)
+    assert dec(prob(dtype=7)) == ssd.SSD_ERR_BAD_DTYPE
+    assert dec(prob(nheads=80, ngroups=3)) == ssd.SSD_ERR_BAD_SHAPE
+    assert dec(prob(dstate=8)) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert dec(prob(headdim=24)) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert dec(prob(), state=FAKE + 4) == ssd.SSD_ERR_UNSUPPORTED_DIMS   # state not 16-byte aligned
+    assert dec(prob(), x=0) == ssd.SSD_ERR_NULL_ARG
+    assert dec(prob(), state=0) == ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_decode_step(None, *([None] * 9)) == ssd.SSD_ERR_NULL_ARG
+    # seqlen and chunk_size play no part in a decode step
+    assert dec(prob(seqlen=0, chunk_size=48), x=0) == ssd.SSD_ERR_NULL_ARG
+
+
 def test_error_strings(lib):
     for code in range(0, -10, -1):
         s = ssd.ssd_error_string(code)
