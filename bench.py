@@ -47,15 +47,14 @@ def algorithmic_counts(p, nseq):
 
 
 def kernel_sources_digest():
-    """Hash of the HIP sources; counter files record the digest they were taken at."""
-    import glob
+    """Hash of the sources the fused kernels are compiled from; counter files
+    record the digest they were taken at."""
     import hashlib
 
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2405_21060_amd", "csrc", "*"))):
-        if f.endswith((".hip", ".cpp", ".h")):
-            with open(f, "rb") as fh:
-                h.update(fh.read())
+    for name in ("ssd_fused.hip", "ssd_device.h", "ssd_internal.h"):
+        with open(os.path.join(ROOT, "paper_2405_21060_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 
