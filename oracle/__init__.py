@@ -10,6 +10,9 @@ shares no code with the HIP path.
 * :mod:`oracle.chunked` -- the block decomposition of Section 6 written out step
   by step in float64 numpy, exposing its intermediates (chunk cumsums, chunk
   states, states entering chunks) for per-step comparisons.
+* :mod:`oracle.block` -- the Mamba-2 block steps on either side of the layer
+  (dt parameterisation; gate ``y * SiLU(z)`` and grouped RMS normalisation of
+  Sections 7.1 and 8.1) around :func:`forward`.
 """
 from __future__ import annotations
 

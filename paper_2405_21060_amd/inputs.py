@@ -36,8 +36,8 @@ from typing import Optional
 import numpy as np
 
 __all__ = [
-    "Problem", "Inputs", "WORKLOADS", "make_inputs", "f32_to_bf16_bits",
-    "bf16_bits_to_f32", "workload",
+    "Problem", "Inputs", "BlockInputs", "WORKLOADS", "make_inputs", "make_block_inputs",
+    "f32_to_bf16_bits", "bf16_bits_to_f32", "workload",
 ]
 
 
@@ -146,6 +146,40 @@ def make_inputs(p: Problem, seed: int) -> Inputs:
     if p.init_states:
         init = _normal_blocks(rng, (nseq, H, P, N), 1.0, "f32")
     return Inputs(p, x, dt, A_log, B, C, D, init, seq_idx, nseq)
+
+
+@dataclasses.dataclass
+class BlockInputs:
+    """Inputs of the layer with the block steps around it: the layer's own
+    (``base``; its ``dt`` is not used) plus the raw dt, its per-head bias, the
+    gate branch ``z`` and the normalisation weight."""
+    base: Inputs
+    dt_raw: np.ndarray       # (b, T, H) activation dtype, before bias and softplus
+    dt_bias: np.ndarray      # (H,) float32
+    z: np.ndarray            # (b, T, H, P) activation dtype
+    norm_weight: np.ndarray  # (H * P,) float32
+
+    def as_f64(self, name: str) -> np.ndarray:
+        a = getattr(self, name)
+        if a.dtype == np.uint16:
+            return bf16_bits_to_f32(a).astype(np.float64)
+        return a.astype(np.float64)
+
+
+def make_block_inputs(p: Problem, seed: int) -> BlockInputs:
+    """``make_inputs(p, seed)`` plus, from a second stream
+    ``default_rng([seed, 0xB10C])`` in this order: ``dt_init ~ U(1e-3, 1e-1)``
+    per head and ``dt_bias = log(expm1(dt_init))`` (float32);
+    ``dt_raw ~ N(0,1)`` per (batch, token, head); ``z ~ N(0,1)``;
+    ``norm_weight ~ 1 + 0.1 N(0,1)`` per channel (float32)."""
+    base = make_inputs(p, seed)
+    rng = np.random.default_rng([seed, 0xB10C])
+    H, P, b, T = p.nheads, p.headdim, p.batch, p.seqlen
+    dt_bias = np.log(np.expm1(rng.uniform(1e-3, 1e-1, H))).astype(np.float32)
+    dt_raw = _normal_blocks(rng, (b, T, H), 1.0, p.dtype)
+    z = _normal_blocks(rng, (b, T, H, P), 1.0, p.dtype)
+    norm_weight = (1.0 + 0.1 * rng.standard_normal(H * P)).astype(np.float32)
+    return BlockInputs(base, dt_raw, dt_bias, z, norm_weight)
 
 
 # The workloads: one tiny fp32 parity case and Mamba-2 layer shapes in bf16.
