@@ -161,11 +161,113 @@ def decode_bench(args, torch, ssd):
     }), flush=True)
 
 
+def block_bench(args, torch, ssd):
+    """The layer with the block steps around it (ssd_forward_block) on the
+    2.7B-layer workload: dt = softplus(dt_raw + bias), the layer, the gate
+    y * SiLU(z) and an RMS normalisation over groups of --block-norm-group
+    channels (default one head, 64).  The same call with the gate and norm left
+    to the separate output pass, and the plain layer, are timed in the same run
+    for comparison."""
+    import os
+
+    from paper_2405_21060_amd.inputs import WORKLOADS, make_block_inputs
+
+    p = WORKLOADS["mamba2_2p7b"]
+    bi = make_block_inputs(p, args.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def act(a):
+        return torch.from_numpy(a.view("int16")).view(torch.bfloat16).to(dev)
+
+    base = bi.base
+    sets = []
+    for _ in range(max(1, args.copies)):
+        sets.append({"x": act(base.x), "dt_raw": act(bi.dt_raw), "dt": act(base.dt), "B": act(base.B),
+                     "C": act(base.C), "z": act(bi.z), "y": torch.empty_like(act(base.x))})
+    A_log = torch.from_numpy(base.A_log).to(dev)
+    D = torch.from_numpy(base.D).to(dev)
+    bias = torch.from_numpy(bi.dt_bias).to(dev)
+    w = torch.from_numpy(bi.norm_weight).to(dev)
+    fin = torch.empty((p.batch, p.nheads, p.headdim, p.dstate), dtype=torch.float32, device=dev)
+    prob = ssd.make_problem(p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups, p.chunk_size,
+                            ssd.SSD_DTYPE_BF16, 0)
+    wsb = ssd.ssd_workspace_bytes(prob)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ptr = lambda t: None if t is None else t.data_ptr()
+    kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, z in kev:
+        a.record(stream)
+        z.record(stream)
+
+    def call(i, mode, events=None):
+        c = sets[i % len(sets)]
+        if mode == "layer":
+            rc = ssd.ssd_forward(prob, ptr(c["x"]), ptr(c["dt"]), ptr(A_log), ptr(c["B"]), ptr(c["C"]),
+                                 ptr(D), None, None, ptr(c["y"]), ptr(fin), ptr(ws), wsb, stream.cuda_stream)
+        else:
+            opts = ssd.make_block_opts(bias, True, 0.0, float("inf"), c["z"], w, args.block_norm_group, 1e-5)
+            a = (prob, opts, ptr(c["x"]), ptr(c["dt_raw"]), ptr(A_log), ptr(c["B"]), ptr(c["C"]), ptr(D),
+                 None, None, ptr(c["y"]), ptr(fin), ptr(ws), wsb, stream.cuda_stream)
+            rc = ssd.ssd_forward_block_timed(*a, events[0].cuda_event, events[1].cuda_event) if events \
+                else ssd.ssd_forward_block(*a)
+        if rc != 0:
+            raise ssd.SsdError(rc, mode)
+
+    def timed(mode, with_events=False):
+        if mode == "separate":
+            os.environ["SSD_BLOCK_POST"] = "separate"
+        try:
+            for i in range(args.warmup):
+                call(i, mode)
+            torch.cuda.synchronize()
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            for i in range(args.steps):
+                call(i, mode, kev[i] if with_events else None)
+            t1.record(stream)
+            torch.cuda.synchronize()
+        finally:
+            os.environ.pop("SSD_BLOCK_POST", None)
+        return t0.elapsed_time(t1) / args.steps
+
+    ms = timed("block")
+    timed("block", with_events=True)   # the chunk kernel's own duration (events add their own cost)
+    ks = sorted(a.elapsed_time(z) for a, z in kev)
+    kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
+           "p90": ks[(9 * len(ks)) // 10]}
+    ms_sep = timed("separate")
+    ms_layer = timed("layer")
+    _, _, byts = algorithmic_counts(p, base.nseq)
+    tokens = p.batch * p.seqlen
+    byts += 2 * tokens * p.nheads * p.headdim + 4 * p.nheads + 4 * p.nheads * p.headdim   # z, bias, weight
+    ksec = kms["mean"] * 1e-3
+    fused_norm = args.block_norm_group == p.headdim
+    print(json.dumps({
+        "metric": "SSD block fwd tokens/s (dt softplus + layer + SiLU gate + RMSNorm, 2.7B-layer shape, 1 GPU)",
+        "value": tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded; Mamba-2 layer shapes)",
+        "config": {"workload": "block_mamba2_2p7b", "batch": p.batch, "seqlen": p.seqlen,
+                   "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate, "ngroups": p.ngroups,
+                   "chunk_size": p.chunk_size, "norm_group_size": args.block_norm_group},
+        "separate_output_pass_ms": ms_sep,
+        "layer_only_ms": ms_layer,
+        "roofline": {"bound": "hbm", "achieved": byts / ksec / 1e9, "peak": PEAK_HBM_BPS / 1e9,
+                     "unit": "GB/s", "frac": byts / ksec / PEAK_HBM_BPS, "traffic": None,
+                     "kernel": "k_fused_main<128> (dt step, gate%s fused)" % (" and norm" if fused_norm else ""),
+                     "kernel_ms": kms, "algorithmic_bytes": byts},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps first (the GPU takes on the order of 100 calls to reach its steady clocks)")
     ap.add_argument("--workload", default="mamba2_2p7b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -175,6 +277,9 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="time the decode step instead (one token per sequence, batch --decode-batch)")
     ap.add_argument("--decode-batch", type=int, default=256)
+    ap.add_argument("--block", action="store_true",
+                    help="time the layer with the block steps around it (ssd_forward_block) instead")
+    ap.add_argument("--block-norm-group", type=int, default=64)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -210,6 +315,8 @@ def main():
 
     if args.decode:
         return decode_bench(args, torch, ssd)
+    if args.block:
+        return block_bench(args, torch, ssd)
 
     p = WORKLOADS[args.workload]
     inp = make_inputs(p, args.seed)
@@ -251,15 +358,22 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    # whole-job time: plain calls, nothing recorded between them
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
     for i in range(args.steps):
-        step(i, None if args.no_kernel_events else kev[i])
+        step(i)
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     kms = None
     if not args.no_kernel_events:
+        # the dominant kernel's own duration: a second pass of the same calls
+        # with events recorded on the launch stream right around it (the
+        # event records add their own cost, so this pass is not the job time)
+        for i in range(args.steps):
+            step(i, kev[i])
+        torch.cuda.synchronize()
         ks = sorted(a.elapsed_time(z) for a, z in kev)
         kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
                "p90": ks[(9 * len(ks)) // 10]}

@@ -73,7 +73,8 @@ typedef enum {
     SSD_ERR_SEQIDX_BATCH = -6,     /* seq_idx given with batch != 1                  */
     SSD_ERR_WORKSPACE = -7,        /* workspace NULL or smaller than required        */
     SSD_ERR_LAUNCH = -8,           /* a kernel launch failed                         */
-    SSD_ERR_TOO_LARGE = -9         /* a tensor exceeds the supported index range     */
+    SSD_ERR_TOO_LARGE = -9,        /* a tensor exceeds the supported index range     */
+    SSD_ERR_BAD_OPTION = -10       /* an ssd_block_opts field out of range           */
 } ssd_status;
 
 typedef struct {
@@ -137,6 +138,64 @@ int ssd_decode_step(const ssd_problem* prob,
                     const void* x, const void* dt, const float* A_log,
                     const void* B, const void* C, const float* D,
                     float* state, void* y, void* stream);
+
+/* Steps of the Mamba-2 block fused on either side of the layer.
+ *
+ * Before the layer, the discretisation parameter (left to the caller by the
+ * paper, which has Delta come out of the block's input projection, Section 7):
+ *     dt = min(max(softplus(dt_in + dt_bias), dt_min), dt_max)   (dt_softplus != 0)
+ *     dt = min(max(dt_in + dt_bias, dt_min), dt_max)             (dt_softplus == 0)
+ * with softplus(v) = log(1 + e^v) and dt_bias NULL meaning 0.
+ * After the layer (y including D x), the gate and the normalisation of the
+ * block equations of Section 8.1 (the norm after the gate, as in Section 7.1):
+ *     y = y * z * sigmoid(z)                                     (z != NULL)
+ *     y = y / sqrt(mean over its group of y^2 + norm_eps) * norm_weight
+ *                                                      (norm_group_size > 0)
+ * where a token's groups are consecutive runs of norm_group_size channels of
+ * its nheads * headdim channel row (head-major).  A zero-initialised struct
+ * with dt_max = INFINITY is the plain layer.
+ *
+ * Limits (else SSD_ERR_BAD_OPTION): 0 <= dt_min <= dt_max (dt_max may be
+ * INFINITY); norm_group_size 0 or a multiple of headdim that divides
+ * nheads * headdim; norm_eps >= 0 and finite. */
+typedef struct {
+    const float* dt_bias;      /* (nheads) float32, or NULL                          */
+    int32_t dt_softplus;       /* nonzero: softplus after the bias                   */
+    float dt_min;              /* clamp of dt (0 = none from below)                  */
+    float dt_max;              /* clamp of dt (INFINITY = none from above)           */
+    const void* z;             /* (batch, seqlen, nheads, headdim) dtype, or NULL    */
+    const float* norm_weight;  /* (nheads * headdim) float32, or NULL (= 1)          */
+    int64_t norm_group_size;   /* channels per normalisation group, 0 = no norm      */
+    float norm_eps;            /* added to each group's mean square                  */
+} ssd_block_opts;
+
+/* Workspace size for ssd_forward_block (at least ssd_workspace_bytes). */
+int ssd_block_workspace_bytes(const ssd_problem* prob, const ssd_block_opts* opts, size_t* bytes);
+
+/* The layer with the block steps above around it.  Arguments, layouts,
+ * ownership and errors as for ssd_forward, except that `dt` holds dt_in (any
+ * sign when dt_softplus != 0) and `opts` (host memory, read during the call;
+ * its device pointers must stay valid until the work completes) selects the
+ * steps; y receives the block's output.  On the Mamba-2 layer shapes of the
+ * fused path the dt step runs inside the chunk kernel and the gate (and a
+ * normalisation of one head per group) inside its output stage; larger
+ * groups are normalised by one more pass over y. */
+int ssd_forward_block(const ssd_problem* prob, const ssd_block_opts* opts,
+                      const void* x, const void* dt, const float* A_log,
+                      const void* B, const void* C, const float* D,
+                      const float* initial_states, const int32_t* seq_idx,
+                      void* y, float* final_states,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ssd_forward_block with the two events of ssd_forward_timed around its
+ * chunk kernel. */
+int ssd_forward_block_timed(const ssd_problem* prob, const ssd_block_opts* opts,
+                            const void* x, const void* dt, const float* A_log,
+                            const void* B, const void* C, const float* D,
+                            const float* initial_states, const int32_t* seq_idx,
+                            void* y, float* final_states,
+                            void* workspace, size_t workspace_bytes, void* stream,
+                            void* event_begin, void* event_end);
 
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdint>
 #include <cstdlib>
 
@@ -115,20 +116,61 @@ extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
     return SSD_OK;
 }
 
+extern "C" int ssd_block_workspace_bytes(const ssd_problem* prob, const ssd_block_opts* opts, size_t* bytes)
+{
+    if (!opts) return SSD_ERR_NULL_ARG;
+    return ssd_workspace_bytes(prob, bytes);   // the block steps need no workspace of their own
+}
+
 namespace {
 
-int forward_impl(const ssd_problem* prob, const void* x, const void* dt, const float* A_log,
-                 const void* B, const void* C, const float* D, const float* initial_states,
-                 const int32_t* seq_idx, void* y, float* final_states, void* workspace,
-                 size_t workspace_bytes, void* stream, hipEvent_t ev_begin, hipEvent_t ev_end)
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+// Block options against the shape; fills the dt parameterisation.
+int validate_block(const ssd_block_opts* o, const ssd::Shape& s, const void* y, ssd::DtTransform* dtx)
+{
+    if (!(o->dt_min >= 0.f) || !(o->dt_max >= o->dt_min)) return SSD_ERR_BAD_OPTION;   // NaN fails too
+    if (!(o->norm_eps >= 0.f) || !std::isfinite(o->norm_eps)) return SSD_ERR_BAD_OPTION;
+    const int64_t C = s.H * s.P;
+    if (o->norm_group_size < 0 || (o->norm_group_size > 0 &&
+                                   (o->norm_group_size % s.P != 0 || C % o->norm_group_size != 0)))
+        return SSD_ERR_BAD_OPTION;
+    if ((o->z || o->norm_group_size > 0) && (!aligned16(y) || (o->z && !aligned16(o->z)) ||
+                                             (o->norm_weight && !aligned16(o->norm_weight))))
+        return SSD_ERR_UNSUPPORTED_DIMS;
+    dtx->bias = o->dt_bias;
+    dtx->softplus = o->dt_softplus != 0;
+    dtx->lo = o->dt_min;
+    dtx->hi = o->dt_max;
+    dtx->active = o->dt_bias || o->dt_softplus || o->dt_min > 0.f || o->dt_max < INFINITY;
+    return SSD_OK;
+}
+
+int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void* x, const void* dt,
+                 const float* A_log, const void* B, const void* C, const float* D,
+                 const float* initial_states, const int32_t* seq_idx, void* y, float* final_states,
+                 void* workspace, size_t workspace_bytes, void* stream, hipEvent_t ev_begin,
+                 hipEvent_t ev_end)
 {
     ssd::Shape s;
     int rc = ssd::validate(prob, seq_idx != nullptr, &s);
     if (rc != SSD_OK) return rc;
     if (!x || !dt || !A_log || !B || !C || !y) return SSD_ERR_NULL_ARG;
+    ssd::DtTransform dtx;
+    if (opts && (rc = validate_block(opts, s, y, &dtx)) != SSD_OK) return rc;
     size_t need = 0;
     if (ssd_workspace_bytes(prob, &need) != SSD_OK || !workspace || workspace_bytes < need)
         return SSD_ERR_WORKSPACE;
+    // output side of the block: gate and grouped normalisation
+    ssd::GateNormParams gn;
+    gn.rows = s.b * s.T;
+    gn.C = s.H * s.P;
+    gn.group = opts ? opts->norm_group_size : 0;
+    gn.y = y;
+    gn.z = opts ? opts->z : nullptr;
+    gn.weight = opts ? opts->norm_weight : nullptr;
+    gn.eps = opts ? opts->norm_eps : 0.f;
+    const bool post = gn.z || gn.group > 0;
     const char* path = std::getenv("SSD_PATH");  // debug knob: "unfused" forces the step-by-step kernels
     const bool force_unfused = path && path[0] == 'u';
     if (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16, seq_idx != nullptr)) {
@@ -157,8 +199,27 @@ int forward_impl(const ssd_problem* prob, const void* x, const void* dt, const f
         f.ring = reinterpret_cast<float*>(base + fw.ring);
         f.flags = reinterpret_cast<int*>(base + fw.flags);
         f.ticket = reinterpret_cast<int*>(base + fw.ticket);
-        const hipError_t err =
-            ssd::launch_fused(f, static_cast<hipStream_t>(stream), ev_begin, ev_end);
+        f.dtx = dtx;
+        // The chunk kernel gates, and normalises one-head groups, in its output
+        // stage.  Wider groups take one more pass, which then also gates (z is
+        // read once either way, and gating in that pass measured faster than in
+        // the chunk kernel).  SSD_BLOCK_POST=separate (a measurement knob) leaves
+        // gate and normalisation to that pass in every case.
+        const char* bp = std::getenv("SSD_BLOCK_POST");
+        const bool separate = bp && bp[0] == 's';
+        if (post && !separate && (gn.group == 0 || gn.group == s.P)) {
+            f.z = gn.z;
+            if (gn.group == s.P) {
+                f.norm_head = 1;
+                f.norm_weight = gn.weight;
+                f.norm_eps = gn.eps;
+            }
+            gn.z = nullptr;
+            gn.group = 0;
+        }
+        hipError_t err = ssd::launch_fused(f, static_cast<hipStream_t>(stream), ev_begin, ev_end);
+        if (err == hipSuccess && (gn.z || gn.group > 0))
+            err = ssd::launch_gate_norm(gn, s.bf16, static_cast<hipStream_t>(stream));
         return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
     }
     const ssd::WorkspaceLayout w = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC);
@@ -188,8 +249,9 @@ int forward_impl(const ssd_problem* prob, const void* x, const void* dt, const f
     p.info = reinterpret_cast<int4*>(ws + w.info);
     p.gram = reinterpret_cast<float*>(ws + w.gram);
     p.states = reinterpret_cast<float*>(ws + w.states);
-    const hipError_t err =
-        ssd::launch_unfused(p, s.bf16, static_cast<hipStream_t>(stream), ev_begin, ev_end);
+    p.dtx = dtx;
+    hipError_t err = ssd::launch_unfused(p, s.bf16, static_cast<hipStream_t>(stream), ev_begin, ev_end);
+    if (err == hipSuccess && post) err = ssd::launch_gate_norm(gn, s.bf16, static_cast<hipStream_t>(stream));
     return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
@@ -201,7 +263,7 @@ extern "C" int ssd_forward(const ssd_problem* prob, const void* x, const void* d
                            float* final_states, void* workspace, size_t workspace_bytes,
                            void* stream)
 {
-    return forward_impl(prob, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
+    return forward_impl(prob, nullptr, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
                         workspace, workspace_bytes, stream, nullptr, nullptr);
 }
 
@@ -212,7 +274,30 @@ extern "C" int ssd_forward_timed(const ssd_problem* prob, const void* x, const v
                                  void* workspace, size_t workspace_bytes, void* stream,
                                  void* event_begin, void* event_end)
 {
-    return forward_impl(prob, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
+    return forward_impl(prob, nullptr, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
+                        workspace, workspace_bytes, stream, static_cast<hipEvent_t>(event_begin),
+                        static_cast<hipEvent_t>(event_end));
+}
+
+extern "C" int ssd_forward_block(const ssd_problem* prob, const ssd_block_opts* opts, const void* x,
+                                 const void* dt, const float* A_log, const void* B, const void* C,
+                                 const float* D, const float* initial_states, const int32_t* seq_idx,
+                                 void* y, float* final_states, void* workspace, size_t workspace_bytes,
+                                 void* stream)
+{
+    if (!opts) return SSD_ERR_NULL_ARG;
+    return forward_impl(prob, opts, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
+                        workspace, workspace_bytes, stream, nullptr, nullptr);
+}
+
+extern "C" int ssd_forward_block_timed(const ssd_problem* prob, const ssd_block_opts* opts, const void* x,
+                                       const void* dt, const float* A_log, const void* B, const void* C,
+                                       const float* D, const float* initial_states, const int32_t* seq_idx,
+                                       void* y, float* final_states, void* workspace, size_t workspace_bytes,
+                                       void* stream, void* event_begin, void* event_end)
+{
+    if (!opts) return SSD_ERR_NULL_ARG;
+    return forward_impl(prob, opts, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states,
                         workspace, workspace_bytes, stream, static_cast<hipEvent_t>(event_begin),
                         static_cast<hipEvent_t>(event_end));
 }
@@ -266,6 +351,7 @@ extern "C" const char* ssd_error_string(int code)
     case SSD_ERR_WORKSPACE: return "workspace missing or smaller than ssd_workspace_bytes()";
     case SSD_ERR_LAUNCH: return "kernel launch failed";
     case SSD_ERR_TOO_LARGE: return "problem exceeds the supported index range";
+    case SSD_ERR_BAD_OPTION: return "block option out of range (dt clamp, norm group size or eps)";
     default: return "unknown ssd status";
     }
 }

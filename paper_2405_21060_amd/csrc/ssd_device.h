@@ -31,6 +31,10 @@ struct Frag8 {
 template <typename T>
 struct Act;
 
+// The block path's dt: softplus(v) = max(v, 0) + log(1 + e^-|v|) (no overflow
+// on either side), after the head's bias, then the clamp.
+__device__ __forceinline__ float softplus_f(float v) { return fmaxf(v, 0.f) + log1pf(expf(-fabsf(v))); }
+
 template <>
 struct Act<float> {
     static __device__ __forceinline__ float load(const float* p, int64_t i) { return p[i]; }

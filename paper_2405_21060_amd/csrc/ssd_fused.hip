@@ -290,6 +290,7 @@ struct MainSmem {
     float cs[2][kQ];          // chunk-local cumsum of dt A (log2 units) of the current / next head
     float dt[2][kQ];
     float wtot[4];            // per-wavefront totals of the cumsum
+    float wn[kP];             // normalisation weights of the current head
     float vf[kQ];             // dt_s exp2(cs[tile end] - cs_s)
     float w[kQ];              // dt_s exp2(cs[Q-1] - cs_s)
     int ticket;
@@ -543,6 +544,27 @@ __device__ __forceinline__ void dma_head(const FusedParams& p, const Item& it, i
     for (int i = 0; i < 4; ++i) copy16_to_lds(xrs, xdst + (4 * wave + i) * 512, o.x[i], hoff);
 }
 
+// Copy of head hh's gate branch z, rows of the two strips of this wavefront,
+// into the LDS buffer zdst with x's swizzled layout: 4 blocks of 8 rows (lane
+// l of a block fetches the 16 bytes that land at block + 16 l).  Rows past a
+// partial last chunk read as zeros (they are never stored).
+__device__ __forceinline__ void dma_z_strips(const FusedParams& p, const Item& it, int hh, u16* zdst,
+                                             const int* strip, int lane)
+{
+    const u16* zchunk = static_cast<const u16*>(p.z) + (static_cast<int64_t>(it.b) * p.T + it.c0) * p.H * kP;
+    const i32x4 zrs = buffer_rsrc(zchunk, (p.T - it.c0) * p.H * kP * 2);
+    const int row_bytes = static_cast<int>(p.H * kP * 2);
+#pragma unroll
+    for (int k4 = 0; k4 < 2; ++k4)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int s0 = 16 * strip[k4] + 8 * i;   // first row of the block
+            const int s = s0 + (lane >> 3);
+            const int grp = (lane & 7) ^ (s & 7);    // logical group landing at physical slot lane % 8
+            copy16_to_lds(zrs, zdst + s0 * kP, s * row_bytes + 16 * grp, hh * kP * 2);
+        }
+}
+
 // dt of token `tid` (clamped to the chunk) of head hh of an item, raw bf16.
 __device__ __forceinline__ u16 load_dt(const FusedParams& p, const Item& it, int hh, int tid)
 {
@@ -605,7 +627,8 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
                                           float* __restrict__ cs, float* __restrict__ dt,
                                           float* __restrict__ wt, float* __restrict__ vf, float* __restrict__ w,
                                           u16* __restrict__ gr, u16* __restrict__ hb, int* __restrict__ tk,
-                                          const float* __restrict__ A_logp, const float* __restrict__ Dp)
+                                          const float* __restrict__ A_logp, const float* __restrict__ Dp,
+                                          const float* __restrict__ biasp, float* __restrict__ wn)
 {
     constexpr int NT = N / 16;
     constexpr int PTW = 4 * NT / kWaves;
@@ -633,6 +656,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     const int64_t c0 = it.c0;
     const bool has_prev = it.has_prev, has_next = it.has_next;
     const float Dh = Dp ? Dp[h] : 0.f;   // scalar loads (read-only kernel arguments)
+    // this head's normalisation weights (one per thread of the first wavefront),
+    // stored to LDS at the state barrier, read by the output stage
+    const bool gate = p.z != nullptr, norm = p.norm_head != 0;
+    float wreg = 0.f;
+    if (norm && tid < kP) wreg = p.norm_weight ? p.norm_weight[h * kP + tid] : 1.f;
     // x (and this thread's dt) of the next head -- of this item, or of the next
     // item once known -- arrive while this head computes
     u16 dtr_next = 0;
@@ -650,7 +678,14 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // per-token weights of the diagonal block and the right factor
     float d = 0.f, incl = 0.f;
     if (tid < kQ) {
-        d = tid < L ? bf(dtr) : 0.f;
+        if (tid < L) {
+            d = bf(dtr);
+            if (p.dtx.active) {   // the block path's dt parameterisation
+                if (biasp) d += biasp[h];
+                if (p.dtx.softplus) d = softplus_f(d);
+                d = fminf(fmaxf(d, p.dtx.lo), p.dtx.hi);
+            }
+        }
         incl = d * (-expf(A_logp[h]) * kLog2e);
 #pragma unroll
         for (int sh = 1; sh < 64; sh <<= 1) {
@@ -684,6 +719,20 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
     diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, gr, r, lg, lane, y[0], y[1]);
+    // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
+    // after the right factor)
+#pragma unroll
+    for (int k4 = 0; k4 < 2; ++k4) {
+        const int t = 16 * strip[k4] + r;
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) {
+            const uint2 xv = *reinterpret_cast<const uint2*>(xs + xs_off(t, 16 * pt + 4 * lg));
+            const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
+                                 __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
+#pragma unroll
+            for (int v = 0; v < 4; ++v) y[k4][pt][v] += Dh * xf[v];
+        }
+    }
 
     // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
     f32x4_t sacc[PTW];
@@ -741,6 +790,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         }
     }
     lds_barrier();   // flag seen by tid 0
+    // The gate branch z of this head's output rows into this head's x buffer:
+    // every wavefront is past the right factor, the last reader of x.  Each
+    // wavefront copies the 32 rows of its own two strips, so its own wait
+    // (in the output stage) suffices.
+    if (gate) dma_z_strips(p, it, h, xs, strip, lane);
     f32x4_t hprev[PTW];
     if (has_prev) {
         const int slot = (c + 1) & 1;
@@ -799,10 +853,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
     // The state stores drain while the left factor runs; the flag is set after
     // the epilogue's barrier, once every wavefront has waited for its stores.
+    if (norm && tid < kP) wn[tid] = wreg;
     lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
     if (hk == 0) next = *tk;
     // The next item's Gram tiles (and, with one head per item, its first head's
-    // x): only the bf16 state and this head's x are read from here on.
+    // x): only the bf16 state and z are read from here on.
     const bool gram_ahead = last && next < nwork;
     if (gram_ahead) {
         const Item nit = decode_item(p, next, per_c, nHG, N);
@@ -841,30 +896,61 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
 
 
-    // ---- skip term; y staged in place over this head's x, then full-row stores
+    // ---- the block's gate and per-head normalisation; y staged in place over
+    // this head's x (or z) buffer, then full-row stores
     {
         u16* xw = xs;
+        // state stores complete (and the next head's x and this head's z have
+        // landed; z was copied before the Gram tiles); the Gram copies (at most 9
+        // per wavefront, at least 8) may stay in flight
+        if (gram_ahead)
+            __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8)
+        else
+            wait_vmem();
+        if (gate) {   // y * SiLU(z), SiLU(z) = z / (1 + 2^(-z log2 e))
+#pragma unroll
+            for (int k4 = 0; k4 < 2; ++k4)
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) {
+                    const uint2 zv = *reinterpret_cast<const uint2*>(xw + xs_off(16 * strip[k4] + r, 16 * pt + 4 * lg));
+                    const float zf[4] = {__uint_as_float(zv.x << 16), __uint_as_float(zv.x & 0xFFFF0000u),
+                                         __uint_as_float(zv.y << 16), __uint_as_float(zv.y & 0xFFFF0000u)};
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        y[k4][pt][v] *= zf[v] * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-zf[v] * kLog2e));
+                }
+        }
+        if (norm) {   // RMS over the head's P channels of each token: the four lanes r, r+16, r+32, r+48
+#pragma unroll
+            for (int k4 = 0; k4 < 2; ++k4) {
+                float ss = 0.f;
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) ss += y[k4][pt][v] * y[k4][pt][v];
+                ss += __shfl_xor(ss, 16, 64);
+                ss += __shfl_xor(ss, 32, 64);
+                const float scale = 1.f / sqrtf(ss * (1.f / kP) + p.norm_eps);
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) {
+                    const float4 w4 = *reinterpret_cast<const float4*>(wn + 16 * pt + 4 * lg);
+                    const float wv[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) y[k4][pt][v] *= scale * wv[v];
+                }
+            }
+        }
 #pragma unroll
         for (int k4 = 0; k4 < 2; ++k4) {
             const int t = 16 * strip[k4] + r;
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) {
-                uint2* cell = reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg));
-                const uint2 xv = *cell;
-                const float xf[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xFFFF0000u),
-                                     __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xFFFF0000u)};
                 uint2 packed;
-                packed.x = pack_bf16x2(y[k4][pt][0] + Dh * xf[0], y[k4][pt][1] + Dh * xf[1]);
-                packed.y = pack_bf16x2(y[k4][pt][2] + Dh * xf[2], y[k4][pt][3] + Dh * xf[3]);
-                *cell = packed;   // same cell this lane just read: in place is safe
+                packed.x = pack_bf16x2(y[k4][pt][0], y[k4][pt][1]);
+                packed.y = pack_bf16x2(y[k4][pt][2], y[k4][pt][3]);
+                *reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg)) = packed;   // cells this lane read
             }
         }
-        // state stores complete (and the next head's x has landed); the Gram copies
-        // issued after them (at most 9 per wavefront, at least 8) may stay in flight
-        if (gram_ahead)
-            __builtin_amdgcn_s_waitcnt(0x0F78);   // vmcnt(8)
-        else
-            wait_vmem();
         lds_barrier();
         if (tid == 0 && has_next)
             __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
@@ -890,11 +976,12 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     dtr = dtr_next;  // here, where the load has long completed (the epilogue waited for it)
 }
 
-// A_log and D come as separate read-only arguments so that their per-head values
+// A_log, D and the dt bias come as separate read-only arguments so that their per-head values
 // are scalar loads (a vector load would wait behind the outstanding copies).
 template <int N>
 __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, const float* __restrict__ A_logp,
-                                                                const float* __restrict__ Dp)
+                                                                const float* __restrict__ Dp,
+                                                                const float* __restrict__ biasp)
 {
     constexpr int NT = N / 16;            // n-tiles of the state
     constexpr int PTW = 4 * NT / kWaves;  // p-tiles per wavefront in the right factor (one n-tile each)
@@ -948,7 +1035,8 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     load_c<N>(p, it, strip, r, lg, cf);
     for (int hk = 0; hk < p.HG; ++hk) {
         head_step<N>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
-                     sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp);
+                     sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp,
+                     biasp, sm.wn);
         q ^= 1;
     }
     if (next >= nwork) break;
@@ -977,7 +1065,7 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
         if (v >= 1 && v < grid) grid = v;
     }
     hipLaunchKernelGGL(k_fused_main<N>, dim3(static_cast<unsigned>(grid)), dim3(kMainThreads), 0, stream, p,
-                       p.A_log, p.D);
+                       p.A_log, p.D, p.dtx.bias);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;

@@ -8,6 +8,15 @@
 
 namespace ssd {
 
+// dt parameterisation of the block path: dt = clamp(softplus?(dt_in + bias)).
+// `active` false = dt is used as given (the plain layer).
+struct DtTransform {
+    const float* bias = nullptr;   // (H) or null
+    int softplus = 0;
+    float lo = 0.f, hi = 0.f;
+    bool active = false;
+};
+
 // One call's shapes, pointers and workspace carve-up.
 struct Params {
     int64_t b, T, H, P, N, G, Q, nC, nseq;
@@ -26,6 +35,7 @@ struct Params {
     int4* info;      // (b, H, nC)     per-chunk scan coefficients (see ssd_unfused.hip)
     float* gram;     // (b, G, nC, Q, Q) C B^T per chunk (lower block triangle only)
     float* states;   // (b, nC, H, P, N) chunk states, then states entering each chunk
+    DtTransform dtx;
 };
 
 struct WorkspaceLayout {
@@ -60,6 +70,12 @@ struct FusedParams {
     float* ring;      // (b, H, 2, P, N) chunk-state ring
     int* flags;       // (b, H, nC)      state-published flags
     int* ticket;      // [0] work ticket, [1] wait-timeout error word
+    DtTransform dtx;
+    // gate / per-head normalisation in the output stage (null: none)
+    const void* z = nullptr;             // (b, T, H, P) bf16
+    const float* norm_weight = nullptr;  // (H * P), with norm_head
+    int norm_head = 0;                   // nonzero: RMS-normalise each head's P channels
+    float norm_eps = 0.f;
 };
 
 struct FusedLayout {
@@ -86,5 +102,18 @@ struct DecodeParams {
 };
 
 hipError_t launch_decode(const DecodeParams& p, bool bf16, hipStream_t stream);
+
+// Gate and grouped RMS normalisation of the block, in place on y (b*T token
+// rows of H*P channels): y = y * silu(z) when z, then the normalisation over
+// groups of `group` channels (a multiple of P) when group > 0.
+struct GateNormParams {
+    int64_t rows, C, group;
+    void* y;
+    const void* z;             // or null
+    const float* weight;       // (C) or null
+    float eps;
+};
+
+hipError_t launch_gate_norm(const GateNormParams& p, bool bf16, hipStream_t stream);
 
 }  // namespace ssd

@@ -47,6 +47,20 @@ __device__ __forceinline__ int chunk_len(const Params& p, int c)
 // y = unit (sequence id, or batch row) of the chunk's last token,
 // z = 1 when the last segment starts a sequence (reset), w = 1 when the
 // chunk's last token is the last token of its unit.
+// dt of token index `idx` of head h, after the block path's parameterisation
+// (bias, softplus, clamp) when one is requested.
+template <typename T>
+__device__ __forceinline__ float load_dt(const Params& p, int64_t idx, int h)
+{
+    float v = Act<T>::load(static_cast<const T*>(p.dt), idx);
+    if (p.dtx.active) {
+        if (p.dtx.bias) v += p.dtx.bias[h];
+        if (p.dtx.softplus) v = softplus_f(v);
+        v = fminf(fmaxf(v, p.dtx.lo), p.dtx.hi);
+    }
+    return v;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_chunk_prep(Params p)
 {
@@ -61,7 +75,7 @@ __global__ __launch_bounds__(kThreads) void k_chunk_prep(Params p)
     const float A2 = -expf(p.A_log[h]) * kLog2e;
     float a2 = 0.f;
     if (t < L)
-        a2 = Act<T>::load(static_cast<const T*>(p.dt), (b * p.T + c0 + t) * p.H + h) * A2;
+        a2 = load_dt<T>(p, (b * p.T + c0 + t) * p.H + h, h) * A2;
     const float cs = block_inclusive_scan(a2, scr);
     if (t < p.Q) p.cs[((b * p.H + h) * p.nC + c) * p.Q + t] = cs;
     cs_s[t] = cs;
@@ -201,7 +215,7 @@ __device__ __forceinline__ void load_chunk_scalars(const Params& p, int b, int c
     const int64_t c0 = static_cast<int64_t>(c) * p.Q;
     if (t < L) {
         sh.cs[t] = p.cs[((b * p.H + h) * p.nC + c) * p.Q + t];
-        sh.dt[t] = Act<T>::load(static_cast<const T*>(p.dt), (b * p.T + c0 + t) * p.H + h);
+        sh.dt[t] = load_dt<T>(p, (b * p.T + c0 + t) * p.H + h, h);
         sh.q[t] = p.seq_idx ? p.seq_idx[c0 + t] : 0;
     }
     __syncthreads();
@@ -309,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void k_chunk_output(Params p)
     if (t0 < kMaxQ) {
         const bool in = t0 < L;
         cs_s[t0] = in ? p.cs[((b * p.H + h) * p.nC + c) * p.Q + t0] : 0.f;
-        dt_s[t0] = in ? Act<T>::load(static_cast<const T*>(p.dt), (b * p.T + c0 + t0) * p.H + h) : 0.f;
+        dt_s[t0] = in ? load_dt<T>(p, (b * p.T + c0 + t0) * p.H + h, h) : 0.f;
         q_s[t0] = (p.seq_idx && in) ? p.seq_idx[c0 + t0] : 0;
     }
     __syncthreads();

@@ -6,9 +6,11 @@ into a ``hipStream_t``.  There is no CPU fallback: if the library is missing
 or cannot be loaded, every call raises.
 
 Names mirror the ABI: :func:`ssd_workspace_bytes`, :func:`ssd_forward`,
-:func:`ssd_error_string`; :func:`forward` is the tensor-level convenience
-wrapper returning ``(y, final_states)`` like the paper's
-``ssd(X, A, B, C, block_len, initial_states)``.
+:func:`ssd_forward_block`, :func:`ssd_decode_step`, :func:`ssd_error_string`;
+:func:`forward` is the tensor-level convenience wrapper returning
+``(y, final_states)`` like the paper's ``ssd(X, A, B, C, block_len,
+initial_states)``, :func:`forward_block` the same with the block steps around
+the layer, :func:`decode_step` one recurrent step.
 """
 from __future__ import annotations
 
@@ -31,8 +33,10 @@ SSD_ERR_SEQIDX_BATCH = -6
 SSD_ERR_WORKSPACE = -7
 SSD_ERR_LAUNCH = -8
 SSD_ERR_TOO_LARGE = -9
+SSD_ERR_BAD_OPTION = -10
 
 EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
+            "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
             "ssd_error_string")
 
 
@@ -47,6 +51,19 @@ class SsdProblem(ctypes.Structure):
         ("chunk_size", ctypes.c_int64),
         ("nseq", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
+    ]
+
+
+class SsdBlockOpts(ctypes.Structure):
+    _fields_ = [
+        ("dt_bias", ctypes.c_void_p),
+        ("dt_softplus", ctypes.c_int32),
+        ("dt_min", ctypes.c_float),
+        ("dt_max", ctypes.c_float),
+        ("z", ctypes.c_void_p),
+        ("norm_weight", ctypes.c_void_p),
+        ("norm_group_size", ctypes.c_int64),
+        ("norm_eps", ctypes.c_float),
     ]
 
 
@@ -78,6 +95,14 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_forward_timed.argtypes = lib.ssd_forward.argtypes + [vp, vp]
     lib.ssd_decode_step.restype = ctypes.c_int
     lib.ssd_decode_step.argtypes = [ctypes.POINTER(SsdProblem)] + [vp] * 9
+    lib.ssd_block_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_block_workspace_bytes.argtypes = [ctypes.POINTER(SsdProblem), ctypes.POINTER(SsdBlockOpts),
+                                              ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_forward_block.restype = ctypes.c_int
+    lib.ssd_forward_block.argtypes = [ctypes.POINTER(SsdProblem), ctypes.POINTER(SsdBlockOpts)] + [vp] * 10 + [
+        vp, ctypes.c_size_t, vp]
+    lib.ssd_forward_block_timed.restype = ctypes.c_int
+    lib.ssd_forward_block_timed.argtypes = lib.ssd_forward_block.argtypes + [vp, vp]
     lib.ssd_error_string.restype = ctypes.c_char_p
     lib.ssd_error_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -124,16 +149,35 @@ def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
-def forward(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=None,
-            seq_idx=None, nseq: Optional[int] = None, return_final_states: bool = True,
-            workspace=None, out=None, final_out=None) -> Tuple[object, object]:
-    """SSD forward on device tensors; returns ``(y, final_states or None)``.
+def ssd_forward_block(prob: SsdProblem, opts: SsdBlockOpts, x, dt, A_log, B, C, D, initial_states,
+                      seq_idx, y, final_states, workspace, workspace_bytes: int, stream) -> int:
+    """Raw ABI call on integer device addresses (0 = NULL); returns the status."""
+    return load_library().ssd_forward_block(
+        ctypes.byref(prob), ctypes.byref(opts), x, dt, A_log, B, C, D or None,
+        initial_states or None, seq_idx or None, y, final_states or None, workspace,
+        int(workspace_bytes), stream or None)
 
-    x (b,T,H,P), dt (b,T,H), B/C (b,T,G,N): float32 or bfloat16, all the same
-    dtype, contiguous, on one HIP device.  A_log, D (H): float32.
-    initial_states (b|nseq,H,P,N) float32.  seq_idx (1,T) int32 with nseq
-    sequences.  Launches on torch's current stream of x's device.
-    """
+
+def ssd_forward_block_timed(prob: SsdProblem, opts: SsdBlockOpts, x, dt, A_log, B, C, D,
+                            initial_states, seq_idx, y, final_states, workspace,
+                            workspace_bytes: int, stream, event_begin, event_end) -> int:
+    """``ssd_forward_block`` with the two events of ``ssd_forward_timed``."""
+    return load_library().ssd_forward_block_timed(
+        ctypes.byref(prob), ctypes.byref(opts), x, dt, A_log, B, C, D or None,
+        initial_states or None, seq_idx or None, y, final_states or None, workspace,
+        int(workspace_bytes), stream or None, event_begin or None, event_end or None)
+
+
+def make_block_opts(dt_bias=None, dt_softplus: bool = True, dt_min: float = 0.0,
+                    dt_max: float = float("inf"), z=None, norm_weight=None,
+                    norm_group_size: int = 0, norm_eps: float = 1e-5) -> SsdBlockOpts:
+    """Block options from tensors (or None) and scalars."""
+    return SsdBlockOpts(_ptr(dt_bias), int(bool(dt_softplus)), float(dt_min), float(dt_max),
+                        _ptr(z), _ptr(norm_weight), int(norm_group_size), float(norm_eps))
+
+
+def _call(opts, x, dt, A_log, B, C, D, chunk_size, initial_states, seq_idx, nseq,
+          return_final_states, workspace, out, final_out, extra=()):
     import torch
 
     dev = x.device
@@ -145,15 +189,18 @@ def forward(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=No
         dtype = SSD_DTYPE_F32
     else:
         raise TypeError("x must be float32 or bfloat16")
-    for name, t in (("dt", dt), ("B", B), ("C", C)):
-        if t.dtype != x.dtype:
+    act = (("dt", dt), ("B", B), ("C", C)) + tuple((n, t) for n, t, f32 in extra if not f32)
+    for name, t in act:
+        if t is not None and t.dtype != x.dtype:
             raise TypeError("%s must have x's dtype" % name)
-    for name, t in (("A_log", A_log), ("D", D), ("initial_states", initial_states)):
+    f32s = (("A_log", A_log), ("D", D), ("initial_states", initial_states)) + tuple(
+        (n, t) for n, t, f32 in extra if f32)
+    for name, t in f32s:
         if t is not None and t.dtype != torch.float32:
             raise TypeError("%s must be float32" % name)
     if seq_idx is not None and seq_idx.dtype != torch.int32:
         raise TypeError("seq_idx must be int32")
-    for t in (x, dt, A_log, B, C, D, initial_states, seq_idx):
+    for t in (x, dt, A_log, B, C, D, initial_states, seq_idx) + tuple(t for _, t, _ in extra):
         if t is not None and (t.device != dev or not t.is_contiguous()):
             raise ValueError("all tensors must be contiguous and on x's device")
     b, T, H, P = x.shape
@@ -171,12 +218,49 @@ def forward(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=No
         fin = final_out if final_out is not None else torch.empty(
             (units, H, P, N), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
-    rc = ssd_forward(prob, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),
-                     _ptr(initial_states), _ptr(seq_idx), _ptr(y), _ptr(fin),
-                     _ptr(workspace), wsb, stream)
+    args = (_ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D), _ptr(initial_states),
+            _ptr(seq_idx), _ptr(y), _ptr(fin), _ptr(workspace), wsb, stream)
+    if opts is None:
+        rc, where = ssd_forward(prob, *args), "ssd_forward"
+    else:
+        rc, where = ssd_forward_block(prob, opts, *args), "ssd_forward_block"
     if rc != SSD_OK:
-        raise SsdError(rc, "ssd_forward")
+        raise SsdError(rc, where)
     return y, fin
+
+
+def forward(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=None,
+            seq_idx=None, nseq: Optional[int] = None, return_final_states: bool = True,
+            workspace=None, out=None, final_out=None) -> Tuple[object, object]:
+    """SSD forward on device tensors; returns ``(y, final_states or None)``.
+
+    x (b,T,H,P), dt (b,T,H), B/C (b,T,G,N): float32 or bfloat16, all the same
+    dtype, contiguous, on one HIP device.  A_log, D (H): float32.
+    initial_states (b|nseq,H,P,N) float32.  seq_idx (1,T) int32 with nseq
+    sequences.  Launches on torch's current stream of x's device.
+    """
+    return _call(None, x, dt, A_log, B, C, D, chunk_size, initial_states, seq_idx, nseq,
+                 return_final_states, workspace, out, final_out)
+
+
+def forward_block(x, dt, A_log, B, C, D=None, chunk_size: int = 256, initial_states=None,
+                  seq_idx=None, nseq: Optional[int] = None, dt_bias=None, dt_softplus: bool = True,
+                  dt_min: float = 0.0, dt_max: float = float("inf"), z=None, norm_weight=None,
+                  norm_group_size: int = 0, norm_eps: float = 1e-5,
+                  return_final_states: bool = True, workspace=None, out=None,
+                  final_out=None) -> Tuple[object, object]:
+    """The layer with the block steps around it (``ssd_forward_block``):
+    ``dt`` is the raw value (softplus of dt + dt_bias, clamped to
+    [dt_min, dt_max]); the output is gated by SiLU(z) when ``z`` is given and
+    RMS-normalised over groups of ``norm_group_size`` channels when that is
+    positive.  z has x's dtype and shape; dt_bias (H) and norm_weight (H*P)
+    are float32."""
+    opts = make_block_opts(dt_bias, dt_softplus, dt_min, dt_max, z, norm_weight,
+                           norm_group_size, norm_eps)
+    return _call(opts, x, dt, A_log, B, C, D, chunk_size, initial_states, seq_idx, nseq,
+                 return_final_states, workspace, out, final_out,
+                 extra=(("z", z, False), ("dt_bias", dt_bias, True),
+                        ("norm_weight", norm_weight, True)))
 
 
 def ssd_decode_step(prob: SsdProblem, x, dt, A_log, B, C, D, state, y, stream) -> int:

@@ -1,5 +1,6 @@
 """Host-side checks of the C ABI: the library loads, exports what the header
 declares, and rejects invalid arguments before touching the device."""
+import ctypes
 import os
 import re
 import subprocess
@@ -121,8 +122,47 @@ def test_decode_step_validation(lib):
     assert dec(prob(seqlen=0, chunk_size=48), x=0) == ssd.SSD_ERR_NULL_ARG
 
 
+def test_block_validation(lib):
+    inf = float("inf")
+
+    def blk(opts, p=None, ws_bytes=0, y=FAKE):
+        return ssd.ssd_forward_block(p or prob(), opts, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, 0, y, 0,
+                                     0, ws_bytes, 0)
+
+    def opts(**kw):
+        base = dict(dt_bias=None, dt_softplus=True, dt_min=0.0, dt_max=inf, z=None, norm_weight=None,
+                    norm_group_size=0, norm_eps=1e-5)
+        base.update(kw)
+        o = ssd.SsdBlockOpts()
+        for k, v in base.items():
+            setattr(o, k, v)
+        return o
+
+    # valid options get as far as the workspace check (no workspace given)
+    assert blk(opts()) == ssd.SSD_ERR_WORKSPACE
+    assert blk(opts(z=FAKE, norm_group_size=64, norm_weight=FAKE)) == ssd.SSD_ERR_WORKSPACE
+    assert blk(opts(norm_group_size=80 * 64)) == ssd.SSD_ERR_WORKSPACE
+    assert blk(opts(dt_min=0.5, dt_max=0.5)) == ssd.SSD_ERR_WORKSPACE
+    assert lib.ssd_forward_block(prob(), None, *([FAKE] * 5), None, None, None, FAKE, None, FAKE,
+                                 0, None) == ssd.SSD_ERR_NULL_ARG
+    for bad in (dict(dt_min=-1.0), dict(dt_min=2.0, dt_max=1.0), dict(dt_max=float("nan")),
+                dict(norm_group_size=32), dict(norm_group_size=64 * 3), dict(norm_group_size=-64),
+                dict(norm_group_size=64, norm_eps=-1.0), dict(norm_group_size=64, norm_eps=inf)):
+        assert blk(opts(**bad)) == ssd.SSD_ERR_BAD_OPTION, bad
+    # the output pass reads 16-byte vectors
+    assert blk(opts(z=FAKE + 2)) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert blk(opts(norm_group_size=64), y=FAKE + 8) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert blk(opts(norm_group_size=64, norm_weight=FAKE + 4)) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    # shape errors come first, as in ssd_forward
+    assert blk(opts(dt_min=-1.0), p=prob(chunk_size=48)) == ssd.SSD_ERR_BAD_CHUNK
+    size = ctypes.c_size_t(0)
+    assert lib.ssd_block_workspace_bytes(prob(), None, ctypes.byref(size)) == ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_block_workspace_bytes(prob(), ctypes.byref(opts()), ctypes.byref(size)) == ssd.SSD_OK
+    assert size.value == ssd.ssd_workspace_bytes(prob())
+
+
 def test_error_strings(lib):
-    for code in range(0, -10, -1):
+    for code in range(0, -11, -1):
         s = ssd.ssd_error_string(code)
         assert s and s != "unknown ssd status"
     assert ssd.ssd_error_string(-100) == "unknown ssd status"
