@@ -68,17 +68,24 @@ int validate(const ssd_problem* prob, bool has_seq_idx, Shape* s)
 
 constexpr int64_t kMaxElemsPublic = kMaxElems;
 
-// Heads per workgroup of the fused path: a divisor of the heads per group
-// (a workgroup's heads share B and C).  SSD_HEADS_PER_WG overrides the default
+// Heads per work item of the fused path: a divisor of the heads per group (an
+// item's heads share B and C).  More heads per item share more of the item's
+// set-up (Gram tiles, B^T and C fragments); fewer give more items.  The
+// largest of 4, 2 that leaves at least two items per compute unit (measured
+// best at the 130M and 2.7B layer shapes), else the largest that leaves one,
+// else 1.  SSD_HEADS_PER_WG overrides it
 // (tuning knob; ignored unless it divides the heads per group).
-int64_t heads_per_workgroup(int64_t heads_per_group)
+int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units)
 {
     if (const char* env = std::getenv("SSD_HEADS_PER_WG")) {
         const long v = std::strtol(env, nullptr, 10);
         if (v >= 1 && heads_per_group % v == 0) return v;
     }
-    for (int64_t hg : {4, 2, 1})
-        if (heads_per_group % hg == 0) return hg;
+    // items_per_head: chunks x batch rows x groups, the items at one head per item
+    for (int64_t need : {2, 1})
+        for (int64_t hg : {4, 2})
+            if (heads_per_group % hg == 0 && items_per_head * (heads_per_group / hg) >= need * compute_units)
+                return hg;
     return 1;
 }
 
@@ -183,7 +190,11 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.N = s.N;
         f.G = s.G;
         f.nC = s.nC;
-        f.HG = ssd::heads_per_workgroup(s.H / s.G);
+        int dev = 0, cus = 256;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return SSD_ERR_LAUNCH;
+        f.HG = ssd::heads_per_workgroup(s.H / s.G, s.nC * s.b * s.G, cus);
         f.x = x;
         f.dt = dt;
         f.A_log = A_log;

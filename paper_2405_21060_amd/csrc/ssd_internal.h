@@ -82,7 +82,7 @@ struct FusedLayout {
     size_t gram, BT, ring, flags, ticket, total;
 };
 
-int64_t heads_per_workgroup(int64_t heads_per_group);
+int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units);
 bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16, bool varlen);
 FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC);
 hipError_t launch_fused(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin,

@@ -195,6 +195,11 @@ WORKLOADS = {
     "sweep_T16384_N256": Problem(4, 16384, 80, 64, 256, 1, 256, "bf16"),
     "varlen_g8": Problem(1, 32768, 64, 64, 128, 8, 256, "bf16", varlen=True,
                          init_states=True),
+    # one GPU's share of the 2.7B layer under 8-way sharding: heads (tensor
+    # parallel, B and C replicated) or the sequence (context parallel: each
+    # rank's span with the state entering it)
+    "tp8_2p7b": Problem(4, 4096, 10, 64, 128, 1, 256, "bf16"),
+    "cp8_2p7b": Problem(4, 512, 80, 64, 128, 1, 256, "bf16", init_states=True),
 }
 
 

@@ -157,7 +157,7 @@ def test_chunk_size_independence_large():
 # Full-size workloads: every head of the GPU result is produced; the oracle
 # checks a sample of heads (first, last, and a middle one per group span).
 FULL = ["mamba2_130m", "mamba2_2p7b", "varlen_g8", "sweep_T512_N128",
-        "sweep_T65536_N128", "sweep_T16384_N64", "sweep_T16384_N256"]
+        "sweep_T65536_N128", "sweep_T16384_N64", "sweep_T16384_N256", "tp8_2p7b", "cp8_2p7b"]
 
 
 @pytest.mark.parametrize("name", FULL)
