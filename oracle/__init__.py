@@ -10,6 +10,9 @@ shares no code with the HIP path.
 * :mod:`oracle.chunked` -- the block decomposition of Section 6 written out step
   by step in float64 numpy, exposing its intermediates (chunk cumsums, chunk
   states, states entering chunks) for per-step comparisons.
+* :mod:`oracle.span` -- a sequence split into spans (Section 8.2 state
+  passing with the scan operator of Appendix B): span decays, the combine of
+  (decay, state) pairs, and the output a span's entering state adds.
 * :mod:`oracle.block` -- the Mamba-2 block steps on either side of the layer
   (dt parameterisation; gate ``y * SiLU(z)`` and grouped RMS normalisation of
   Sections 7.1 and 8.1) around :func:`forward`.
