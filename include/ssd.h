@@ -197,6 +197,45 @@ int ssd_forward_block_timed(const ssd_problem* prob, const ssd_block_opts* opts,
                             void* workspace, size_t workspace_bytes, void* stream,
                             void* event_begin, void* event_end);
 
+/* Sequence spans (context parallelism, Section 8.2).  A sequence cut into
+ * consecutive spans (one per GPU, say) is computed span by span from zero
+ * states with ssd_forward, giving each span's outputs and final state; then
+ *   ssd_span_decay     the span's total decay exp(A_h sum_t dt_t), per
+ *                      (batch, head);
+ *   ssd_span_combine   from every span's (decay, final state) pair, the state
+ *                      entering every span and the final state of the whole
+ *                      sequence: the exclusive scan under the scalar-SSM
+ *                      operator of Appendix B, (a, h) then (a', h') =
+ *                      (a a', a' h + h');
+ *   ssd_span_correct   y_t += exp(A_h sum_{s<=t} dt_s) (h_in C_t) over the
+ *                      span (sums from its first token), which turns the
+ *                      zero-state outputs into those of the whole sequence.
+ * Across GPUs the (decay, final state) pairs are exchanged between the first
+ * and the second step (an all-gather); that exchange is not part of this
+ * library.  `prob` describes one span (seqlen = its length); chunk_size and
+ * nseq are ignored; packed rows are not supported.  Layouts: dt (batch,
+ * seqlen, nheads) dtype, already positive; A_log (nheads) float32; decay
+ * (batch, nheads) float32; states (batch, nheads, headdim, dstate) float32,
+ * 16-byte aligned; for ssd_span_combine, decay (nspans, batch, nheads) and
+ * local_final / entering (nspans, batch, nheads, headdim, dstate), span
+ * order; initial_states may be NULL (zero), final_states may be NULL; C
+ * (batch, seqlen, ngroups, dstate) dtype; y (batch, seqlen, nheads, headdim)
+ * dtype, updated in place (rounded to dtype).  bf16 products run on the
+ * matrix cores with the entering state rounded to bf16.  Errors as for
+ * ssd_forward. */
+int ssd_span_decay(const ssd_problem* prob, const void* dt, const float* A_log, float* decay, void* stream);
+
+int ssd_span_combine(int64_t nspans, const ssd_problem* prob, const float* decay,
+                     const float* local_final, const float* initial_states, float* entering,
+                     float* final_states, void* stream);
+
+/* Workspace of ssd_span_correct (per-chunk dt sums). */
+int ssd_span_correct_workspace_bytes(const ssd_problem* prob, size_t* bytes);
+
+int ssd_span_correct(const ssd_problem* prob, const void* dt, const float* A_log, const void* C,
+                     const float* entering, void* y, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);
 

@@ -348,6 +348,91 @@ extern "C" int ssd_decode_step(const ssd_problem* prob, const void* x, const voi
     return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
+namespace {
+
+// Shape checks of the span entry points: those of ssd_forward, without the
+// chunk size (spans use their own tiling) and without packed rows.
+int validate_span(const ssd_problem* prob)
+{
+    if (!prob) return SSD_ERR_NULL_ARG;
+    ssd_problem q = *prob;
+    q.chunk_size = 256;
+    ssd::Shape s;
+    return ssd::validate(&q, false, &s);
+}
+
+}  // namespace
+
+extern "C" int ssd_span_decay(const ssd_problem* prob, const void* dt, const float* A_log, float* decay,
+                              void* stream)
+{
+    const int rc = validate_span(prob);
+    if (rc != SSD_OK) return rc;
+    if (!dt || !A_log || !decay) return SSD_ERR_NULL_ARG;
+    const hipError_t err = ssd::launch_span_decay(prob->batch, prob->seqlen, prob->nheads, dt, A_log, decay,
+                                                  prob->dtype == SSD_DTYPE_BF16, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
+extern "C" int ssd_span_combine(int64_t nspans, const ssd_problem* prob, const float* decay,
+                                const float* local_final, const float* initial_states, float* entering,
+                                float* final_states, void* stream)
+{
+    const int rc = validate_span(prob);
+    if (rc != SSD_OK) return rc;
+    if (nspans < 1 || nspans > 65536) return SSD_ERR_BAD_SHAPE;
+    if (!decay || !local_final || !entering) return SSD_ERR_NULL_ARG;
+    const auto a16 = [](const void* q) { return reinterpret_cast<uintptr_t>(q) % 16 == 0; };
+    if (!a16(local_final) || !a16(entering) || !a16(initial_states) || !a16(final_states))
+        return SSD_ERR_UNSUPPORTED_DIMS;
+    const int64_t PN = prob->headdim * prob->dstate;
+    if (static_cast<double>(nspans) * prob->batch * prob->nheads * PN > 16.0 * ssd::kMaxElemsPublic)
+        return SSD_ERR_TOO_LARGE;
+    const hipError_t err = ssd::launch_span_combine(nspans, prob->batch * prob->nheads, PN, decay, local_final,
+                                                    initial_states, entering, final_states,
+                                                    static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
+extern "C" int ssd_span_correct_workspace_bytes(const ssd_problem* prob, size_t* bytes)
+{
+    if (!bytes) return SSD_ERR_NULL_ARG;
+    const int rc = validate_span(prob);
+    if (rc != SSD_OK) return rc;
+    *bytes = sizeof(float) * static_cast<size_t>(prob->batch * prob->nheads * ssd::span_chunks(prob->seqlen));
+    return SSD_OK;
+}
+
+extern "C" int ssd_span_correct(const ssd_problem* prob, const void* dt, const float* A_log, const void* C,
+                                const float* entering, void* y, void* workspace, size_t workspace_bytes,
+                                void* stream)
+{
+    size_t need = 0;
+    const int rc = ssd_span_correct_workspace_bytes(prob, &need);
+    if (rc != SSD_OK) return rc;
+    if (!dt || !A_log || !C || !entering || !y) return SSD_ERR_NULL_ARG;
+    const auto a16 = [](const void* q) { return reinterpret_cast<uintptr_t>(q) % 16 == 0; };
+    if (!a16(C) || !a16(entering) || !a16(y)) return SSD_ERR_UNSUPPORTED_DIMS;   // 16-byte vectors
+    if (!workspace || workspace_bytes < need) return SSD_ERR_WORKSPACE;
+    ssd::SpanParams p;
+    p.b = prob->batch;
+    p.T = prob->seqlen;
+    p.H = prob->nheads;
+    p.P = prob->headdim;
+    p.N = prob->dstate;
+    p.G = prob->ngroups;
+    p.nC = ssd::span_chunks(prob->seqlen);
+    p.dt = dt;
+    p.A_log = A_log;
+    p.C = C;
+    p.entering = entering;
+    p.y = y;
+    p.sums = static_cast<float*>(workspace);
+    const hipError_t err =
+        ssd::launch_span_correct(p, prob->dtype == SSD_DTYPE_BF16, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
 extern "C" const char* ssd_error_string(int code)
 {
     switch (code) {

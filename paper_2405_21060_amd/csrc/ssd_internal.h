@@ -116,4 +116,22 @@ struct GateNormParams {
 
 hipError_t launch_gate_norm(const GateNormParams& p, bool bf16, hipStream_t stream);
 
+// Sequence spans (context parallelism).
+struct SpanParams {
+    int64_t b, T, H, P, N, G, nC;   // T: the span's length; nC: its 256-token chunks
+    const void* dt;                 // (b, T, H)
+    const float* A_log;
+    const void* C;                  // (b, T, G, N)
+    const float* entering;          // (b, H, P, N)
+    void* y;                        // (b, T, H, P), updated in place
+    float* sums;                    // workspace (b, H, nC): dt sums per chunk
+};
+
+int64_t span_chunks(int64_t T);
+hipError_t launch_span_decay(int64_t b, int64_t T, int64_t H, const void* dt, const float* A_log, float* decay,
+                             bool bf16, hipStream_t stream);
+hipError_t launch_span_combine(int64_t R, int64_t bh, int64_t PN, const float* decay, const float* local,
+                               const float* init, float* entering, float* fin, hipStream_t stream);
+hipError_t launch_span_correct(const SpanParams& p, bool bf16, hipStream_t stream);
+
 }  // namespace ssd

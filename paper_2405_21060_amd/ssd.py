@@ -37,6 +37,7 @@ SSD_ERR_BAD_OPTION = -10
 
 EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
             "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
+            "ssd_span_decay", "ssd_span_combine", "ssd_span_correct_workspace_bytes", "ssd_span_correct",
             "ssd_error_string")
 
 
@@ -103,6 +104,15 @@ def load_library(path: str = LIB_PATH):
         vp, ctypes.c_size_t, vp]
     lib.ssd_forward_block_timed.restype = ctypes.c_int
     lib.ssd_forward_block_timed.argtypes = lib.ssd_forward_block.argtypes + [vp, vp]
+    pp = ctypes.POINTER(SsdProblem)
+    lib.ssd_span_decay.restype = ctypes.c_int
+    lib.ssd_span_decay.argtypes = [pp, vp, vp, vp, vp]
+    lib.ssd_span_combine.restype = ctypes.c_int
+    lib.ssd_span_combine.argtypes = [ctypes.c_int64, pp, vp, vp, vp, vp, vp, vp]
+    lib.ssd_span_correct_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_span_correct_workspace_bytes.argtypes = [pp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_span_correct.restype = ctypes.c_int
+    lib.ssd_span_correct.argtypes = [pp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ssd_error_string.restype = ctypes.c_char_p
     lib.ssd_error_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -304,4 +314,65 @@ def decode_step(x, dt, A_log, B, C, state, D=None, out=None):
                          _ptr(state), _ptr(y), torch.cuda.current_stream(dev).cuda_stream)
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_decode_step")
+    return y
+
+
+def _span_problem(dt, C, P):
+    import torch
+
+    b, T, H = dt.shape
+    G, N = C.shape[2], C.shape[3]
+    dtype = SSD_DTYPE_BF16 if dt.dtype == torch.bfloat16 else SSD_DTYPE_F32
+    return make_problem(b, T, H, P, N, G, 256, dtype, 0)
+
+
+def span_decay(dt, A_log, P: int = 64, N: int = 16, out=None):
+    """Total decay exp(A_h sum_t dt_t) of a span, (batch, nheads) float32.
+    P and N only need to be valid layer dimensions (they play no part)."""
+    import torch
+
+    b, T, H = dt.shape
+    prob = make_problem(b, T, H, P, N, 1, 256, SSD_DTYPE_BF16 if dt.dtype == torch.bfloat16 else SSD_DTYPE_F32, 0)
+    out = out if out is not None else torch.empty((b, H), dtype=torch.float32, device=dt.device)
+    rc = load_library().ssd_span_decay(ctypes.byref(prob), _ptr(dt), _ptr(A_log), _ptr(out),
+                                       torch.cuda.current_stream(dt.device).cuda_stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_span_decay")
+    return out
+
+
+def span_combine(decays, local_finals, initial_states=None):
+    """States entering every span and the final state, from per-span (decay,
+    zero-state final state) pairs: decays (R, b, H), local_finals (R, b, H, P, N)."""
+    import torch
+
+    R, b, H, P, N = local_finals.shape
+    prob = make_problem(b, 1, H, P, N, 1, 256, SSD_DTYPE_F32, 0)
+    entering = torch.empty_like(local_finals)
+    final = torch.empty_like(local_finals[0])
+    rc = load_library().ssd_span_combine(R, ctypes.byref(prob), _ptr(decays), _ptr(local_finals),
+                                         _ptr(initial_states), _ptr(entering), _ptr(final),
+                                         torch.cuda.current_stream(local_finals.device).cuda_stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_span_combine")
+    return entering, final
+
+
+def span_correct(dt, A_log, C, entering, y, workspace=None):
+    """y += the output the entering state (b, H, P, N) produces over the span
+    (in place); dt (b, T, H), C (b, T, G, N), y (b, T, H, P)."""
+    import torch
+
+    prob = _span_problem(dt, C, y.shape[3])
+    need = ctypes.c_size_t(0)
+    rc = load_library().ssd_span_correct_workspace_bytes(ctypes.byref(prob), ctypes.byref(need))
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_span_correct_workspace_bytes")
+    if workspace is None or workspace.numel() < need.value:
+        workspace = torch.empty(max(int(need.value), 1), dtype=torch.uint8, device=y.device)
+    rc = load_library().ssd_span_correct(ctypes.byref(prob), _ptr(dt), _ptr(A_log), _ptr(C), _ptr(entering),
+                                         _ptr(y), _ptr(workspace), int(need.value),
+                                         torch.cuda.current_stream(y.device).cuda_stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_span_correct")
     return y

@@ -161,6 +161,27 @@ def test_block_validation(lib):
     assert size.value == ssd.ssd_workspace_bytes(prob())
 
 
+def test_span_validation(lib):
+    size = ctypes.c_size_t(0)
+    assert ssd.load_library().ssd_span_decay(None, FAKE, FAKE, FAKE, 0) == ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_span_decay(ctypes.byref(prob(dstate=8)), FAKE, FAKE, FAKE, None) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert lib.ssd_span_decay(ctypes.byref(prob()), None, FAKE, FAKE, None) == ssd.SSD_ERR_NULL_ARG
+    # chunk_size plays no part in the span entry points
+    assert lib.ssd_span_decay(ctypes.byref(prob(chunk_size=48)), None, FAKE, FAKE, None) == ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_span_combine(0, ctypes.byref(prob()), FAKE, FAKE, None, FAKE, None, None) == ssd.SSD_ERR_BAD_SHAPE
+    assert lib.ssd_span_combine(2, ctypes.byref(prob()), FAKE, FAKE + 4, None, FAKE, None, None) == \
+        ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert lib.ssd_span_combine(2, ctypes.byref(prob()), FAKE, None, None, FAKE, None, None) == ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_span_correct_workspace_bytes(ctypes.byref(prob()), ctypes.byref(size)) == ssd.SSD_OK
+    assert size.value == 4 * 4 * 80 * 16   # one float per (batch, head, 256-token chunk)
+    assert lib.ssd_span_correct(ctypes.byref(prob()), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == \
+        ssd.SSD_ERR_WORKSPACE
+    assert lib.ssd_span_correct(ctypes.byref(prob()), FAKE, FAKE, FAKE + 8, FAKE, FAKE, FAKE, 1 << 30, None) == \
+        ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert lib.ssd_span_correct(ctypes.byref(prob()), FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == \
+        ssd.SSD_ERR_NULL_ARG
+
+
 def test_error_strings(lib):
     for code in range(0, -11, -1):
         s = ssd.ssd_error_string(code)
