@@ -262,6 +262,80 @@ def block_bench(args, torch, ssd):
     }), flush=True)
 
 
+def cp_bench(args, torch, ssd):
+    """One rank's share of an 8-way sequence split of the 2.7B layer (512 of
+    4096 tokens per batch row): the layer from a zero state on the span, the
+    span decay and the correction by the state entering the span (the
+    exchange of (decay, state) pairs between GPUs is not part of this build;
+    the combine of all 8 pairs runs here on one GPU and is timed apart)."""
+    from paper_2405_21060_amd.inputs import Problem, make_inputs
+    from tests.ssd_harness import to_device
+
+    R = 8
+    p = Problem(4, 4096 // R, 80, 64, 128, 1, 256, "bf16", init_states=True)
+    inp = make_inputs(p, args.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sets = [to_device(inp) for _ in range(max(1, args.copies))]
+    prob = ssd.make_problem(p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups, p.chunk_size,
+                            ssd.SSD_DTYPE_BF16, 0)
+    wsb = ssd.ssd_workspace_bytes(prob)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    y = [torch.empty_like(c["x"]) for c in sets]
+    fin = torch.empty((p.batch, p.nheads, p.headdim, p.dstate), dtype=torch.float32, device=dev)
+    decay = torch.empty((p.batch, p.nheads), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ptr = lambda t: None if t is None else t.data_ptr()
+    decays = torch.rand((R, p.batch, p.nheads), device=dev)
+    locals_ = torch.randn((R, p.batch, p.nheads, p.headdim, p.dstate), device=dev)
+
+    lib = ssd.load_library()
+    import ctypes
+
+    cwsb = ctypes.c_size_t(0)
+    lib.ssd_span_correct_workspace_bytes(ctypes.byref(prob), ctypes.byref(cwsb))
+    cws = torch.empty(max(int(cwsb.value), 1), dtype=torch.uint8, device=dev)
+
+    def rank_step(i):
+        # raw ABI calls (no per-call Python work beyond the calls themselves)
+        c = sets[i % len(sets)]
+        s_ = stream.cuda_stream
+        rc = ssd.ssd_forward(prob, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]), ptr(c["C"]),
+                             ptr(c["D"]), None, None, ptr(y[i % len(sets)]), ptr(fin), ptr(ws), wsb, s_)
+        rc = rc or lib.ssd_span_decay(ctypes.byref(prob), ptr(c["dt"]), ptr(c["A_log"]), ptr(decay), s_)
+        rc = rc or lib.ssd_span_correct(ctypes.byref(prob), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["C"]),
+                                        ptr(c["initial_states"]), ptr(y[i % len(sets)]), ptr(cws),
+                                        int(cwsb.value), s_)
+        if rc != 0:
+            raise ssd.SsdError(rc, "context-parallel rank step")
+
+    def timed(fn):
+        for i in range(args.warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for i in range(args.steps):
+            fn(i)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / args.steps
+
+    ms = timed(rank_step)
+    ms_combine = timed(lambda i: ssd.span_combine(decays, locals_, None))
+    tokens = p.batch * p.seqlen
+    print(json.dumps({
+        "metric": "SSD context-parallel rank share tokens/s (2.7B layer, 8-way sequence split, 1 GPU's span)",
+        "value": tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded; Mamba-2 layer shapes)",
+        "config": {"workload": "cp8_rank_2p7b", "batch": p.batch, "span": p.seqlen, "ranks": R,
+                   "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate},
+        "combine_8_spans_ms": ms_combine,
+        "note": "per rank: layer from a zero state, span decay, entering-state correction",
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,6 +354,8 @@ def main():
     ap.add_argument("--block", action="store_true",
                     help="time the layer with the block steps around it (ssd_forward_block) instead")
     ap.add_argument("--block-norm-group", type=int, default=64)
+    ap.add_argument("--cp-share", action="store_true",
+                    help="time one rank's share of an 8-way sequence split instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -317,6 +393,8 @@ def main():
         return decode_bench(args, torch, ssd)
     if args.block:
         return block_bench(args, torch, ssd)
+    if args.cp_share:
+        return cp_bench(args, torch, ssd)
 
     p = WORKLOADS[args.workload]
     inp = make_inputs(p, args.seed)

@@ -22,6 +22,7 @@ namespace {
 
 constexpr int kSpanThreads = 256;
 constexpr int kSpanQ = 256;          // tokens per workgroup of the correction
+constexpr int kMaxPT = 8;            // 16-row p-tiles of the largest head dimension (128)
 
 template <typename T>
 __device__ __forceinline__ float ld_act(const T* p, int64_t i) { return Act<T>::load(p, i); }
@@ -137,18 +138,28 @@ __global__ __launch_bounds__(kSpanThreads) void k_span_correct_bf16(SpanParams p
     const int L = static_cast<int>(kSpanQ < p.T - t0 ? kSpanQ : p.T - t0);
     const int P = static_cast<int>(p.P), N = static_cast<int>(p.N);
 
-    // the entering state, rounded to bf16 (zero-padded columns up to NP)
-    const float* Eg = p.entering + bh * p.P * p.N;
-    for (int i = threadIdx.x; i < P * NP; i += kSpanThreads) {
-        const int pr = i / NP, n = i - pr * NP;
-        uint16_t v = 0;
-        if (n < N) {   // round to nearest even
-            uint32_t u = __float_as_uint(Eg[pr * N + n]);
-            u += 0x7FFFu + ((u >> 16) & 1u);
-            v = static_cast<uint16_t>(u >> 16);
+    // the entering state, rounded to bf16 (zero-padded columns up to NP): float4
+    // loads, 8-byte LDS stores
+    const float4* Eg4 = reinterpret_cast<const float4*>(p.entering + bh * p.P * p.N);
+    const int quads = P * N / 4, qrow = N / 4;
+#pragma unroll 8
+    for (int i = threadIdx.x; i < quads; i += kSpanThreads) {
+        const float4 f = Eg4[i];
+        const int pr = i / qrow, n = 4 * (i - pr * qrow);
+        const float fv[4] = {f.x, f.y, f.z, f.w};
+        uint32_t hv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {   // round to nearest even
+            const uint32_t u = __float_as_uint(fv[e]);
+            hv[e] = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
         }
-        E[pr * ES + n] = v;
+        *reinterpret_cast<uint2*>(E + pr * ES + n) = make_uint2(hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16));
     }
+    if (NP > N)
+        for (int i = threadIdx.x; i < P * (NP - N); i += kSpanThreads) {
+            const int pr = i / (NP - N);
+            E[pr * ES + N + (i - pr * (NP - N))] = 0;
+        }
     chunk_decays<uint16_t>(p, c, b, h, L, ev, scr);   // ends with a barrier
 
     const int lane = threadIdx.x & 63, r = lane & 15, lg = lane >> 4;
@@ -160,22 +171,37 @@ __global__ __launch_bounds__(kSpanThreads) void k_span_correct_bf16(SpanParams p
         if (16 * (4 * w + s) >= L) break;                        // strip entirely past the span's end
         const int tc = tl < L ? tl : L - 1;
         const uint16_t* crow = Cb + ((b * p.T + t0 + tc) * p.G + g) * p.N;
-        for (int pt = 0; pt < P / 16; ++pt) {
+        // the strip's C fragments (shared by every p-tile) and the y values the
+        // lane updates, requested together
+        uint4 cf[KN];
+#pragma unroll
+        for (int k = 0; k < KN; ++k) {
+            const int n0 = 32 * k + 8 * lg;
+            cf[k] = n0 < N ? *reinterpret_cast<const uint4*>(crow + n0) : make_uint4(0, 0, 0, 0);
+        }
+        const int64_t yrow = ((b * p.T + t0 + tc) * p.H + h) * p.P + 4 * lg;
+        uint2 yo[kMaxPT];
+#pragma unroll
+        for (int pt = 0; pt < kMaxPT; ++pt)
+            if (pt < P / 16) yo[pt] = *reinterpret_cast<const uint2*>(y + yrow + 16 * pt);
+        const float e = ev[tl];
+#pragma unroll
+        for (int pt = 0; pt < kMaxPT; ++pt) {
+            if (pt >= P / 16) break;
             f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int k = 0; k < KN; ++k) {
-                const int n0 = 32 * k + 8 * lg;
-                const uint4 bv = n0 < N ? *reinterpret_cast<const uint4*>(crow + n0) : make_uint4(0, 0, 0, 0);
-                const uint4 av = *reinterpret_cast<const uint4*>(E + (16 * pt + r) * ES + n0);
+                const uint4 av = *reinterpret_cast<const uint4*>(E + (16 * pt + r) * ES + 32 * k + 8 * lg);
                 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                              __builtin_bit_cast(bf16x8_t, bv), acc, 0, 0, 0);
+                                                              __builtin_bit_cast(bf16x8_t, cf[k]), acc, 0, 0, 0);
             }
             if (tl < L) {
-                const float e = ev[tl];
-                const int64_t yi = ((b * p.T + t0 + tl) * p.H + h) * p.P + 16 * pt + 4 * lg;
+                const uint2 o = yo[pt];
+                const float yv[4] = {__uint_as_float(o.x << 16), __uint_as_float(o.x & 0xFFFF0000u),
+                                     __uint_as_float(o.y << 16), __uint_as_float(o.y & 0xFFFF0000u)};
+                uint16_t* dst = y + yrow + 16 * pt;
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    Act<uint16_t>::store(y, yi + v, Act<uint16_t>::load(y, yi + v) + e * acc[v]);
+                for (int v = 0; v < 4; ++v) Act<uint16_t>::store(dst, v, yv[v] + e * acc[v]);
             }
         }
     }
