@@ -103,6 +103,34 @@ __device__ __forceinline__ f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c)
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront, in registers (DPP):
+// shifts by 1, 2, 4 and 8 lanes scan each 16-lane row; broadcasts of lane 15
+// (into rows 1 and 3) and of lane 31 (into rows 2 and 3) carry the row totals
+// upward.  Lanes without a source add the `old` operand, zero.
+__device__ __forceinline__ float wave_inclusive_scan(float v)
+{
+#define SSD_DPP_ADD(ctrl, rows) \
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, rows, 0xF, false))
+    SSD_DPP_ADD(0x111, 0xF);   // row_shr:1
+    SSD_DPP_ADD(0x112, 0xF);   // row_shr:2
+    SSD_DPP_ADD(0x114, 0xF);   // row_shr:4
+    SSD_DPP_ADD(0x118, 0xF);   // row_shr:8
+    SSD_DPP_ADD(0x142, 0xA);   // row_bcast:15
+    SSD_DPP_ADD(0x143, 0xC);   // row_bcast:31
+#undef SSD_DPP_ADD
+    return v;
+}
+
+// The value of the last lane of this lane's 16-lane row.
+__device__ __forceinline__ float row_last(float v, int lane)
+{
+    const int i = __float_as_int(v);
+    const int r0 = __builtin_amdgcn_readlane(i, 15), r1 = __builtin_amdgcn_readlane(i, 31);
+    const int r2 = __builtin_amdgcn_readlane(i, 47), r3 = __builtin_amdgcn_readlane(i, 63);
+    const int g = lane >> 4;
+    return __int_as_float(g == 0 ? r0 : g == 1 ? r1 : g == 2 ? r2 : r3);
+}
+
 // Drain this wavefront's outstanding vector-memory operations.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -687,11 +715,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             }
         }
         incl = d * (-expf(A_logp[h]) * kLog2e);
-#pragma unroll
-        for (int sh = 1; sh < 64; sh <<= 1) {
-            const float o = __shfl_up(incl, sh, 64);
-            if (lane >= sh) incl += o;
-        }
+        incl = wave_inclusive_scan(incl);
         if (lane == 63) wt[wave] = incl;
     }
     lds_barrier();
@@ -704,7 +728,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             if (k < wave) pre += v;
         }
         const float cst = incl + pre;
-        const float cend = __shfl(cst, lane | 15, 64);   // end of this token's 16-token tile
+        const float cend = row_last(cst, lane);   // end of this token's 16-token tile
         cs[tid] = cst;
         dt[tid] = d;
         vf[tid] = d * exp2f(cend - cst);
