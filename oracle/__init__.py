@@ -10,6 +10,9 @@ shares no code with the HIP path.
 * :mod:`oracle.chunked` -- the block decomposition of Section 6 written out step
   by step in float64 numpy, exposing its intermediates (chunk cumsums, chunk
   states, states entering chunks) for per-step comparisons.
+* :mod:`oracle.backward` -- gradients of the layer: the adjoint of the
+  recurrence, token by token in reverse (the paper gives no backward
+  algorithm); pinned by finite differences of :func:`forward`.
 * :mod:`oracle.span` -- a sequence split into spans (Section 8.2 state
   passing with the scan operator of Appendix B): span decays, the combine of
   (decay, state) pairs, and the output a span's entering state adds.
