@@ -610,6 +610,22 @@ __device__ __forceinline__ void dma_gram(u16* gr, const FusedParams& p, const It
     for (int blk = wave; blk < kBlocks; blk += kWaves) copy16_to_lds(rs, gr + blk * 512, o.l16, blk * 1024);
 }
 
+// The Gram tile rows {wave, 15 - wave} of an item (the only rows this
+// wavefront's diagonal block reads) into LDS: 1 KiB copies, the last one of
+// the odd-length row by half the lanes -- 9 copies for every wavefront.
+__device__ __forceinline__ void dma_gram_rows(u16* gr, const FusedParams& p, const Item& it, int wave, int lane)
+{
+    const i32x4 rs = buffer_rsrc(p.gram + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * kTiles * 256,
+                                 kTiles * 512);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int row = k == 0 ? wave : kNQ - 1 - wave;
+        const int off = tile_index(row, 0) * 512, bytes = (row + 1) * 512;
+        for (int o = 0; o < bytes; o += 1024)
+            if (bytes - o >= 1024 || lane < 32) copy16_to_lds(rs, gr + (off + o) / 2, 16 * lane, off + o);
+    }
+}
+
 // B^T fragments of n-tile ntw for the right factor, in the diagonal block's
 // contraction order (slots 0-3: tokens 32m + 4 lg + e, slots 4-7:
 // 32m + 16 + 4 lg + e - 4), so that both share the x^T reads.
@@ -630,7 +646,7 @@ __device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, in
 // chunk's end are clamped; they are never stored).
 template <int N>
 __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, const int* strip, int r, int lg,
-                                       bf16x8_t (&cf)[2][N / 32])
+                                       uint4 (&cf)[2][N / 32])
 {
     const unsigned crow = static_cast<unsigned>(p.G * N);
 #pragma unroll
@@ -639,7 +655,7 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
         const unsigned tc = static_cast<unsigned>(t < it.L ? t : it.L - 1);
 #pragma unroll
         for (int k = 0; k < N / 32; ++k)
-            cf[k4][k] = as_bf16x8(*reinterpret_cast<const uint4*>(it.cchunk + (tc * crow + 32u * k + 8u * lg)));
+            cf[k4][k] = *reinterpret_cast<const uint4*>(it.cchunk + (tc * crow + 32u * k + 8u * lg));
     }
 }
 
@@ -650,7 +666,7 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
 template <int N>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
-                                          uint2 (&btf)[kQ / 32][2], bf16x8_t (&cf)[2][N / 32],
+                                          uint2 (&btf)[kQ / 32][2], uint4 (&cf)[2][N / 32],
                                           u16& dtr, u16* __restrict__ xs, u16* __restrict__ xs_n,
                                           float* __restrict__ cs, float* __restrict__ dt,
                                           float* __restrict__ wt, float* __restrict__ vf, float* __restrict__ w,
@@ -743,6 +759,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
     diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, gr, r, lg, lane, y[0], y[1]);
+    // Last head of an item with the next item known: this wavefront refills the
+    // Gram rows it has just finished with (no other wavefront reads them) for
+    // the next item, well ahead of that item's diagonal block.
+    const bool gram_early = last && hk > 0 && next < nwork;
+    if (gram_early) dma_gram_rows(gr, p, decode_item(p, next, per_c, nHG, N), wave, lane);
     // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
     // after the right factor)
 #pragma unroll
@@ -882,14 +903,14 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     if (hk == 0) next = *tk;
     // The next item's Gram tiles (and, with one head per item, its first head's
     // x): only the bf16 state and z are read from here on.
-    const bool gram_ahead = last && next < nwork;
+    // (With one head per item the next item is known only here: its Gram tiles
+    // and its first head's x follow now, by all wavefronts.)
+    const bool gram_ahead = last && hk == 0 && next < nwork;
     if (gram_ahead) {
         const Item nit = decode_item(p, next, per_c, nHG, N);
         dma_gram(gr, p, nit, wave, dmo);
-        if (hk == 0) {   // one head per item: its successor's x and dt only now
-            dma_head(p, nit, nit.h0, xs_n, wave, dmo);
-            if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
-        }
+        dma_head(p, nit, nit.h0, xs_n, wave, dmo);
+        if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
     }
 
     // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
@@ -904,8 +925,8 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) {
                 const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&hb[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
-                tq[0][pt] = mfma(aop, cf[0][k], tq[0][pt]);
-                tq[1][pt] = mfma(aop, cf[1][k], tq[1][pt]);
+                tq[0][pt] = mfma(aop, as_bf16x8(cf[0][k]), tq[0][pt]);
+                tq[1][pt] = mfma(aop, as_bf16x8(cf[1][k]), tq[1][pt]);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -996,6 +1017,14 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
         }
     }
+    // The next item's B^T and C fragments (their last uses in this item are
+    // behind us), requested after the waits above so that none of those waits
+    // for them.
+    if (last && next < nwork) {
+        const Item nit = decode_item(p, next, per_c, nHG, N);
+        load_bt<N>(p, nit, ntw, r, lg, btf);
+        load_c<N>(p, nit, strip, r, lg, cf);
+    }
     lds_barrier();   // this head's LDS buffers may be refilled from here on
     dtr = dtr_next;  // here, where the load has long completed (the epilogue waited for it)
 }
@@ -1048,15 +1077,19 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     __syncthreads();
 
     int q = 0;      // LDS buffer of the current head
+    // register operands shared by an item's heads (see load_bt / load_c): loaded
+    // here for the first item, and for every later item by the last head of the
+    // item before it, right after their last use there
+    uint2 btf[kQ / 32][2];
+    uint4 cf[2][KN];   // raw bf16 (as a bf16 vector type the compiler merges lanes right at the loads)
+    {
+        const Item it = decode_item(p, work, per_c, nHG, N);
+        load_bt<N>(p, it, ntw, r, lg, btf);
+        load_c<N>(p, it, strip, r, lg, cf);
+    }
     for (;;) {
     const Item it = decode_item(p, work, per_c, nHG, N);
     int next = nwork;
-    // register operands shared by the item's heads (see load_bt / load_c); first
-    // needed by the right factor, after the first head's diagonal block
-    uint2 btf[kQ / 32][2];
-    bf16x8_t cf[2][KN];
-    load_bt<N>(p, it, ntw, r, lg, btf);
-    load_c<N>(p, it, strip, r, lg, cf);
     for (int hk = 0; hk < p.HG; ++hk) {
         head_step<N>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
                      sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp,
