@@ -236,6 +236,55 @@ int ssd_span_correct(const ssd_problem* prob, const void* dt, const float* A_log
                      const float* entering, void* y, void* workspace, size_t workspace_bytes,
                      void* stream);
 
+/* ---- Gradients (training; the cost of Section 6.3) --------------------------
+ *
+ * ssd_backward: the gradients of a scalar loss L with respect to every input
+ * of ssd_forward, given dy = dL/dy and dfinal_states = dL/d(final_states)
+ * (NULL = 0), for the layer defined at the top of this header without packed
+ * rows (no seq_idx).  The paper states no backward algorithm; this is the
+ * adjoint of the recurrence, evaluated chunk by chunk like the forward of
+ * Section 6 (chunk-local terms, then a scan over chunks in each direction).
+ *   Inputs: prob, x, dt, A_log, B, C, D (may be NULL = 0), initial_states
+ *           (may be NULL = 0) exactly as given to ssd_forward, and dy (layout
+ *           and dtype of y).  prob->chunk_size and prob->nseq are not used
+ *           (the backward has its own chunking; the result does not depend on it).
+ *   Outputs (every one overwritten):
+ *     dx  (batch, seqlen, nheads, headdim)   dtype
+ *     ddt (batch, seqlen, nheads)            dtype (gradient of dt as given,
+ *                                            i.e. after any softplus)
+ *     dA_log (nheads)                        float32 (through A = -exp(A_log))
+ *     dB, dC (batch, seqlen, ngroups, dstate) dtype (summed over a group's heads)
+ *     dD (nheads)                            float32; not written when D or dD is NULL
+ *     dinitial_states (batch, nheads, headdim, dstate) float32; may be NULL
+ * initial_states, dfinal_states and dinitial_states must be 16-byte aligned
+ * (else SSD_ERR_UNSUPPORTED_DIMS).  Arithmetic in float32; dtype outputs are
+ * rounded to nearest even.  Workspace: ssd_backward_workspace_bytes() bytes of
+ * device memory (it holds a state per 32 tokens and head, twice).  Ownership,
+ * asynchrony, determinism and errors as for ssd_forward. */
+int ssd_backward_workspace_bytes(const ssd_problem* prob, size_t* bytes);
+
+int ssd_backward(const ssd_problem* prob,
+                 const void* x, const void* dt, const float* A_log,
+                 const void* B, const void* C, const float* D,
+                 const float* initial_states,
+                 const void* dy, const float* dfinal_states,
+                 void* dx, void* ddt, float* dA_log, void* dB, void* dC,
+                 float* dD, float* dinitial_states,
+                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* ssd_backward, plus two hipEvent_t (either may be NULL) recorded right before
+ * and right after the launch of its dominant kernel (the per-chunk gradient
+ * kernel), as in ssd_forward_timed. */
+int ssd_backward_timed(const ssd_problem* prob,
+                       const void* x, const void* dt, const float* A_log,
+                       const void* B, const void* C, const float* D,
+                       const float* initial_states,
+                       const void* dy, const float* dfinal_states,
+                       void* dx, void* ddt, float* dA_log, void* dB, void* dC,
+                       float* dD, float* dinitial_states,
+                       void* workspace, size_t workspace_bytes, void* stream,
+                       void* event_begin, void* event_end);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);
 

@@ -9,6 +9,7 @@
 #include <cstdint>
 #include <cstdlib>
 
+#include "ssd_bwd.h"
 #include "ssd_internal.h"
 
 namespace ssd {
@@ -431,6 +432,110 @@ extern "C" int ssd_span_correct(const ssd_problem* prob, const void* dt, const f
     const hipError_t err =
         ssd::launch_span_correct(p, prob->dtype == SSD_DTYPE_BF16, static_cast<hipStream_t>(stream));
     return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
+namespace {
+
+// Shape checks of the backward: those of ssd_forward without packed rows; the
+// chunk size is not used (the backward has its own decomposition).
+int backward_plan(const ssd_problem* prob, ssd::BwdParams* p, ssd::BwdLayout* l)
+{
+    if (!prob) return SSD_ERR_NULL_ARG;
+    ssd_problem q = *prob;
+    q.chunk_size = 256;
+    ssd::Shape s;
+    const int rc = ssd::validate(&q, false, &s);
+    if (rc != SSD_OK) return rc;
+    p->b = s.b;
+    p->T = s.T;
+    p->H = s.H;
+    p->P = s.P;
+    p->N = s.N;
+    p->G = s.G;
+    p->nC = (s.T + ssd::kBwdQ - 1) / ssd::kBwdQ;
+    if (static_cast<double>(p->b) * p->nC * p->H * p->P * p->N > 16.0 * ssd::kMaxElemsPublic)
+        return SSD_ERR_TOO_LARGE;
+    ssd::bwd_slices(p->b, p->nC, p->G, p->H / p->G, &p->S, &p->hs);
+    *l = ssd::bwd_layout(p->b, p->T, p->H, p->P, p->N, p->G, p->nC, p->S);
+    return SSD_OK;
+}
+
+int backward_impl(const ssd_problem* prob, const void* x, const void* dt, const float* A_log, const void* B,
+                  const void* C, const float* D, const float* initial_states, const void* dy,
+                  const float* dfinal_states, void* dx, void* ddt, float* dA_log, void* dB, void* dC, float* dD,
+                  float* dinitial_states, void* workspace, size_t workspace_bytes, void* stream,
+                  void* ev_begin, void* ev_end)
+{
+    ssd::BwdParams p{};
+    ssd::BwdLayout l{};
+    const int rc = backward_plan(prob, &p, &l);
+    if (rc != SSD_OK) return rc;
+    if (!x || !dt || !A_log || !B || !C || !dy || !dx || !ddt || !dA_log || !dB || !dC)
+        return SSD_ERR_NULL_ARG;
+    if (!aligned16(initial_states) || !aligned16(dfinal_states) || !aligned16(dinitial_states))
+        return SSD_ERR_UNSUPPORTED_DIMS;   // read and written as 16-byte vectors
+    if (!workspace || workspace_bytes < l.total) return SSD_ERR_WORKSPACE;
+    char* ws = static_cast<char*>(workspace);
+    p.x = x;
+    p.dt = dt;
+    p.A_log = A_log;
+    p.B = B;
+    p.C = C;
+    p.D = D;
+    p.init = initial_states;
+    p.dy = dy;
+    p.dfinal = dfinal_states;
+    p.dx = dx;
+    p.ddt = ddt;
+    p.dA_log = dA_log;
+    p.dB = dB;
+    p.dC = dC;
+    p.dD = D ? dD : nullptr;
+    p.dinit = dinitial_states;
+    p.cs = reinterpret_cast<float*>(ws + l.cs);
+    p.hin = reinterpret_cast<float*>(ws + l.hin);
+    p.gn = reinterpret_cast<float*>(ws + l.gn);
+    p.dBp = reinterpret_cast<float*>(ws + l.dBp);
+    p.dCp = reinterpret_cast<float*>(ws + l.dCp);
+    p.dAp = reinterpret_cast<float*>(ws + l.dAp);
+    p.dDp = reinterpret_cast<float*>(ws + l.dDp);
+    const hipError_t err = ssd::launch_backward(p, prob->dtype == SSD_DTYPE_BF16, static_cast<hipStream_t>(stream),
+                                                static_cast<hipEvent_t>(ev_begin), static_cast<hipEvent_t>(ev_end));
+    return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" int ssd_backward_workspace_bytes(const ssd_problem* prob, size_t* bytes)
+{
+    if (!bytes) return SSD_ERR_NULL_ARG;
+    ssd::BwdParams p{};
+    ssd::BwdLayout l{};
+    const int rc = backward_plan(prob, &p, &l);
+    if (rc != SSD_OK) return rc;
+    *bytes = l.total;
+    return SSD_OK;
+}
+
+extern "C" int ssd_backward(const ssd_problem* prob, const void* x, const void* dt, const float* A_log,
+                            const void* B, const void* C, const float* D, const float* initial_states,
+                            const void* dy, const float* dfinal_states, void* dx, void* ddt, float* dA_log,
+                            void* dB, void* dC, float* dD, float* dinitial_states, void* workspace,
+                            size_t workspace_bytes, void* stream)
+{
+    return backward_impl(prob, x, dt, A_log, B, C, D, initial_states, dy, dfinal_states, dx, ddt, dA_log, dB, dC,
+                         dD, dinitial_states, workspace, workspace_bytes, stream, nullptr, nullptr);
+}
+
+extern "C" int ssd_backward_timed(const ssd_problem* prob, const void* x, const void* dt, const float* A_log,
+                                  const void* B, const void* C, const float* D, const float* initial_states,
+                                  const void* dy, const float* dfinal_states, void* dx, void* ddt,
+                                  float* dA_log, void* dB, void* dC, float* dD, float* dinitial_states,
+                                  void* workspace, size_t workspace_bytes, void* stream, void* event_begin,
+                                  void* event_end)
+{
+    return backward_impl(prob, x, dt, A_log, B, C, D, initial_states, dy, dfinal_states, dx, ddt, dA_log, dB, dC,
+                         dD, dinitial_states, workspace, workspace_bytes, stream, event_begin, event_end);
 }
 
 extern "C" const char* ssd_error_string(int code)

@@ -1,0 +1,59 @@
+// Internal interface of the backward kernels (ssd_backward.hip) for the C-ABI
+// host layer.  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ssd {
+
+// Tokens per chunk of the backward's own decomposition (independent of the
+// forward's chunk size: the gradient of the layer does not depend on it).
+constexpr int64_t kBwdQ = 32;
+
+struct BwdParams {
+    int64_t b, T, H, P, N, G, nC;   // nC = ceil(T / kBwdQ)
+    int64_t S, hs;                  // head slices per group, heads per slice
+    const void* x;
+    const void* dt;
+    const float* A_log;
+    const void* B;
+    const void* C;
+    const float* D;        // may be null
+    const float* init;     // may be null
+    const void* dy;
+    const float* dfinal;   // may be null
+    void* dx;
+    void* ddt;
+    float* dA_log;
+    void* dB;
+    void* dC;
+    float* dD;             // may be null
+    float* dinit;          // may be null
+    // workspace (float32)
+    float* cs;     // (b, H, nC, kBwdQ)   chunk-local inclusive cumsum of dt*A, log2 units
+    float* hin;    // (b, nC, H, P, N)    chunk states, then the state entering each chunk
+    float* gn;     // (b, nC, H, P, N)    output-to-state terms, then the gradient of the state
+                   //                     leaving each chunk
+    float* dBp;    // (S, b, T, G, N)     dB over one slice of a group's heads
+    float* dCp;    // (S, b, T, G, N)
+    float* dAp;    // (b, H, nC)          per-chunk terms of dA
+    float* dDp;    // (b, H, nC)          per-chunk terms of dD
+};
+
+struct BwdLayout {
+    size_t cs, hin, gn, dBp, dCp, dAp, dDp, total;
+};
+
+// Head slices: enough (b, chunk, group, slice) workgroups to fill the chip.
+void bwd_slices(int64_t b, int64_t nC, int64_t G, int64_t heads_per_group, int64_t* S, int64_t* hs);
+
+BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int64_t G, int64_t nC, int64_t S);
+
+// Enqueue the whole backward on `stream`; `ev_begin` / `ev_end` (may be null)
+// are recorded right before and right after the chunk-gradient kernel.
+hipError_t launch_backward(const BwdParams& p, bool bf16, hipStream_t stream, hipEvent_t ev_begin,
+                           hipEvent_t ev_end);
+
+}  // namespace ssd

@@ -36,7 +36,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = [
-    "Problem", "Inputs", "BlockInputs", "WORKLOADS", "make_inputs", "make_block_inputs",
+    "Problem", "Inputs", "BlockInputs", "WORKLOADS", "make_inputs", "make_block_inputs", "make_grad_inputs",
     "f32_to_bf16_bits", "bf16_bits_to_f32", "workload",
 ]
 
@@ -164,6 +164,16 @@ class BlockInputs:
         if a.dtype == np.uint16:
             return bf16_bits_to_f32(a).astype(np.float64)
         return a.astype(np.float64)
+
+
+def make_grad_inputs(p: Problem, seed: int):
+    """Output gradients for the backward, from their own stream
+    ``default_rng([seed, 0x6AD])``: ``dy`` (b, T, H, P) ~ N(0, 1) in the
+    activation dtype, then ``dfinal`` (b, H, P, N) ~ N(0, 1) float32."""
+    rng = np.random.default_rng([seed, 0x6AD])
+    dy = _normal_blocks(rng, (p.batch, p.seqlen, p.nheads, p.headdim), 1.0, p.dtype)
+    dfinal = _normal_blocks(rng, (p.batch, p.nheads, p.headdim, p.dstate), 1.0, "f32")
+    return dy, dfinal
 
 
 def make_block_inputs(p: Problem, seed: int) -> BlockInputs:

@@ -38,7 +38,7 @@ SSD_ERR_BAD_OPTION = -10
 EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
             "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
             "ssd_span_decay", "ssd_span_combine", "ssd_span_correct_workspace_bytes", "ssd_span_correct",
-            "ssd_error_string")
+            "ssd_backward_workspace_bytes", "ssd_backward", "ssd_backward_timed", "ssd_error_string")
 
 
 class SsdProblem(ctypes.Structure):
@@ -114,6 +114,12 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_span_correct.restype = ctypes.c_int
     lib.ssd_span_correct.argtypes = [pp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.ssd_error_string.restype = ctypes.c_char_p
+    lib.ssd_backward_workspace_bytes.argtypes = [pp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_backward_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_backward.argtypes = [pp] + [vp] * 16 + [vp, ctypes.c_size_t, vp]
+    lib.ssd_backward.restype = ctypes.c_int
+    lib.ssd_backward_timed.argtypes = lib.ssd_backward.argtypes + [vp, vp]
+    lib.ssd_backward_timed.restype = ctypes.c_int
     lib.ssd_error_string.argtypes = [ctypes.c_int]
     _lib = lib
     return lib
@@ -376,3 +382,72 @@ def span_correct(dt, A_log, C, entering, y, workspace=None):
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_span_correct")
     return y
+
+
+def ssd_backward_workspace_bytes(prob: SsdProblem) -> int:
+    out = ctypes.c_size_t(0)
+    rc = load_library().ssd_backward_workspace_bytes(ctypes.byref(prob), ctypes.byref(out))
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_backward_workspace_bytes")
+    return int(out.value)
+
+
+def ssd_backward(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, dy, dfinal_states, dx, ddt,
+                 dA_log, dB, dC, dD, dinitial_states, workspace, workspace_bytes: int, stream,
+                 event_begin=None, event_end=None) -> int:
+    """Raw ABI call on integer device addresses (0 = NULL); with events, the
+    timed variant.  Returns the status."""
+    lib = load_library()
+    args = [ctypes.byref(prob), x, dt, A_log, B, C, D or None, initial_states or None, dy,
+            dfinal_states or None, dx, ddt, dA_log, dB, dC, dD or None, dinitial_states or None,
+            workspace, int(workspace_bytes), stream or None]
+    if event_begin or event_end:
+        return lib.ssd_backward_timed(*args, event_begin or None, event_end or None)
+    return lib.ssd_backward(*args)
+
+
+def backward(x, dt, A_log, B, C, dy, D=None, initial_states=None, dfinal_states=None,
+             workspace=None, event_begin=None, event_end=None):
+    """Gradients of the SSD layer on device tensors, given dy (and optionally
+    the gradient of the final states).  Inputs as for ``forward`` (no packed
+    rows).  Returns a dict: dx, ddt, dB, dC (x's dtype), dA_log, dD (float32;
+    dD None without D), dinit (float32, zeros-shaped like the states)."""
+    import torch
+
+    dev = x.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    if x.dtype == torch.bfloat16:
+        dtype = SSD_DTYPE_BF16
+    elif x.dtype == torch.float32:
+        dtype = SSD_DTYPE_F32
+    else:
+        raise TypeError("x must be float32 or bfloat16")
+    for name, t in (("dt", dt), ("B", B), ("C", C), ("dy", dy)):
+        if t.dtype != x.dtype:
+            raise TypeError("%s must have x's dtype" % name)
+    for name, t in (("A_log", A_log), ("D", D), ("initial_states", initial_states),
+                    ("dfinal_states", dfinal_states)):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("%s must be float32" % name)
+    for t in (x, dt, A_log, B, C, dy, D, initial_states, dfinal_states):
+        if t is not None and (t.device != dev or not t.is_contiguous()):
+            raise ValueError("all tensors must be contiguous and on x's device")
+    b, T, H, P = x.shape
+    G, N = B.shape[2], B.shape[3]
+    prob = make_problem(b, T, H, P, N, G, 256, dtype)
+    wsb = ssd_backward_workspace_bytes(prob)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    g = {"dx": torch.empty_like(x), "ddt": torch.empty_like(dt), "dB": torch.empty_like(B),
+         "dC": torch.empty_like(C), "dA_log": torch.empty_like(A_log),
+         "dD": torch.empty_like(D) if D is not None else None,
+         "dinit": torch.empty((b, H, P, N), dtype=torch.float32, device=dev)}
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = ssd_backward(prob, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D), _ptr(initial_states),
+                      _ptr(dy), _ptr(dfinal_states), _ptr(g["dx"]), _ptr(g["ddt"]), _ptr(g["dA_log"]),
+                      _ptr(g["dB"]), _ptr(g["dC"]), _ptr(g["dD"]), _ptr(g["dinit"]), _ptr(workspace), wsb,
+                      stream, event_begin, event_end)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_backward")
+    return g

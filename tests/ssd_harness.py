@@ -11,14 +11,19 @@ from paper_2405_21060_amd.inputs import Inputs, bf16_bits_to_f32
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
+def act_to_device(a: np.ndarray):
+    """An activation array (float32, or bfloat16 bits as uint16) on the device."""
+    import torch
+
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
 def to_device(inp: Inputs):
     import torch
 
-    def act(a):
-        if a.dtype == np.uint16:
-            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
-        return torch.from_numpy(a).cuda()
-
+    act = act_to_device
     d = {
         "x": act(inp.x), "dt": act(inp.dt), "B": act(inp.B), "C": act(inp.C),
         "A_log": torch.from_numpy(inp.A_log).cuda(), "D": torch.from_numpy(inp.D).cuda(),

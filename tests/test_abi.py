@@ -182,6 +182,36 @@ def test_span_validation(lib):
         ssd.SSD_ERR_NULL_ARG
 
 
+def bwd(p, ws_bytes=1 << 40, init=0, dfinal=0, dinit=0, dy=FAKE, D=0, dD=0):
+    return ssd.ssd_backward(p, FAKE, FAKE, FAKE, FAKE, FAKE, D, init, dy, dfinal, FAKE, FAKE, FAKE, FAKE,
+                            FAKE, dD, dinit, FAKE, ws_bytes, 0)
+
+
+def test_backward_validation(lib):
+    size = ctypes.c_size_t(0)
+    assert lib.ssd_backward_workspace_bytes(None, ctypes.byref(size)) == ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_backward_workspace_bytes(ctypes.byref(prob()), None) == ssd.SSD_ERR_NULL_ARG
+    assert bwd(prob(dtype=7)) == ssd.SSD_ERR_BAD_DTYPE
+    assert bwd(prob(nheads=80, ngroups=3)) == ssd.SSD_ERR_BAD_SHAPE
+    assert bwd(prob(headdim=24)) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert bwd(prob(dstate=272)) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    # chunk_size plays no part in the backward
+    assert bwd(prob(chunk_size=48), dy=0) == ssd.SSD_ERR_NULL_ARG
+    assert bwd(prob(), dy=0) == ssd.SSD_ERR_NULL_ARG
+    assert bwd(prob(), init=FAKE + 4) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert bwd(prob(), dfinal=FAKE + 8) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert bwd(prob(), dinit=FAKE + 12) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    need = ssd.ssd_backward_workspace_bytes(prob())
+    assert bwd(prob(), ws_bytes=need - 1) == ssd.SSD_ERR_WORKSPACE
+    assert ssd.ssd_backward(prob(), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE,
+                            0, 0, 0, need, 0) == ssd.SSD_ERR_WORKSPACE
+    # two float32 states per (batch, 32-token chunk, head) dominate the workspace
+    states = 4 * (4096 // 32) * 80 * 64 * 128 * 4
+    assert 2 * states <= need <= 2 * states + (128 << 20)
+    assert ssd.ssd_backward(prob(seqlen=0), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, 0, FAKE, FAKE, FAKE,
+                            FAKE, FAKE, 0, 0, FAKE, need, 0, FAKE, FAKE) == ssd.SSD_ERR_BAD_SHAPE
+
+
 def test_error_strings(lib):
     for code in range(0, -11, -1):
         s = ssd.ssd_error_string(code)
