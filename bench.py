@@ -24,6 +24,7 @@ if ROOT not in sys.path:
 # MI355X published peaks
 PEAK_BF16_FLOPS = 2.5e15
 PEAK_F32_MFMA_FLOPS = 157.3e12
+PEAK_F32_VECTOR_FLOPS = 157.3e12
 PEAK_HBM_BPS = 8.0e12
 
 
@@ -262,6 +263,100 @@ def block_bench(args, torch, ssd):
     }), flush=True)
 
 
+BWD_CHUNK = 32   # tokens per chunk of the backward's decomposition
+
+
+def backward_counts(p, Qb=BWD_CHUNK):
+    """Algorithmic FLOPs of the backward's chunk-gradient kernel (the chunked
+    adjoint at Qb tokens per chunk: the causal score products, their uses, and
+    the four state-sized products per token; C B^T once per group) and the
+    compulsory HBM bytes of the whole backward (inputs x, dt, B, C, dy read,
+    gradients dx, ddt, dB, dC written, A_log, D and their gradients)."""
+    b, T, H, P, N, G = p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups
+    nC = -(-T // Qb)
+    pairs = b * nC * Qb * (Qb + 1) // 2          # (u >= t) pairs over all chunks of one head
+    flops = pairs * G * N * 2 + H * (pairs * (2 * P + 2 * N) * 2 + b * T * 4 * P * N * 2)
+    act = 2 if p.dtype == "bf16" else 4
+    byts = act * (3 * b * T * H * P + 2 * b * T * H + 4 * b * T * G * N) + 4 * 4 * H
+    return flops, byts
+
+
+def backward_bench(args, torch, ssd):
+    """Gradients of the 2.7B-shape layer (ssd_backward): dy seeded, no initial
+    state and no final-state gradient (the training case)."""
+    from paper_2405_21060_amd.inputs import WORKLOADS, make_grad_inputs, make_inputs
+    from tests.ssd_harness import act_to_device, to_device
+
+    p = WORKLOADS[args.workload]
+    inp = make_inputs(p, args.seed)
+    dy, _ = make_grad_inputs(p, args.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sets = []
+    for _ in range(max(1, args.copies)):
+        c = to_device(inp)
+        c["dy"] = act_to_device(dy)
+        c["dx"], c["ddt"] = torch.empty_like(c["x"]), torch.empty_like(c["dt"])
+        c["dB"], c["dC"] = torch.empty_like(c["B"]), torch.empty_like(c["C"])
+        c["dA_log"], c["dD"] = torch.empty_like(c["A_log"]), torch.empty_like(c["D"])
+        sets.append(c)
+    prob = ssd.make_problem(p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups, p.chunk_size,
+                            ssd.SSD_DTYPE_BF16 if p.dtype == "bf16" else ssd.SSD_DTYPE_F32, 0)
+    wsb = ssd.ssd_backward_workspace_bytes(prob)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ptr = lambda t: None if t is None else t.data_ptr()
+    kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, z in kev:
+        a.record(stream)
+        z.record(stream)
+
+    def call(i, events=None):
+        c = sets[i % len(sets)]
+        rc = ssd.ssd_backward(prob, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]), ptr(c["C"]),
+                              ptr(c["D"]), None, ptr(c["dy"]), None, ptr(c["dx"]), ptr(c["ddt"]),
+                              ptr(c["dA_log"]), ptr(c["dB"]), ptr(c["dC"]), ptr(c["dD"]), None, ptr(ws), wsb,
+                              stream.cuda_stream, events[0].cuda_event if events else None,
+                              events[1].cuda_event if events else None)
+        if rc != 0:
+            raise ssd.SsdError(rc, "ssd_backward")
+
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        call(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    for i in range(args.steps):
+        call(i, kev[i])
+    torch.cuda.synchronize()
+    ks = sorted(a.elapsed_time(z) for a, z in kev)
+    kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
+           "p90": ks[(9 * len(ks)) // 10]}
+    flops, byts = backward_counts(p)
+    ksec = kms["mean"] * 1e-3
+    tokens = p.batch * p.seqlen
+    print(json.dumps({
+        "metric": "SSD bwd tokens/s (gradients of the 2.7B-layer shape, 1 GPU)",
+        "value": tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if p.dtype == "f32" else "bf16 in, f32 arithmetic",
+        "data": "synthetic (seeded; Mamba-2 layer shapes)",
+        "config": {"workload": "backward_" + args.workload, "batch": p.batch, "seqlen": p.seqlen,
+                   "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate, "ngroups": p.ngroups,
+                   "backward_chunk": BWD_CHUNK},
+        "algorithmic_flops": flops, "compulsory_bytes": byts,
+        "roofline": {"bound": "alu", "achieved": flops / ksec / 1e12, "peak": PEAK_F32_VECTOR_FLOPS / 1e12,
+                     "unit": "TFLOP/s", "frac": flops / ksec / PEAK_F32_VECTOR_FLOPS, "traffic": None,
+                     "kernel": "k_bwd_chunk", "kernel_ms": kms},
+    }), flush=True)
+
+
 def cp_bench(args, torch, ssd):
     """One rank's share of an 8-way sequence split of the 2.7B layer (512 of
     4096 tokens per batch row): the layer from a zero state on the span, the
@@ -354,6 +449,8 @@ def main():
     ap.add_argument("--block", action="store_true",
                     help="time the layer with the block steps around it (ssd_forward_block) instead")
     ap.add_argument("--block-norm-group", type=int, default=64)
+    ap.add_argument("--backward", action="store_true",
+                    help="time the layer's gradients (ssd_backward) instead")
     ap.add_argument("--cp-share", action="store_true",
                     help="time one rank's share of an 8-way sequence split instead")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -395,6 +492,8 @@ def main():
         return block_bench(args, torch, ssd)
     if args.cp_share:
         return cp_bench(args, torch, ssd)
+    if args.backward:
+        return backward_bench(args, torch, ssd)
 
     p = WORKLOADS[args.workload]
     inp = make_inputs(p, args.seed)

@@ -256,10 +256,12 @@ int ssd_span_correct(const ssd_problem* prob, const void* dt, const float* A_log
  *     dB, dC (batch, seqlen, ngroups, dstate) dtype (summed over a group's heads)
  *     dD (nheads)                            float32; not written when D or dD is NULL
  *     dinitial_states (batch, nheads, headdim, dstate) float32; may be NULL
- * initial_states, dfinal_states and dinitial_states must be 16-byte aligned
- * (else SSD_ERR_UNSUPPORTED_DIMS).  Arithmetic in float32; dtype outputs are
+ * x, B, C, dy, dx, initial_states, dfinal_states and dinitial_states must be
+ * 16-byte aligned (else SSD_ERR_UNSUPPORTED_DIMS).  Arithmetic in float32; dtype outputs are
  * rounded to nearest even.  Workspace: ssd_backward_workspace_bytes() bytes of
- * device memory (it holds a state per 32 tokens and head, twice).  Ownership,
+ * device memory (it holds a state per 64 tokens and head three times in bf16
+ * for bf16 with headdim 64 and dstate 64 or 128, which run on the matrix
+ * cores; otherwise one per 32 tokens and head twice in float32).  Ownership,
  * asynchrony, determinism and errors as for ssd_forward. */
 int ssd_backward_workspace_bytes(const ssd_problem* prob, size_t* bytes);
 

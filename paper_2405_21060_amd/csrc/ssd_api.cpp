@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <cstring>
 
 #include "ssd_bwd.h"
 #include "ssd_internal.h"
@@ -438,7 +439,16 @@ namespace {
 
 // Shape checks of the backward: those of ssd_forward without packed rows; the
 // chunk size is not used (the backward has its own decomposition).
-int backward_plan(const ssd_problem* prob, ssd::BwdParams* p, ssd::BwdLayout* l)
+// The matrix-core path where it applies; SSD_PATH=unfused (a debug knob, as
+// for the forward) forces the general one.
+bool backward_fast(const ssd::Shape& s)
+{
+    const char* path = std::getenv("SSD_PATH");
+    if (path && std::strcmp(path, "unfused") == 0) return false;
+    return ssd::bwd_fast_supported(s.bf16, s.P, s.N);
+}
+
+int backward_plan(const ssd_problem* prob, ssd::BwdParams* p, ssd::BwdLayout* l, bool* fast)
 {
     if (!prob) return SSD_ERR_NULL_ARG;
     ssd_problem q = *prob;
@@ -446,17 +456,26 @@ int backward_plan(const ssd_problem* prob, ssd::BwdParams* p, ssd::BwdLayout* l)
     ssd::Shape s;
     const int rc = ssd::validate(&q, false, &s);
     if (rc != SSD_OK) return rc;
+    *fast = backward_fast(s);
+    const int64_t Q = *fast ? ssd::kBwdQFast : ssd::kBwdQ;
     p->b = s.b;
     p->T = s.T;
     p->H = s.H;
     p->P = s.P;
     p->N = s.N;
     p->G = s.G;
-    p->nC = (s.T + ssd::kBwdQ - 1) / ssd::kBwdQ;
+    p->nC = (s.T + Q - 1) / Q;
     if (static_cast<double>(p->b) * p->nC * p->H * p->P * p->N > 16.0 * ssd::kMaxElemsPublic)
         return SSD_ERR_TOO_LARGE;
     ssd::bwd_slices(p->b, p->nC, p->G, p->H / p->G, &p->S, &p->hs);
-    *l = ssd::bwd_layout(p->b, p->T, p->H, p->P, p->N, p->G, p->nC, p->S);
+    if (const char* env = std::getenv("SSD_BWD_HEADS_PER_SLICE")) {   // debug knob
+        const long v = std::strtol(env, nullptr, 10);
+        if (v >= 1) {
+            p->hs = v < p->H / p->G ? v : p->H / p->G;
+            p->S = (p->H / p->G + p->hs - 1) / p->hs;
+        }
+    }
+    *l = ssd::bwd_layout(p->b, p->T, p->H, p->P, p->N, p->G, p->nC, p->S, *fast);
     return SSD_OK;
 }
 
@@ -468,11 +487,13 @@ int backward_impl(const ssd_problem* prob, const void* x, const void* dt, const 
 {
     ssd::BwdParams p{};
     ssd::BwdLayout l{};
-    const int rc = backward_plan(prob, &p, &l);
+    bool fast = false;
+    const int rc = backward_plan(prob, &p, &l, &fast);
     if (rc != SSD_OK) return rc;
     if (!x || !dt || !A_log || !B || !C || !dy || !dx || !ddt || !dA_log || !dB || !dC)
         return SSD_ERR_NULL_ARG;
-    if (!aligned16(initial_states) || !aligned16(dfinal_states) || !aligned16(dinitial_states))
+    if (!aligned16(initial_states) || !aligned16(dfinal_states) || !aligned16(dinitial_states) ||
+        !aligned16(x) || !aligned16(B) || !aligned16(C) || !aligned16(dy) || !aligned16(dx))
         return SSD_ERR_UNSUPPORTED_DIMS;   // read and written as 16-byte vectors
     if (!workspace || workspace_bytes < l.total) return SSD_ERR_WORKSPACE;
     char* ws = static_cast<char*>(workspace);
@@ -495,12 +516,15 @@ int backward_impl(const ssd_problem* prob, const void* x, const void* dt, const 
     p.cs = reinterpret_cast<float*>(ws + l.cs);
     p.hin = reinterpret_cast<float*>(ws + l.hin);
     p.gn = reinterpret_cast<float*>(ws + l.gn);
+    p.gnT = fast ? reinterpret_cast<float*>(ws + l.gnT) : nullptr;
     p.dBp = reinterpret_cast<float*>(ws + l.dBp);
     p.dCp = reinterpret_cast<float*>(ws + l.dCp);
     p.dAp = reinterpret_cast<float*>(ws + l.dAp);
     p.dDp = reinterpret_cast<float*>(ws + l.dDp);
-    const hipError_t err = ssd::launch_backward(p, prob->dtype == SSD_DTYPE_BF16, static_cast<hipStream_t>(stream),
-                                                static_cast<hipEvent_t>(ev_begin), static_cast<hipEvent_t>(ev_end));
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    const hipEvent_t e0 = static_cast<hipEvent_t>(ev_begin), e1 = static_cast<hipEvent_t>(ev_end);
+    const hipError_t err = fast ? ssd::launch_backward_fast(p, st, e0, e1)
+                                : ssd::launch_backward(p, prob->dtype == SSD_DTYPE_BF16, st, e0, e1);
     return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
@@ -511,7 +535,8 @@ extern "C" int ssd_backward_workspace_bytes(const ssd_problem* prob, size_t* byt
     if (!bytes) return SSD_ERR_NULL_ARG;
     ssd::BwdParams p{};
     ssd::BwdLayout l{};
-    const int rc = backward_plan(prob, &p, &l);
+    bool fast = false;
+    const int rc = backward_plan(prob, &p, &l, &fast);
     if (rc != SSD_OK) return rc;
     *bytes = l.total;
     return SSD_OK;

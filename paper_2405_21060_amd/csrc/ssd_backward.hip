@@ -463,10 +463,17 @@ hipError_t launch_all(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEve
                        dim3(kThreads), sm_chunk, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
+    return launch_backward_reduce(p, sizeof(T) == 2, st);
+}
+
+template <typename T>
+hipError_t launch_reduce(const BwdParams& p, hipStream_t st)
+{
     const int64_t nbc = p.b * p.T * p.G * p.N;
     hipLaunchKernelGGL(k_bwd_reduce_bc<T>, dim3(static_cast<unsigned>((nbc + kThreads - 1) / kThreads)),
                        dim3(kThreads), 0, st, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_bwd_reduce_head, dim3(static_cast<unsigned>(p.H)), dim3(kThreads), 0, st, p);
     return hipGetLastError();
 }
@@ -485,24 +492,33 @@ void bwd_slices(int64_t b, int64_t nC, int64_t G, int64_t hpg, int64_t* S, int64
     *S = (hpg + *hs - 1) / *hs;
 }
 
-BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int64_t G, int64_t nC, int64_t S)
+BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int64_t G, int64_t nC, int64_t S,
+                     bool fast)
 {
     BwdLayout l{};
     size_t off = 0;
-    const auto take = [&](size_t n) {
+    const auto take_bytes = [&](size_t bytes) {
         const size_t o = off;
-        off += al(n * sizeof(float));
+        off += al(bytes);
         return o;
     };
-    l.cs = take(static_cast<size_t>(b * H * nC * kQ));
-    l.hin = take(static_cast<size_t>(b * nC * H * P * N));
-    l.gn = take(static_cast<size_t>(b * nC * H * P * N));
+    const auto take = [&](size_t n) { return take_bytes(n * sizeof(float)); };
+    const size_t state_bytes = static_cast<size_t>(b * nC * H * P * N) * (fast ? 2 : 4);
+    l.cs = take(static_cast<size_t>(b * H * nC * (fast ? kBwdQFast : kBwdQ)));
+    l.hin = take_bytes(state_bytes);
+    l.gn = take_bytes(state_bytes);
+    l.gnT = fast ? take_bytes(state_bytes) : 0;
     l.dBp = take(static_cast<size_t>(S * b * T * G * N));
     l.dCp = take(static_cast<size_t>(S * b * T * G * N));
     l.dAp = take(static_cast<size_t>(b * nC * H));
     l.dDp = take(static_cast<size_t>(b * nC * H));
     l.total = off;
     return l;
+}
+
+hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream)
+{
+    return bf16 ? launch_reduce<uint16_t>(p, stream) : launch_reduce<float>(p, stream);
 }
 
 hipError_t launch_backward(const BwdParams& p, bool bf16, hipStream_t stream, hipEvent_t ev_begin,

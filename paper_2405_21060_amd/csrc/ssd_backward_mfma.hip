@@ -1,0 +1,670 @@
+// Gradients of the SSD layer on the matrix cores: bf16 inputs, headdim 64,
+// dstate 64 or 128.  Same chunked adjoint as ssd_backward.hip (formulas at the
+// top of that file), with chunks of 64 tokens and every contraction on
+// v_mfma_f32_16x16x32_bf16 (bf16 operands, float32 accumulation):
+//
+//   k_bwd2_states  per (chunk, row, group, head slice): the cumsum, and per
+//                  head H_c^T (n x p), W_c (p x n) and W_c^T (n x p), rounded
+//                  to bf16 in the layouts the chunk kernel reads them in
+//   k_bwd2_scan    the two scans over chunks, in place on those bf16 arrays
+//                  with float32 running sums: H^T -> h_in^T, W -> Gn, W^T -> Gn^T;
+//                  the initial-state gradient in float32
+//   k_bwd2_chunk   per (chunk, row, group, head slice): all chunk terms.  Score
+//                  tiles (u >= t) R0 = dy x^T and G0 = C B^T (once per
+//                  workgroup), then dX~^T = dy^T Gs + Gn B^T, dB^T = C^T Rs +
+//                  Gn^T x~^T, dC^T = B^T Rs^T + h_in^T dy^T, each as 16 x 16
+//                  tiles whose operands are k-contiguous rows: in shared memory
+//                  (B, B^T, C^T, x, dy, dy^T and the score tiles), or straight
+//                  from global memory (Gn, Gn^T, h_in^T).
+//
+// An MFMA operand row holds the contraction index contiguously; a lane
+// (row r = lane % 16, group q = lane / 16) reads 8 of them (k = 32 s + 8 q ..
+// + 7) as one 16-byte load, and the result tile D[4 q + v][r] lands in its
+// four accumulator registers.  Shared arrays are padded by 8 elements per
+// row so that the 16 rows of a fragment read fall in distinct banks.
+#include "ssd_bwd.h"
+#include "ssd_device.h"
+
+namespace ssd {
+namespace {
+
+constexpr int kQ2 = 64;          // tokens per chunk
+constexpr int kP2 = 64;          // head dimension
+constexpr int kT2 = 512;         // threads per workgroup (8 wavefronts)
+constexpr int kLd = kQ2 + 8;     // row stride (elements) of 64-wide shared rows
+
+typedef uint16_t u16;
+
+__device__ __forceinline__ bf16x8_t frag(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+__device__ __forceinline__ f32x4_t mma(uint4 a, uint4 b, f32x4_t c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag(a), frag(b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t bf16_bits(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;   // nearest even (finite inputs)
+}
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_bits(lo) | (bf16_bits(hi) << 16); }
+
+__device__ __forceinline__ float bf(u16 v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
+
+__device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// One operand fragment of a row-major bf16 array: row `row`, k-step `ks`.
+__device__ __forceinline__ uint4 ldfrag(const u16* a, int ld, int row, int ks, int lane)
+{
+    return *reinterpret_cast<const uint4*>(a + row * ld + ks * 32 + 8 * (lane >> 4));
+}
+
+__device__ __forceinline__ uint4 ldfrag_g(const u16* a, int64_t ld, int row, int ks, int lane)
+{
+    return *reinterpret_cast<const uint4*>(a + static_cast<int64_t>(row) * ld + ks * 32 + 8 * (lane >> 4));
+}
+
+__device__ __forceinline__ int chunk_len2(int64_t T, int64_t c)
+{
+    const int64_t r = T - c * kQ2;
+    return static_cast<int>(r < kQ2 ? r : kQ2);
+}
+
+// Slice of a group's heads handled by this workgroup.
+struct HeadRange {
+    int64_t g, slice, lo, hi;
+};
+
+__device__ __forceinline__ HeadRange head_range(const BwdParams& p)
+{
+    HeadRange r;
+    const int64_t hpg = p.H / p.G;
+    r.g = blockIdx.z / p.S;
+    r.slice = blockIdx.z - r.g * p.S;
+    r.lo = r.g * hpg + r.slice * p.hs;
+    r.hi = (r.slice + 1) * p.hs < hpg ? r.lo + p.hs : r.g * hpg + hpg;
+    return r;
+}
+
+// Inclusive cumsum of dt*A (log2 units) over the chunk by wavefront 0; fills
+// scs, sdt and the workspace copy.  Lanes beyond the chunk carry zero dt.
+__device__ __forceinline__ void chunk_cumsum(const BwdParams& p, int64_t b, int64_t c, int64_t h, int L,
+                                             float* scs, float* sdt)
+{
+    const int lane = threadIdx.x;
+    const u16* dt = static_cast<const u16*>(p.dt);
+    const float A2 = -expf(p.A_log[h]) * kLog2e;
+    const float dtv = lane < L ? bf(dt[(b * p.T + c * kQ2 + lane) * p.H + h]) : 0.f;
+    float v = dtv * A2;
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) {
+        const float o = __shfl_up(v, sh, 64);
+        if (lane >= sh) v += o;
+    }
+    scs[lane] = v;
+    sdt[lane] = dtv;
+    p.cs[((b * p.H + h) * p.nC + c) * kQ2 + lane] = v;
+}
+
+// ---------------------------------------------------------------------------
+// States: per head, H^T (n x p) = sum_s B_s[n] (e(end,s) dt_s x_s[p]) and
+// W (p x n) = sum_u (exp(cs_u) dy_u[p]) C_u[n], plus W^T; bf16 outputs.
+template <int N>
+__global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
+{
+    extern __shared__ __attribute__((aligned(16))) u16 sm2[];
+    u16* BT = sm2;                  // N x kLd   B^T  (row n, k = s)
+    u16* CT = BT + N * kLd;         // N x kLd   C^T
+    u16* XwT = CT + N * kLd;        // 64 x kLd  (e(end,s) dt_s x_s)^T (row p, k = s)
+    u16* DwT = XwT + kP2 * kLd;     // 64 x kLd  (exp(cs_u) dy_u)^T
+    __shared__ float scs[kQ2], sdt[kQ2];
+
+    const int64_t c = blockIdx.x, b = blockIdx.y;
+    const HeadRange hr = head_range(p);
+    const int L = chunk_len2(p.T, c);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t t0 = b * p.T + c * kQ2;
+    const u16* Bg = static_cast<const u16*>(p.B);
+    const u16* Cg = static_cast<const u16*>(p.C);
+    const u16* xg = static_cast<const u16*>(p.x);
+    const u16* dyg = static_cast<const u16*>(p.dy);
+    u16* HT = reinterpret_cast<u16*>(p.hin);
+    u16* Wn = reinterpret_cast<u16*>(p.gn);
+    u16* WT = reinterpret_cast<u16*>(p.gnT);
+
+    // B^T and C^T of the chunk (zero beyond its end)
+    for (int i = tid; i < kQ2 * N / 8; i += kT2) {
+        const int s = i / (N / 8), n0 = 8 * (i - s * (N / 8));
+        uint4 vb = make_uint4(0, 0, 0, 0), vc = vb;
+        if (s < L) {
+            const int64_t gi = ((t0 + s) * p.G + hr.g) * N + n0;
+            vb = *reinterpret_cast<const uint4*>(Bg + gi);
+            vc = *reinterpret_cast<const uint4*>(Cg + gi);
+        }
+        const uint32_t eb[4] = {vb.x, vb.y, vb.z, vb.w}, ec[4] = {vc.x, vc.y, vc.z, vc.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            BT[(n0 + 2 * e) * kLd + s] = static_cast<u16>(eb[e]);
+            BT[(n0 + 2 * e + 1) * kLd + s] = static_cast<u16>(eb[e] >> 16);
+            CT[(n0 + 2 * e) * kLd + s] = static_cast<u16>(ec[e]);
+            CT[(n0 + 2 * e + 1) * kLd + s] = static_cast<u16>(ec[e] >> 16);
+        }
+    }
+
+    for (int64_t h = hr.lo; h < hr.hi; ++h) {
+        __syncthreads();   // the previous head is done with XwT, DwT, scs, sdt
+        if (w == 0) chunk_cumsum(p, b, c, h, L, scs, sdt);
+        __syncthreads();
+        const float csend = scs[L - 1];
+        for (int i = tid; i < kQ2 * kP2 / 8; i += kT2) {
+            const int s = i >> 3, p0 = 8 * (i & 7);
+            float xw[8], dw[8];
+            if (s < L) {
+                const int64_t gi = ((t0 + s) * p.H + h) * kP2 + p0;
+                const uint4 vx = *reinterpret_cast<const uint4*>(xg + gi);
+                const uint4 vd = *reinterpret_cast<const uint4*>(dyg + gi);
+                const float fx = exp2f(csend - scs[s]) * sdt[s], fd = exp2f(scs[s]);
+                const uint32_t ex[4] = {vx.x, vx.y, vx.z, vx.w}, ed[4] = {vd.x, vd.y, vd.z, vd.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    xw[2 * e] = fx * lo_f(ex[e]);
+                    xw[2 * e + 1] = fx * hi_f(ex[e]);
+                    dw[2 * e] = fd * lo_f(ed[e]);
+                    dw[2 * e + 1] = fd * hi_f(ed[e]);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xw[e] = dw[e] = 0.f;
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                XwT[(p0 + e) * kLd + s] = static_cast<u16>(bf16_bits(xw[e]));
+                DwT[(p0 + e) * kLd + s] = static_cast<u16>(bf16_bits(dw[e]));
+            }
+        }
+        __syncthreads();
+
+        const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
+        const int r = lane & 15, q = lane >> 4;
+        // 3 products x (N/16) x 4 tiles of 16 x 16, spread over the 8 wavefronts
+        constexpr int kTiles = 3 * (N / 16) * 4;
+        for (int i = w; i < kTiles; i += 8) {
+            const int prod = i / ((N / 16) * 4), j = i - prod * ((N / 16) * 4);
+            const int nt = j >> 2, pt = j & 3;
+            f32x4_t acc = zero4();
+            if (prod == 1) {
+                // W (p x n): rows n of C^T, columns p of Dw^T -> D[n][p]
+#pragma unroll
+                for (int ks = 0; ks < kQ2 / 32; ++ks)
+                    acc = mma(ldfrag(CT, kLd, 16 * nt + r, ks, lane), ldfrag(DwT, kLd, 16 * pt + r, ks, lane), acc);
+                const int pp = 16 * pt + r, n0 = 16 * nt + 4 * q;
+                *reinterpret_cast<uint2*>(Wn + sbase + pp * N + n0) =
+                    make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
+            } else {
+                // H^T or W^T (n x p): rows p of Xw^T / Dw^T, columns n -> D[p][n]
+                const u16* X = prod == 0 ? XwT : DwT;
+                const u16* Y = prod == 0 ? BT : CT;
+#pragma unroll
+                for (int ks = 0; ks < kQ2 / 32; ++ks)
+                    acc = mma(ldfrag(X, kLd, 16 * pt + r, ks, lane), ldfrag(Y, kLd, 16 * nt + r, ks, lane), acc);
+                const int nn = 16 * nt + r, p0 = 16 * pt + 4 * q;
+                u16* dst = prod == 0 ? HT : WT;
+                *reinterpret_cast<uint2*>(dst + sbase + nn * kP2 + p0) =
+                    make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Scans, one thread per 8 consecutive bf16 of one (row, head) state in one of
+// the three arrays: 0 = H^T (n x p, forward from the initial state),
+// 1 = W (p x n, backward from dfinal; writes dinit), 2 = W^T (n x p, backward).
+template <int N>
+__global__ __launch_bounds__(256) void k_bwd2_scan(BwdParams p)
+{
+    constexpr int64_t PN8 = kP2 * N / 8;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t per = p.b * p.H * PN8;
+    if (i >= 3 * per) return;
+    const int arr = static_cast<int>(i / per);
+    const int64_t rem = i - arr * per;
+    const int64_t bh = rem / PN8, e8 = rem - bh * PN8;
+    const int64_t b = bh / p.H, h = bh - b * p.H;
+    // element coordinates of the first of the 8 values
+    int64_t pp, nn;
+    if (arr == 1) {
+        pp = e8 / (N / 8);
+        nn = 8 * (e8 - pp * (N / 8));
+    } else {
+        nn = e8 / (kP2 / 8);
+        pp = 8 * (e8 - nn * (kP2 / 8));
+    }
+    const float* src0 = arr == 0 ? p.init : p.dfinal;   // (b, H, P, N) float32 or null
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        float v = 0.f;
+        if (src0) {
+            const int64_t pe = arr == 1 ? pp : pp + e, ne = arr == 1 ? nn + e : nn;
+            v = src0[bh * kP2 * N + pe * N + ne];
+        }
+        acc[e] = v;
+    }
+    u16* base = reinterpret_cast<u16*>(arr == 0 ? p.hin : arr == 1 ? p.gn : p.gnT);
+    const int64_t off = (b * p.nC * p.H + h) * kP2 * N + 8 * e8;
+    const int64_t stride = p.H * kP2 * N;
+    const float* cs = p.cs + bh * p.nC * kQ2;
+    const bool fwd = arr == 0;
+    for (int64_t k = 0; k < p.nC; ++k) {
+        const int64_t c = fwd ? k : p.nC - 1 - k;
+        const float a = exp2f(cs[c * kQ2 + chunk_len2(p.T, c) - 1]);
+        uint4* slot = reinterpret_cast<uint4*>(base + off + c * stride);
+        const uint4 v = *slot;
+        *slot = make_uint4(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]), pack2(acc[4], acc[5]),
+                           pack2(acc[6], acc[7]));
+        const uint32_t ev[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc[2 * e] = fmaf(a, acc[2 * e], lo_f(ev[e]));
+            acc[2 * e + 1] = fmaf(a, acc[2 * e + 1], hi_f(ev[e]));
+        }
+    }
+    if (arr == 1 && p.dinit) {
+        float4* d = reinterpret_cast<float4*>(p.dinit + bh * kP2 * N + pp * N + nn);
+        d[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        d[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Chunk gradients.
+template <int N>
+struct ChunkSmem {
+    static constexpr int kLdN = N + 8;
+    static constexpr size_t kBytes =
+        sizeof(u16) * (static_cast<size_t>(kQ2) * kLdN + 2 * N * kLd + 6 * kQ2 * kLd);
+};
+
+// The score tiles (u-tile, t-tile) with u >= t, and those above the diagonal,
+// dealt to the wavefronts: wavefront w evaluates kLowerTile[w] and, for w < 2,
+// kLowerTile[w + 8]; wavefronts 2..7 clear kUpperTile[w - 2].
+__constant__ int2 kLowerTile[10] = {{0, 0}, {1, 0}, {1, 1}, {2, 0}, {2, 1}, {2, 2}, {3, 0}, {3, 1}, {3, 2}, {3, 3}};
+__constant__ int2 kUpperTile[6] = {{0, 1}, {0, 2}, {0, 3}, {1, 2}, {1, 3}, {2, 3}};
+
+template <int N>
+__global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
+{
+    constexpr int kLdN = ChunkSmem<N>::kLdN;
+    constexpr int kNT = N / 16;             // n-tiles
+    constexpr int kBW = N / 32;             // dB / dC tiles per wavefront
+    extern __shared__ __attribute__((aligned(16))) u16 sm2[];
+    u16* Bs = sm2;                      // 64 x kLdN  B   (row t, k = n)
+    u16* BT = Bs + kQ2 * kLdN;          // N x kLd    B^T (row n, k = t)
+    u16* CT = BT + N * kLd;             // N x kLd    C^T (row n, k = u)
+    u16* xs = CT + N * kLd;             // 64 x kLd   x   (row t, k = p)
+    u16* dys = xs + kQ2 * kLd;          // 64 x kLd   dy  (row u, k = p)
+    u16* dyT = dys + kQ2 * kLd;         // 64 x kLd   dy^T (row p, k = u)
+    u16* GsT = dyT + kQ2 * kLd;         // 64 x kLd   Gs^T (row t, k = u)
+    u16* Rs = GsT + kQ2 * kLd;          // 64 x kLd   Rs  (row u, k = t)
+    u16* RsT = Rs + kQ2 * kLd;          // 64 x kLd   Rs^T (row t, k = u)
+    __shared__ float scs[kQ2], sdt[kQ2], seend[kQ2], secs[kQ2];
+    __shared__ float rowp[kQ2][4], colp[kQ2][4], xdxp[kQ2][4], q2p[kQ2][4], dyxp[kQ2][4], q1p[kQ2][kNT];
+    __shared__ float sq2[kQ2], sdcs[kQ2], sda[kQ2], scr[8];
+
+    const int64_t c = blockIdx.x, b = blockIdx.y;
+    const HeadRange hr = head_range(p);
+    const int L = chunk_len2(p.T, c);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r = lane & 15, q = lane >> 4;
+    const int64_t t0 = b * p.T + c * kQ2;
+    const u16* Bg = static_cast<const u16*>(p.B);
+    const u16* Cg = static_cast<const u16*>(p.C);
+    const u16* xg = static_cast<const u16*>(p.x);
+    const u16* dyg = static_cast<const u16*>(p.dy);
+    u16* dxg = static_cast<u16*>(p.dx);
+    u16* ddtg = static_cast<u16*>(p.ddt);
+
+    // B, B^T, C^T of the chunk
+    for (int i = tid; i < kQ2 * N / 8; i += kT2) {
+        const int s = i / (N / 8), n0 = 8 * (i - s * (N / 8));
+        uint4 vb = make_uint4(0, 0, 0, 0), vc = vb;
+        if (s < L) {
+            const int64_t gi = ((t0 + s) * p.G + hr.g) * N + n0;
+            vb = *reinterpret_cast<const uint4*>(Bg + gi);
+            vc = *reinterpret_cast<const uint4*>(Cg + gi);
+        }
+        *reinterpret_cast<uint4*>(Bs + s * kLdN + n0) = vb;
+        const uint32_t eb[4] = {vb.x, vb.y, vb.z, vb.w}, ec[4] = {vc.x, vc.y, vc.z, vc.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            BT[(n0 + 2 * e) * kLd + s] = static_cast<u16>(eb[e]);
+            BT[(n0 + 2 * e + 1) * kLd + s] = static_cast<u16>(eb[e] >> 16);
+            CT[(n0 + 2 * e) * kLd + s] = static_cast<u16>(ec[e]);
+            CT[(n0 + 2 * e + 1) * kLd + s] = static_cast<u16>(ec[e] >> 16);
+        }
+    }
+    __syncthreads();
+
+    // G0 = C B^T on this wavefront's score tiles (C rows straight from global memory)
+    const int ntile = w < 2 ? 2 : 1;
+    f32x4_t g0[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        g0[k] = zero4();
+        if (k < ntile) {
+            const int2 tl = kLowerTile[w + 8 * k];
+            const int u = 16 * tl.x + r;
+            const int64_t crow = ((t0 + (u < L ? u : 0)) * p.G + hr.g) * N;
+#pragma unroll
+            for (int ks = 0; ks < N / 32; ++ks) {
+                uint4 a = *reinterpret_cast<const uint4*>(Cg + crow + ks * 32 + 8 * q);
+                if (u >= L) a = make_uint4(0, 0, 0, 0);
+                g0[k] = mma(a, ldfrag(Bs, kLdN, 16 * tl.y + r, ks, lane), g0[k]);
+            }
+        }
+    }
+
+    f32x4_t dBacc[kBW], dCacc[kBW];
+#pragma unroll
+    for (int j = 0; j < kBW; ++j) dBacc[j] = dCacc[j] = zero4();
+
+    for (int64_t h = hr.lo; h < hr.hi; ++h) {
+        const int64_t bh = b * p.H + h;
+        const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
+        const u16* Gn = reinterpret_cast<const u16*>(p.gn) + sbase;     // p x n
+        const u16* GnT = reinterpret_cast<const u16*>(p.gnT) + sbase;   // n x p
+        const u16* HinT = reinterpret_cast<const u16*>(p.hin) + sbase;  // n x p
+        const float Ah = -expf(p.A_log[h]);
+        const float Dh = p.D ? p.D[h] : 0.f;
+
+        // this wavefront's state fragments (issued first: they come from HBM)
+        const int pw = w >> 1;                       // p-tile of dX^T
+        uint4 gnf[N / 32], gntf[2], hinf[2];
+#pragma unroll
+        for (int ks = 0; ks < N / 32; ++ks) gnf[ks] = ldfrag_g(Gn, N, 16 * pw + r, ks, lane);
+        {
+            const int nt = (w * kBW) >> 2;   // this wavefront's n-tile of dB^T / dC^T (one per wavefront)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                gntf[ks] = ldfrag_g(GnT, kP2, 16 * nt + r, ks, lane);
+                hinf[ks] = ldfrag_g(HinT, kP2, 16 * nt + r, ks, lane);
+            }
+        }
+        // <Gn, h_in> partial over this thread's 8-element pieces
+        float gh = 0.f;
+        for (int i = tid; i < kP2 * N / 8; i += kT2) {
+            const uint4 a = reinterpret_cast<const uint4*>(GnT)[i];
+            const uint4 z = reinterpret_cast<const uint4*>(HinT)[i];
+            const uint32_t ea[4] = {a.x, a.y, a.z, a.w}, ez[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) gh = fmaf(lo_f(ea[e]), lo_f(ez[e]), fmaf(hi_f(ea[e]), hi_f(ez[e]), gh));
+        }
+
+        __syncthreads();   // the previous head is done with every per-head array
+        if (w == 0) {
+            chunk_cumsum(p, b, c, h, L, scs, sdt);
+            const float csend = __shfl(scs[lane], L - 1, 64);
+            seend[lane] = lane < L ? exp2f(csend - scs[lane]) : 0.f;
+            secs[lane] = lane < L ? exp2f(scs[lane]) : 0.f;
+        }
+        for (int i = tid; i < kQ2 * kP2 / 8; i += kT2) {
+            const int s = i >> 3, p0 = 8 * (i & 7);
+            uint4 vx = make_uint4(0, 0, 0, 0), vd = vx;
+            if (s < L) {
+                const int64_t gi = ((t0 + s) * p.H + h) * kP2 + p0;
+                vx = *reinterpret_cast<const uint4*>(xg + gi);
+                vd = *reinterpret_cast<const uint4*>(dyg + gi);
+            }
+            *reinterpret_cast<uint4*>(xs + s * kLd + p0) = vx;
+            *reinterpret_cast<uint4*>(dys + s * kLd + p0) = vd;
+            const uint32_t ed[4] = {vd.x, vd.y, vd.z, vd.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                dyT[(p0 + 2 * e) * kLd + s] = static_cast<u16>(ed[e]);
+                dyT[(p0 + 2 * e + 1) * kLd + s] = static_cast<u16>(ed[e] >> 16);
+            }
+        }
+        __syncthreads();
+
+        // --- score tiles: R0 = dy x^T (then dt_t), Gs, Rs, l and their sums
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            if (k < ntile) {
+                const int2 tl = kLowerTile[w + 8 * k];
+                f32x4_t acc = zero4();
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+                    acc = mma(ldfrag(dys, kLd, 16 * tl.x + r, ks, lane), ldfrag(xs, kLd, 16 * tl.y + r, ks, lane),
+                              acc);
+                const int t = 16 * tl.y + r;
+                const float dtt = sdt[t], cst = scs[t];
+                float gs[4], rs[4], colsum = 0.f;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int u = 16 * tl.x + 4 * q + v;
+                    float gv = 0.f, rv = 0.f, lv = 0.f;
+                    if (u >= t && u < L) {
+                        const float e = exp2f(scs[u] - cst);
+                        const float r0 = acc[v] * dtt;
+                        gv = e * g0[k][v];
+                        rv = e * r0;
+                        lv = gv * r0;
+                    }
+                    gs[v] = gv;
+                    rs[v] = rv;
+                    colsum += lv;
+                    // row sum of l over the tile's 16 columns t
+                    float rsum = lv;
+                    rsum += __shfl_xor(rsum, 1, 64);
+                    rsum += __shfl_xor(rsum, 2, 64);
+                    rsum += __shfl_xor(rsum, 4, 64);
+                    rsum += __shfl_xor(rsum, 8, 64);
+                    if (r == 0) rowp[16 * tl.x + 4 * q + v][tl.y] = rsum;
+                }
+                colsum += __shfl_xor(colsum, 16, 64);
+                colsum += __shfl_xor(colsum, 32, 64);
+                if (q == 0) colp[t][tl.x] = colsum;
+                const int u0 = 16 * tl.x + 4 * q;
+                *reinterpret_cast<uint2*>(GsT + t * kLd + u0) = make_uint2(pack2(gs[0], gs[1]), pack2(gs[2], gs[3]));
+                *reinterpret_cast<uint2*>(RsT + t * kLd + u0) = make_uint2(pack2(rs[0], rs[1]), pack2(rs[2], rs[3]));
+#pragma unroll
+                for (int v = 0; v < 4; ++v) Rs[(u0 + v) * kLd + t] = static_cast<u16>(bf16_bits(rs[v]));
+            }
+        }
+        if (w >= 2) {
+            const int2 tl = kUpperTile[w - 2];
+            const int t = 16 * tl.y + r, u0 = 16 * tl.x + 4 * q;
+            *reinterpret_cast<uint2*>(GsT + t * kLd + u0) = make_uint2(0, 0);
+            *reinterpret_cast<uint2*>(RsT + t * kLd + u0) = make_uint2(0, 0);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) Rs[(u0 + v) * kLd + t] = 0;
+            if (r == 0)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) rowp[u0 + v][tl.y] = 0.f;
+            if (q == 0) colp[t][tl.x] = 0.f;
+        }
+        gh = [&] {
+            // block sum of <Gn, h_in> (fixed order); its barriers also publish the score tiles
+            float v = gh;
+            for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+            if (lane == 0) scr[w] = v;
+            __syncthreads();
+            const float s = ((scr[0] + scr[1]) + (scr[2] + scr[3])) + ((scr[4] + scr[5]) + (scr[6] + scr[7]));
+            __syncthreads();
+            return s;
+        }();
+
+        // --- dX~^T (p x t): dy^T Gs + e(end,t) Gn B^T; dx, and per-token sums
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int tt = 2 * (w & 1) + j;
+            f32x4_t ai = zero4(), ag = zero4();
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                ai = mma(ldfrag(dyT, kLd, 16 * pw + r, ks, lane), ldfrag(GsT, kLd, 16 * tt + r, ks, lane), ai);
+#pragma unroll
+            for (int ks = 0; ks < N / 32; ++ks) ag = mma(gnf[ks], ldfrag(Bs, kLdN, 16 * tt + r, ks, lane), ag);
+            const int t = 16 * tt + r, p0 = 16 * pw + 4 * q;
+            const float ee = seend[t], dtt = sdt[t];
+            const uint2 xv = *reinterpret_cast<const uint2*>(xs + t * kLd + p0);
+            const uint2 dv = *reinterpret_cast<const uint2*>(dys + t * kLd + p0);
+            const float xf[4] = {lo_f(xv.x), hi_f(xv.x), lo_f(xv.y), hi_f(xv.y)};
+            const float df[4] = {lo_f(dv.x), hi_f(dv.x), lo_f(dv.y), hi_f(dv.y)};
+            float dx[4], sxd = 0.f, sxg = 0.f, sdx = 0.f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float dX = fmaf(ee, ag[v], ai[v]);
+                dx[v] = fmaf(dtt, dX, Dh * df[v]);
+                sxd = fmaf(xf[v], dX, sxd);
+                sxg = fmaf(xf[v], ag[v], sxg);
+                sdx = fmaf(df[v], xf[v], sdx);
+            }
+            if (t < L)
+                *reinterpret_cast<uint2*>(dxg + (t0 + t) * p.H * kP2 + h * kP2 + p0) =
+                    make_uint2(pack2(dx[0], dx[1]), pack2(dx[2], dx[3]));
+            sxd += __shfl_xor(sxd, 16, 64);
+            sxd += __shfl_xor(sxd, 32, 64);
+            sxg += __shfl_xor(sxg, 16, 64);
+            sxg += __shfl_xor(sxg, 32, 64);
+            sdx += __shfl_xor(sdx, 16, 64);
+            sdx += __shfl_xor(sdx, 32, 64);
+            if (q == 0) {
+                xdxp[t][pw] = sxd;
+                q2p[t][pw] = sxg;
+                dyxp[t][pw] = sdx;
+            }
+        }
+
+        // --- dB^T (n x t) += C^T Rs + e(end,t) dt_t Gn^T x^T;  dC^T (n x u) += B^T Rs^T + exp(cs_u) h_in^T dy^T
+#pragma unroll
+        for (int j = 0; j < kBW; ++j) {
+            const int idx = w * kBW + j, nt = idx >> 2, tt = idx & 3;
+            f32x4_t bi = zero4(), bx = zero4(), ci = zero4(), ch = zero4();
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                bi = mma(ldfrag(CT, kLd, 16 * nt + r, ks, lane), ldfrag(RsT, kLd, 16 * tt + r, ks, lane), bi);
+                bx = mma(gntf[ks], ldfrag(xs, kLd, 16 * tt + r, ks, lane), bx);
+                ci = mma(ldfrag(BT, kLd, 16 * nt + r, ks, lane), ldfrag(Rs, kLd, 16 * tt + r, ks, lane), ci);
+                ch = mma(hinf[ks], ldfrag(dys, kLd, 16 * tt + r, ks, lane), ch);
+            }
+            const int t = 16 * tt + r;
+            const float fb = seend[t] * sdt[t], fc = secs[t];
+            float q1 = 0.f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                dBacc[j][v] += fmaf(fb, bx[v], bi[v]);
+                dCacc[j][v] += fmaf(fc, ch[v], ci[v]);
+                q1 = fmaf(bf(CT[(16 * nt + 4 * q + v) * kLd + t]), ch[v], q1);
+            }
+            q1 += __shfl_xor(q1, 16, 64);
+            q1 += __shfl_xor(q1, 32, 64);
+            if (q == 0) q1p[t][nt] = q1;
+        }
+        __syncthreads();
+
+        // --- per token: dcs, then the decay gradients
+        if (tid < kQ2) {
+            const int t = tid;
+            float s2 = 0.f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) s2 += q2p[t][k];
+            sq2[t] = t < L ? sdt[t] * s2 : 0.f;   // X~_t . (Gn B_t)
+        }
+        __syncthreads();
+        if (tid < kQ2) {
+            const int t = tid;
+            float dcs = 0.f;
+            if (t < L) {
+                float row = 0.f, col = 0.f, s1 = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    row += rowp[t][k];
+                    col += colp[t][k];
+                }
+#pragma unroll
+                for (int k = 0; k < kNT; ++k) s1 += q1p[t][k];
+                dcs = row - col + secs[t] * s1 - seend[t] * sq2[t];
+                if (t == L - 1) {
+                    float hout = secs[t] * gh;
+                    for (int s = 0; s < L; ++s) hout = fmaf(seend[s], sq2[s], hout);
+                    dcs += hout;
+                }
+            }
+            sdcs[t] = dcs;
+        }
+        __syncthreads();
+        if (tid < kQ2) {
+            const int k = tid;
+            float da = 0.f;
+            for (int t = L - 1; t >= k; --t) da += sdcs[t];
+            float xd = 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) xd += xdxp[k][j];
+            if (k < L) ddtg[(t0 + k) * p.H + h] = static_cast<u16>(bf16_bits(fmaf(Ah, da, xd)));
+            sda[k] = k < L ? sdt[k] * da : 0.f;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            float sa = 0.f, sd = 0.f;
+            for (int k = 0; k < L; ++k) {
+                sa += sda[k];
+                sd += (dyxp[k][0] + dyxp[k][1]) + (dyxp[k][2] + dyxp[k][3]);
+            }
+            p.dAp[bh * p.nC + c] = sa;
+            p.dDp[bh * p.nC + c] = sd;
+        }
+    }
+
+    // this slice's dB and dC for the chunk: lane holds n = 16 nt + 4 q + v, t = 16 tt + r
+#pragma unroll
+    for (int j = 0; j < kBW; ++j) {
+        const int idx = w * kBW + j, nt = idx >> 2, tt = idx & 3;
+        const int t = 16 * tt + r;
+        if (t < L) {
+            const int64_t o = ((hr.slice * p.b * p.T + t0 + t) * p.G + hr.g) * N + 16 * nt + 4 * q;
+            *reinterpret_cast<float4*>(p.dBp + o) = make_float4(dBacc[j][0], dBacc[j][1], dBacc[j][2], dBacc[j][3]);
+            *reinterpret_cast<float4*>(p.dCp + o) = make_float4(dCacc[j][0], dCacc[j][1], dCacc[j][2], dCacc[j][3]);
+        }
+    }
+}
+
+template <int N>
+hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
+{
+    const size_t sm_states = sizeof(u16) * static_cast<size_t>(2 * N * kLd + 2 * kP2 * kLd);
+    const size_t sm_chunk = ChunkSmem<N>::kBytes;
+    hipError_t e;
+    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bwd2_states<N>),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_states))) !=
+        hipSuccess)
+        return e;
+    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bwd2_chunk<N>),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
+        hipSuccess)
+        return e;
+    const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
+    hipLaunchKernelGGL(k_bwd2_states<N>, grid, dim3(kT2), sm_states, st, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int64_t nscan = 3 * p.b * p.H * kP2 * N / 8;
+    hipLaunchKernelGGL(k_bwd2_scan<N>, dim3(static_cast<unsigned>((nscan + 255) / 256)), dim3(256), 0, st, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_bwd2_chunk<N>, grid, dim3(kT2), sm_chunk, st, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
+    return launch_backward_reduce(p, true, st);
+}
+
+}  // namespace
+
+bool bwd_fast_supported(bool bf16, int64_t P, int64_t N) { return bf16 && P == kP2 && (N == 64 || N == 128); }
+
+hipError_t launch_backward_fast(const BwdParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
+{
+    return p.N == 64 ? launch_fast<64>(p, stream, ev_begin, ev_end) : launch_fast<128>(p, stream, ev_begin, ev_end);
+}
+
+}  // namespace ssd

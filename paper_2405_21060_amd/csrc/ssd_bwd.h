@@ -9,11 +9,13 @@
 namespace ssd {
 
 // Tokens per chunk of the backward's own decomposition (independent of the
-// forward's chunk size: the gradient of the layer does not depend on it).
+// forward's chunk size: the gradient of the layer does not depend on it):
+// 32 on the general path, 64 on the matrix-core path.
 constexpr int64_t kBwdQ = 32;
+constexpr int64_t kBwdQFast = 64;
 
 struct BwdParams {
-    int64_t b, T, H, P, N, G, nC;   // nC = ceil(T / kBwdQ)
+    int64_t b, T, H, P, N, G, nC;   // nC = ceil(T / chunk) (kBwdQ, or kBwdQFast)
     int64_t S, hs;                  // head slices per group, heads per slice
     const void* x;
     const void* dt;
@@ -32,10 +34,12 @@ struct BwdParams {
     float* dD;             // may be null
     float* dinit;          // may be null
     // workspace (float32)
-    float* cs;     // (b, H, nC, kBwdQ)   chunk-local inclusive cumsum of dt*A, log2 units
+    float* cs;     // (b, H, nC, chunk)   chunk-local inclusive cumsum of dt*A, log2 units
     float* hin;    // (b, nC, H, P, N)    chunk states, then the state entering each chunk
+                   //                     (matrix-core path: bf16, (b, nC, H, N, P))
     float* gn;     // (b, nC, H, P, N)    output-to-state terms, then the gradient of the state
-                   //                     leaving each chunk
+                   //                     leaving each chunk (matrix-core path: bf16)
+    float* gnT;    // matrix-core path only: gn transposed, bf16 (b, nC, H, N, P)
     float* dBp;    // (S, b, T, G, N)     dB over one slice of a group's heads
     float* dCp;    // (S, b, T, G, N)
     float* dAp;    // (b, H, nC)          per-chunk terms of dA
@@ -43,13 +47,22 @@ struct BwdParams {
 };
 
 struct BwdLayout {
-    size_t cs, hin, gn, dBp, dCp, dAp, dDp, total;
+    size_t cs, hin, gn, gnT, dBp, dCp, dAp, dDp, total;
 };
 
 // Head slices: enough (b, chunk, group, slice) workgroups to fill the chip.
 void bwd_slices(int64_t b, int64_t nC, int64_t G, int64_t heads_per_group, int64_t* S, int64_t* hs);
 
-BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int64_t G, int64_t nC, int64_t S);
+BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int64_t G, int64_t nC, int64_t S,
+                     bool fast);
+
+// The matrix-core path covers bf16 with headdim 64 and dstate 64 or 128.
+bool bwd_fast_supported(bool bf16, int64_t P, int64_t N);
+hipError_t launch_backward_fast(const BwdParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end);
+
+// The final sums over head slices (dB, dC) and over rows and chunks (dA_log,
+// dD), shared by both paths.
+hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream);
 
 // Enqueue the whole backward on `stream`; `ev_begin` / `ev_end` (may be null)
 // are recorded right before and right after the chunk-gradient kernel.

@@ -205,9 +205,14 @@ def test_backward_validation(lib):
     assert bwd(prob(), ws_bytes=need - 1) == ssd.SSD_ERR_WORKSPACE
     assert ssd.ssd_backward(prob(), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE,
                             0, 0, 0, need, 0) == ssd.SSD_ERR_WORKSPACE
-    # two float32 states per (batch, 32-token chunk, head) dominate the workspace
+    # three bf16 states per (batch, 64-token chunk, head) dominate the workspace of the
+    # matrix-core shapes, two float32 states per 32 tokens the others'
+    states = 4 * (4096 // 64) * 80 * 64 * 128 * 2
+    assert 3 * states <= need <= 3 * states + (256 << 20)
     states = 4 * (4096 // 32) * 80 * 64 * 128 * 4
-    assert 2 * states <= need <= 2 * states + (128 << 20)
+    need32 = ssd.ssd_backward_workspace_bytes(prob(dtype=ssd.SSD_DTYPE_F32))
+    assert 2 * states <= need32 <= 2 * states + (128 << 20)
+    assert bwd(prob(), dy=FAKE + 2) == ssd.SSD_ERR_UNSUPPORTED_DIMS
     assert ssd.ssd_backward(prob(seqlen=0), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, 0, FAKE, FAKE, FAKE,
                             FAKE, FAKE, 0, 0, FAKE, need, 0, FAKE, FAKE) == ssd.SSD_ERR_BAD_SHAPE
 

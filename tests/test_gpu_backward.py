@@ -81,6 +81,19 @@ CASES = [
     (1, 2048, 80, 16, 16, 1, "f32", True, True, True),
     # six heads per group over 1024 (row, chunk, group) units: slices of 4 and 2 heads
     (1, 16384, 12, 16, 16, 2, "f32", True, True, True),
+    # matrix-core shapes (bf16, headdim 64, dstate 64 or 128)
+    (1, 1, 2, 64, 64, 1, "bf16", True, True, True),
+    (2, 130, 4, 64, 128, 2, "bf16", True, True, True),
+    (1, 64, 3, 64, 64, 3, "bf16", False, False, False),
+    (2, 200, 8, 64, 128, 1, "bf16", True, False, True),
+    (1, 63, 2, 64, 128, 1, "bf16", True, True, False),
+]
+
+# shapes of the matrix-core path, also run on the general path (SSD_PATH=unfused),
+# and with heads split into slices of 3 per workgroup (SSD_BWD_HEADS_PER_SLICE)
+FAST_SHAPES = [
+    (2, 257, 6, 64, 128, 2, "bf16", True, True, True),
+    (3, 96, 8, 64, 64, 1, "bf16", True, False, True),
 ]
 
 
@@ -102,6 +115,14 @@ def test_backward_matches_oracle(case):
         check("dD", got["dD"], ref["dD"], tol)
     else:
         assert got["dD"] is None
+
+
+@pytest.mark.parametrize("knob", ["SSD_PATH=unfused", "SSD_BWD_HEADS_PER_SLICE=3"])
+@pytest.mark.parametrize("case", FAST_SHAPES, ids=lambda c: "b%d_T%d_H%d_P%d_N%d_G%d_%s_D%d_i%d_f%d" % c)
+def test_backward_knobs_match_oracle(case, knob, monkeypatch):
+    name, value = knob.split("=")
+    monkeypatch.setenv(name, value)
+    test_backward_matches_oracle(case)
 
 
 def test_backward_full_size_head_subset():
