@@ -66,6 +66,14 @@ __device__ __forceinline__ uint4 ldfrag_g(const u16* a, int64_t ld, int row, int
     return *reinterpret_cast<const uint4*>(a + static_cast<int64_t>(row) * ld + ks * 32 + 8 * (lane >> 4));
 }
 
+// Sum over the 64 lanes of a wavefront (butterfly: every lane gets it).
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
 __device__ __forceinline__ int chunk_len2(int64_t T, int64_t c)
 {
     const int64_t r = T - c * kQ2;
@@ -88,26 +96,6 @@ __device__ __forceinline__ HeadRange head_range(const BwdParams& p)
     return r;
 }
 
-// Inclusive cumsum of dt*A (log2 units) over the chunk by wavefront 0; fills
-// scs, sdt and the workspace copy.  Lanes beyond the chunk carry zero dt.
-__device__ __forceinline__ void chunk_cumsum(const BwdParams& p, int64_t b, int64_t c, int64_t h, int L,
-                                             float* scs, float* sdt)
-{
-    const int lane = threadIdx.x;
-    const u16* dt = static_cast<const u16*>(p.dt);
-    const float A2 = -expf(p.A_log[h]) * kLog2e;
-    const float dtv = lane < L ? bf(dt[(b * p.T + c * kQ2 + lane) * p.H + h]) : 0.f;
-    float v = dtv * A2;
-#pragma unroll
-    for (int sh = 1; sh < 64; sh <<= 1) {
-        const float o = __shfl_up(v, sh, 64);
-        if (lane >= sh) v += o;
-    }
-    scs[lane] = v;
-    sdt[lane] = dtv;
-    p.cs[((b * p.H + h) * p.nC + c) * kQ2 + lane] = v;
-}
-
 // ---------------------------------------------------------------------------
 // States: per head, H^T (n x p) = sum_s B_s[n] (e(end,s) dt_s x_s[p]) and
 // W (p x n) = sum_u (exp(cs_u) dy_u[p]) C_u[n], plus W^T; bf16 outputs.
@@ -119,13 +107,13 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
     u16* CT = BT + N * kLd;         // N x kLd   C^T
     u16* XwT = CT + N * kLd;        // 64 x kLd  (e(end,s) dt_s x_s)^T (row p, k = s)
     u16* DwT = XwT + kP2 * kLd;     // 64 x kLd  (exp(cs_u) dy_u)^T
-    __shared__ float scs[kQ2], sdt[kQ2];
 
     const int64_t c = blockIdx.x, b = blockIdx.y;
     const HeadRange hr = head_range(p);
     const int L = chunk_len2(p.T, c);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t t0 = b * p.T + c * kQ2;
+    const u16* dtg = static_cast<const u16*>(p.dt);
     const u16* Bg = static_cast<const u16*>(p.B);
     const u16* Cg = static_cast<const u16*>(p.C);
     const u16* xg = static_cast<const u16*>(p.x);
@@ -153,38 +141,47 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
         }
     }
 
+    // one head's inputs, fetched a head ahead: dt (every wavefront, lane =
+    // token) and one 8-wide piece of x and of dy per thread (row s_me)
+    const int s_me = tid >> 3, p0_me = 8 * (tid & 7);
+    float pdt = 0.f;
+    uint4 px = make_uint4(0, 0, 0, 0), pd = px;
+    const auto fetch = [&](int64_t h) {
+        pdt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
+        px = pd = make_uint4(0, 0, 0, 0);
+        if (s_me < L) {
+            const int64_t gi = ((t0 + s_me) * p.H + h) * kP2 + p0_me;
+            px = *reinterpret_cast<const uint4*>(xg + gi);
+            pd = *reinterpret_cast<const uint4*>(dyg + gi);
+        }
+    };
+    fetch(hr.lo);
+
     for (int64_t h = hr.lo; h < hr.hi; ++h) {
-        __syncthreads();   // the previous head is done with XwT, DwT, scs, sdt
-        if (w == 0) chunk_cumsum(p, b, c, h, L, scs, sdt);
-        __syncthreads();
-        const float csend = scs[L - 1];
-        for (int i = tid; i < kQ2 * kP2 / 8; i += kT2) {
-            const int s = i >> 3, p0 = 8 * (i & 7);
-            float xw[8], dw[8];
-            if (s < L) {
-                const int64_t gi = ((t0 + s) * p.H + h) * kP2 + p0;
-                const uint4 vx = *reinterpret_cast<const uint4*>(xg + gi);
-                const uint4 vd = *reinterpret_cast<const uint4*>(dyg + gi);
-                const float fx = exp2f(csend - scs[s]) * sdt[s], fd = exp2f(scs[s]);
-                const uint32_t ex[4] = {vx.x, vx.y, vx.z, vx.w}, ed[4] = {vd.x, vd.y, vd.z, vd.w};
+        // inclusive cumsum of dt*A (log2 units), each wavefront for itself
+        const float A2 = -expf(p.A_log[h]) * kLog2e;
+        float cs = pdt * A2;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    xw[2 * e] = fx * lo_f(ex[e]);
-                    xw[2 * e + 1] = fx * hi_f(ex[e]);
-                    dw[2 * e] = fd * lo_f(ed[e]);
-                    dw[2 * e + 1] = fd * hi_f(ed[e]);
-                }
-            } else {
+        for (int sh = 1; sh < 64; sh <<= 1) {
+            const float o = __shfl_up(cs, sh, 64);
+            if (lane >= sh) cs += o;
+        }
+        if (w == 0) p.cs[((b * p.H + h) * p.nC + c) * kQ2 + lane] = cs;
+        const float csend = __shfl(cs, L - 1, 64);
+        const float cs_s = __shfl(cs, s_me, 64), dt_s = __shfl(pdt, s_me, 64);
+        {
+            const float fx = exp2f(csend - cs_s) * dt_s, fd = exp2f(cs_s);   // rows beyond L hold zeros
+            const uint32_t ex[4] = {px.x, px.y, px.z, px.w}, ed[4] = {pd.x, pd.y, pd.z, pd.w};
 #pragma unroll
-                for (int e = 0; e < 8; ++e) xw[e] = dw[e] = 0.f;
-            }
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                XwT[(p0 + e) * kLd + s] = static_cast<u16>(bf16_bits(xw[e]));
-                DwT[(p0 + e) * kLd + s] = static_cast<u16>(bf16_bits(dw[e]));
+            for (int e = 0; e < 4; ++e) {
+                XwT[(p0_me + 2 * e) * kLd + s_me] = static_cast<u16>(bf16_bits(fx * lo_f(ex[e])));
+                XwT[(p0_me + 2 * e + 1) * kLd + s_me] = static_cast<u16>(bf16_bits(fx * hi_f(ex[e])));
+                DwT[(p0_me + 2 * e) * kLd + s_me] = static_cast<u16>(bf16_bits(fd * lo_f(ed[e])));
+                DwT[(p0_me + 2 * e + 1) * kLd + s_me] = static_cast<u16>(bf16_bits(fd * hi_f(ed[e])));
             }
         }
-        __syncthreads();
+        if (h + 1 < hr.hi) fetch(h + 1);
+        __syncthreads();   // XwT, DwT (and, the first time, B^T, C^T) are in place
 
         const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
         const int r = lane & 15, q = lane >> 4;
@@ -215,6 +212,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
                     make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
             }
         }
+        __syncthreads();   // done with XwT, DwT before the next head overwrites them
     }
 }
 
@@ -310,9 +308,11 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     u16* GsT = dyT + kQ2 * kLd;         // 64 x kLd   Gs^T (row t, k = u)
     u16* Rs = GsT + kQ2 * kLd;          // 64 x kLd   Rs  (row u, k = t)
     u16* RsT = Rs + kQ2 * kLd;          // 64 x kLd   Rs^T (row t, k = u)
-    __shared__ float scs[kQ2], sdt[kQ2], seend[kQ2], secs[kQ2];
+    // per-token factors, double-buffered by head parity (the per-token phase of
+    // one head overlaps the next head's set-up)
+    __shared__ float scs2[2][kQ2], sdt2[2][kQ2], seend2[2][kQ2], secs2[2][kQ2];
     __shared__ float rowp[kQ2][4], colp[kQ2][4], xdxp[kQ2][4], q2p[kQ2][4], dyxp[kQ2][4], q1p[kQ2][kNT];
-    __shared__ float sq2[kQ2], sdcs[kQ2], sda[kQ2], scr[8];
+    __shared__ float scr[8];
 
     const int64_t c = blockIdx.x, b = blockIdx.y;
     const HeadRange hr = head_range(p);
@@ -324,6 +324,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     const u16* Cg = static_cast<const u16*>(p.C);
     const u16* xg = static_cast<const u16*>(p.x);
     const u16* dyg = static_cast<const u16*>(p.dy);
+    const u16* dtg = static_cast<const u16*>(p.dt);
     u16* dxg = static_cast<u16*>(p.dx);
     u16* ddtg = static_cast<u16*>(p.ddt);
 
@@ -371,6 +372,22 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 #pragma unroll
     for (int j = 0; j < kBW; ++j) dBacc[j] = dCacc[j] = zero4();
 
+    // one head's inputs, fetched a head ahead: dt (wavefront 0, lane = token)
+    // and one 8-wide piece of x and of dy per thread (row s_me)
+    const int s_me = tid >> 3, p0_me = 8 * (tid & 7);
+    float pdt = 0.f;
+    uint4 px = make_uint4(0, 0, 0, 0), pd = px;
+    const auto fetch = [&](int64_t h) {
+        if (w == 0) pdt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
+        px = pd = make_uint4(0, 0, 0, 0);
+        if (s_me < L) {
+            const int64_t gi = ((t0 + s_me) * p.H + h) * kP2 + p0_me;
+            px = *reinterpret_cast<const uint4*>(xg + gi);
+            pd = *reinterpret_cast<const uint4*>(dyg + gi);
+        }
+    };
+    fetch(hr.lo);
+
     for (int64_t h = hr.lo; h < hr.hi; ++h) {
         const int64_t bh = b * p.H + h;
         const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
@@ -379,6 +396,11 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
         const u16* HinT = reinterpret_cast<const u16*>(p.hin) + sbase;  // n x p
         const float Ah = -expf(p.A_log[h]);
         const float Dh = p.D ? p.D[h] : 0.f;
+        const int hb = static_cast<int>((h - hr.lo) & 1);
+        float* const scs = scs2[hb];
+        float* const sdt = sdt2[hb];
+        float* const seend = seend2[hb];
+        float* const secs = secs2[hb];
 
         // this wavefront's state fragments (issued first: they come from HBM)
         const int pw = w >> 1;                       // p-tile of dX^T
@@ -393,41 +415,34 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
                 hinf[ks] = ldfrag_g(HinT, kP2, 16 * nt + r, ks, lane);
             }
         }
-        // <Gn, h_in> partial over this thread's 8-element pieces
-        float gh = 0.f;
-        for (int i = tid; i < kP2 * N / 8; i += kT2) {
-            const uint4 a = reinterpret_cast<const uint4*>(GnT)[i];
-            const uint4 z = reinterpret_cast<const uint4*>(HinT)[i];
-            const uint32_t ea[4] = {a.x, a.y, a.z, a.w}, ez[4] = {z.x, z.y, z.z, z.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) gh = fmaf(lo_f(ea[e]), lo_f(ez[e]), fmaf(hi_f(ea[e]), hi_f(ez[e]), gh));
-        }
-
-        __syncthreads();   // the previous head is done with every per-head array
-        if (w == 0) {
-            chunk_cumsum(p, b, c, h, L, scs, sdt);
-            const float csend = __shfl(scs[lane], L - 1, 64);
-            seend[lane] = lane < L ? exp2f(csend - scs[lane]) : 0.f;
-            secs[lane] = lane < L ? exp2f(scs[lane]) : 0.f;
-        }
-        for (int i = tid; i < kQ2 * kP2 / 8; i += kT2) {
-            const int s = i >> 3, p0 = 8 * (i & 7);
-            uint4 vx = make_uint4(0, 0, 0, 0), vd = vx;
-            if (s < L) {
-                const int64_t gi = ((t0 + s) * p.H + h) * kP2 + p0;
-                vx = *reinterpret_cast<const uint4*>(xg + gi);
-                vd = *reinterpret_cast<const uint4*>(dyg + gi);
-            }
-            *reinterpret_cast<uint4*>(xs + s * kLd + p0) = vx;
-            *reinterpret_cast<uint4*>(dys + s * kLd + p0) = vd;
-            const uint32_t ed[4] = {vd.x, vd.y, vd.z, vd.w};
+        // this head's x, dy (fetched during the previous head) into shared memory
+        *reinterpret_cast<uint4*>(xs + s_me * kLd + p0_me) = px;
+        *reinterpret_cast<uint4*>(dys + s_me * kLd + p0_me) = pd;
+        {
+            const uint32_t ed[4] = {pd.x, pd.y, pd.z, pd.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                dyT[(p0 + 2 * e) * kLd + s] = static_cast<u16>(ed[e]);
-                dyT[(p0 + 2 * e + 1) * kLd + s] = static_cast<u16>(ed[e] >> 16);
+                dyT[(p0_me + 2 * e) * kLd + s_me] = static_cast<u16>(ed[e]);
+                dyT[(p0_me + 2 * e + 1) * kLd + s_me] = static_cast<u16>(ed[e] >> 16);
             }
         }
-        __syncthreads();
+        if (w == 0) {
+            // cumsum of dt*A (log2 units) and the per-token factors
+            const float A2 = Ah * kLog2e;
+            float cs = pdt * A2;
+#pragma unroll
+            for (int sh = 1; sh < 64; sh <<= 1) {
+                const float o = __shfl_up(cs, sh, 64);
+                if (lane >= sh) cs += o;
+            }
+            const float csend = __shfl(cs, L - 1, 64);
+            scs[lane] = cs;
+            sdt[lane] = pdt;
+            seend[lane] = lane < L ? exp2f(csend - cs) : 0.f;
+            secs[lane] = lane < L ? exp2f(cs) : 0.f;
+        }
+        if (h + 1 < hr.hi) fetch(h + 1);
+        __syncthreads();   // (1) per-head inputs in place
 
         // --- score tiles: R0 = dy x^T (then dt_t), Gs, Rs, l and their sums
 #pragma unroll
@@ -486,16 +501,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
                 for (int v = 0; v < 4; ++v) rowp[u0 + v][tl.y] = 0.f;
             if (q == 0) colp[t][tl.x] = 0.f;
         }
-        gh = [&] {
-            // block sum of <Gn, h_in> (fixed order); its barriers also publish the score tiles
-            float v = gh;
-            for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-            if (lane == 0) scr[w] = v;
-            __syncthreads();
-            const float s = ((scr[0] + scr[1]) + (scr[2] + scr[3])) + ((scr[4] + scr[5]) + (scr[6] + scr[7]));
-            __syncthreads();
-            return s;
-        }();
+        __syncthreads();   // (2) score tiles and their sums in place
 
         // --- dX~^T (p x t): dy^T Gs + e(end,t) Gn B^T; dx, and per-token sums
 #pragma unroll
@@ -565,56 +571,62 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
         }
         __syncthreads();
 
-        // --- per token: dcs, then the decay gradients
-        if (tid < kQ2) {
-            const int t = tid;
-            float s2 = 0.f;
+        {
+            // <Gn, h_in> from this wavefront's fragments of Gn^T and h_in^T (one
+            // n-tile; with dstate 64 two wavefronts hold each tile, the even one counts it)
+            float gh = 0.f;
+            if (kBW == 4 || (w & 1) == 0) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k) s2 += q2p[t][k];
-            sq2[t] = t < L ? sdt[t] * s2 : 0.f;   // X~_t . (Gn B_t)
-        }
-        __syncthreads();
-        if (tid < kQ2) {
-            const int t = tid;
-            float dcs = 0.f;
-            if (t < L) {
-                float row = 0.f, col = 0.f, s1 = 0.f;
+                for (int ks = 0; ks < 2; ++ks) {
+                    const uint32_t ea[4] = {gntf[ks].x, gntf[ks].y, gntf[ks].z, gntf[ks].w};
+                    const uint32_t ez[4] = {hinf[ks].x, hinf[ks].y, hinf[ks].z, hinf[ks].w};
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    row += rowp[t][k];
-                    col += colp[t][k];
-                }
-#pragma unroll
-                for (int k = 0; k < kNT; ++k) s1 += q1p[t][k];
-                dcs = row - col + secs[t] * s1 - seend[t] * sq2[t];
-                if (t == L - 1) {
-                    float hout = secs[t] * gh;
-                    for (int s = 0; s < L; ++s) hout = fmaf(seend[s], sq2[s], hout);
-                    dcs += hout;
+                    for (int e = 0; e < 4; ++e)
+                        gh = fmaf(lo_f(ea[e]), lo_f(ez[e]), fmaf(hi_f(ea[e]), hi_f(ez[e]), gh));
                 }
             }
-            sdcs[t] = dcs;
+            gh = wave_sum(gh);
+            if (lane == 0) scr[w] = gh;
         }
-        __syncthreads();
-        if (tid < kQ2) {
-            const int k = tid;
-            float da = 0.f;
-            for (int t = L - 1; t >= k; --t) da += sdcs[t];
-            float xd = 0.f;
+        __syncthreads();   // (3) per-token partial sums in place
+
+        // --- per token (wavefront 1, lane = token): dcs, then the decay gradients.
+        // The other wavefronts go on to the next head's set-up meanwhile; what
+        // they write there (inputs, the other buffer of per-token factors) this
+        // does not read, and the partial sums are rewritten only after the next
+        // barrier (1).
+        if (w == 1) {
+            const int t = lane;
+            const bool in = t < L;
+            float s2 = 0.f, row = 0.f, col = 0.f, s1 = 0.f, xd = 0.f, dyx = 0.f;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) xd += xdxp[k][j];
-            if (k < L) ddtg[(t0 + k) * p.H + h] = static_cast<u16>(bf16_bits(fmaf(Ah, da, xd)));
-            sda[k] = k < L ? sdt[k] * da : 0.f;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            float sa = 0.f, sd = 0.f;
-            for (int k = 0; k < L; ++k) {
-                sa += sda[k];
-                sd += (dyxp[k][0] + dyxp[k][1]) + (dyxp[k][2] + dyxp[k][3]);
+            for (int k = 0; k < 4; ++k) {
+                s2 += q2p[t][k];
+                row += rowp[t][k];
+                col += colp[t][k];
+                xd += xdxp[t][k];
+                dyx += dyxp[t][k];
             }
-            p.dAp[bh * p.nC + c] = sa;
-            p.dDp[bh * p.nC + c] = sd;
+#pragma unroll
+            for (int k = 0; k < kNT; ++k) s1 += q1p[t][k];
+            const float q2 = in ? sdt[t] * s2 : 0.f;   // X~_t . (Gn B_t)
+            const float ghs = ((scr[0] + scr[1]) + (scr[2] + scr[3])) + ((scr[4] + scr[5]) + (scr[6] + scr[7]));
+            const float hsum = wave_sum(seend[t] * q2);
+            float dcs = in ? row - col + secs[t] * s1 - seend[t] * q2 : 0.f;
+            if (t == L - 1) dcs += secs[t] * ghs + hsum;   // <Gn, h_out>
+            float da = dcs;   // suffix sum: over tokens t >= this one
+#pragma unroll
+            for (int sh = 1; sh < 64; sh <<= 1) {
+                const float o = __shfl_down(da, sh, 64);
+                if (lane + sh < 64) da += o;
+            }
+            if (in) ddtg[(t0 + t) * p.H + h] = static_cast<u16>(bf16_bits(fmaf(Ah, da, xd)));
+            const float sa = wave_sum(in ? sdt[t] * da : 0.f);
+            const float sd = wave_sum(in ? dyx : 0.f);
+            if (lane == 0) {
+                p.dAp[bh * p.nC + c] = sa;
+                p.dDp[bh * p.nC + c] = sd;
+            }
         }
     }
 
