@@ -259,7 +259,7 @@ int ssd_span_correct(const ssd_problem* prob, const void* dt, const float* A_log
  * x, B, C, dy, dx, initial_states, dfinal_states and dinitial_states must be
  * 16-byte aligned (else SSD_ERR_UNSUPPORTED_DIMS).  Arithmetic in float32; dtype outputs are
  * rounded to nearest even.  Workspace: ssd_backward_workspace_bytes() bytes of
- * device memory (it holds a state per 64 tokens and head three times in bf16
+ * device memory (it holds a state per 64 tokens and head twice in bf16
  * for bf16 with headdim 64 and dstate 64 or 128, which run on the matrix
  * cores; otherwise one per 32 tokens and head twice in float32).  Ownership,
  * asynchrony, determinism and errors as for ssd_forward. */

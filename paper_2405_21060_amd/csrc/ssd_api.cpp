@@ -515,7 +515,7 @@ int backward_impl(const ssd_problem* prob, const void* x, const void* dt, const 
     p.dinit = dinitial_states;
     p.cs = reinterpret_cast<float*>(ws + l.cs);
     p.hin = reinterpret_cast<float*>(ws + l.hin);
-    p.gn = reinterpret_cast<float*>(ws + l.gn);
+    p.gn = fast ? nullptr : reinterpret_cast<float*>(ws + l.gn);
     p.gnT = fast ? reinterpret_cast<float*>(ws + l.gnT) : nullptr;
     p.dBp = reinterpret_cast<float*>(ws + l.dBp);
     p.dCp = reinterpret_cast<float*>(ws + l.dCp);

@@ -506,7 +506,7 @@ BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int6
     const size_t state_bytes = static_cast<size_t>(b * nC * H * P * N) * (fast ? 2 : 4);
     l.cs = take(static_cast<size_t>(b * H * nC * (fast ? kBwdQFast : kBwdQ)));
     l.hin = take_bytes(state_bytes);
-    l.gn = take_bytes(state_bytes);
+    l.gn = fast ? 0 : take_bytes(state_bytes);
     l.gnT = fast ? take_bytes(state_bytes) : 0;
     l.dBp = take(static_cast<size_t>(S * b * T * G * N));
     l.dCp = take(static_cast<size_t>(S * b * T * G * N));

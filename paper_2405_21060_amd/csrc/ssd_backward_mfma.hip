@@ -4,18 +4,17 @@
 // v_mfma_f32_16x16x32_bf16 (bf16 operands, float32 accumulation):
 //
 //   k_bwd2_states  per (chunk, row, group, head slice): the cumsum, and per
-//                  head H_c^T (n x p), W_c (p x n) and W_c^T (n x p), rounded
-//                  to bf16 in the layouts the chunk kernel reads them in
+//                  head H_c^T and W_c^T (n x p), rounded to bf16
 //   k_bwd2_scan    the two scans over chunks, in place on those bf16 arrays
-//                  with float32 running sums: H^T -> h_in^T, W -> Gn, W^T -> Gn^T;
+//                  with float32 running sums: H^T -> h_in^T, W^T -> Gn^T;
 //                  the initial-state gradient in float32
 //   k_bwd2_chunk   per (chunk, row, group, head slice): all chunk terms.  Score
 //                  tiles (u >= t) R0 = dy x^T and G0 = C B^T (once per
 //                  workgroup), then dX~^T = dy^T Gs + Gn B^T, dB^T = C^T Rs +
 //                  Gn^T x~^T, dC^T = B^T Rs^T + h_in^T dy^T, each as 16 x 16
 //                  tiles whose operands are k-contiguous rows: in shared memory
-//                  (B, B^T, C^T, x, dy, dy^T and the score tiles), or straight
-//                  from global memory (Gn, Gn^T, h_in^T).
+//                  (B, B^T, C^T, x, dy, dy^T, the score tiles and Gn, transposed
+//                  there from Gn^T), or straight from global memory (Gn^T, h_in^T).
 //
 // An MFMA operand row holds the contraction index contiguously; a lane
 // (row r = lane % 16, group q = lane / 16) reads 8 of them (k = 32 s + 8 q ..
@@ -98,7 +97,7 @@ __device__ __forceinline__ HeadRange head_range(const BwdParams& p)
 
 // ---------------------------------------------------------------------------
 // States: per head, H^T (n x p) = sum_s B_s[n] (e(end,s) dt_s x_s[p]) and
-// W (p x n) = sum_u (exp(cs_u) dy_u[p]) C_u[n], plus W^T; bf16 outputs.
+// W^T (n x p) = sum_u C_u[n] (exp(cs_u) dy_u[p]); bf16 outputs.
 template <int N>
 __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
 {
@@ -119,12 +118,11 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
     const u16* xg = static_cast<const u16*>(p.x);
     const u16* dyg = static_cast<const u16*>(p.dy);
     u16* HT = reinterpret_cast<u16*>(p.hin);
-    u16* Wn = reinterpret_cast<u16*>(p.gn);
     u16* WT = reinterpret_cast<u16*>(p.gnT);
 
     // B^T and C^T of the chunk (zero beyond its end)
     for (int i = tid; i < kQ2 * N / 8; i += kT2) {
-        const int s = i / (N / 8), n0 = 8 * (i - s * (N / 8));
+        const int s = i & 63, n0 = 8 * (i >> 6);   // consecutive lanes: consecutive tokens
         uint4 vb = make_uint4(0, 0, 0, 0), vc = vb;
         if (s < L) {
             const int64_t gi = ((t0 + s) * p.G + hr.g) * N + n0;
@@ -142,8 +140,8 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
     }
 
     // one head's inputs, fetched a head ahead: dt (every wavefront, lane =
-    // token) and one 8-wide piece of x and of dy per thread (row s_me)
-    const int s_me = tid >> 3, p0_me = 8 * (tid & 7);
+    // token) and one 8-wide piece of x and of dy per thread (token s_me = lane)
+    const int s_me = lane, p0_me = 8 * w;   // token = lane, 8 p values per wavefront
     float pdt = 0.f;
     uint4 px = make_uint4(0, 0, 0, 0), pd = px;
     const auto fetch = [&](int64_t h) {
@@ -168,7 +166,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
         }
         if (w == 0) p.cs[((b * p.H + h) * p.nC + c) * kQ2 + lane] = cs;
         const float csend = __shfl(cs, L - 1, 64);
-        const float cs_s = __shfl(cs, s_me, 64), dt_s = __shfl(pdt, s_me, 64);
+        const float cs_s = cs, dt_s = pdt;   // this lane's token
         {
             const float fx = exp2f(csend - cs_s) * dt_s, fd = exp2f(cs_s);   // rows beyond L hold zeros
             const uint32_t ex[4] = {px.x, px.y, px.z, px.w}, ed[4] = {pd.x, pd.y, pd.z, pd.w};
@@ -185,73 +183,53 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
 
         const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
         const int r = lane & 15, q = lane >> 4;
-        // 3 products x (N/16) x 4 tiles of 16 x 16, spread over the 8 wavefronts
-        constexpr int kTiles = 3 * (N / 16) * 4;
+        // 2 products x (N/16) x 4 tiles of 16 x 16, spread over the 8 wavefronts:
+        // H^T and W^T (n x p), rows p of Xw^T / Dw^T against rows n of B^T / C^T -> D[p][n]
+        constexpr int kTiles = 2 * (N / 16) * 4;
         for (int i = w; i < kTiles; i += 8) {
             const int prod = i / ((N / 16) * 4), j = i - prod * ((N / 16) * 4);
             const int nt = j >> 2, pt = j & 3;
+            const u16* X = prod == 0 ? XwT : DwT;
+            const u16* Y = prod == 0 ? BT : CT;
             f32x4_t acc = zero4();
-            if (prod == 1) {
-                // W (p x n): rows n of C^T, columns p of Dw^T -> D[n][p]
 #pragma unroll
-                for (int ks = 0; ks < kQ2 / 32; ++ks)
-                    acc = mma(ldfrag(CT, kLd, 16 * nt + r, ks, lane), ldfrag(DwT, kLd, 16 * pt + r, ks, lane), acc);
-                const int pp = 16 * pt + r, n0 = 16 * nt + 4 * q;
-                *reinterpret_cast<uint2*>(Wn + sbase + pp * N + n0) =
-                    make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
-            } else {
-                // H^T or W^T (n x p): rows p of Xw^T / Dw^T, columns n -> D[p][n]
-                const u16* X = prod == 0 ? XwT : DwT;
-                const u16* Y = prod == 0 ? BT : CT;
-#pragma unroll
-                for (int ks = 0; ks < kQ2 / 32; ++ks)
-                    acc = mma(ldfrag(X, kLd, 16 * pt + r, ks, lane), ldfrag(Y, kLd, 16 * nt + r, ks, lane), acc);
-                const int nn = 16 * nt + r, p0 = 16 * pt + 4 * q;
-                u16* dst = prod == 0 ? HT : WT;
-                *reinterpret_cast<uint2*>(dst + sbase + nn * kP2 + p0) =
-                    make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
-            }
+            for (int ks = 0; ks < kQ2 / 32; ++ks)
+                acc = mma(ldfrag(X, kLd, 16 * pt + r, ks, lane), ldfrag(Y, kLd, 16 * nt + r, ks, lane), acc);
+            const int nn = 16 * nt + r, p0 = 16 * pt + 4 * q;
+            u16* dst = prod == 0 ? HT : WT;
+            *reinterpret_cast<uint2*>(dst + sbase + nn * kP2 + p0) =
+                make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
         }
         __syncthreads();   // done with XwT, DwT before the next head overwrites them
     }
 }
 
 // ---------------------------------------------------------------------------
-// Scans, one thread per 8 consecutive bf16 of one (row, head) state in one of
-// the three arrays: 0 = H^T (n x p, forward from the initial state),
-// 1 = W (p x n, backward from dfinal; writes dinit), 2 = W^T (n x p, backward).
+// Scans, one thread per 8 consecutive bf16 (along p) of one (row, head) state
+// in one of the two n x p arrays: 0 = H^T (forward from the initial state),
+// 1 = W^T (backward from dfinal; writes dinit).
 template <int N>
 __global__ __launch_bounds__(256) void k_bwd2_scan(BwdParams p)
 {
     constexpr int64_t PN8 = kP2 * N / 8;
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     const int64_t per = p.b * p.H * PN8;
-    if (i >= 3 * per) return;
+    if (i >= 2 * per) return;
     const int arr = static_cast<int>(i / per);
     const int64_t rem = i - arr * per;
     const int64_t bh = rem / PN8, e8 = rem - bh * PN8;
     const int64_t b = bh / p.H, h = bh - b * p.H;
-    // element coordinates of the first of the 8 values
-    int64_t pp, nn;
-    if (arr == 1) {
-        pp = e8 / (N / 8);
-        nn = 8 * (e8 - pp * (N / 8));
-    } else {
-        nn = e8 / (kP2 / 8);
-        pp = 8 * (e8 - nn * (kP2 / 8));
-    }
+    // coordinates of the first of the 8 values
+    const int64_t nn = e8 / (kP2 / 8), pp = 8 * (e8 - nn * (kP2 / 8));
     const float* src0 = arr == 0 ? p.init : p.dfinal;   // (b, H, P, N) float32 or null
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         float v = 0.f;
-        if (src0) {
-            const int64_t pe = arr == 1 ? pp : pp + e, ne = arr == 1 ? nn + e : nn;
-            v = src0[bh * kP2 * N + pe * N + ne];
-        }
+        if (src0) v = src0[bh * kP2 * N + (pp + e) * N + nn];
         acc[e] = v;
     }
-    u16* base = reinterpret_cast<u16*>(arr == 0 ? p.hin : arr == 1 ? p.gn : p.gnT);
+    u16* base = reinterpret_cast<u16*>(arr == 0 ? p.hin : p.gnT);
     const int64_t off = (b * p.nC * p.H + h) * kP2 * N + 8 * e8;
     const int64_t stride = p.H * kP2 * N;
     const float* cs = p.cs + bh * p.nC * kQ2;
@@ -270,11 +248,9 @@ __global__ __launch_bounds__(256) void k_bwd2_scan(BwdParams p)
             acc[2 * e + 1] = fmaf(a, acc[2 * e + 1], hi_f(ev[e]));
         }
     }
-    if (arr == 1 && p.dinit) {
-        float4* d = reinterpret_cast<float4*>(p.dinit + bh * kP2 * N + pp * N + nn);
-        d[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-        d[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-    }
+    if (arr == 1 && p.dinit)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p.dinit[bh * kP2 * N + (pp + e) * N + nn] = acc[e];
 }
 
 // ---------------------------------------------------------------------------
@@ -283,7 +259,7 @@ template <int N>
 struct ChunkSmem {
     static constexpr int kLdN = N + 8;
     static constexpr size_t kBytes =
-        sizeof(u16) * (static_cast<size_t>(kQ2) * kLdN + 2 * N * kLd + 6 * kQ2 * kLd);
+        sizeof(u16) * (2 * static_cast<size_t>(kQ2) * kLdN + 2 * N * kLd + 6 * kQ2 * kLd);
 };
 
 // The score tiles (u-tile, t-tile) with u >= t, and those above the diagonal,
@@ -308,6 +284,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     u16* GsT = dyT + kQ2 * kLd;         // 64 x kLd   Gs^T (row t, k = u)
     u16* Rs = GsT + kQ2 * kLd;          // 64 x kLd   Rs  (row u, k = t)
     u16* RsT = Rs + kQ2 * kLd;          // 64 x kLd   Rs^T (row t, k = u)
+    u16* GnS = RsT + kQ2 * kLd;         // 64 x kLdN  Gn  (row p, k = n), from Gn^T
     // per-token factors, double-buffered by head parity (the per-token phase of
     // one head overlaps the next head's set-up)
     __shared__ float scs2[2][kQ2], sdt2[2][kQ2], seend2[2][kQ2], secs2[2][kQ2];
@@ -330,7 +307,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 
     // B, B^T, C^T of the chunk
     for (int i = tid; i < kQ2 * N / 8; i += kT2) {
-        const int s = i / (N / 8), n0 = 8 * (i - s * (N / 8));
+        const int s = i & 63, n0 = 8 * (i >> 6);   // consecutive lanes: consecutive tokens
         uint4 vb = make_uint4(0, 0, 0, 0), vc = vb;
         if (s < L) {
             const int64_t gi = ((t0 + s) * p.G + hr.g) * N + n0;
@@ -373,8 +350,8 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     for (int j = 0; j < kBW; ++j) dBacc[j] = dCacc[j] = zero4();
 
     // one head's inputs, fetched a head ahead: dt (wavefront 0, lane = token)
-    // and one 8-wide piece of x and of dy per thread (row s_me)
-    const int s_me = tid >> 3, p0_me = 8 * (tid & 7);
+    // and one 8-wide piece of x and of dy per thread (token s_me = lane)
+    const int s_me = lane, p0_me = 8 * w;   // token = lane, 8 p values per wavefront
     float pdt = 0.f;
     uint4 px = make_uint4(0, 0, 0, 0), pd = px;
     const auto fetch = [&](int64_t h) {
@@ -391,7 +368,6 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     for (int64_t h = hr.lo; h < hr.hi; ++h) {
         const int64_t bh = b * p.H + h;
         const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
-        const u16* Gn = reinterpret_cast<const u16*>(p.gn) + sbase;     // p x n
         const u16* GnT = reinterpret_cast<const u16*>(p.gnT) + sbase;   // n x p
         const u16* HinT = reinterpret_cast<const u16*>(p.hin) + sbase;  // n x p
         const float Ah = -expf(p.A_log[h]);
@@ -404,9 +380,13 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 
         // this wavefront's state fragments (issued first: they come from HBM)
         const int pw = w >> 1;                       // p-tile of dX^T
-        uint4 gnf[N / 32], gntf[2], hinf[2];
+        uint4 gpc[N / 64], gntf[2], hinf[2];   // pieces of Gn^T for GnS; operand fragments
 #pragma unroll
-        for (int ks = 0; ks < N / 32; ++ks) gnf[ks] = ldfrag_g(Gn, N, 16 * pw + r, ks, lane);
+        for (int k = 0; k < N / 64; ++k) {
+            // piece (row n = pc % N, p = 8 (pc / N) ..): consecutive lanes, consecutive rows
+            const int pc = tid + kT2 * k, nn = pc % N, p0 = 8 * (pc / N);
+            gpc[k] = reinterpret_cast<const uint4*>(GnT)[nn * (kP2 / 8) + p0 / 8];
+        }
         {
             const int nt = (w * kBW) >> 2;   // this wavefront's n-tile of dB^T / dC^T (one per wavefront)
 #pragma unroll
@@ -501,7 +481,18 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
                 for (int v = 0; v < 4; ++v) rowp[u0 + v][tl.y] = 0.f;
             if (q == 0) colp[t][tl.x] = 0.f;
         }
-        __syncthreads();   // (2) score tiles and their sums in place
+        // Gn (p x n) into shared memory from the pieces of Gn^T
+#pragma unroll
+        for (int k = 0; k < N / 64; ++k) {
+            const int pc = tid + kT2 * k, nn = pc % N, p0 = 8 * (pc / N);
+            const uint32_t eg[4] = {gpc[k].x, gpc[k].y, gpc[k].z, gpc[k].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                GnS[(p0 + 2 * e) * kLdN + nn] = static_cast<u16>(eg[e]);
+                GnS[(p0 + 2 * e + 1) * kLdN + nn] = static_cast<u16>(eg[e] >> 16);
+            }
+        }
+        __syncthreads();   // (2) score tiles, their sums and Gn in place
 
         // --- dX~^T (p x t): dy^T Gs + e(end,t) Gn B^T; dx, and per-token sums
 #pragma unroll
@@ -512,7 +503,8 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             for (int ks = 0; ks < 2; ++ks)
                 ai = mma(ldfrag(dyT, kLd, 16 * pw + r, ks, lane), ldfrag(GsT, kLd, 16 * tt + r, ks, lane), ai);
 #pragma unroll
-            for (int ks = 0; ks < N / 32; ++ks) ag = mma(gnf[ks], ldfrag(Bs, kLdN, 16 * tt + r, ks, lane), ag);
+            for (int ks = 0; ks < N / 32; ++ks)
+                ag = mma(ldfrag(GnS, kLdN, 16 * pw + r, ks, lane), ldfrag(Bs, kLdN, 16 * tt + r, ks, lane), ag);
             const int t = 16 * tt + r, p0 = 16 * pw + 4 * q;
             const float ee = seend[t], dtt = sdt[t];
             const uint2 xv = *reinterpret_cast<const uint2*>(xs + t * kLd + p0);
@@ -544,24 +536,36 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             }
         }
 
-        // --- dB^T (n x t) += C^T Rs + e(end,t) dt_t Gn^T x^T;  dC^T (n x u) += B^T Rs^T + exp(cs_u) h_in^T dy^T
+        // --- dB^T (n x t) += C^T Rs + e(end,t) dt_t Gn^T x^T
 #pragma unroll
         for (int j = 0; j < kBW; ++j) {
             const int idx = w * kBW + j, nt = idx >> 2, tt = idx & 3;
-            f32x4_t bi = zero4(), bx = zero4(), ci = zero4(), ch = zero4();
+            f32x4_t bi = zero4(), bx = zero4();
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 bi = mma(ldfrag(CT, kLd, 16 * nt + r, ks, lane), ldfrag(RsT, kLd, 16 * tt + r, ks, lane), bi);
                 bx = mma(gntf[ks], ldfrag(xs, kLd, 16 * tt + r, ks, lane), bx);
+            }
+            const int t = 16 * tt + r;
+            const float fb = seend[t] * sdt[t];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) dBacc[j][v] += fmaf(fb, bx[v], bi[v]);
+        }
+        // --- dC^T (n x u) += B^T Rs^T + exp(cs_u) h_in^T dy^T, and dy_u . (h_in C_u)
+#pragma unroll
+        for (int j = 0; j < kBW; ++j) {
+            const int idx = w * kBW + j, nt = idx >> 2, tt = idx & 3;
+            f32x4_t ci = zero4(), ch = zero4();
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
                 ci = mma(ldfrag(BT, kLd, 16 * nt + r, ks, lane), ldfrag(Rs, kLd, 16 * tt + r, ks, lane), ci);
                 ch = mma(hinf[ks], ldfrag(dys, kLd, 16 * tt + r, ks, lane), ch);
             }
             const int t = 16 * tt + r;
-            const float fb = seend[t] * sdt[t], fc = secs[t];
+            const float fc = secs[t];
             float q1 = 0.f;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                dBacc[j][v] += fmaf(fb, bx[v], bi[v]);
                 dCacc[j][v] += fmaf(fc, ch[v], ci[v]);
                 q1 = fmaf(bf(CT[(16 * nt + 4 * q + v) * kLd + t]), ch[v], q1);
             }
@@ -569,7 +573,6 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             q1 += __shfl_xor(q1, 32, 64);
             if (q == 0) q1p[t][nt] = q1;
         }
-        __syncthreads();
 
         {
             // <Gn, h_in> from this wavefront's fragments of Gn^T and h_in^T (one
@@ -660,7 +663,7 @@ hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEv
     const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
     hipLaunchKernelGGL(k_bwd2_states<N>, grid, dim3(kT2), sm_states, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t nscan = 3 * p.b * p.H * kP2 * N / 8;
+    const int64_t nscan = 2 * p.b * p.H * kP2 * N / 8;
     hipLaunchKernelGGL(k_bwd2_scan<N>, dim3(static_cast<unsigned>((nscan + 255) / 256)), dim3(256), 0, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;

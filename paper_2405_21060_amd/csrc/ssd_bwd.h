@@ -38,8 +38,8 @@ struct BwdParams {
     float* hin;    // (b, nC, H, P, N)    chunk states, then the state entering each chunk
                    //                     (matrix-core path: bf16, (b, nC, H, N, P))
     float* gn;     // (b, nC, H, P, N)    output-to-state terms, then the gradient of the state
-                   //                     leaving each chunk (matrix-core path: bf16)
-    float* gnT;    // matrix-core path only: gn transposed, bf16 (b, nC, H, N, P)
+                   //                     leaving each chunk (general path only)
+    float* gnT;    // matrix-core path only: the same, transposed, bf16 (b, nC, H, N, P)
     float* dBp;    // (S, b, T, G, N)     dB over one slice of a group's heads
     float* dCp;    // (S, b, T, G, N)
     float* dAp;    // (b, H, nC)          per-chunk terms of dA

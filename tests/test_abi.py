@@ -205,10 +205,10 @@ def test_backward_validation(lib):
     assert bwd(prob(), ws_bytes=need - 1) == ssd.SSD_ERR_WORKSPACE
     assert ssd.ssd_backward(prob(), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, 0, FAKE, FAKE, FAKE, FAKE, FAKE,
                             0, 0, 0, need, 0) == ssd.SSD_ERR_WORKSPACE
-    # three bf16 states per (batch, 64-token chunk, head) dominate the workspace of the
+    # two bf16 states per (batch, 64-token chunk, head) dominate the workspace of the
     # matrix-core shapes, two float32 states per 32 tokens the others'
     states = 4 * (4096 // 64) * 80 * 64 * 128 * 2
-    assert 3 * states <= need <= 3 * states + (256 << 20)
+    assert 2 * states <= need <= 2 * states + (256 << 20)
     states = 4 * (4096 // 32) * 80 * 64 * 128 * 4
     need32 = ssd.ssd_backward_workspace_bytes(prob(dtype=ssd.SSD_DTYPE_F32))
     assert 2 * states <= need32 <= 2 * states + (128 << 20)
