@@ -47,13 +47,17 @@ def algorithmic_counts(p, nseq):
     return f_full, f_causal, byts
 
 
-def kernel_sources_digest():
-    """Hash of the sources the fused kernels are compiled from; counter files
+FWD_SOURCES = ("ssd_fused.hip", "ssd_device.h", "ssd_internal.h")
+BWD_SOURCES = ("ssd_backward_mfma.hip", "ssd_backward.hip", "ssd_device.h", "ssd_bwd.h")
+
+
+def kernel_sources_digest(sources=FWD_SOURCES):
+    """Hash of the sources the measured kernels are compiled from; counter files
     record the digest they were taken at."""
     import hashlib
 
     h = hashlib.sha256()
-    for name in ("ssd_fused.hip", "ssd_device.h", "ssd_internal.h"):
+    for name in sources:
         with open(os.path.join(ROOT, "paper_2405_21060_amd", "csrc", name), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -65,17 +69,17 @@ def dominant_kernel_name(p):
     return ("k_fused_main<%d>" % p.dstate) if fused else "k_chunk_output"
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, prefix="ssd_fused", sources=FWD_SOURCES):
     """HBM bytes per launch of the dominant kernel from the FETCH_SIZE / WRITE_SIZE
     counter runs committed under profiles/, scaled by the plain-copy calibration;
     None when there is no record for this workload or the kernels have changed
     since it was taken."""
-    path = os.path.join(ROOT, "profiles", "ssd_fused_%s_traffic.json" % workload)
+    path = os.path.join(ROOT, "profiles", "%s_%s_traffic.json" % (prefix, workload))
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         rec = json.load(fh)
-    if rec.get("kernel_sources_sha256_16") != kernel_sources_digest():
+    if rec.get("kernel_sources_sha256_16") != kernel_sources_digest(sources):
         return None
     cal = rec["calibration"]
     k = rec["per_dispatch_kib"][rec["dominant_kernel"]]
@@ -263,22 +267,33 @@ def block_bench(args, torch, ssd):
     }), flush=True)
 
 
-BWD_CHUNK = 32   # tokens per chunk of the backward's decomposition
+def backward_fast(p):
+    """Whether the backward runs on its matrix-core path (bf16, headdim 64, dstate 64 or 128)."""
+    return p.dtype == "bf16" and p.headdim == 64 and p.dstate in (64, 128)
 
 
-def backward_counts(p, Qb=BWD_CHUNK):
-    """Algorithmic FLOPs of the backward's chunk-gradient kernel (the chunked
-    adjoint at Qb tokens per chunk: the causal score products, their uses, and
-    the four state-sized products per token; C B^T once per group) and the
-    compulsory HBM bytes of the whole backward (inputs x, dt, B, C, dy read,
-    gradients dx, ddt, dB, dC written, A_log, D and their gradients)."""
+def backward_counts(p):
+    """Counts for the backward's dominant kernel, the chunk-gradient kernel, at
+    its chunk length Qb (64 on the matrix-core path, 32 otherwise):
+
+    * FLOPs: per head the causal (u >= t) pairs of four score-sized products
+      (dy x^T and dy^T Gs over the head dimension, C^T Rs and B^T Rs^T over the
+      state dimension), C B^T once per group, and three state-sized products
+      per token (Gn B, Gn^T x~, h_in^T dy);
+    * bytes: the backward's compulsory bytes (x, dt, B, C, dy read; dx, ddt,
+      dB, dC written; A_log, D and their gradients) plus the two chunk-state
+      arrays the kernel reads (h_in and Gn per chunk and head, P x N each, bf16
+      on the matrix-core path, float32 otherwise)."""
     b, T, H, P, N, G = p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups
+    fast = backward_fast(p)
+    Qb = 64 if fast else 32
     nC = -(-T // Qb)
-    pairs = b * nC * Qb * (Qb + 1) // 2          # (u >= t) pairs over all chunks of one head
-    flops = pairs * G * N * 2 + H * (pairs * (2 * P + 2 * N) * 2 + b * T * 4 * P * N * 2)
+    pairs = b * nC * Qb * (Qb + 1) // 2
+    flops = pairs * G * N * 2 + H * (pairs * (2 * P + 2 * N) * 2 + b * T * 3 * P * N * 2)
     act = 2 if p.dtype == "bf16" else 4
-    byts = act * (3 * b * T * H * P + 2 * b * T * H + 4 * b * T * G * N) + 4 * 4 * H
-    return flops, byts
+    compulsory = act * (3 * b * T * H * P + 2 * b * T * H + 4 * b * T * G * N) + 4 * 4 * H
+    states = 2 * b * nC * H * P * N * (2 if fast else 4)
+    return flops, compulsory + states, compulsory, Qb
 
 
 def backward_bench(args, torch, ssd):
@@ -338,22 +353,41 @@ def backward_bench(args, torch, ssd):
     ks = sorted(a.elapsed_time(z) for a, z in kev)
     kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
            "p90": ks[(9 * len(ks)) // 10]}
-    flops, byts = backward_counts(p)
+    flops, kbytes, compulsory, Qb = backward_counts(p)
     ksec = kms["mean"] * 1e-3
     tokens = p.batch * p.seqlen
+    fast = backward_fast(p)
+    if fast:
+        t_hbm, t_mfma = kbytes / PEAK_HBM_BPS, flops / PEAK_BF16_FLOPS
+        if t_hbm >= t_mfma:
+            roof = {"bound": "hbm", "achieved": kbytes / ksec / 1e9, "peak": PEAK_HBM_BPS / 1e9, "unit": "GB/s"}
+        else:
+            roof = {"bound": "mfma", "achieved": flops / ksec / 1e12, "peak": PEAK_BF16_FLOPS / 1e12,
+                    "unit": "TFLOP/s"}
+        kname = "k_bwd2_chunk<%d>" % p.dstate
+    else:
+        roof = {"bound": "alu", "achieved": flops / ksec / 1e12, "peak": PEAK_F32_VECTOR_FLOPS / 1e12,
+                "unit": "TFLOP/s"}
+        kname = "k_bwd_chunk"
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = measured_traffic(args.workload, "ssd_backward", BWD_SOURCES)
+    roof["kernel"] = kname
+    roof["kernel_ms"] = kms
+    roof["algorithmic_bytes"] = kbytes
+    roof["algorithmic_flops"] = flops
     print(json.dumps({
         "metric": "SSD bwd tokens/s (gradients of the 2.7B-layer shape, 1 GPU)",
         "value": tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32" if p.dtype == "f32" else "bf16 in, f32 arithmetic",
+        "vs_baseline": None, "dtype": "bf16" if fast else p.dtype,
         "data": "synthetic (seeded; Mamba-2 layer shapes)",
         "config": {"workload": "backward_" + args.workload, "batch": p.batch, "seqlen": p.seqlen,
                    "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate, "ngroups": p.ngroups,
-                   "backward_chunk": BWD_CHUNK},
-        "algorithmic_flops": flops, "compulsory_bytes": byts,
-        "roofline": {"bound": "alu", "achieved": flops / ksec / 1e12, "peak": PEAK_F32_VECTOR_FLOPS / 1e12,
-                     "unit": "TFLOP/s", "frac": flops / ksec / PEAK_F32_VECTOR_FLOPS, "traffic": None,
-                     "kernel": "k_bwd_chunk", "kernel_ms": kms},
+                   "backward_chunk": Qb},
+        "compulsory_bytes": compulsory,
+        "hbm_gbps_compulsory": compulsory / (ms * 1e-3) / 1e9,
+        "pct_mfma_peak_whole_backward": 100.0 * flops / (ms * 1e-3) / PEAK_BF16_FLOPS if fast else None,
+        "roofline": roof,
     }), flush=True)
 
 
