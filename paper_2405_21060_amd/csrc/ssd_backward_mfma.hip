@@ -65,12 +65,56 @@ __device__ __forceinline__ uint4 ldfrag_g(const u16* a, int64_t ld, int row, int
     return *reinterpret_cast<const uint4*>(a + static_cast<int64_t>(row) * ld + ks * 32 + 8 * (lane >> 4));
 }
 
-// Sum over the 64 lanes of a wavefront (butterfly: every lane gets it).
-__device__ __forceinline__ float wave_sum(float v)
+// Cross-lane sums in registers (DPP and the permlane swaps; no trip through
+// shared memory).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp(float v)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xF, false));
+}
+
+// Sum over the 16 lanes of each row (row_ror by 8, 4, 2, 1): every lane of the row gets it.
+__device__ __forceinline__ float row_sum16(float v)
+{
+    v += dpp<0x128, 0xF>(v);
+    v += dpp<0x124, 0xF>(v);
+    v += dpp<0x122, 0xF>(v);
+    v += dpp<0x121, 0xF>(v);
     return v;
+}
+
+// Sum over the four rows at each position (lanes r, r + 16, r + 32, r + 48):
+// swapping odd rows with even ones, then the halves, and adding.
+__device__ __forceinline__ float col_sum4(float v)
+{
+    uint32_t u = __float_as_uint(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    u = __float_as_uint(v);
+    const auto b = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Sum over the 64 lanes of a wavefront (every lane gets it).
+__device__ __forceinline__ float wave_sum(float v) { return col_sum4(row_sum16(v)); }
+
+// Inclusive prefix sum over the 64 lanes: shifts by 1, 2, 4, 8 within each
+// row, then the row totals carried up by broadcasts of lanes 15 (into rows 1
+// and 3) and 31 (into rows 2 and 3).  Lanes with no source add zero.
+__device__ __forceinline__ float wave_scan(float v)
+{
+    v += dpp<0x111, 0xF>(v);
+    v += dpp<0x112, 0xF>(v);
+    v += dpp<0x114, 0xF>(v);
+    v += dpp<0x118, 0xF>(v);
+    v += dpp<0x142, 0xA>(v);
+    v += dpp<0x143, 0xC>(v);
+    return v;
+}
+
+__device__ __forceinline__ float lane_value(float v, int lane)
+{
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
 __device__ __forceinline__ int chunk_len2(int64_t T, int64_t c)
@@ -158,14 +202,9 @@ __global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
     for (int64_t h = hr.lo; h < hr.hi; ++h) {
         // inclusive cumsum of dt*A (log2 units), each wavefront for itself
         const float A2 = -expf(p.A_log[h]) * kLog2e;
-        float cs = pdt * A2;
-#pragma unroll
-        for (int sh = 1; sh < 64; sh <<= 1) {
-            const float o = __shfl_up(cs, sh, 64);
-            if (lane >= sh) cs += o;
-        }
+        const float cs = wave_scan(pdt * A2);
         if (w == 0) p.cs[((b * p.H + h) * p.nC + c) * kQ2 + lane] = cs;
-        const float csend = __shfl(cs, L - 1, 64);
+        const float csend = lane_value(cs, L - 1);
         const float cs_s = cs, dt_s = pdt;   // this lane's token
         {
             const float fx = exp2f(csend - cs_s) * dt_s, fd = exp2f(cs_s);   // rows beyond L hold zeros
@@ -409,13 +448,8 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
         if (w == 0) {
             // cumsum of dt*A (log2 units) and the per-token factors
             const float A2 = Ah * kLog2e;
-            float cs = pdt * A2;
-#pragma unroll
-            for (int sh = 1; sh < 64; sh <<= 1) {
-                const float o = __shfl_up(cs, sh, 64);
-                if (lane >= sh) cs += o;
-            }
-            const float csend = __shfl(cs, L - 1, 64);
+            const float cs = wave_scan(pdt * A2);
+            const float csend = lane_value(cs, L - 1);
             scs[lane] = cs;
             sdt[lane] = pdt;
             seend[lane] = lane < L ? exp2f(csend - cs) : 0.f;
@@ -452,15 +486,10 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
                     rs[v] = rv;
                     colsum += lv;
                     // row sum of l over the tile's 16 columns t
-                    float rsum = lv;
-                    rsum += __shfl_xor(rsum, 1, 64);
-                    rsum += __shfl_xor(rsum, 2, 64);
-                    rsum += __shfl_xor(rsum, 4, 64);
-                    rsum += __shfl_xor(rsum, 8, 64);
+                    const float rsum = row_sum16(lv);
                     if (r == 0) rowp[16 * tl.x + 4 * q + v][tl.y] = rsum;
                 }
-                colsum += __shfl_xor(colsum, 16, 64);
-                colsum += __shfl_xor(colsum, 32, 64);
+                colsum = col_sum4(colsum);
                 if (q == 0) colp[t][tl.x] = colsum;
                 const int u0 = 16 * tl.x + 4 * q;
                 *reinterpret_cast<uint2*>(GsT + t * kLd + u0) = make_uint2(pack2(gs[0], gs[1]), pack2(gs[2], gs[3]));
@@ -523,12 +552,9 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             if (t < L)
                 *reinterpret_cast<uint2*>(dxg + (t0 + t) * p.H * kP2 + h * kP2 + p0) =
                     make_uint2(pack2(dx[0], dx[1]), pack2(dx[2], dx[3]));
-            sxd += __shfl_xor(sxd, 16, 64);
-            sxd += __shfl_xor(sxd, 32, 64);
-            sxg += __shfl_xor(sxg, 16, 64);
-            sxg += __shfl_xor(sxg, 32, 64);
-            sdx += __shfl_xor(sdx, 16, 64);
-            sdx += __shfl_xor(sdx, 32, 64);
+            sxd = col_sum4(sxd);
+            sxg = col_sum4(sxg);
+            sdx = col_sum4(sdx);
             if (q == 0) {
                 xdxp[t][pw] = sxd;
                 q2p[t][pw] = sxg;
@@ -569,8 +595,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
                 dCacc[j][v] += fmaf(fc, ch[v], ci[v]);
                 q1 = fmaf(bf(CT[(16 * nt + 4 * q + v) * kLd + t]), ch[v], q1);
             }
-            q1 += __shfl_xor(q1, 16, 64);
-            q1 += __shfl_xor(q1, 32, 64);
+            q1 = col_sum4(q1);
             if (q == 0) q1p[t][nt] = q1;
         }
 
@@ -593,13 +618,14 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
         }
         __syncthreads();   // (3) per-token partial sums in place
 
-        // --- per token (wavefront 1, lane = token): dcs, then the decay gradients.
-        // The other wavefronts go on to the next head's set-up meanwhile; what
-        // they write there (inputs, the other buffer of per-token factors) this
-        // does not read, and the partial sums are rewritten only after the next
-        // barrier (1).
+        // --- per token (wavefront 1; lane k holds token t = 63 - k, so that a
+        // prefix sum over lanes is a suffix sum over tokens): dcs, then the decay
+        // gradients.  The other wavefronts go on to the next head's set-up
+        // meanwhile; what they write there (inputs, the other buffer of
+        // per-token factors) this does not read, and the partial sums are
+        // rewritten only after the next barrier (1).
         if (w == 1) {
-            const int t = lane;
+            const int t = kQ2 - 1 - lane;
             const bool in = t < L;
             float s2 = 0.f, row = 0.f, col = 0.f, s1 = 0.f, xd = 0.f, dyx = 0.f;
 #pragma unroll
@@ -617,12 +643,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             const float hsum = wave_sum(seend[t] * q2);
             float dcs = in ? row - col + secs[t] * s1 - seend[t] * q2 : 0.f;
             if (t == L - 1) dcs += secs[t] * ghs + hsum;   // <Gn, h_out>
-            float da = dcs;   // suffix sum: over tokens t >= this one
-#pragma unroll
-            for (int sh = 1; sh < 64; sh <<= 1) {
-                const float o = __shfl_down(da, sh, 64);
-                if (lane + sh < 64) da += o;
-            }
+            const float da = wave_scan(dcs);   // over tokens t' >= t
             if (in) ddtg[(t0 + t) * p.H + h] = static_cast<u16>(bf16_bits(fmaf(Ah, da, xd)));
             const float sa = wave_sum(in ? sdt[t] * da : 0.f);
             const float sd = wave_sum(in ? dyx : 0.f);
