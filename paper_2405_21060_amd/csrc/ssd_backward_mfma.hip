@@ -3,11 +3,11 @@
 // top of that file), with chunks of 64 tokens and every contraction on
 // v_mfma_f32_16x16x32_bf16 (bf16 operands, float32 accumulation):
 //
-//   k_bwd2_states  per (chunk, row, group, head slice): the cumsum, and per
-//                  head H_c^T and W_c^T (n x p), rounded to bf16
-//   k_bwd2_scan    the two scans over chunks, in place on those bf16 arrays
-//                  with float32 running sums: H^T -> h_in^T, W^T -> Gn^T;
-//                  the initial-state gradient in float32
+//   k_bwd2_pass    the chunk states: per (row, head, 64 state columns,
+//                  direction) a walk over the chunks with a float32 running
+//                  state, writing h_in^T (forward) or Gn^T (backward, from the
+//                  final-state gradient) per chunk in bf16; the initial-state
+//                  gradient in float32
 //   k_bwd2_chunk   per (chunk, row, group, head slice): all chunk terms.  Score
 //                  tiles (u >= t) R0 = dy x^T and G0 = C B^T (once per
 //                  workgroup), then dX~^T = dy^T Gs + Gn B^T, dB^T = C^T Rs +
@@ -140,156 +140,126 @@ __device__ __forceinline__ HeadRange head_range(const BwdParams& p)
 }
 
 // ---------------------------------------------------------------------------
-// States: per head, H^T (n x p) = sum_s B_s[n] (e(end,s) dt_s x_s[p]) and
-// W^T (n x p) = sum_u C_u[n] (exp(cs_u) dy_u[p]); bf16 outputs.
+// State passes: one workgroup per (row, head, 64 columns n of the state,
+// direction) walks the chunks in order with a float32 running state S (64 p x
+// 64 n) in registers, and writes S (bf16, n x p) for every chunk before adding
+// the chunk's own term:
+//   direction 0 (forward, from the initial state): h_in(c) = S, then
+//     S <- exp(cs_end) S + sum_s (e(end,s) dt_s x_s) B_s^T;
+//   direction 1 (backward, from the final-state gradient): Gn(c) = S, then
+//     S <- exp(cs_end) S + sum_u (exp(cs_u) dy_u) C_u^T;
+//   at the end of direction 1, S is the initial-state gradient (float32).
+// The chunk term is a 64 x 64 x 64 product on the matrix cores from x^T (or
+// dy^T) and B^T (or C^T) slices transposed into shared memory (inputs
+// fetched two chunks ahead).  Wavefront w owns p rows 16 w .. 16 w + 15 of S
+// (four 16 x 16 tiles).
+constexpr int kPassT = 256;
+
 template <int N>
-__global__ __launch_bounds__(kT2) void k_bwd2_states(BwdParams p)
+__global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
 {
-    extern __shared__ __attribute__((aligned(16))) u16 sm2[];
-    u16* BT = sm2;                  // N x kLd   B^T  (row n, k = s)
-    u16* CT = BT + N * kLd;         // N x kLd   C^T
-    u16* XwT = CT + N * kLd;        // 64 x kLd  (e(end,s) dt_s x_s)^T (row p, k = s)
-    u16* DwT = XwT + kP2 * kLd;     // 64 x kLd  (exp(cs_u) dy_u)^T
+    __shared__ __attribute__((aligned(16))) u16 XT[kP2 * kLd];   // rows p, k = token
+    __shared__ __attribute__((aligned(16))) u16 YT[64 * kLd];    // rows n (this slice), k = token
 
-    const int64_t c = blockIdx.x, b = blockIdx.y;
-    const HeadRange hr = head_range(p);
-    const int L = chunk_len2(p.T, c);
+    const int64_t bh = blockIdx.x;
+    const int64_t b = bh / p.H, h = bh - b * p.H, g = h / (p.H / p.G);
+    const int n0 = 64 * static_cast<int>(blockIdx.y);
+    const int dir = static_cast<int>(blockIdx.z);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int64_t t0 = b * p.T + c * kQ2;
+    const int r = lane & 15, q = lane >> 4;
+    const u16* src = static_cast<const u16*>(dir == 0 ? p.x : p.dy);
+    const u16* bc = static_cast<const u16*>(dir == 0 ? p.B : p.C);
     const u16* dtg = static_cast<const u16*>(p.dt);
-    const u16* Bg = static_cast<const u16*>(p.B);
-    const u16* Cg = static_cast<const u16*>(p.C);
-    const u16* xg = static_cast<const u16*>(p.x);
-    const u16* dyg = static_cast<const u16*>(p.dy);
-    u16* HT = reinterpret_cast<u16*>(p.hin);
-    u16* WT = reinterpret_cast<u16*>(p.gnT);
+    u16* out = reinterpret_cast<u16*>(dir == 0 ? p.hin : p.gnT);
+    const float A2 = -expf(p.A_log[h]) * kLog2e;
 
-    // B^T and C^T of the chunk (zero beyond its end)
-    for (int i = tid; i < kQ2 * N / 8; i += kT2) {
-        const int s = i & 63, n0 = 8 * (i >> 6);   // consecutive lanes: consecutive tokens
-        uint4 vb = make_uint4(0, 0, 0, 0), vc = vb;
-        if (s < L) {
-            const int64_t gi = ((t0 + s) * p.G + hr.g) * N + n0;
-            vb = *reinterpret_cast<const uint4*>(Bg + gi);
-            vc = *reinterpret_cast<const uint4*>(Cg + gi);
-        }
-        const uint32_t eb[4] = {vb.x, vb.y, vb.z, vb.w}, ec[4] = {vc.x, vc.y, vc.z, vc.w};
+    // running state: lane holds S[p = 16 w + 4 q + v][n = n0 + 16 nt + r]
+    f32x4_t S[4];
+    const float* s0 = dir == 0 ? p.init : p.dfinal;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            BT[(n0 + 2 * e) * kLd + s] = static_cast<u16>(eb[e]);
-            BT[(n0 + 2 * e + 1) * kLd + s] = static_cast<u16>(eb[e] >> 16);
-            CT[(n0 + 2 * e) * kLd + s] = static_cast<u16>(ec[e]);
-            CT[(n0 + 2 * e + 1) * kLd + s] = static_cast<u16>(ec[e] >> 16);
-        }
-    }
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            S[nt][v] = s0 ? s0[(bh * kP2 + 16 * w + 4 * q + v) * N + n0 + 16 * nt + r] : 0.f;
 
-    // one head's inputs, fetched a head ahead: dt (every wavefront, lane =
-    // token) and one 8-wide piece of x and of dy per thread (token s_me = lane)
-    const int s_me = lane, p0_me = 8 * w;   // token = lane, 8 p values per wavefront
-    float pdt = 0.f;
-    uint4 px = make_uint4(0, 0, 0, 0), pd = px;
-    const auto fetch = [&](int64_t h) {
-        pdt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
-        px = pd = make_uint4(0, 0, 0, 0);
-        if (s_me < L) {
-            const int64_t gi = ((t0 + s_me) * p.H + h) * kP2 + p0_me;
-            px = *reinterpret_cast<const uint4*>(xg + gi);
-            pd = *reinterpret_cast<const uint4*>(dyg + gi);
-        }
+    // One chunk's inputs: dt (lane = token), two 8-wide pieces of x (or dy) and
+    // of the B (or C) slice per thread (token = lane, columns 8 (w + 4 k) ..).
+    // Two stages in flight: the chunk after next is fetched while one is used.
+    struct Stage {
+        float dt;
+        uint4 x[2], bc[2];
     };
-    fetch(hr.lo);
-
-    for (int64_t h = hr.lo; h < hr.hi; ++h) {
-        // inclusive cumsum of dt*A (log2 units), each wavefront for itself
-        const float A2 = -expf(p.A_log[h]) * kLog2e;
-        const float cs = wave_scan(pdt * A2);
-        if (w == 0) p.cs[((b * p.H + h) * p.nC + c) * kQ2 + lane] = cs;
-        const float csend = lane_value(cs, L - 1);
-        const float cs_s = cs, dt_s = pdt;   // this lane's token
-        {
-            const float fx = exp2f(csend - cs_s) * dt_s, fd = exp2f(cs_s);   // rows beyond L hold zeros
-            const uint32_t ex[4] = {px.x, px.y, px.z, px.w}, ed[4] = {pd.x, pd.y, pd.z, pd.w};
+    const auto chunk_at = [&](int64_t k) { return dir == 0 ? k : p.nC - 1 - k; };
+    const auto fetch = [&](Stage& st, int64_t k) {
+        if (k >= p.nC) return;
+        const int64_t c = chunk_at(k);
+        const int L = chunk_len2(p.T, c);
+        const int64_t tok = b * p.T + c * kQ2 + lane;
+        st.dt = lane < L ? bf(dtg[tok * p.H + h]) : 0.f;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                XwT[(p0_me + 2 * e) * kLd + s_me] = static_cast<u16>(bf16_bits(fx * lo_f(ex[e])));
-                XwT[(p0_me + 2 * e + 1) * kLd + s_me] = static_cast<u16>(bf16_bits(fx * hi_f(ex[e])));
-                DwT[(p0_me + 2 * e) * kLd + s_me] = static_cast<u16>(bf16_bits(fd * lo_f(ed[e])));
-                DwT[(p0_me + 2 * e + 1) * kLd + s_me] = static_cast<u16>(bf16_bits(fd * hi_f(ed[e])));
+        for (int kk = 0; kk < 2; ++kk) {
+            st.x[kk] = st.bc[kk] = make_uint4(0, 0, 0, 0);
+            if (lane < L) {
+                st.x[kk] = *reinterpret_cast<const uint4*>(src + (tok * p.H + h) * kP2 + 8 * (w + 4 * kk));
+                st.bc[kk] = *reinterpret_cast<const uint4*>(bc + (tok * p.G + g) * N + n0 + 8 * (w + 4 * kk));
             }
         }
-        if (h + 1 < hr.hi) fetch(h + 1);
-        __syncthreads();   // XwT, DwT (and, the first time, B^T, C^T) are in place
-
-        const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
-        const int r = lane & 15, q = lane >> 4;
-        // 2 products x (N/16) x 4 tiles of 16 x 16, spread over the 8 wavefronts:
-        // H^T and W^T (n x p), rows p of Xw^T / Dw^T against rows n of B^T / C^T -> D[p][n]
-        constexpr int kTiles = 2 * (N / 16) * 4;
-        for (int i = w; i < kTiles; i += 8) {
-            const int prod = i / ((N / 16) * 4), j = i - prod * ((N / 16) * 4);
-            const int nt = j >> 2, pt = j & 3;
-            const u16* X = prod == 0 ? XwT : DwT;
-            const u16* Y = prod == 0 ? BT : CT;
-            f32x4_t acc = zero4();
+    };
+    const auto step = [&](Stage& st, int64_t k) {
+        const int64_t c = chunk_at(k);
+        const int L = chunk_len2(p.T, c);
+        // token weights (lane = token; tokens beyond the chunk hold zero inputs)
+        const float cs = wave_scan(st.dt * A2);
+        const float csend = lane_value(cs, L - 1);
+        const float wt = dir == 0 ? exp2f(csend - cs) * st.dt : exp2f(cs);
+        __syncthreads();   // the previous chunk's product is done with XT, YT
 #pragma unroll
-            for (int ks = 0; ks < kQ2 / 32; ++ks)
-                acc = mma(ldfrag(X, kLd, 16 * pt + r, ks, lane), ldfrag(Y, kLd, 16 * nt + r, ks, lane), acc);
-            const int nn = 16 * nt + r, p0 = 16 * pt + 4 * q;
-            u16* dst = prod == 0 ? HT : WT;
-            *reinterpret_cast<uint2*>(dst + sbase + nn * kP2 + p0) =
-                make_uint2(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]));
+        for (int kk = 0; kk < 2; ++kk) {
+            const int c0 = 8 * (w + 4 * kk);
+            const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
+            const uint32_t eb[4] = {st.bc[kk].x, st.bc[kk].y, st.bc[kk].z, st.bc[kk].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                XT[(c0 + 2 * e) * kLd + lane] = static_cast<u16>(bf16_bits(wt * lo_f(ex[e])));
+                XT[(c0 + 2 * e + 1) * kLd + lane] = static_cast<u16>(bf16_bits(wt * hi_f(ex[e])));
+                YT[(c0 + 2 * e) * kLd + lane] = static_cast<u16>(eb[e]);
+                YT[(c0 + 2 * e + 1) * kLd + lane] = static_cast<u16>(eb[e] >> 16);
+            }
         }
-        __syncthreads();   // done with XwT, DwT before the next head overwrites them
-    }
-}
+        fetch(st, k + 2);
 
-// ---------------------------------------------------------------------------
-// Scans, one thread per 8 consecutive bf16 (along p) of one (row, head) state
-// in one of the two n x p arrays: 0 = H^T (forward from the initial state),
-// 1 = W^T (backward from dfinal; writes dinit).
-template <int N>
-__global__ __launch_bounds__(256) void k_bwd2_scan(BwdParams p)
-{
-    constexpr int64_t PN8 = kP2 * N / 8;
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    const int64_t per = p.b * p.H * PN8;
-    if (i >= 2 * per) return;
-    const int arr = static_cast<int>(i / per);
-    const int64_t rem = i - arr * per;
-    const int64_t bh = rem / PN8, e8 = rem - bh * PN8;
-    const int64_t b = bh / p.H, h = bh - b * p.H;
-    // coordinates of the first of the 8 values
-    const int64_t nn = e8 / (kP2 / 8), pp = 8 * (e8 - nn * (kP2 / 8));
-    const float* src0 = arr == 0 ? p.init : p.dfinal;   // (b, H, P, N) float32 or null
-    float acc[8];
+        // S before this chunk's term -> out(c), bf16 (n x p)
+        u16* o = out + ((b * p.nC + c) * p.H + h) * kP2 * N;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        float v = 0.f;
-        if (src0) v = src0[bh * kP2 * N + (pp + e) * N + nn];
-        acc[e] = v;
-    }
-    u16* base = reinterpret_cast<u16*>(arr == 0 ? p.hin : p.gnT);
-    const int64_t off = (b * p.nC * p.H + h) * kP2 * N + 8 * e8;
-    const int64_t stride = p.H * kP2 * N;
-    const float* cs = p.cs + bh * p.nC * kQ2;
-    const bool fwd = arr == 0;
-    for (int64_t k = 0; k < p.nC; ++k) {
-        const int64_t c = fwd ? k : p.nC - 1 - k;
-        const float a = exp2f(cs[c * kQ2 + chunk_len2(p.T, c) - 1]);
-        uint4* slot = reinterpret_cast<uint4*>(base + off + c * stride);
-        const uint4 v = *slot;
-        *slot = make_uint4(pack2(acc[0], acc[1]), pack2(acc[2], acc[3]), pack2(acc[4], acc[5]),
-                           pack2(acc[6], acc[7]));
-        const uint32_t ev[4] = {v.x, v.y, v.z, v.w};
+        for (int nt = 0; nt < 4; ++nt)
+            *reinterpret_cast<uint2*>(o + (n0 + 16 * nt + r) * kP2 + 16 * w + 4 * q) =
+                make_uint2(pack2(S[nt][0], S[nt][1]), pack2(S[nt][2], S[nt][3]));
+
+        __syncthreads();   // this chunk's operands in place
+        const float a = exp2f(csend);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            acc[2 * e] = fmaf(a, acc[2 * e], lo_f(ev[e]));
-            acc[2 * e + 1] = fmaf(a, acc[2 * e + 1], hi_f(ev[e]));
+        for (int nt = 0; nt < 4; ++nt) {
+            f32x4_t t = zero4();
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                t = mma(ldfrag(XT, kLd, 16 * w + r, ks, lane), ldfrag(YT, kLd, 16 * nt + r, ks, lane), t);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) S[nt][v] = fmaf(a, S[nt][v], t[v]);
         }
+    };
+    Stage s0st, s1st;
+    fetch(s0st, 0);
+    fetch(s1st, 1);
+    for (int64_t k = 0; k < p.nC; k += 2) {
+        step(s0st, k);
+        if (k + 1 < p.nC) step(s1st, k + 1);
     }
-    if (arr == 1 && p.dinit)
+    if (dir == 1 && p.dinit) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) p.dinit[bh * kP2 * N + (pp + e) * N + nn] = acc[e];
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) p.dinit[(bh * kP2 + 16 * w + 4 * q + v) * N + n0 + 16 * nt + r] = S[nt][v];
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -670,24 +640,16 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 template <int N>
 hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
 {
-    const size_t sm_states = sizeof(u16) * static_cast<size_t>(2 * N * kLd + 2 * kP2 * kLd);
     const size_t sm_chunk = ChunkSmem<N>::kBytes;
     hipError_t e;
-    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bwd2_states<N>),
-                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_states))) !=
-        hipSuccess)
-        return e;
     if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bwd2_chunk<N>),
                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
         hipSuccess)
         return e;
-    const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
-    hipLaunchKernelGGL(k_bwd2_states<N>, grid, dim3(kT2), sm_states, st, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t nscan = 2 * p.b * p.H * kP2 * N / 8;
-    hipLaunchKernelGGL(k_bwd2_scan<N>, dim3(static_cast<unsigned>((nscan + 255) / 256)), dim3(256), 0, st, p);
+    hipLaunchKernelGGL(k_bwd2_pass<N>, dim3(static_cast<unsigned>(p.b * p.H), N / 64, 2), dim3(kPassT), 0, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
+    const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
     hipLaunchKernelGGL(k_bwd2_chunk<N>, grid, dim3(kT2), sm_chunk, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
