@@ -513,7 +513,7 @@ int backward_impl(const ssd_problem* prob, const void* x, const void* dt, const 
     p.dC = dC;
     p.dD = D ? dD : nullptr;
     p.dinit = dinitial_states;
-    p.cs = reinterpret_cast<float*>(ws + l.cs);
+    p.cs = fast ? nullptr : reinterpret_cast<float*>(ws + l.cs);
     p.hin = reinterpret_cast<float*>(ws + l.hin);
     p.gn = fast ? nullptr : reinterpret_cast<float*>(ws + l.gn);
     p.gnT = fast ? reinterpret_cast<float*>(ws + l.gnT) : nullptr;

@@ -504,7 +504,7 @@ BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int6
     };
     const auto take = [&](size_t n) { return take_bytes(n * sizeof(float)); };
     const size_t state_bytes = static_cast<size_t>(b * nC * H * P * N) * (fast ? 2 : 4);
-    l.cs = take(static_cast<size_t>(b * H * nC * (fast ? kBwdQFast : kBwdQ)));
+    l.cs = fast ? 0 : take(static_cast<size_t>(b * H * nC * kBwdQ));
     l.hin = take_bytes(state_bytes);
     l.gn = fast ? 0 : take_bytes(state_bytes);
     l.gnT = fast ? take_bytes(state_bytes) : 0;

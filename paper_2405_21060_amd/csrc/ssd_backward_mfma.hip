@@ -3,8 +3,8 @@
 // top of that file), with chunks of 64 tokens and every contraction on
 // v_mfma_f32_16x16x32_bf16 (bf16 operands, float32 accumulation):
 //
-//   k_bwd2_pass    the chunk states: per (row, head, 64 state columns,
-//                  direction) a walk over the chunks with a float32 running
+//   k_bwd2_pass    the chunk states: per (row, head, direction) a walk
+//                  over the chunks with a float32 running
 //                  state, writing h_in^T (forward) or Gn^T (backward, from the
 //                  final-state gradient) per chunk in bf16; the initial-state
 //                  gradient in float32
@@ -140,31 +140,29 @@ __device__ __forceinline__ HeadRange head_range(const BwdParams& p)
 }
 
 // ---------------------------------------------------------------------------
-// State passes: one workgroup per (row, head, 64 columns n of the state,
-// direction) walks the chunks in order with a float32 running state S (64 p x
-// 64 n) in registers, and writes S (bf16, n x p) for every chunk before adding
-// the chunk's own term:
+// State passes: one workgroup per (row, head, direction) walks the chunks in
+// order with a float32 running state S (64 p x N) in registers, and writes S
+// (bf16, n x p) for every chunk before adding the chunk's own term:
 //   direction 0 (forward, from the initial state): h_in(c) = S, then
 //     S <- exp(cs_end) S + sum_s (e(end,s) dt_s x_s) B_s^T;
 //   direction 1 (backward, from the final-state gradient): Gn(c) = S, then
 //     S <- exp(cs_end) S + sum_u (exp(cs_u) dy_u) C_u^T;
 //   at the end of direction 1, S is the initial-state gradient (float32).
-// The chunk term is a 64 x 64 x 64 product on the matrix cores from x^T (or
-// dy^T) and B^T (or C^T) slices transposed into shared memory (inputs
-// fetched two chunks ahead).  Wavefront w owns p rows 16 w .. 16 w + 15 of S
-// (four 16 x 16 tiles).
+// The chunk term is a 64 x N x 64 product on the matrix cores from x^T (or
+// dy^T) and B^T (or C^T) transposed into shared memory (inputs fetched two
+// chunks ahead).  Wavefront w owns p rows 16 w .. 16 w + 15 of S (N / 16
+// tiles of 16 x 16).
 constexpr int kPassT = 256;
 
 template <int N>
 __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
 {
     __shared__ __attribute__((aligned(16))) u16 XT[kP2 * kLd];   // rows p, k = token
-    __shared__ __attribute__((aligned(16))) u16 YT[64 * kLd];    // rows n (this slice), k = token
+    __shared__ __attribute__((aligned(16))) u16 YT[N * kLd];     // rows n, k = token
 
     const int64_t bh = blockIdx.x;
     const int64_t b = bh / p.H, h = bh - b * p.H, g = h / (p.H / p.G);
-    const int n0 = 64 * static_cast<int>(blockIdx.y);
-    const int dir = static_cast<int>(blockIdx.z);
+    const int dir = static_cast<int>(blockIdx.y);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, q = lane >> 4;
     const u16* src = static_cast<const u16*>(dir == 0 ? p.x : p.dy);
@@ -173,21 +171,22 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     u16* out = reinterpret_cast<u16*>(dir == 0 ? p.hin : p.gnT);
     const float A2 = -expf(p.A_log[h]) * kLog2e;
 
-    // running state: lane holds S[p = 16 w + 4 q + v][n = n0 + 16 nt + r]
-    f32x4_t S[4];
+    // running state: lane holds S[p = 16 w + 4 q + v][n = 16 nt + r]
+    constexpr int kNT = N / 16;
+    f32x4_t S[kNT];
     const float* s0 = dir == 0 ? p.init : p.dfinal;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+    for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-            S[nt][v] = s0 ? s0[(bh * kP2 + 16 * w + 4 * q + v) * N + n0 + 16 * nt + r] : 0.f;
+            S[nt][v] = s0 ? s0[(bh * kP2 + 16 * w + 4 * q + v) * N + 16 * nt + r] : 0.f;
 
     // One chunk's inputs: dt (lane = token), two 8-wide pieces of x (or dy) and
-    // of the B (or C) slice per thread (token = lane, columns 8 (w + 4 k) ..).
+    // N / 32 of B (or C) per thread (token = lane, columns 8 (w + 4 k) ..).
     // Two stages in flight: the chunk after next is fetched while one is used.
     struct Stage {
         float dt;
-        uint4 x[2], bc[2];
+        uint4 x[2], bc[N / 32];
     };
     const auto chunk_at = [&](int64_t k) { return dir == 0 ? k : p.nC - 1 - k; };
     const auto fetch = [&](Stage& st, int64_t k) {
@@ -198,11 +197,13 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         st.dt = lane < L ? bf(dtg[tok * p.H + h]) : 0.f;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            st.x[kk] = st.bc[kk] = make_uint4(0, 0, 0, 0);
-            if (lane < L) {
-                st.x[kk] = *reinterpret_cast<const uint4*>(src + (tok * p.H + h) * kP2 + 8 * (w + 4 * kk));
-                st.bc[kk] = *reinterpret_cast<const uint4*>(bc + (tok * p.G + g) * N + n0 + 8 * (w + 4 * kk));
-            }
+            st.x[kk] = make_uint4(0, 0, 0, 0);
+            if (lane < L) st.x[kk] = *reinterpret_cast<const uint4*>(src + (tok * p.H + h) * kP2 + 8 * (w + 4 * kk));
+        }
+#pragma unroll
+        for (int kk = 0; kk < N / 32; ++kk) {
+            st.bc[kk] = make_uint4(0, 0, 0, 0);
+            if (lane < L) st.bc[kk] = *reinterpret_cast<const uint4*>(bc + (tok * p.G + g) * N + 8 * (w + 4 * kk));
         }
     };
     const auto step = [&](Stage& st, int64_t k) {
@@ -217,11 +218,18 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         for (int kk = 0; kk < 2; ++kk) {
             const int c0 = 8 * (w + 4 * kk);
             const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
-            const uint32_t eb[4] = {st.bc[kk].x, st.bc[kk].y, st.bc[kk].z, st.bc[kk].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 XT[(c0 + 2 * e) * kLd + lane] = static_cast<u16>(bf16_bits(wt * lo_f(ex[e])));
                 XT[(c0 + 2 * e + 1) * kLd + lane] = static_cast<u16>(bf16_bits(wt * hi_f(ex[e])));
+            }
+        }
+#pragma unroll
+        for (int kk = 0; kk < N / 32; ++kk) {
+            const int c0 = 8 * (w + 4 * kk);
+            const uint32_t eb[4] = {st.bc[kk].x, st.bc[kk].y, st.bc[kk].z, st.bc[kk].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
                 YT[(c0 + 2 * e) * kLd + lane] = static_cast<u16>(eb[e]);
                 YT[(c0 + 2 * e + 1) * kLd + lane] = static_cast<u16>(eb[e] >> 16);
             }
@@ -231,14 +239,14 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         // S before this chunk's term -> out(c), bf16 (n x p)
         u16* o = out + ((b * p.nC + c) * p.H + h) * kP2 * N;
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-            *reinterpret_cast<uint2*>(o + (n0 + 16 * nt + r) * kP2 + 16 * w + 4 * q) =
+        for (int nt = 0; nt < kNT; ++nt)
+            *reinterpret_cast<uint2*>(o + (16 * nt + r) * kP2 + 16 * w + 4 * q) =
                 make_uint2(pack2(S[nt][0], S[nt][1]), pack2(S[nt][2], S[nt][3]));
 
         __syncthreads();   // this chunk's operands in place
         const float a = exp2f(csend);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
+        for (int nt = 0; nt < kNT; ++nt) {
             f32x4_t t = zero4();
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks)
@@ -256,9 +264,9 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     }
     if (dir == 1 && p.dinit) {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) p.dinit[(bh * kP2 + 16 * w + 4 * q + v) * N + n0 + 16 * nt + r] = S[nt][v];
+            for (int v = 0; v < 4; ++v) p.dinit[(bh * kP2 + 16 * w + 4 * q + v) * N + 16 * nt + r] = S[nt][v];
     }
 }
 
@@ -646,7 +654,7 @@ hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEv
                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
         hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_bwd2_pass<N>, dim3(static_cast<unsigned>(p.b * p.H), N / 64, 2), dim3(kPassT), 0, st, p);
+    hipLaunchKernelGGL(k_bwd2_pass<N>, dim3(static_cast<unsigned>(p.b * p.H), 2), dim3(kPassT), 0, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));

@@ -34,7 +34,8 @@ struct BwdParams {
     float* dD;             // may be null
     float* dinit;          // may be null
     // workspace (float32)
-    float* cs;     // (b, H, nC, chunk)   chunk-local inclusive cumsum of dt*A, log2 units
+    float* cs;     // (b, H, nC, kBwdQ)   chunk-local inclusive cumsum of dt*A, log2 units
+                   //                     (general path only)
     float* hin;    // (b, nC, H, P, N)    chunk states, then the state entering each chunk
                    //                     (matrix-core path: bf16, (b, nC, H, N, P))
     float* gn;     // (b, nC, H, P, N)    output-to-state terms, then the gradient of the state
