@@ -19,6 +19,9 @@ shares no code with the HIP path.
 * :mod:`oracle.block` -- the Mamba-2 block steps on either side of the layer
   (dt parameterisation; gate ``y * SiLU(z)`` and grouped RMS normalisation of
   Sections 7.1 and 8.1) around :func:`forward`.
+* :mod:`oracle.block_backward` -- gradients of those block steps by the chain
+  rule around :mod:`oracle.backward`; pinned by finite differences of
+  :mod:`oracle.block`.
 """
 from __future__ import annotations
 
