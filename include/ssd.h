@@ -287,6 +287,32 @@ int ssd_backward_timed(const ssd_problem* prob,
                        void* workspace, size_t workspace_bytes, void* stream,
                        void* event_begin, void* event_end);
 
+/* ssd_backward_block: the gradients of ssd_forward_block (same `prob`,
+ * `opts` and inputs; no packed rows), given dout = dL/d(block output) and
+ * dfinal_states (NULL = 0).  The paper gives no backward; this is the chain
+ * rule through the normalisation, the gate (Section 8.1), the layer
+ * (ssd_backward) and the dt step, with the layer's output recomputed from the
+ * inputs.  Outputs as for ssd_backward with `ddt` the gradient of `dt` as
+ * given (before bias, softplus and clamp), plus
+ *   ddt_bias      (nheads) float32, written when opts->dt_bias (may be NULL)
+ *   dz            like y, dtype; required when opts->z
+ *   dnorm_weight  (nheads * headdim) float32, written when the normalisation
+ *                 and its weight are on (may be NULL)
+ * x, B, C, dout, dx, dz and the state arrays must be 16-byte aligned (else
+ * SSD_ERR_UNSUPPORTED_DIMS).  Workspace: ssd_backward_block_workspace_bytes()
+ * bytes.  Ownership, asynchrony, determinism and errors as for ssd_forward. */
+int ssd_backward_block_workspace_bytes(const ssd_problem* prob, const ssd_block_opts* opts, size_t* bytes);
+
+int ssd_backward_block(const ssd_problem* prob, const ssd_block_opts* opts,
+                       const void* x, const void* dt, const float* A_log,
+                       const void* B, const void* C, const float* D,
+                       const float* initial_states,
+                       const void* dout, const float* dfinal_states,
+                       void* dx, void* ddt, float* dA_log, void* dB, void* dC,
+                       float* dD, float* dinitial_states,
+                       float* ddt_bias, void* dz, float* dnorm_weight,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);
 

@@ -10,6 +10,7 @@
 #include <cstdlib>
 #include <cstring>
 
+#include "ssd_block_bwd.h"
 #include "ssd_bwd.h"
 #include "ssd_internal.h"
 
@@ -561,6 +562,131 @@ extern "C" int ssd_backward_timed(const ssd_problem* prob, const void* x, const 
 {
     return backward_impl(prob, x, dt, A_log, B, C, D, initial_states, dy, dfinal_states, dx, ddt, dA_log, dB, dC,
                          dD, dinitial_states, workspace, workspace_bytes, stream, event_begin, event_end);
+}
+
+namespace {
+
+// Workspace of the block backward: the dt step's output, the layer's output
+// (recomputed), its gradient, the layer's dt gradient, the normalisation's
+// 1 / r per (row, group), the row-chunk partials of d weight and d bias, and
+// one region shared by the forward and the layer backward (they run one after
+// the other).
+struct BlockBwdLayout {
+    size_t dt, y, dy, ddt, inv_rms, dw_part, db_part, shared, total;
+};
+
+int block_backward_plan(const ssd_problem* prob, const ssd_block_opts* opts, BlockBwdLayout* l)
+{
+    if (!prob || !opts) return SSD_ERR_NULL_ARG;
+    size_t fwd = 0, bwd = 0;
+    int rc = ssd_workspace_bytes(prob, &fwd);
+    if (rc != SSD_OK) return rc;
+    if ((rc = ssd_backward_workspace_bytes(prob, &bwd)) != SSD_OK) return rc;
+    const size_t act = prob->dtype == SSD_DTYPE_BF16 ? 2 : 4;
+    const size_t rows = static_cast<size_t>(prob->batch * prob->seqlen);
+    const size_t H = static_cast<size_t>(prob->nheads), Cc = H * static_cast<size_t>(prob->headdim);
+    if (rows > static_cast<size_t>(65535) * 64) return SSD_ERR_TOO_LARGE;   // row chunks on grid y
+    const size_t nch = static_cast<size_t>(ssd::block_bwd_row_chunks(static_cast<int64_t>(rows)));
+    const size_t groups = opts->norm_group_size > 0 ? Cc / static_cast<size_t>(opts->norm_group_size) : 0;
+    size_t off = 0;
+    const auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += ssd::align_up(bytes);
+        return o;
+    };
+    l->dt = take(rows * H * act);
+    l->y = take(rows * Cc * act);
+    l->dy = take(rows * Cc * act);
+    l->ddt = take(rows * H * act);
+    l->inv_rms = take(rows * groups * 4);
+    l->dw_part = take(opts->norm_weight && groups ? nch * Cc * 4 : 0);
+    l->db_part = take(opts->dt_bias ? nch * H * 4 : 0);
+    l->shared = take(fwd > bwd ? fwd : bwd);
+    l->total = off;
+    return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" int ssd_backward_block_workspace_bytes(const ssd_problem* prob, const ssd_block_opts* opts,
+                                                  size_t* bytes)
+{
+    if (!bytes) return SSD_ERR_NULL_ARG;
+    BlockBwdLayout l{};
+    const int rc = block_backward_plan(prob, opts, &l);
+    if (rc != SSD_OK) return rc;
+    *bytes = l.total;
+    return SSD_OK;
+}
+
+extern "C" int ssd_backward_block(const ssd_problem* prob, const ssd_block_opts* opts, const void* x,
+                                  const void* dt, const float* A_log, const void* B, const void* C,
+                                  const float* D, const float* initial_states, const void* dout,
+                                  const float* dfinal_states, void* dx, void* ddt, float* dA_log, void* dB,
+                                  void* dC, float* dD, float* dinitial_states, float* ddt_bias, void* dz,
+                                  float* dnorm_weight, void* workspace, size_t workspace_bytes, void* stream)
+{
+    BlockBwdLayout l{};
+    int rc = block_backward_plan(prob, opts, &l);
+    if (rc != SSD_OK) return rc;
+    ssd::Shape s;
+    if ((rc = ssd::validate(prob, false, &s)) != SSD_OK) return rc;
+    ssd::DtTransform dtx;
+    if ((rc = validate_block(opts, s, dout, &dtx)) != SSD_OK) return rc;
+    if (!x || !dt || !A_log || !B || !C || !dout || !dx || !ddt || !dA_log || !dB || !dC) return SSD_ERR_NULL_ARG;
+    if (opts->z && !dz) return SSD_ERR_NULL_ARG;
+    // every check of the steps below is made here, before any work is enqueued
+    if (!aligned16(x) || !aligned16(B) || !aligned16(C) || !aligned16(dx) || !aligned16(dout) ||
+        (dz && !aligned16(dz)) || !aligned16(initial_states) || !aligned16(dfinal_states) ||
+        !aligned16(dinitial_states))
+        return SSD_ERR_UNSUPPORTED_DIMS;
+    if (!workspace || workspace_bytes < l.total) return SSD_ERR_WORKSPACE;
+    char* ws = static_cast<char*>(workspace);
+    const bool bf16 = s.bf16;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    const size_t shared_bytes = l.total - l.shared;
+
+    ssd::BlockBwdParams p{};
+    p.rows = s.b * s.T;
+    p.H = s.H;
+    p.C = s.H * s.P;
+    p.group = opts->norm_group_size;
+    p.dt_raw = dt;
+    p.bias = opts->dt_bias;
+    p.softplus = opts->dt_softplus != 0;
+    p.lo = opts->dt_min;
+    p.hi = opts->dt_max;
+    p.dt = ws + l.dt;
+    p.ddt = ws + l.ddt;
+    p.ddt_raw = ddt;
+    p.dbias_part = opts->dt_bias ? reinterpret_cast<float*>(ws + l.db_part) : nullptr;
+    p.ddt_bias = opts->dt_bias ? ddt_bias : nullptr;
+    p.y = ws + l.y;
+    p.z = opts->z;
+    p.w = opts->norm_group_size > 0 ? opts->norm_weight : nullptr;
+    p.eps = opts->norm_eps;
+    p.dout = dout;
+    p.dy = ws + l.dy;
+    p.dz = dz;
+    p.inv_rms = opts->norm_group_size > 0 ? reinterpret_cast<float*>(ws + l.inv_rms) : nullptr;
+    p.dw_part = reinterpret_cast<float*>(ws + l.dw_part);
+    p.dw = p.w ? dnorm_weight : nullptr;
+
+    // 1. the dt step; 2. the layer's output, recomputed
+    if (ssd::launch_block_dt_apply(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
+    rc = forward_impl(prob, nullptr, x, p.dt, A_log, B, C, D, initial_states, nullptr, ws + l.y, nullptr,
+                      ws + l.shared, shared_bytes, stream, nullptr, nullptr);
+    if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
+    // 3. gate and normalisation: dy (the block's output gradient when neither is on)
+    const bool post = opts->z || opts->norm_group_size > 0;
+    if (post && ssd::launch_block_out_bwd(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
+    // 4. the layer
+    rc = backward_impl(prob, x, p.dt, A_log, B, C, D, initial_states, post ? p.dy : dout, dfinal_states, dx,
+                       ws + l.ddt, dA_log, dB, dC, dD, dinitial_states, ws + l.shared, shared_bytes, stream,
+                       nullptr, nullptr);
+    if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
+    // 5. the dt step
+    return ssd::launch_block_dt_bwd(p, bf16, st) == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
 extern "C" const char* ssd_error_string(int code)

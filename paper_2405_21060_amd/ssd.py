@@ -38,7 +38,8 @@ SSD_ERR_BAD_OPTION = -10
 EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
             "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
             "ssd_span_decay", "ssd_span_combine", "ssd_span_correct_workspace_bytes", "ssd_span_correct",
-            "ssd_backward_workspace_bytes", "ssd_backward", "ssd_backward_timed", "ssd_error_string")
+            "ssd_backward_workspace_bytes", "ssd_backward", "ssd_backward_timed",
+            "ssd_backward_block_workspace_bytes", "ssd_backward_block", "ssd_error_string")
 
 
 class SsdProblem(ctypes.Structure):
@@ -120,6 +121,11 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_backward.restype = ctypes.c_int
     lib.ssd_backward_timed.argtypes = lib.ssd_backward.argtypes + [vp, vp]
     lib.ssd_backward_timed.restype = ctypes.c_int
+    lib.ssd_backward_block_workspace_bytes.argtypes = [pp, ctypes.POINTER(SsdBlockOpts),
+                                                       ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_backward_block_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_backward_block.argtypes = [pp, ctypes.POINTER(SsdBlockOpts)] + [vp] * 19 + [vp, ctypes.c_size_t, vp]
+    lib.ssd_backward_block.restype = ctypes.c_int
     lib.ssd_error_string.argtypes = [ctypes.c_int]
     _lib = lib
     return lib
@@ -450,4 +456,73 @@ def backward(x, dt, A_log, B, C, dy, D=None, initial_states=None, dfinal_states=
                       stream, event_begin, event_end)
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_backward")
+    return g
+
+
+def ssd_backward_block_workspace_bytes(prob: SsdProblem, opts: SsdBlockOpts) -> int:
+    out = ctypes.c_size_t(0)
+    rc = load_library().ssd_backward_block_workspace_bytes(ctypes.byref(prob), ctypes.byref(opts),
+                                                           ctypes.byref(out))
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_backward_block_workspace_bytes")
+    return int(out.value)
+
+
+def ssd_backward_block(prob: SsdProblem, opts: SsdBlockOpts, x, dt, A_log, B, C, D, initial_states, dout,
+                       dfinal_states, dx, ddt, dA_log, dB, dC, dD, dinitial_states, ddt_bias, dz, dnorm_weight,
+                       workspace, workspace_bytes: int, stream) -> int:
+    """Raw ABI call on integer device addresses (0 = NULL); returns the status."""
+    return load_library().ssd_backward_block(
+        ctypes.byref(prob), ctypes.byref(opts), x, dt, A_log, B, C, D or None, initial_states or None, dout,
+        dfinal_states or None, dx, ddt, dA_log, dB, dC, dD or None, dinitial_states or None, ddt_bias or None,
+        dz or None, dnorm_weight or None, workspace, int(workspace_bytes), stream or None)
+
+
+def backward_block(x, dt, A_log, B, C, dout, D=None, initial_states=None, dfinal_states=None, dt_bias=None,
+                   dt_softplus: bool = True, dt_min: float = 0.0, dt_max: float = float("inf"), z=None,
+                   norm_weight=None, norm_group_size: int = 0, norm_eps: float = 1e-5, workspace=None):
+    """Gradients of ``forward_block`` on device tensors (``dt`` is the raw dt,
+    before bias / softplus / clamp).  Returns a dict: dx, ddt, dB, dC, dz (x's
+    dtype; dz None without z), dA_log, dD, dinit, ddt_bias, dnorm_weight
+    (float32; None where the input is absent)."""
+    import torch
+
+    dev = x.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must live on a HIP device")
+    if x.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError("x must be float32 or bfloat16")
+    for name, t in (("dt", dt), ("B", B), ("C", C), ("dout", dout), ("z", z)):
+        if t is not None and t.dtype != x.dtype:
+            raise TypeError("%s must have x's dtype" % name)
+    for name, t in (("A_log", A_log), ("D", D), ("initial_states", initial_states),
+                    ("dfinal_states", dfinal_states), ("dt_bias", dt_bias), ("norm_weight", norm_weight)):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("%s must be float32" % name)
+    for t in (x, dt, A_log, B, C, dout, D, initial_states, dfinal_states, dt_bias, z, norm_weight):
+        if t is not None and (t.device != dev or not t.is_contiguous()):
+            raise ValueError("all tensors must be contiguous and on x's device")
+    b, T, H, P = x.shape
+    G, N = B.shape[2], B.shape[3]
+    prob = make_problem(b, T, H, P, N, G, 256, SSD_DTYPE_BF16 if x.dtype == torch.bfloat16 else SSD_DTYPE_F32)
+    opts = make_block_opts(dt_bias, dt_softplus, dt_min, dt_max, z, norm_weight, norm_group_size, norm_eps)
+    wsb = ssd_backward_block_workspace_bytes(prob, opts)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    g = {"dx": torch.empty_like(x), "ddt": torch.empty_like(dt), "dB": torch.empty_like(B),
+         "dC": torch.empty_like(C), "dA_log": torch.empty_like(A_log),
+         "dD": torch.empty_like(D) if D is not None else None,
+         "dinit": torch.empty((b, H, P, N), dtype=torch.float32, device=dev),
+         "ddt_bias": torch.empty_like(dt_bias) if dt_bias is not None else None,
+         "dz": torch.empty_like(z) if z is not None else None,
+         "dnorm_weight": torch.empty_like(norm_weight) if norm_weight is not None and norm_group_size > 0
+         else None}
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = ssd_backward_block(prob, opts, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),
+                            _ptr(initial_states), _ptr(dout), _ptr(dfinal_states), _ptr(g["dx"]), _ptr(g["ddt"]),
+                            _ptr(g["dA_log"]), _ptr(g["dB"]), _ptr(g["dC"]), _ptr(g["dD"]), _ptr(g["dinit"]),
+                            _ptr(g["ddt_bias"]), _ptr(g["dz"]), _ptr(g["dnorm_weight"]), _ptr(workspace), wsb,
+                            stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_backward_block")
     return g

@@ -217,6 +217,29 @@ def test_backward_validation(lib):
                             FAKE, FAKE, 0, 0, FAKE, need, 0, FAKE, FAKE) == ssd.SSD_ERR_BAD_SHAPE
 
 
+def test_block_backward_validation(lib):
+    size = ctypes.c_size_t(0)
+    o = ssd.SsdBlockOpts(0, 1, 0.0, float("inf"), 0, 0, 0, 1e-5)
+    assert lib.ssd_backward_block_workspace_bytes(ctypes.byref(prob()), None, ctypes.byref(size)) == \
+        ssd.SSD_ERR_NULL_ARG
+    assert lib.ssd_backward_block_workspace_bytes(ctypes.byref(prob()), ctypes.byref(o), ctypes.byref(size)) == \
+        ssd.SSD_OK
+    need = size.value
+    # at least the layer's backward workspace (shared with the recomputed forward)
+    assert need >= ssd.ssd_backward_workspace_bytes(prob())
+
+    def call(opts, dz=0, ws=need, x=FAKE, dout=FAKE):
+        return ssd.ssd_backward_block(prob(), opts, x, FAKE, FAKE, FAKE, FAKE, 0, 0, dout, 0, FAKE, FAKE, FAKE,
+                                      FAKE, FAKE, 0, 0, 0, dz, 0, FAKE, ws, 0)
+
+    assert call(ssd.SsdBlockOpts(0, 1, 2.0, 1.0, 0, 0, 0, 1e-5)) == ssd.SSD_ERR_BAD_OPTION   # max < min
+    assert call(ssd.SsdBlockOpts(0, 1, 0.0, float("inf"), 0, 0, 48, 1e-5)) == ssd.SSD_ERR_BAD_OPTION
+    assert call(ssd.SsdBlockOpts(0, 1, 0.0, float("inf"), FAKE, 0, 0, 1e-5)) == ssd.SSD_ERR_NULL_ARG  # dz
+    assert call(o, dout=0) == ssd.SSD_ERR_NULL_ARG
+    assert call(o, x=FAKE + 2) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert call(o, ws=need - 1) == ssd.SSD_ERR_WORKSPACE
+
+
 def test_error_strings(lib):
     for code in range(0, -11, -1):
         s = ssd.ssd_error_string(code)
