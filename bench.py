@@ -391,6 +391,80 @@ def backward_bench(args, torch, ssd):
     }), flush=True)
 
 
+def block_backward_bench(args, torch, ssd):
+    """Gradients of the block at the 2.7B layer shape (ssd_backward_block):
+    dt softplus with bias, the layer, the SiLU gate and one-head RMS
+    normalisation groups with weight; dout seeded, no initial state, no
+    final-state gradient."""
+    from paper_2405_21060_amd.inputs import WORKLOADS, make_block_inputs, make_grad_inputs
+    from tests.ssd_harness import act_to_device
+
+    p = WORKLOADS[args.workload]
+    bi = make_block_inputs(p, args.seed)
+    dout, _ = make_grad_inputs(p, args.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    f32 = lambda a: torch.from_numpy(a).to(dev)
+    base = bi.base
+    sets = []
+    for _ in range(max(1, args.copies)):
+        c = {"x": act_to_device(base.x), "dt": act_to_device(bi.dt_raw), "B": act_to_device(base.B),
+             "C": act_to_device(base.C), "z": act_to_device(bi.z), "dout": act_to_device(dout)}
+        for k in ("x", "dt", "B", "C", "z"):
+            c["d" + k] = torch.empty_like(c[k])
+        sets.append(c)
+    A_log, D, bias, w = f32(base.A_log), f32(base.D), f32(bi.dt_bias), f32(bi.norm_weight)
+    dA, dD, dbias, dw = torch.empty_like(A_log), torch.empty_like(D), torch.empty_like(bias), torch.empty_like(w)
+    prob = ssd.make_problem(p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups, p.chunk_size,
+                            ssd.SSD_DTYPE_BF16 if p.dtype == "bf16" else ssd.SSD_DTYPE_F32, 0)
+    group = p.headdim
+    stream = torch.cuda.current_stream(dev)
+    ptr = lambda t: None if t is None else t.data_ptr()
+
+    def call(i):
+        c = sets[i % len(sets)]
+        opts = ssd.make_block_opts(bias, True, 0.0, float("inf"), c["z"], w, group, 1e-5)
+        rc = ssd.ssd_backward_block(prob, opts, ptr(c["x"]), ptr(c["dt"]), ptr(A_log), ptr(c["B"]), ptr(c["C"]),
+                                    ptr(D), None, ptr(c["dout"]), None, ptr(c["dx"]), ptr(c["ddt"]), ptr(dA),
+                                    ptr(c["dB"]), ptr(c["dC"]), ptr(dD), None, ptr(dbias), ptr(c["dz"]), ptr(dw),
+                                    ptr(ws), wsb, stream.cuda_stream)
+        if rc != 0:
+            raise ssd.SsdError(rc, "ssd_backward_block")
+
+    opts0 = ssd.make_block_opts(bias, True, 0.0, float("inf"), sets[0]["z"], w, group, 1e-5)
+    wsb = ssd.ssd_backward_block_workspace_bytes(prob, opts0)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        call(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    _, _, compulsory, Qb = backward_counts(p)
+    tokens = p.batch * p.seqlen
+    act = 2 if p.dtype == "bf16" else 4
+    byts = compulsory + 2 * act * tokens * p.nheads * p.headdim + 8 * p.nheads * p.headdim   # z, dz, w, dw
+    sec = ms * 1e-3
+    print(json.dumps({
+        "metric": "SSD block bwd tokens/s (dt softplus + layer + SiLU gate + RMSNorm gradients, 2.7B-layer shape, "
+                  "1 GPU)",
+        "value": tokens / sec, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": p.dtype, "data": "synthetic (seeded; Mamba-2 layer shapes)",
+        "config": {"workload": "block_backward_" + args.workload, "batch": p.batch, "seqlen": p.seqlen,
+                   "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate, "ngroups": p.ngroups,
+                   "norm_group_size": group, "backward_chunk": Qb},
+        "roofline": {"bound": "hbm", "achieved": byts / sec / 1e9, "peak": PEAK_HBM_BPS / 1e9, "unit": "GB/s",
+                     "frac": byts / sec / PEAK_HBM_BPS, "traffic": None,
+                     "kernel": "whole call (forward recomputation, gate/norm and dt steps, layer backward)",
+                     "algorithmic_bytes": byts},
+    }), flush=True)
+
+
 def cp_bench(args, torch, ssd):
     """One rank's share of an 8-way sequence split of the 2.7B layer (512 of
     4096 tokens per batch row): the layer from a zero state on the span, the
@@ -485,6 +559,8 @@ def main():
     ap.add_argument("--block-norm-group", type=int, default=64)
     ap.add_argument("--backward", action="store_true",
                     help="time the layer's gradients (ssd_backward) instead")
+    ap.add_argument("--block-backward", action="store_true",
+                    help="time the block's gradients (ssd_backward_block) instead")
     ap.add_argument("--cp-share", action="store_true",
                     help="time one rank's share of an 8-way sequence split instead")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -528,6 +604,8 @@ def main():
         return cp_bench(args, torch, ssd)
     if args.backward:
         return backward_bench(args, torch, ssd)
+    if args.block_backward:
+        return block_backward_bench(args, torch, ssd)
 
     p = WORKLOADS[args.workload]
     inp = make_inputs(p, args.seed)

@@ -585,8 +585,8 @@ int block_backward_plan(const ssd_problem* prob, const ssd_block_opts* opts, Blo
     const size_t act = prob->dtype == SSD_DTYPE_BF16 ? 2 : 4;
     const size_t rows = static_cast<size_t>(prob->batch * prob->seqlen);
     const size_t H = static_cast<size_t>(prob->nheads), Cc = H * static_cast<size_t>(prob->headdim);
-    if (rows > static_cast<size_t>(65535) * 64) return SSD_ERR_TOO_LARGE;   // row chunks on grid y
     const size_t nch = static_cast<size_t>(ssd::block_bwd_row_chunks(static_cast<int64_t>(rows)));
+    if (nch > 65535) return SSD_ERR_TOO_LARGE;   // row chunks on grid y
     const size_t groups = opts->norm_group_size > 0 ? Cc / static_cast<size_t>(opts->norm_group_size) : 0;
     size_t off = 0;
     const auto take = [&](size_t bytes) {
