@@ -26,8 +26,14 @@ S_t (G starts at dfinal):
     G       = a_t G
 
 and finally d(initial state) = G, dA_log = A_h dA_h.  Float64 throughout,
-vectorised over batch rows and heads, one loop over tokens.  Packed rows
-(seq_idx) are not covered.
+vectorised over batch rows and heads, one loop over tokens.
+
+Packed rows (Section 8.3: one row holding several sequences, ``seq_idx``
+naming each token's sequence; the state starts from that sequence's initial
+state at its first token): the sequences do not interact, so the gradients
+are those of each sequence as a problem of its own -- concatenated along the
+tokens for dx, ddt, dB, dC, one initial-state gradient per sequence, and
+dA_log, dD summed over the sequences.
 """
 from __future__ import annotations
 
@@ -49,11 +55,16 @@ def _forward_states(x, dt, A, B, C, D, init):
     return states, y
 
 
-def backward(x, dt, A_log, B, C, dy, D=None, initial_states=None, dfinal=None):
+def backward(x, dt, A_log, B, C, dy, D=None, initial_states=None, dfinal=None, seq_idx=None):
     """Gradients of the layer.  x (b,T,H,P), dt (b,T,H), A_log (H), B/C
     (b,T,G,N), dy (b,T,H,P), D (H) or None, initial_states (b,H,P,N) or None,
     dfinal (b,H,P,N) or None.  Returns a dict with dx, ddt, dA_log, dB, dC,
-    dD, dinit (float64; dD and dinit zero-filled when not used)."""
+    dD, dinit (float64; dD and dinit zero-filled when not used).
+
+    With ``seq_idx`` (1, T) (packed rows, batch 1) initial_states, dfinal and
+    dinit are (nseq, H, P, N)."""
+    if seq_idx is not None:
+        return _backward_packed(x, dt, A_log, B, C, dy, D, initial_states, dfinal, seq_idx)
     f = lambda a: None if a is None else np.asarray(a, dtype=np.float64)
     x, dt, A_log, B, C, dy, D, init, dfinal = map(f, (x, dt, A_log, B, C, dy, D, initial_states, dfinal))
     b, T, H, P = x.shape
@@ -91,3 +102,26 @@ def backward(x, dt, A_log, B, C, dy, D=None, initial_states=None, dfinal=None):
         dB[:, :, grp[h]] += dBh[:, :, h]
         dC[:, :, grp[h]] += dCh[:, :, h]
     return {"dx": dx, "ddt": ddt, "dA_log": A * dA, "dB": dB, "dC": dC, "dD": dD, "dinit": Gs}
+
+
+def _backward_packed(x, dt, A_log, B, C, dy, D, init, dfinal, seq_idx):
+    """Packed rows: each sequence's gradients on its own (see the module text)."""
+    seq = np.asarray(seq_idx).reshape(-1)
+    if np.asarray(x).shape[0] != 1:
+        raise ValueError("packed rows use batch 1")
+    nseq = int(seq.max()) + 1
+    bounds = np.flatnonzero(np.diff(seq)) + 1
+    starts = np.concatenate([[0], bounds])
+    ends = np.concatenate([bounds, [seq.size]])
+    parts = []
+    for s, (t0, t1) in enumerate(zip(starts, ends)):
+        sl = slice(t0, t1)
+        one = lambda a: None if a is None else np.asarray(a)[s:s + 1]
+        parts.append(backward(np.asarray(x)[:, sl], np.asarray(dt)[:, sl], A_log, np.asarray(B)[:, sl],
+                              np.asarray(C)[:, sl], np.asarray(dy)[:, sl], D=D, initial_states=one(init),
+                              dfinal=one(dfinal)))
+    assert len(parts) == nseq
+    cat = lambda k: np.concatenate([q[k] for q in parts], axis=1)
+    return {"dx": cat("dx"), "ddt": cat("ddt"), "dB": cat("dB"), "dC": cat("dC"),
+            "dA_log": sum(q["dA_log"] for q in parts), "dD": sum(q["dD"] for q in parts),
+            "dinit": np.concatenate([q["dinit"] for q in parts], axis=0)}

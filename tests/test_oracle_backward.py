@@ -105,3 +105,66 @@ def _mutant(name):
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_backward_mutant_is_caught(name):
     assert not finite_difference_ok(_mutant(name))
+
+
+def _packed_problem(seed=7, T=11, H=3, P=2, N=4, G=1):
+    rng = np.random.default_rng(seed)
+    seq_idx = np.array([[0] * 3 + [1] * 1 + [2] * 5 + [3] * 2], dtype=np.int32)   # lengths 3, 1, 5, 2
+    nseq = 4
+    inp = dict(x=rng.standard_normal((1, T, H, P)), dt=rng.uniform(0.05, 0.6, (1, T, H)),
+               A_log=rng.uniform(-0.5, 1.0, H), B=rng.standard_normal((1, T, G, N)) / 2,
+               C=rng.standard_normal((1, T, G, N)) / 2, D=rng.standard_normal(H),
+               init=rng.standard_normal((nseq, H, P, N)))
+    W = rng.standard_normal((1, T, H, P))
+    V = rng.standard_normal((nseq, H, P, N))
+    return inp, seq_idx, nseq, W, V
+
+
+def packed_finite_difference_ok(m, samples=6, h=1e-6):
+    inp, seq_idx, nseq, W, V = _packed_problem()
+    g = m.backward(inp["x"], inp["dt"], inp["A_log"], inp["B"], inp["C"], W, D=inp["D"],
+                   initial_states=inp["init"], dfinal=V, seq_idx=seq_idx)
+
+    def loss():
+        y, fin = oracle.forward(inp["x"], inp["dt"], inp["A_log"], inp["B"], inp["C"], inp["D"],
+                                initial_states=inp["init"], seq_idx=seq_idx, nseq=nseq)
+        return float(np.sum(W * y) + np.sum(V * fin))
+
+    rng = np.random.default_rng(8)
+    for name, gname in NAMES.items():
+        arr = inp[name]
+        for _ in range(samples):
+            idx = tuple(rng.integers(0, s) for s in arr.shape)
+            old = arr[idx]
+            arr[idx] = old + h
+            lp = loss()
+            arr[idx] = old - h
+            lm = loss()
+            arr[idx] = old
+            fd = (lp - lm) / (2 * h)
+            if abs(g[gname][idx] - fd) > 1e-5 * max(1.0, abs(fd)):
+                return False
+    return True
+
+
+def test_packed_rows_match_finite_differences():
+    # the C oracle's forward resets the state token by token at each boundary
+    assert packed_finite_difference_ok(ob)
+
+
+def test_packed_rows_planted_mistake_is_caught():
+    # a packed gradient that lets the carried state gradient cross a boundary
+    src = open(SRC).read()
+    a = "one = lambda a: None if a is None else np.asarray(a)[s:s + 1]"
+    assert src.count(a) == 1
+    bad = src.replace("    for s, (t0, t1) in enumerate(zip(starts, ends)):",
+                      "    starts, ends = np.array([0]), np.array([seq.size])\n"
+                      "    for s, (t0, t1) in enumerate(zip(starts, ends)):")
+    bad = bad.replace("    assert len(parts) == nseq\n", "")
+    mod = types.ModuleType("oracle_backward_packed_mutant")
+    exec(compile(bad, SRC, "exec"), mod.__dict__)
+    try:
+        ok = packed_finite_difference_ok(mod)
+    except Exception:
+        ok = False
+    assert not ok
