@@ -287,6 +287,28 @@ int ssd_backward_timed(const ssd_problem* prob,
                        void* workspace, size_t workspace_bytes, void* stream,
                        void* event_begin, void* event_end);
 
+/* ssd_backward_varlen: ssd_backward for one packed row of nseq sequences
+ * (Section 8.3; batch must be 1, else SSD_ERR_SEQIDX_BATCH).  seq_starts is
+ * host memory: nseq + 1 token offsets, seq_starts[0] = 0, strictly
+ * increasing, seq_starts[nseq] = seqlen (else SSD_ERR_BAD_SHAPE); token t
+ * belongs to sequence s when seq_starts[s] <= t < seq_starts[s + 1] (the
+ * seq_idx of ssd_forward).  initial_states, dfinal_states and
+ * dinitial_states are (nseq, nheads, headdim, dstate).  The sequences do not
+ * interact: each runs as a problem of its own on its slice of the packed
+ * tensors, and dA_log and dD are summed over the sequences in order.
+ * Workspace: ssd_backward_varlen_workspace_bytes() bytes.  Otherwise as
+ * ssd_backward (every check is made before any work is enqueued). */
+int ssd_backward_varlen_workspace_bytes(const ssd_problem* prob, const int64_t* seq_starts, size_t* bytes);
+
+int ssd_backward_varlen(const ssd_problem* prob, const int64_t* seq_starts,
+                        const void* x, const void* dt, const float* A_log,
+                        const void* B, const void* C, const float* D,
+                        const float* initial_states,
+                        const void* dy, const float* dfinal_states,
+                        void* dx, void* ddt, float* dA_log, void* dB, void* dC,
+                        float* dD, float* dinitial_states,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
 /* ssd_backward_block: the gradients of ssd_forward_block (same `prob`,
  * `opts` and inputs; no packed rows), given dout = dL/d(block output) and
  * dfinal_states (NULL = 0).  The paper gives no backward; this is the chain

@@ -689,6 +689,90 @@ extern "C" int ssd_backward_block(const ssd_problem* prob, const ssd_block_opts*
     return ssd::launch_block_dt_bwd(p, bf16, st) == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
+namespace {
+
+// Packed rows: the sequences are independent, so the backward runs on each
+// sequence's token range as a problem of its own (pointer slices of the
+// packed tensors; one state per sequence), and the per-sequence dA_log and dD
+// are summed at the end.  seq_starts (host): nseq + 1 offsets, 0 = first <
+// ... < last = seqlen.
+int varlen_plan(const ssd_problem* prob, const int64_t* seq_starts, size_t* sub_bytes, size_t* total)
+{
+    if (!prob || !seq_starts) return SSD_ERR_NULL_ARG;
+    if (prob->batch != 1) return SSD_ERR_SEQIDX_BATCH;
+    if (prob->nseq < 1 || prob->nseq > prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    if (seq_starts[0] != 0 || seq_starts[prob->nseq] != prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    size_t need = 0;
+    for (int64_t s = 0; s < prob->nseq; ++s) {
+        if (seq_starts[s + 1] <= seq_starts[s]) return SSD_ERR_BAD_SHAPE;
+        ssd_problem q = *prob;
+        q.seqlen = seq_starts[s + 1] - seq_starts[s];
+        size_t b = 0;
+        const int rc = ssd_backward_workspace_bytes(&q, &b);
+        if (rc != SSD_OK) return rc;
+        if (b > need) need = b;
+    }
+    *sub_bytes = need;
+    *total = ssd::align_up(2 * sizeof(float) * static_cast<size_t>(prob->nseq * prob->nheads)) + need;
+    return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" int ssd_backward_varlen_workspace_bytes(const ssd_problem* prob, const int64_t* seq_starts,
+                                                   size_t* bytes)
+{
+    if (!bytes) return SSD_ERR_NULL_ARG;
+    size_t sub = 0;
+    return varlen_plan(prob, seq_starts, &sub, bytes);
+}
+
+extern "C" int ssd_backward_varlen(const ssd_problem* prob, const int64_t* seq_starts, const void* x,
+                                   const void* dt, const float* A_log, const void* B, const void* C, const float* D,
+                                   const float* initial_states, const void* dy, const float* dfinal_states,
+                                   void* dx, void* ddt, float* dA_log, void* dB, void* dC, float* dD,
+                                   float* dinitial_states, void* workspace, size_t workspace_bytes, void* stream)
+{
+    size_t sub = 0, total = 0;
+    int rc = varlen_plan(prob, seq_starts, &sub, &total);
+    if (rc != SSD_OK) return rc;
+    ssd::Shape s;
+    {
+        ssd_problem q = *prob;
+        q.chunk_size = 256;
+        if ((rc = ssd::validate(&q, true, &s)) != SSD_OK) return rc;
+    }
+    if (!x || !dt || !A_log || !B || !C || !dy || !dx || !ddt || !dA_log || !dB || !dC) return SSD_ERR_NULL_ARG;
+    if (!aligned16(initial_states) || !aligned16(dfinal_states) || !aligned16(dinitial_states) ||
+        !aligned16(x) || !aligned16(B) || !aligned16(C) || !aligned16(dy) || !aligned16(dx))
+        return SSD_ERR_UNSUPPORTED_DIMS;   // (every slice below keeps the alignment: rows are multiples of 32 bytes)
+    if (!workspace || workspace_bytes < total) return SSD_ERR_WORKSPACE;
+    const size_t act = s.bf16 ? 2 : 4;
+    const int64_t H = s.H, HP = s.H * s.P, GN = s.G * s.N, HPN = s.H * s.P * s.N;
+    float* partA = static_cast<float*>(workspace);
+    float* partD = partA + prob->nseq * H;
+    char* sub_ws = static_cast<char*>(workspace) + (total - sub);
+    const auto at = [](const void* p, int64_t off) { return static_cast<const char*>(p) + off; };
+    const auto atw = [](void* p, int64_t off) { return static_cast<char*>(p) + off; };
+    for (int64_t q = 0; q < prob->nseq; ++q) {
+        const int64_t t0 = seq_starts[q];
+        ssd_problem pq = *prob;
+        pq.seqlen = seq_starts[q + 1] - t0;
+        rc = backward_impl(&pq, at(x, t0 * HP * act), at(dt, t0 * H * act), A_log, at(B, t0 * GN * act),
+                           at(C, t0 * GN * act), D, initial_states ? initial_states + q * HPN : nullptr,
+                           at(dy, t0 * HP * act), dfinal_states ? dfinal_states + q * HPN : nullptr,
+                           atw(dx, t0 * HP * act), atw(ddt, t0 * H * act), partA + q * H, atw(dB, t0 * GN * act),
+                           atw(dC, t0 * GN * act), D ? partD + q * H : nullptr,
+                           dinitial_states ? dinitial_states + q * HPN : nullptr, sub_ws, sub, stream, nullptr,
+                           nullptr);
+        if (rc != SSD_OK) return SSD_ERR_LAUNCH;   // every check passed above: only a launch can fail here
+    }
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (ssd::launch_sum_rows(partA, prob->nseq, H, dA_log, st) != hipSuccess) return SSD_ERR_LAUNCH;
+    if (D && dD && ssd::launch_sum_rows(partD, prob->nseq, H, dD, st) != hipSuccess) return SSD_ERR_LAUNCH;
+    return SSD_OK;
+}
+
 extern "C" const char* ssd_error_string(int code)
 {
     switch (code) {

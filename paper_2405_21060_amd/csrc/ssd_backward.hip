@@ -516,6 +516,27 @@ BwdLayout bwd_layout(int64_t b, int64_t T, int64_t H, int64_t P, int64_t N, int6
     return l;
 }
 
+namespace {
+
+// out[c] = sum over rows r (in order) of part[r][c].
+__global__ __launch_bounds__(kThreads) void k_sum_rows(const float* part, int64_t nrows, int64_t ncols, float* out)
+{
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    if (c >= ncols) return;
+    float s = 0.f;
+    for (int64_t r = 0; r < nrows; ++r) s += part[r * ncols + c];
+    out[c] = s;
+}
+
+}  // namespace
+
+hipError_t launch_sum_rows(const float* part, int64_t nrows, int64_t ncols, float* out, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_sum_rows, dim3(static_cast<unsigned>((ncols + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                       stream, part, nrows, ncols, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream)
 {
     return bf16 ? launch_reduce<uint16_t>(p, stream) : launch_reduce<float>(p, stream);

@@ -65,6 +65,9 @@ hipError_t launch_backward_fast(const BwdParams& p, hipStream_t stream, hipEvent
 // dD), shared by both paths.
 hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream);
 
+// out[c] = sum over r of part[r * ncols + c], r in order (float32).
+hipError_t launch_sum_rows(const float* part, int64_t nrows, int64_t ncols, float* out, hipStream_t stream);
+
 // Enqueue the whole backward on `stream`; `ev_begin` / `ev_end` (may be null)
 // are recorded right before and right after the chunk-gradient kernel.
 hipError_t launch_backward(const BwdParams& p, bool bf16, hipStream_t stream, hipEvent_t ev_begin,

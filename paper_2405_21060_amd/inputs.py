@@ -166,13 +166,14 @@ class BlockInputs:
         return a.astype(np.float64)
 
 
-def make_grad_inputs(p: Problem, seed: int):
+def make_grad_inputs(p: Problem, seed: int, units: int = None):
     """Output gradients for the backward, from their own stream
     ``default_rng([seed, 0x6AD])``: ``dy`` (b, T, H, P) ~ N(0, 1) in the
-    activation dtype, then ``dfinal`` (b, H, P, N) ~ N(0, 1) float32."""
+    activation dtype, then ``dfinal`` (units, H, P, N) ~ N(0, 1) float32, one
+    state per batch row (or per sequence of a packed row: ``units``)."""
     rng = np.random.default_rng([seed, 0x6AD])
     dy = _normal_blocks(rng, (p.batch, p.seqlen, p.nheads, p.headdim), 1.0, p.dtype)
-    dfinal = _normal_blocks(rng, (p.batch, p.nheads, p.headdim, p.dstate), 1.0, "f32")
+    dfinal = _normal_blocks(rng, (units or p.batch, p.nheads, p.headdim, p.dstate), 1.0, "f32")
     return dy, dfinal
 
 

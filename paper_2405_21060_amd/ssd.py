@@ -39,6 +39,7 @@ EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_deco
             "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
             "ssd_span_decay", "ssd_span_combine", "ssd_span_correct_workspace_bytes", "ssd_span_correct",
             "ssd_backward_workspace_bytes", "ssd_backward", "ssd_backward_timed",
+            "ssd_backward_varlen_workspace_bytes", "ssd_backward_varlen",
             "ssd_backward_block_workspace_bytes", "ssd_backward_block", "ssd_error_string")
 
 
@@ -121,6 +122,11 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_backward.restype = ctypes.c_int
     lib.ssd_backward_timed.argtypes = lib.ssd_backward.argtypes + [vp, vp]
     lib.ssd_backward_timed.restype = ctypes.c_int
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    lib.ssd_backward_varlen_workspace_bytes.argtypes = [pp, i64p, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_backward_varlen_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_backward_varlen.argtypes = [pp, i64p] + [vp] * 16 + [vp, ctypes.c_size_t, vp]
+    lib.ssd_backward_varlen.restype = ctypes.c_int
     lib.ssd_backward_block_workspace_bytes.argtypes = [pp, ctypes.POINTER(SsdBlockOpts),
                                                        ctypes.POINTER(ctypes.c_size_t)]
     lib.ssd_backward_block_workspace_bytes.restype = ctypes.c_int
@@ -525,4 +531,66 @@ def backward_block(x, dt, A_log, B, C, dout, D=None, initial_states=None, dfinal
                             stream)
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_backward_block")
+    return g
+
+
+def _starts(seq_starts):
+    arr = (ctypes.c_int64 * len(seq_starts))(*[int(v) for v in seq_starts])
+    return arr
+
+
+def ssd_backward_varlen_workspace_bytes(prob: SsdProblem, seq_starts) -> int:
+    out = ctypes.c_size_t(0)
+    rc = load_library().ssd_backward_varlen_workspace_bytes(ctypes.byref(prob), _starts(seq_starts),
+                                                            ctypes.byref(out))
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_backward_varlen_workspace_bytes")
+    return int(out.value)
+
+
+def ssd_backward_varlen(prob: SsdProblem, seq_starts, x, dt, A_log, B, C, D, initial_states, dy, dfinal_states,
+                        dx, ddt, dA_log, dB, dC, dD, dinitial_states, workspace, workspace_bytes: int,
+                        stream) -> int:
+    """Raw ABI call: ``seq_starts`` a host sequence of nseq + 1 offsets,
+    integer device addresses (0 = NULL); returns the status."""
+    return load_library().ssd_backward_varlen(
+        ctypes.byref(prob), _starts(seq_starts), x, dt, A_log, B, C, D or None, initial_states or None, dy,
+        dfinal_states or None, dx, ddt, dA_log, dB, dC, dD or None, dinitial_states or None, workspace,
+        int(workspace_bytes), stream or None)
+
+
+def backward_varlen(x, dt, A_log, B, C, dy, seq_starts, D=None, initial_states=None, dfinal_states=None,
+                    workspace=None):
+    """Gradients of the layer for one packed row (batch 1) of sequences with
+    host offsets ``seq_starts`` (nseq + 1).  Returns the dict of ``backward``
+    with dinit (nseq, H, P, N)."""
+    import torch
+
+    dev = x.device
+    if x.shape[0] != 1:
+        raise ValueError("packed rows use batch 1")
+    for name, t in (("dt", dt), ("B", B), ("C", C), ("dy", dy)):
+        if t.dtype != x.dtype:
+            raise TypeError("%s must have x's dtype" % name)
+    for t in (x, dt, A_log, B, C, dy, D, initial_states, dfinal_states):
+        if t is not None and (t.device != dev or not t.is_contiguous()):
+            raise ValueError("all tensors must be contiguous and on x's device")
+    _, T, H, P = x.shape
+    G, N = B.shape[2], B.shape[3]
+    nseq = len(seq_starts) - 1
+    prob = make_problem(1, T, H, P, N, G, 256, SSD_DTYPE_BF16 if x.dtype == torch.bfloat16 else SSD_DTYPE_F32,
+                        nseq)
+    wsb = ssd_backward_varlen_workspace_bytes(prob, seq_starts)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    g = {"dx": torch.empty_like(x), "ddt": torch.empty_like(dt), "dB": torch.empty_like(B),
+         "dC": torch.empty_like(C), "dA_log": torch.empty_like(A_log),
+         "dD": torch.empty_like(D) if D is not None else None,
+         "dinit": torch.empty((nseq, H, P, N), dtype=torch.float32, device=dev)}
+    rc = ssd_backward_varlen(prob, seq_starts, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),
+                             _ptr(initial_states), _ptr(dy), _ptr(dfinal_states), _ptr(g["dx"]), _ptr(g["ddt"]),
+                             _ptr(g["dA_log"]), _ptr(g["dB"]), _ptr(g["dC"]), _ptr(g["dD"]), _ptr(g["dinit"]),
+                             _ptr(workspace), wsb, torch.cuda.current_stream(dev).cuda_stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_backward_varlen")
     return g

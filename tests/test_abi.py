@@ -240,6 +240,26 @@ def test_block_backward_validation(lib):
     assert call(o, ws=need - 1) == ssd.SSD_ERR_WORKSPACE
 
 
+def test_varlen_backward_validation(lib):
+    p = prob(batch=1, seqlen=1000, nseq=3)
+    starts = [0, 100, 600, 1000]
+    need = ssd.ssd_backward_varlen_workspace_bytes(p, starts)
+    # at least the backward workspace of the longest sequence (500 tokens)
+    assert need >= ssd.ssd_backward_workspace_bytes(prob(batch=1, seqlen=500))
+
+    def call(pp, st, ws=need, x=FAKE):
+        return ssd.ssd_backward_varlen(pp, st, x, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, 0, FAKE, FAKE, FAKE, FAKE,
+                                       FAKE, 0, 0, FAKE, ws, 0)
+
+    assert call(prob(batch=2, seqlen=1000, nseq=3), starts) == ssd.SSD_ERR_SEQIDX_BATCH
+    assert call(p, [0, 100, 100, 1000]) == ssd.SSD_ERR_BAD_SHAPE        # empty sequence
+    assert call(p, [1, 100, 600, 1000]) == ssd.SSD_ERR_BAD_SHAPE        # does not start at 0
+    assert call(p, [0, 100, 600, 999]) == ssd.SSD_ERR_BAD_SHAPE         # does not end at seqlen
+    assert call(prob(batch=1, seqlen=1000, nseq=0), [0]) == ssd.SSD_ERR_BAD_SHAPE
+    assert call(p, starts, x=FAKE + 2) == ssd.SSD_ERR_UNSUPPORTED_DIMS
+    assert call(p, starts, ws=need - 1) == ssd.SSD_ERR_WORKSPACE
+
+
 def test_error_strings(lib):
     for code in range(0, -11, -1):
         s = ssd.ssd_error_string(code)

@@ -166,3 +166,81 @@ def test_backward_full_size_prefix_loss():
         assert not np.any(got[k][:, K:]), k
     for k in ("dA_log", "dD", "dinit"):
         check(k, got[k], ref[k], tol)
+
+
+
+# ---- packed rows (ssd_backward_varlen): sequences given by host offsets
+
+def gpu_backward_varlen(inp, dy, dfinal, starts, use_D=True):
+    import torch
+    from paper_2405_21060_amd import ssd
+
+    d = to_device(inp)
+    g = ssd.backward_varlen(d["x"], d["dt"], d["A_log"], d["B"], d["C"], act_to_device(dy), starts,
+                            D=d["D"] if use_D else None, initial_states=d["initial_states"],
+                            dfinal_states=None if dfinal is None else torch.from_numpy(dfinal).cuda())
+    torch.cuda.synchronize()
+    return {k: (None if v is None else to_f64(v)) for k, v in g.items()}
+
+
+def packed_inputs(p, lengths, seed):
+    inp = make_inputs(p, seed)
+    seq = np.repeat(np.arange(len(lengths), dtype=np.int32), lengths).reshape(1, -1)
+    starts = [0] + list(np.cumsum(lengths))
+    if inp.initial_states is not None:
+        rng = np.random.default_rng([seed, 5])
+        inp.initial_states = rng.standard_normal((len(lengths),) + inp.initial_states.shape[1:]).astype(np.float32)
+    return inp, seq, starts
+
+
+# (dtype, (T, H, P, N, G), sequence lengths, initial states, final-state gradient, D)
+VARLEN_CASES = [
+    ("bf16", (500, 4, 64, 128, 2), [37, 1, 200, 262], True, True, True),
+    ("bf16", (300, 3, 64, 64, 1), [64, 64, 1, 171], False, True, False),
+    ("f32", (300, 3, 32, 16, 1), [100, 64, 136], False, True, True),
+    ("f32", (97, 2, 16, 32, 2), [5, 3, 1, 40, 48], True, False, True),
+]
+
+
+@pytest.mark.parametrize("case", VARLEN_CASES, ids=lambda c: "%s_T%d_%dseq" % (c[0], c[1][0], len(c[2])))
+def test_backward_packed_rows_match_oracle(case):
+    dtype, (T, H, P, N, G), lengths, use_init, use_dfinal, use_D = case
+    assert sum(lengths) == T
+    p = Problem(1, T, H, P, N, G, 256, dtype, init_states=use_init)
+    announce("backward packed rows %s" % (case,))
+    inp, seq, starts = packed_inputs(p, lengths, 13)
+    dy, dfinal = make_grad_inputs(p, 13, units=len(lengths))
+    if not use_dfinal:
+        dfinal = None
+    got = gpu_backward_varlen(inp, dy, dfinal, starts, use_D)
+    ref = ob.backward(f64(inp.x), f64(inp.dt), inp.A_log.astype(np.float64), f64(inp.B), f64(inp.C), f64(dy),
+                      D=inp.D.astype(np.float64) if use_D else None, initial_states=inp.initial_states,
+                      dfinal=dfinal, seq_idx=seq)
+    tol = TOL[dtype]
+    for k in ("dx", "ddt", "dB", "dC", "dA_log", "dinit"):
+        check(k, got[k], ref[k], tol)
+    if use_D:
+        check("dD", got["dD"], ref["dD"], tol)
+
+
+def test_backward_packed_rows_full_size_head_subset():
+    """The packed 32768-token workload (64 heads in 8 groups, sequences of 256
+    to 4096 tokens, initial states), full launch: dx, ddt and the initial-state
+    gradients of heads 0, 8 and 63 (each depends only on its own head and
+    group)."""
+    p = workload("varlen_g8")
+    announce("backward packed rows full size, head subset %s" % (p,))
+    inp = make_inputs(p, 3)
+    seq = inp.seq_idx.reshape(-1)
+    starts = [0] + list(np.flatnonzero(np.diff(seq)) + 1) + [seq.size]
+    dy, dfinal = make_grad_inputs(p, 3, units=inp.nseq)
+    got = gpu_backward_varlen(inp, dy, dfinal, starts)
+    heads, groups = [0, 8, 63], [0, 1, 7]
+    ref = ob.backward(f64(inp.x)[:, :, heads], f64(inp.dt)[:, :, heads], inp.A_log.astype(np.float64)[heads],
+                      f64(inp.B)[:, :, groups], f64(inp.C)[:, :, groups], f64(dy)[:, :, heads],
+                      D=inp.D.astype(np.float64)[heads], initial_states=inp.initial_states[:, heads],
+                      dfinal=dfinal[:, heads], seq_idx=inp.seq_idx)
+    tol = TOL[p.dtype]
+    check("dx", got["dx"][:, :, heads], ref["dx"], tol)
+    check("ddt", got["ddt"][:, :, heads], ref["ddt"], tol)
+    check("dinit", got["dinit"][:, heads], ref["dinit"], tol)
