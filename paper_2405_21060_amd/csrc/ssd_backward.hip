@@ -484,11 +484,16 @@ size_t al(size_t v) { return (v + 255) / 256 * 256; }
 
 void bwd_slices(int64_t b, int64_t nC, int64_t G, int64_t hpg, int64_t* S, int64_t* hs)
 {
-    // smallest slice (most workgroups) that still gives each workgroup several
-    // heads to share B, C and G0 over, once 2048 workgroups are reached
-    int64_t h = 1;
-    while (h < hpg && b * nC * G * ((hpg + 2 * h - 1) / (2 * h)) >= 2048) h *= 2;
-    *hs = h < hpg ? h : hpg;
+    // as few slices as still give every compute unit of the chip (256 CUs) a
+    // workgroup: a workgroup shares B, C and the chunk's Gram tiles over its
+    // heads and accumulates dB, dC over them (measured at the 2.7B shape:
+    // 80 heads per workgroup 1.130 ms, 40: 1.139, 16: 1.165, 8: 1.217)
+    constexpr int64_t kCUs = 256;
+    const int64_t units = b * nC * G;
+    int64_t s = (kCUs + units - 1) / units;
+    if (s > hpg) s = hpg;
+    if (s < 1) s = 1;
+    *hs = (hpg + s - 1) / s;
     *S = (hpg + *hs - 1) / *hs;
 }
 

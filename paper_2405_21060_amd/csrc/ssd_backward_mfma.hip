@@ -155,7 +155,7 @@ __device__ __forceinline__ HeadRange head_range(const BwdParams& p)
 constexpr int kPassT = 256;
 
 template <int N>
-__global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
+__global__ __launch_bounds__(kPassT, 3) void k_bwd2_pass(BwdParams p)   // 3 waves per SIMD: 3 workgroups per CU
 {
     __shared__ __attribute__((aligned(16))) u16 XT[kP2 * kLd];   // rows p, k = token
     __shared__ __attribute__((aligned(16))) u16 YT[N * kLd];     // rows n, k = token

@@ -77,9 +77,9 @@ CASES = [
     (1, 200, 3, 128, 256, 1, "f32", True, True, False),
     (1, 33, 3, 48, 64, 3, "bf16", False, True, True),
     (3, 96, 8, 64, 64, 1, "bf16", True, False, True),
-    # 80 heads per group over 64 chunks: two heads per workgroup
+    # 80 heads per group over 64 chunks: four slices of 20 heads per workgroup
     (1, 2048, 80, 16, 16, 1, "f32", True, True, True),
-    # six heads per group over 1024 (row, chunk, group) units: slices of 4 and 2 heads
+    # six heads per group over 1024 (row, chunk, group) units: a whole group per workgroup
     (1, 16384, 12, 16, 16, 2, "f32", True, True, True),
     # matrix-core shapes (bf16, headdim 64, dstate 64 or 128)
     (1, 1, 2, 64, 64, 1, "bf16", True, True, True),
