@@ -148,17 +148,48 @@ __device__ __forceinline__ HeadRange head_range(const BwdParams& p)
 //   direction 1 (backward, from the final-state gradient): Gn(c) = S, then
 //     S <- exp(cs_end) S + sum_u (exp(cs_u) dy_u) C_u^T;
 //   at the end of direction 1, S is the initial-state gradient (float32).
-// The chunk term is a 64 x N x 64 product on the matrix cores from x^T (or
-// dy^T) and B^T (or C^T) transposed into shared memory (inputs fetched two
-// chunks ahead).  Wavefront w owns p rows 16 w .. 16 w + 15 of S (N / 16
-// tiles of 16 x 16).
+// The chunk term is a 64 x N x 64 product over the chunk's tokens on the
+// matrix cores.  Both operands stay token-major in shared memory (whole
+// 16-byte pieces of rows, as loaded: the global loads are coalesced), with
+// each row's 8-element groups XOR-swizzled by the row index, and the
+// contraction fragments come out of transposing reads (ds_read_b64_tr_b16):
+// within a 16-lane group, source lane j reads row k0 + j/4, elements f0 +
+// 4 (j%4) .. +3, and lane i receives element f0 + i of rows k0 .. k0 + 3.
+// Lane group g takes rows 4 g .. 4 g + 3 and 16 + 4 g .. 16 + 4 g + 3 of each
+// 32-token step for its eight contraction slots (the same map for both
+// operands).  Inputs are fetched two chunks ahead.  Wavefront w owns p rows
+// 16 w .. 16 w + 15 of S (N / 16 tiles of 16 x 16).
 constexpr int kPassT = 256;
 
-template <int N>
-__global__ __launch_bounds__(kPassT, 3) void k_bwd2_pass(BwdParams p)   // 3 waves per SIMD: 3 workgroups per CU
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// Element offset of (row s, element f) in a token-major buffer of F elements
+// per row, 8-element groups swizzled by (s & 7).
+template <int F>
+__device__ __forceinline__ int tok_off(int s, int f)
 {
-    __shared__ __attribute__((aligned(16))) u16 XT[kP2 * kLd];   // rows p, k = token
-    __shared__ __attribute__((aligned(16))) u16 YT[N * kLd];     // rows n, k = token
+    return s * F + ((((f >> 3) ^ (s & 7)) << 3) | (f & 7));
+}
+
+// Contraction fragment over tokens 32 m .. 32 m + 31 of elements f0 .. f0 + 15.
+template <int F>
+__device__ __forceinline__ uint4 tr_frag(const u16* buf, int m, int f0, int lane)
+{
+    const int j = lane & 15, g = lane >> 4;
+    const int row = 32 * m + 4 * g + (j >> 2), f = f0 + 4 * (j & 3);
+    const uint2 lo = __builtin_bit_cast(
+        uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(buf + tok_off<F>(row, f))));
+    const uint2 hi = __builtin_bit_cast(
+        uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(buf + tok_off<F>(row + 16, f))));
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
+template <int N>
+__global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
+{
+    __shared__ __attribute__((aligned(16))) u16 XS[kQ2 * kP2];   // weighted x (or dy), token-major
+    __shared__ __attribute__((aligned(16))) u16 YS[kQ2 * N];     // B (or C), token-major
 
     const int64_t bh = blockIdx.x;
     const int64_t b = bh / p.H, h = bh - b * p.H, g = h / (p.H / p.G);
@@ -181,58 +212,57 @@ __global__ __launch_bounds__(kPassT, 3) void k_bwd2_pass(BwdParams p)   // 3 wav
         for (int v = 0; v < 4; ++v)
             S[nt][v] = s0 ? s0[(bh * kP2 + 16 * w + 4 * q + v) * N + 16 * nt + r] : 0.f;
 
-    // One chunk's inputs: dt (lane = token), two 8-wide pieces of x (or dy) and
-    // N / 32 of B (or C) per thread (token = lane, columns 8 (w + 4 k) ..).
-    // Two stages in flight: the chunk after next is fetched while one is used.
+    // One chunk's inputs: dt (lane = token), and 16-byte pieces of x (or dy)
+    // and of B (or C): piece i = tid + 256 k is row i / (F/8), group i % (F/8),
+    // so consecutive lanes read consecutive bytes of a row.
+    constexpr int kXK = kQ2 * kP2 / 8 / kPassT;   // 2
+    constexpr int kYK = kQ2 * N / 8 / kPassT;     // N / 32
     struct Stage {
         float dt;
-        uint4 x[2], bc[N / 32];
+        uint4 x[kXK], y[kYK];
     };
     const auto chunk_at = [&](int64_t k) { return dir == 0 ? k : p.nC - 1 - k; };
     const auto fetch = [&](Stage& st, int64_t k) {
         if (k >= p.nC) return;
         const int64_t c = chunk_at(k);
         const int L = chunk_len2(p.T, c);
-        const int64_t tok = b * p.T + c * kQ2 + lane;
-        st.dt = lane < L ? bf(dtg[tok * p.H + h]) : 0.f;
+        const int64_t t0 = b * p.T + c * kQ2;
+        st.dt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            st.x[kk] = make_uint4(0, 0, 0, 0);
-            if (lane < L) st.x[kk] = *reinterpret_cast<const uint4*>(src + (tok * p.H + h) * kP2 + 8 * (w + 4 * kk));
+        for (int kk = 0; kk < kXK; ++kk) {
+            const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
+            st.x[kk] = s < L ? *reinterpret_cast<const uint4*>(src + ((t0 + s) * p.H + h) * kP2 + f)
+                             : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
-        for (int kk = 0; kk < N / 32; ++kk) {
-            st.bc[kk] = make_uint4(0, 0, 0, 0);
-            if (lane < L) st.bc[kk] = *reinterpret_cast<const uint4*>(bc + (tok * p.G + g) * N + 8 * (w + 4 * kk));
+        for (int kk = 0; kk < kYK; ++kk) {
+            const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
+            st.y[kk] = s < L ? *reinterpret_cast<const uint4*>(bc + ((t0 + s) * p.G + g) * N + f)
+                             : make_uint4(0, 0, 0, 0);
         }
     };
     const auto step = [&](Stage& st, int64_t k) {
         const int64_t c = chunk_at(k);
         const int L = chunk_len2(p.T, c);
-        // token weights (lane = token; tokens beyond the chunk hold zero inputs)
+        // token weights: cumsum with lane = token, then each piece's token's weight
         const float cs = wave_scan(st.dt * A2);
         const float csend = lane_value(cs, L - 1);
         const float wt = dir == 0 ? exp2f(csend - cs) * st.dt : exp2f(cs);
-        __syncthreads();   // the previous chunk's product is done with XT, YT
+        __syncthreads();   // the previous chunk's product is done with XS, YS
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            const int c0 = 8 * (w + 4 * kk);
+        for (int kk = 0; kk < kXK; ++kk) {
+            const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
+            const float ws = __shfl(wt, s, 64);
             const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
+            uint32_t o[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                XT[(c0 + 2 * e) * kLd + lane] = static_cast<u16>(bf16_bits(wt * lo_f(ex[e])));
-                XT[(c0 + 2 * e + 1) * kLd + lane] = static_cast<u16>(bf16_bits(wt * hi_f(ex[e])));
-            }
+            for (int e = 0; e < 4; ++e) o[e] = pack2(ws * lo_f(ex[e]), ws * hi_f(ex[e]));
+            *reinterpret_cast<uint4*>(XS + tok_off<kP2>(s, f)) = make_uint4(o[0], o[1], o[2], o[3]);
         }
 #pragma unroll
-        for (int kk = 0; kk < N / 32; ++kk) {
-            const int c0 = 8 * (w + 4 * kk);
-            const uint32_t eb[4] = {st.bc[kk].x, st.bc[kk].y, st.bc[kk].z, st.bc[kk].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                YT[(c0 + 2 * e) * kLd + lane] = static_cast<u16>(eb[e]);
-                YT[(c0 + 2 * e + 1) * kLd + lane] = static_cast<u16>(eb[e] >> 16);
-            }
+        for (int kk = 0; kk < kYK; ++kk) {
+            const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
+            *reinterpret_cast<uint4*>(YS + tok_off<N>(s, f)) = st.y[kk];
         }
         fetch(st, k + 2);
 
@@ -245,12 +275,12 @@ __global__ __launch_bounds__(kPassT, 3) void k_bwd2_pass(BwdParams p)   // 3 wav
 
         __syncthreads();   // this chunk's operands in place
         const float a = exp2f(csend);
+        const uint4 xf0 = tr_frag<kP2>(XS, 0, 16 * w, lane), xf1 = tr_frag<kP2>(XS, 1, 16 * w, lane);
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) {
             f32x4_t t = zero4();
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-                t = mma(ldfrag(XT, kLd, 16 * w + r, ks, lane), ldfrag(YT, kLd, 16 * nt + r, ks, lane), t);
+            t = mma(xf0, tr_frag<N>(YS, 0, 16 * nt, lane), t);
+            t = mma(xf1, tr_frag<N>(YS, 1, 16 * nt, lane), t);
 #pragma unroll
             for (int v = 0; v < 4; ++v) S[nt][v] = fmaf(a, S[nt][v], t[v]);
         }
