@@ -573,6 +573,8 @@ def main():
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="time whole calls only (no events around the dominant kernel)")
+    ap.add_argument("--host-offsets", action="store_true",
+                    help="packed workloads: time ssd_forward_varlen (host sequence offsets) instead of seq_idx")
     ap.add_argument("--decode", action="store_true",
                     help="time the decode step instead (one token per sequence, batch --decode-batch)")
     ap.add_argument("--decode-batch", type=int, default=256)
@@ -652,9 +654,26 @@ def main():
         a.record(stream)
         z.record(stream)
 
+    starts = None
+    if p.varlen and args.host_offsets:
+        # packed row with the sequences' host offsets: one forward per sequence
+        seq = inp.seq_idx.reshape(-1)
+        starts = [0] + [int(v) for v in (seq[1:] != seq[:-1]).nonzero()[0] + 1] + [int(seq.size)]
+        wsb = ssd.ssd_forward_varlen_workspace_bytes(prob, starts)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        args.no_kernel_events = True
+
     def step(i, events=None):
         c = copies[i % len(copies)]
         ptr = lambda t: None if t is None else t.data_ptr()
+        if starts is not None:
+            rc = ssd.ssd_forward_varlen(prob, starts, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]),
+                                        ptr(c["C"]), ptr(c["D"]), ptr(c["initial_states"]),
+                                        ptr(outs[i % len(copies)]), ptr(fins[i % len(copies)]), ws.data_ptr(),
+                                        wsb, stream.cuda_stream)
+            if rc != 0:
+                raise ssd.SsdError(rc, "ssd_forward_varlen")
+            return
         args_ = (prob, ptr(c["x"]), ptr(c["dt"]), ptr(c["A_log"]), ptr(c["B"]), ptr(c["C"]),
                  ptr(c["D"]), ptr(c["initial_states"]), ptr(c["seq_idx"]),
                  ptr(outs[i % len(copies)]), ptr(fins[i % len(copies)]), ws.data_ptr(), wsb,
@@ -710,7 +729,8 @@ def main():
     roof["kernel_ms"] = kms
     roof["algorithmic_bytes"] = byts
     line = {
-        "metric": "SSD fwd tokens/s (2.7B-layer shape, 1 GPU)",
+        "metric": "SSD fwd tokens/s (%s, 1 GPU)" % (
+            "2.7B-layer shape" if args.workload == "mamba2_2p7b" else args.workload + " workload"),
         "value": tokens / sec,
         "unit": "tokens/s",
         "n_gpus": 1,

@@ -118,6 +118,24 @@ int ssd_forward_timed(const ssd_problem* prob,
                       void* workspace, size_t workspace_bytes, void* stream,
                       void* event_begin, void* event_end);
 
+/* ssd_forward for one packed row (batch 1) of nseq sequences given by host
+ * offsets instead of the device seq_idx: seq_starts (host memory) holds nseq +
+ * 1 token offsets, seq_starts[0] = 0, strictly increasing, seq_starts[nseq] =
+ * seqlen (else SSD_ERR_BAD_SHAPE); token t belongs to sequence s when
+ * seq_starts[s] <= t < seq_starts[s + 1].  Each sequence runs as a problem of
+ * its own on its slice of the packed tensors (on the fused chunk kernel where
+ * the shape allows), so the result equals ssd_forward with the matching
+ * seq_idx.  initial_states / final_states are (nseq, nheads, headdim, dstate)
+ * (either may be NULL).  Workspace: ssd_forward_varlen_workspace_bytes().
+ * Errors as for ssd_forward. */
+int ssd_forward_varlen_workspace_bytes(const ssd_problem* prob, const int64_t* seq_starts, size_t* bytes);
+
+int ssd_forward_varlen(const ssd_problem* prob, const int64_t* seq_starts,
+                       const void* x, const void* dt, const float* A_log,
+                       const void* B, const void* C, const float* D,
+                       const float* initial_states, void* y, float* final_states,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 /* One decode step (one new token per sequence) of the same layer, in the
  * recurrent form of eq. s6 with scalar A (the per-token inference cost of
  * Section 6.3): per batch row and head h (group g = h / (H/G)),

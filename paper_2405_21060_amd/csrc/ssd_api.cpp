@@ -773,6 +773,71 @@ extern "C" int ssd_backward_varlen(const ssd_problem* prob, const int64_t* seq_s
     return SSD_OK;
 }
 
+namespace {
+
+// Packed rows with host offsets: the forward of each sequence on its slice of
+// the packed tensors (the fused kernel where the shape allows), one initial
+// and final state per sequence.
+int fwd_varlen_plan(const ssd_problem* prob, const int64_t* seq_starts, size_t* bytes)
+{
+    if (!prob || !seq_starts) return SSD_ERR_NULL_ARG;
+    if (prob->batch != 1) return SSD_ERR_SEQIDX_BATCH;
+    if (prob->nseq < 1 || prob->nseq > prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    if (seq_starts[0] != 0 || seq_starts[prob->nseq] != prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    size_t need = 0;
+    for (int64_t s = 0; s < prob->nseq; ++s) {
+        if (seq_starts[s + 1] <= seq_starts[s]) return SSD_ERR_BAD_SHAPE;
+        ssd_problem q = *prob;
+        q.seqlen = seq_starts[s + 1] - seq_starts[s];
+        size_t b = 0;
+        const int rc = ssd_workspace_bytes(&q, &b);
+        if (rc != SSD_OK) return rc;
+        if (b > need) need = b;
+    }
+    *bytes = need;
+    return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" int ssd_forward_varlen_workspace_bytes(const ssd_problem* prob, const int64_t* seq_starts,
+                                                  size_t* bytes)
+{
+    if (!bytes) return SSD_ERR_NULL_ARG;
+    return fwd_varlen_plan(prob, seq_starts, bytes);
+}
+
+extern "C" int ssd_forward_varlen(const ssd_problem* prob, const int64_t* seq_starts, const void* x,
+                                  const void* dt, const float* A_log, const void* B, const void* C,
+                                  const float* D, const float* initial_states, void* y, float* final_states,
+                                  void* workspace, size_t workspace_bytes, void* stream)
+{
+    size_t need = 0;
+    int rc = fwd_varlen_plan(prob, seq_starts, &need);
+    if (rc != SSD_OK) return rc;
+    ssd::Shape s;
+    if ((rc = ssd::validate(prob, true, &s)) != SSD_OK) return rc;
+    if (!x || !dt || !A_log || !B || !C || !y) return SSD_ERR_NULL_ARG;
+    if (!workspace || workspace_bytes < need) return SSD_ERR_WORKSPACE;
+    const size_t act = s.bf16 ? 2 : 4;
+    const int64_t H = s.H, HP = s.H * s.P, GN = s.G * s.N, HPN = s.H * s.P * s.N;
+    for (int64_t q = 0; q < prob->nseq; ++q) {
+        const int64_t t0 = seq_starts[q];
+        ssd_problem pq = *prob;
+        pq.seqlen = seq_starts[q + 1] - t0;
+        rc = forward_impl(&pq, nullptr, static_cast<const char*>(x) + t0 * HP * act,
+                          static_cast<const char*>(dt) + t0 * H * act, A_log,
+                          static_cast<const char*>(B) + t0 * GN * act, static_cast<const char*>(C) + t0 * GN * act,
+                          D, initial_states ? initial_states + q * HPN : nullptr, nullptr,
+                          static_cast<char*>(y) + t0 * HP * act, final_states ? final_states + q * HPN : nullptr,
+                          workspace, workspace_bytes, stream, nullptr, nullptr);
+        // the first call validates everything the later ones check (same shapes
+        // but for seqlen): an error after it is a launch failure
+        if (rc != SSD_OK) return q == 0 ? rc : SSD_ERR_LAUNCH;
+    }
+    return SSD_OK;
+}
+
 extern "C" const char* ssd_error_string(int code)
 {
     switch (code) {

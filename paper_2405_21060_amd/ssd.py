@@ -40,6 +40,7 @@ EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_deco
             "ssd_span_decay", "ssd_span_combine", "ssd_span_correct_workspace_bytes", "ssd_span_correct",
             "ssd_backward_workspace_bytes", "ssd_backward", "ssd_backward_timed",
             "ssd_backward_varlen_workspace_bytes", "ssd_backward_varlen",
+            "ssd_forward_varlen_workspace_bytes", "ssd_forward_varlen",
             "ssd_backward_block_workspace_bytes", "ssd_backward_block", "ssd_error_string")
 
 
@@ -127,6 +128,10 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_backward_varlen_workspace_bytes.restype = ctypes.c_int
     lib.ssd_backward_varlen.argtypes = [pp, i64p] + [vp] * 16 + [vp, ctypes.c_size_t, vp]
     lib.ssd_backward_varlen.restype = ctypes.c_int
+    lib.ssd_forward_varlen_workspace_bytes.argtypes = [pp, i64p, ctypes.POINTER(ctypes.c_size_t)]
+    lib.ssd_forward_varlen_workspace_bytes.restype = ctypes.c_int
+    lib.ssd_forward_varlen.argtypes = [pp, i64p] + [vp] * 9 + [vp, ctypes.c_size_t, vp]
+    lib.ssd_forward_varlen.restype = ctypes.c_int
     lib.ssd_backward_block_workspace_bytes.argtypes = [pp, ctypes.POINTER(SsdBlockOpts),
                                                        ctypes.POINTER(ctypes.c_size_t)]
     lib.ssd_backward_block_workspace_bytes.restype = ctypes.c_int
@@ -594,3 +599,48 @@ def backward_varlen(x, dt, A_log, B, C, dy, seq_starts, D=None, initial_states=N
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_backward_varlen")
     return g
+
+
+def ssd_forward_varlen(prob: SsdProblem, seq_starts, x, dt, A_log, B, C, D, initial_states, y, final_states,
+                       workspace, workspace_bytes: int, stream) -> int:
+    """Raw ABI call: ``seq_starts`` a host sequence of nseq + 1 offsets,
+    integer device addresses (0 = NULL); returns the status."""
+    return load_library().ssd_forward_varlen(
+        ctypes.byref(prob), _starts(seq_starts), x, dt, A_log, B, C, D or None, initial_states or None, y,
+        final_states or None, workspace, int(workspace_bytes), stream or None)
+
+
+def ssd_forward_varlen_workspace_bytes(prob: SsdProblem, seq_starts) -> int:
+    out = ctypes.c_size_t(0)
+    rc = load_library().ssd_forward_varlen_workspace_bytes(ctypes.byref(prob), _starts(seq_starts),
+                                                           ctypes.byref(out))
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_forward_varlen_workspace_bytes")
+    return int(out.value)
+
+
+def forward_varlen(x, dt, A_log, B, C, seq_starts, D=None, chunk_size: int = 256, initial_states=None,
+                   return_final_states: bool = True, workspace=None, out=None):
+    """The forward of one packed row (batch 1) with host sequence offsets
+    ``seq_starts`` (nseq + 1); returns ``(y, final_states (nseq,H,P,N) or None)``."""
+    import torch
+
+    dev = x.device
+    if x.shape[0] != 1:
+        raise ValueError("packed rows use batch 1")
+    _, T, H, P = x.shape
+    G, N = B.shape[2], B.shape[3]
+    nseq = len(seq_starts) - 1
+    prob = make_problem(1, T, H, P, N, G, chunk_size,
+                        SSD_DTYPE_BF16 if x.dtype == torch.bfloat16 else SSD_DTYPE_F32, nseq)
+    wsb = ssd_forward_varlen_workspace_bytes(prob, seq_starts)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    y = out if out is not None else torch.empty_like(x)
+    fin = torch.empty((nseq, H, P, N), dtype=torch.float32, device=dev) if return_final_states else None
+    rc = ssd_forward_varlen(prob, seq_starts, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),
+                            _ptr(initial_states), _ptr(y), _ptr(fin), _ptr(workspace), wsb,
+                            torch.cuda.current_stream(dev).cuda_stream)
+    if rc != SSD_OK:
+        raise SsdError(rc, "ssd_forward_varlen")
+    return y, fin

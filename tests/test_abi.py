@@ -260,6 +260,22 @@ def test_varlen_backward_validation(lib):
     assert call(p, starts, ws=need - 1) == ssd.SSD_ERR_WORKSPACE
 
 
+def test_varlen_forward_validation(lib):
+    p = prob(batch=1, seqlen=1000, nseq=3)
+    starts = [0, 100, 600, 1000]
+    need = ssd.ssd_forward_varlen_workspace_bytes(p, starts)
+    assert need >= ssd.ssd_workspace_bytes(prob(batch=1, seqlen=500))
+
+    def call(pp, st, ws=need, y=FAKE):
+        return ssd.ssd_forward_varlen(pp, st, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, y, 0, FAKE, ws, 0)
+
+    assert call(prob(batch=2, seqlen=1000, nseq=3), starts) == ssd.SSD_ERR_SEQIDX_BATCH
+    assert call(p, [0, 600, 100, 1000]) == ssd.SSD_ERR_BAD_SHAPE
+    assert call(p, [0, 100, 600, 1001]) == ssd.SSD_ERR_BAD_SHAPE
+    assert call(p, starts, y=0) == ssd.SSD_ERR_NULL_ARG
+    assert call(p, starts, ws=need - 1) == ssd.SSD_ERR_WORKSPACE
+
+
 def test_error_strings(lib):
     for code in range(0, -11, -1):
         s = ssd.ssd_error_string(code)

@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 from paper_2405_21060_amd.inputs import WORKLOADS, Problem, make_inputs
-from tests.ssd_harness import TOL, announce, rel_err, run_gpu, to_f64
+from tests.ssd_harness import TOL, announce, rel_err, run_gpu, to_f64, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -168,3 +168,42 @@ def test_full_size_sampled_heads(name):
     # the middle (items are groups of up to 4 consecutive heads)
     heads = sorted({0, 1, p.nheads // 2, p.nheads // 2 + 1, p.nheads - 1})
     check(inp, heads=heads, tag=name)
+
+
+
+# ---- packed rows given by host offsets (ssd_forward_varlen): each sequence on
+# its slice, on the fused kernel where the shape allows
+
+def check_varlen_host(inp, heads=None, tag=""):
+    import torch
+    from paper_2405_21060_amd import ssd
+
+    p = inp.problem
+    seq = inp.seq_idx.reshape(-1)
+    starts = [0] + [int(v) for v in np.flatnonzero(np.diff(seq)) + 1] + [int(seq.size)]
+    announce("%s host offsets, %d sequences" % (tag, len(starts) - 1))
+    d = to_device(inp)
+    y, fin = ssd.forward_varlen(d["x"], d["dt"], d["A_log"], d["B"], d["C"], starts, D=d["D"],
+                                chunk_size=p.chunk_size, initial_states=d["initial_states"])
+    torch.cuda.synchronize()
+    y_ref, fin_ref = oracle.forward_inputs(inp, heads=heads)
+    y_gpu, fin_gpu = to_f64(y), fin.cpu().numpy().astype(np.float64)
+    if heads is not None:
+        y_gpu, fin_gpu = y_gpu[:, :, heads], fin_gpu[:, heads]
+    ey, ef = rel_err(y_gpu, y_ref), rel_err(fin_gpu, fin_ref)
+    announce("  rel err y %.3e final %.3e (tol %.0e)" % (ey, ef, TOL[p.dtype]))
+    assert ey <= TOL[p.dtype] and ef <= TOL[p.dtype], (ey, ef)
+
+
+def test_varlen_host_offsets_small():
+    p = Problem(1, 3000, 8, 64, 128, 4, 256, "bf16", varlen=True, len_lo=1, len_hi=700, init_states=True)
+    check_varlen_host(make_inputs(p, 9), tag="varlen_bf16_small")
+    p = Problem(1, 700, 4, 32, 64, 2, 64, "f32", varlen=True, len_lo=1, len_hi=200, init_states=True)
+    check_varlen_host(make_inputs(p, 4), tag="varlen_f32_small")
+
+
+def test_varlen_host_offsets_full_size():
+    p = WORKLOADS["varlen_g8"]
+    inp = make_inputs(p, 0)
+    heads = sorted({0, 1, p.nheads // 2, p.nheads // 2 + 1, p.nheads - 1})
+    check_varlen_host(inp, heads=heads, tag="varlen_g8")
