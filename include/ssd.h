@@ -1,5 +1,6 @@
 /*
- * ssd.h -- C ABI of the MI355X (gfx950) SSD layer forward.
+ * ssd.h -- C ABI of the MI355X (gfx950) SSD layer: forward, decode step,
+ * block steps, span state passing, and gradients.
  *
  * Computes y = SSM(A, B, C)(x) for the scalar-transition selective SSM of the
  * SSD layer (Section 5 of "Transformers are SSMs"), by the chunked block
