@@ -491,7 +491,7 @@ def cp_bench(args, torch, ssd):
     """One rank's share of an 8-way sequence split of the 2.7B layer (512 of
     4096 tokens per batch row): the layer from a zero state on the span, the
     span decay and the correction by the state entering the span (the
-    exchange of (decay, state) pairs between GPUs is not part of this build;
+    exchange of (decay, state) pairs between GPUs is not implemented here;
     the combine of all 8 pairs runs here on one GPU and is timed apart)."""
     from paper_2405_21060_amd.inputs import Problem, make_inputs
     from tests.ssd_harness import to_device
@@ -592,7 +592,7 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (--gpus 1); the sequence/head "
+        print("bench.py: runs on one GPU only (--gpus 1); the sequence/head "
               "sharding across GPUs is designed but not built", file=sys.stderr)
         sys.exit(2)
 
