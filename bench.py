@@ -64,8 +64,7 @@ def kernel_sources_digest(sources=FWD_SOURCES):
 
 
 def dominant_kernel_name(p):
-    fused = (p.dtype == "bf16" and not p.varlen and p.headdim == 64 and p.chunk_size == 256
-             and p.dstate in (64, 128))
+    fused = (p.dtype == "bf16" and p.headdim == 64 and p.chunk_size == 256 and p.dstate in (64, 128))
     return ("k_fused_main<%d>" % p.dstate) if fused else "k_chunk_output"
 
 

@@ -33,7 +33,9 @@
  * arithmetic accumulates in float32; y is rounded to dtype (nearest even).
  *
  * seq_idx contract (not checked on the device): non-decreasing, starting at 0,
- * consecutive ids, last value nseq - 1; batch must be 1.
+ * consecutive ids, last value nseq - 1; batch must be 1.  Ids that break it
+ * give unspecified values in y and final_states but no access outside the
+ * buffers described here.
  *
  * Ownership: every pointer is device memory owned by the caller; the library
  * allocates nothing on the call path.  `workspace` is caller-provided device
@@ -91,7 +93,10 @@ typedef struct {
 } ssd_problem;
 
 /* Workspace size in bytes for `prob` (Section 6 intermediates: chunk cumsums,
- * chunk states).  Returns SSD_OK and writes *bytes, or a validation error. */
+ * chunk states, the packed row's chunk table).  The size covers calls with and
+ * without seq_idx; with batch 1 it depends on prob->nseq, so size it with the
+ * nseq the call will pass.  Returns SSD_OK and writes *bytes, or a validation
+ * error. */
 int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes);
 
 /* The SSD forward (Section 6 algorithm; definition above).  `D`,

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -111,6 +112,17 @@ WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int
 
 }  // namespace ssd
 
+namespace {
+
+// A packed row (seq_idx) runs through the fused kernels when it is one row of
+// at most 2^31 - 1 tokens and nseq is valid.
+bool fused_packed_ok(const ssd_problem* prob)
+{
+    return prob->batch == 1 && prob->nseq >= 1 && prob->nseq <= prob->seqlen && prob->seqlen <= INT32_MAX;
+}
+
+}  // namespace
+
 extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
 {
     if (!bytes) return SSD_ERR_NULL_ARG;
@@ -118,8 +130,10 @@ extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
     const int rc = ssd::validate(prob, /*has_seq_idx=*/false, &s);  // size does not depend on it
     if (rc != SSD_OK) return rc;
     size_t need = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC).total;
-    if (ssd::fused_supported(s.P, s.N, s.Q, s.bf16, false)) {
-        const size_t f = ssd::fused_layout(s.b, s.H, s.N, s.G, s.nC).total;
+    if (ssd::fused_supported(s.P, s.N, s.Q, s.bf16)) {
+        size_t f = ssd::fused_layout(s.b, s.T, s.H, s.N, s.G, s.nC, 0).total;
+        // a packed row of prob->nseq sequences (when seq_idx is passed) needs its chunk table
+        if (fused_packed_ok(prob)) f = std::max(f, ssd::fused_layout(1, s.T, s.H, s.N, s.G, s.nC, prob->nseq).total);
         if (f > need) need = f;
     }
     *bytes = need;
@@ -183,8 +197,9 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
     const bool post = gn.z || gn.group > 0;
     const char* path = std::getenv("SSD_PATH");  // debug knob: "unfused" forces the step-by-step kernels
     const bool force_unfused = path && path[0] == 'u';
-    if (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16, seq_idx != nullptr)) {
-        const ssd::FusedLayout fw = ssd::fused_layout(s.b, s.H, s.N, s.G, s.nC);
+    if (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16) && (!seq_idx || fused_packed_ok(prob))) {
+        const int64_t nseq = seq_idx ? s.nseq : 0;
+        const ssd::FusedLayout fw = ssd::fused_layout(s.b, s.T, s.H, s.N, s.G, s.nC, nseq);
         ssd::FusedParams f;
         f.b = s.b;
         f.T = s.T;
@@ -192,12 +207,12 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.P = s.P;
         f.N = s.N;
         f.G = s.G;
-        f.nC = s.nC;
+        f.nC = fw.nC;
         int dev = 0, cus = 256;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
             return SSD_ERR_LAUNCH;
-        f.HG = ssd::heads_per_workgroup(s.H / s.G, s.nC * s.b * s.G, cus);
+        f.HG = ssd::heads_per_workgroup(s.H / s.G, fw.nC * s.b * s.G, cus);
         f.x = x;
         f.dt = dt;
         f.A_log = A_log;
@@ -213,6 +228,14 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.ring = reinterpret_cast<float*>(base + fw.ring);
         f.flags = reinterpret_cast<int*>(base + fw.flags);
         f.ticket = reinterpret_cast<int*>(base + fw.ticket);
+        f.ring_rows = fw.ring_rows;
+        if (seq_idx) {
+            f.seq_idx = seq_idx;
+            f.nseq = nseq;
+            f.starts = reinterpret_cast<int*>(base + fw.starts);
+            f.vtab = reinterpret_cast<int4*>(base + fw.vtab);
+            f.vcount = f.ticket + 2;
+        }
         f.dtx = dtx;
         // The chunk kernel gates, and normalises one-head groups, in its output
         // stage.  Wider groups take one more pass, which then also gates (z is

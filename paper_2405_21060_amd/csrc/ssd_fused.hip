@@ -45,6 +45,7 @@
 // Two ring slots suffice: chunk c+2 overwrites the slot of chunk c only after
 // reading the state of chunk c+1, which chunk c+1 published only after it had
 // read (consumed) the state of chunk c.
+#include <algorithm>
 #include <cstdlib>
 #include <utility>
 
@@ -187,6 +188,78 @@ struct PrepSmem {
 // {z, 7 - z, 8 + z, 15 - z} on MFMA (34 tiles, two wavefronts per row); a
 // quarter of B^T from LDS; z == 0 also zeroes the flags of (b, c, g) and, once,
 // the ticket counter.
+// ---------------------------------------------------------------------------
+// packed row: the chunk table (Section 8.3: sequences packed into one row, the
+// state reset at every sequence start)
+// ---------------------------------------------------------------------------
+// First token of every sequence: where seq_idx changes (ids outside [0, nseq)
+// are ignored; the caller guarantees ids 0 .. nseq-1 in order).
+__global__ __launch_bounds__(256) void k_seq_starts(const int32_t* __restrict__ seq_idx, int T, int nseq,
+                                                    int* __restrict__ starts)
+{
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t == 0) starts[nseq] = T;
+    if (t >= T) return;
+    const int v = seq_idx[t];
+    if ((t == 0 || seq_idx[t - 1] != v) && v >= 0 && v < nseq) starts[v] = t;
+}
+
+constexpr int kTabThreads = 1024;
+
+// Exclusive prefix sum over the workgroup (kTabThreads lanes), plus the total.
+__device__ long long block_exclusive_sum(long long v, long long* s_w, long long* total)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    long long inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const long long u = __shfl_up(inc, d);
+        if (lane >= d) inc += u;
+    }
+    if (lane == 63) s_w[w] = inc;
+    __syncthreads();
+    long long before = 0, all = 0;
+    for (int k = 0; k < kTabThreads / 64; ++k) {
+        before += k < w ? s_w[k] : 0;
+        all += s_w[k];
+    }
+    __syncthreads();   // s_w is reused by the next call
+    *total = all;
+    return before + inc - v;
+}
+
+// The chunks of every sequence, in token order (one workgroup): sequence r
+// of length len gives ceil(len / Q) chunks from its first token on.  Every
+// entry stays inside [0, T) and the table's capacity whatever the ids hold.
+__global__ __launch_bounds__(kTabThreads) void k_seq_chunks(const int* __restrict__ starts, int T, int nseq,
+                                                            int cap, int ring_cap, int4* __restrict__ vtab,
+                                                            int* __restrict__ vcount)
+{
+    __shared__ long long s_w[kTabThreads / 64];
+    // 64-bit sums: ids that break the contract may describe more chunks than T
+    long long base = 0, rbase = 0;
+    for (int r0 = 0; r0 < nseq; r0 += kTabThreads) {
+        const int r = r0 + static_cast<int>(threadIdx.x);
+        int st = 0, len = 0;
+        if (r < nseq) {
+            st = min(max(starts[r], 0), T);
+            len = min(max(starts[r + 1], st), T) - st;
+        }
+        const int nch = len / kQ + (len % kQ != 0 ? 1 : 0);
+        long long tot = 0, rtot = 0;
+        const long long v0 = base + block_exclusive_sum(nch, s_w, &tot);
+        const long long rr = rbase + block_exclusive_sum(nch > 1 ? 1 : 0, s_w, &rtot);
+        const int ring = static_cast<int>(rr < ring_cap ? rr : ring_cap - 1);
+        for (int k = 0; k < nch && v0 + k < cap; ++k) {
+            const int flags = (k == 0 ? 1 : 0) | (k == nch - 1 ? 2 : 0) | (ring << 2);
+            vtab[v0 + k] = make_int4(st + k * kQ, min(kQ, len - k * kQ), r, flags);
+        }
+        base += tot;
+        rbase += rtot;
+    }
+    if (threadIdx.x == 0) *vcount = static_cast<int>(base < cap ? base : cap);
+}
+
 template <int N>
 __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
 {
@@ -197,20 +270,24 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
     const int part = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t c0 = static_cast<int64_t>(c) * kQ;
-    const int L = static_cast<int>(kQ < p.T - c0 ? kQ : p.T - c0);
     const int hpg = static_cast<int>(p.H / p.G);
+    if (part == 0 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
+        p.ticket[0] = 0;
+        p.ticket[1] = 0;  // error word: set when a state wait times out
+    }
+    int64_t c0 = static_cast<int64_t>(c) * kQ;
+    int L = static_cast<int>(kQ < p.T - c0 ? kQ : p.T - c0);
+    if (p.vtab) {   // packed row: chunk c of the table (entries past its end: nothing to do)
+        if (c >= *p.vcount) return;
+        const int4 e = p.vtab[c];
+        c0 = e.x;
+        L = e.y;
+    }
 
-
-    // ---- flags of this (batch, chunk) and group, and the ticket counter
-    if (part == 0) {
+    // ---- flags of this (batch, chunk) and group
+    if (part == 0)
         for (int hh = tid; hh < hpg; hh += kPrepThreads)
             p.flags[(static_cast<int64_t>(b) * p.H + g * hpg + hh) * p.nC + c] = 0;
-        if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
-            p.ticket[0] = 0;
-            p.ticket[1] = 0;  // error word: set when a state wait times out
-        }
-    }
     // t-tile rows of this part (balanced: 34 tiles)
     const int rows[4] = {part, 7 - part, 8 + part, kNQ - 1 - part};
 
@@ -486,7 +563,9 @@ __device__ __forceinline__ void diag_block(int wave, const char* xsb, const int*
 // One work item of the chunk kernel: (chunk, batch row, group of HG heads).
 struct Item {
     int c, b, h0, g, L;
+    int seq, ring;       // row of the initial / final states, row of the state ring
     int64_t c0;
+    int64_t rows;        // tokens readable from c0 on (the rest of the row or sequence)
     const u16* xchunk;   // x at token c0, head 0
     const u16* cchunk;   // C at token c0, group g
     bool has_prev, has_next;
@@ -499,12 +578,26 @@ __device__ __forceinline__ Item decode_item(const FusedParams& p, int work, int 
     it.b = (work % per_c) / nHG;
     it.h0 = (work % nHG) * static_cast<int>(p.HG);
     it.g = it.h0 / static_cast<int>(p.H / p.G);
-    it.c0 = static_cast<int64_t>(it.c) * kQ;
-    it.L = static_cast<int>(kQ < p.T - it.c0 ? kQ : p.T - it.c0);
+    if (p.vtab) {   // packed row (batch 1): chunk it.c of the sequence chunk table
+        const int4 e = p.vtab[it.c];
+        it.c0 = e.x;
+        it.L = e.y;
+        it.rows = e.y;
+        it.seq = e.z;
+        it.ring = e.w >> 2;
+        it.has_prev = (e.w & 1) == 0;
+        it.has_next = (e.w & 2) == 0;
+    } else {
+        it.c0 = static_cast<int64_t>(it.c) * kQ;
+        it.L = static_cast<int>(kQ < p.T - it.c0 ? kQ : p.T - it.c0);
+        it.rows = p.T - it.c0;
+        it.seq = it.b;
+        it.ring = it.b;
+        it.has_prev = it.c > 0;
+        it.has_next = it.c + 1 < p.nC;
+    }
     it.xchunk = static_cast<const u16*>(p.x) + (static_cast<int64_t>(it.b) * p.T + it.c0) * p.H * kP;
     it.cchunk = static_cast<const u16*>(p.C) + ((static_cast<int64_t>(it.b) * p.T + it.c0) * p.G + it.g) * N;
-    it.has_prev = it.c > 0;
-    it.has_next = it.c + 1 < p.nC;
     return it;
 }
 
@@ -566,7 +659,7 @@ __device__ __forceinline__ DmaOffsets dma_offsets(const FusedParams& p, int wave
 __device__ __forceinline__ void dma_head(const FusedParams& p, const Item& it, int hh, u16* xdst, int wave,
                                          const DmaOffsets& o)
 {
-    const i32x4 xrs = buffer_rsrc(it.xchunk, (p.T - it.c0) * p.H * kP * 2);
+    const i32x4 xrs = buffer_rsrc(it.xchunk, it.rows * p.H * kP * 2);
     const int hoff = hh * kP * 2;
 #pragma unroll
     for (int i = 0; i < 4; ++i) copy16_to_lds(xrs, xdst + (4 * wave + i) * 512, o.x[i], hoff);
@@ -580,7 +673,7 @@ __device__ __forceinline__ void dma_z_strips(const FusedParams& p, const Item& i
                                              const int* strip, int lane)
 {
     const u16* zchunk = static_cast<const u16*>(p.z) + (static_cast<int64_t>(it.b) * p.T + it.c0) * p.H * kP;
-    const i32x4 zrs = buffer_rsrc(zchunk, (p.T - it.c0) * p.H * kP * 2);
+    const i32x4 zrs = buffer_rsrc(zchunk, it.rows * p.H * kP * 2);
     const int row_bytes = static_cast<int>(p.H * kP * 2);
 #pragma unroll
     for (int k4 = 0; k4 < 2; ++k4)
@@ -815,7 +908,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 
 
     // ---- centre factor: state entering the chunk, state leaving it ----------
-    float* ring_h = p.ring + (static_cast<int64_t>(b) * p.H + h) * 2 * PN;
+    float* ring_h = p.ring + (static_cast<int64_t>(it.ring) * p.H + h) * 2 * PN;
     const __amdgpu_buffer_rsrc_t ring_rs =
         __builtin_amdgcn_make_buffer_rsrc(ring_h, 0, static_cast<int>(2 * PN * sizeof(float)), 0x00020000);
     const int frag_base = wave * PTW * 64 + lane;   // private ring layout: [wave][frag][lane][4]
@@ -851,7 +944,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     } else if (p.init) {
         // (P, N) layout of the caller's initial state: lane offset + uniform row offsets
         const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<float*>(p.init + (static_cast<int64_t>(b) * p.H + h) * PN), 0,
+            const_cast<float*>(p.init + (static_cast<int64_t>(it.seq) * p.H + h) * PN), 0,
             static_cast<int>(PN * sizeof(float)), 0x00020000);
         const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
 #pragma unroll
@@ -882,7 +975,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         }
     } else if (p.fin) {
         const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
-            p.fin + (static_cast<int64_t>(b) * p.H + h) * PN, 0,
+            p.fin + (static_cast<int64_t>(it.seq) * p.H + h) * PN, 0,
             static_cast<int>(PN * sizeof(float)), 0x00020000);
         const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
 #pragma unroll
@@ -1053,7 +1146,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nHG = static_cast<int>(p.H / p.HG);
     const int per_c = static_cast<int>(p.b) * nHG;
-    const int nwork = static_cast<int>(p.nC) * per_c;
+    const int nwork = (p.vtab ? *p.vcount : static_cast<int>(p.nC)) * per_c;
     const DmaOffsets dmo = dma_offsets(p, wave, lane);
     const int ntw = (PTW == 4) ? wave : (wave & 3);
     const int strip[2] = {wave, kNQ - 1 - wave};
@@ -1104,6 +1197,13 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
 template <int N>
 hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
+    if (p.seq_idx) {   // packed row: the chunk table first
+        const int T = static_cast<int>(p.T), nseq = static_cast<int>(p.nseq);
+        hipLaunchKernelGGL(k_seq_starts, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream,
+                           p.seq_idx, T, nseq, p.starts);
+        hipLaunchKernelGGL(k_seq_chunks, dim3(1), dim3(kTabThreads), 0, stream, p.starts, T, nseq,
+                           static_cast<int>(p.nC), static_cast<int>(p.ring_rows), p.vtab, p.vcount);
+    }
     const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), kGramParts);
     hipLaunchKernelGGL(k_fused_prep<N>, g_prep, dim3(kPrepThreads), 0, stream, p);
     hipError_t err = hipGetLastError();
@@ -1130,26 +1230,35 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
 
 }  // namespace
 
-bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16, bool varlen)
+bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16)
 {
-    return bf16 && !varlen && P == kP && Q == kQ && (N == 64 || N == 128);
+    return bf16 && P == kP && Q == kQ && (N == 64 || N == 128);
 }
 
-FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC)
+FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, int64_t nC, int64_t nseq)
 {
     auto al = [](size_t v) { return (v + 255) / 256 * 256; };
     FusedLayout w;
+    // A packed row cut at its sequence starts has at most nC + nseq - 1 chunks
+    // (and no more than T); only sequences longer than one chunk pass a state
+    // between chunks, and there are fewer of them than chunks.
+    w.nC = nseq > 0 ? std::min(nC + nseq - 1, T) : nC;
+    w.ring_rows = nseq > 0 ? std::min(nseq, nC) : b;
     size_t off = 0;
     w.gram = off;
-    off = al(off + sizeof(u16) * static_cast<size_t>(b * G * nC) * kTiles * 256);
+    off = al(off + sizeof(u16) * static_cast<size_t>(b * G * w.nC) * kTiles * 256);
     w.BT = off;
-    off = al(off + sizeof(u16) * static_cast<size_t>(b * G * nC) * static_cast<size_t>(N * kQ));
+    off = al(off + sizeof(u16) * static_cast<size_t>(b * G * w.nC) * static_cast<size_t>(N * kQ));
     w.ring = off;
-    off = al(off + sizeof(float) * static_cast<size_t>(b * H) * 2 * kP * static_cast<size_t>(N));
+    off = al(off + sizeof(float) * static_cast<size_t>(w.ring_rows * H) * 2 * kP * static_cast<size_t>(N));
     w.flags = off;
-    off = al(off + sizeof(int) * static_cast<size_t>(b * H * nC));
+    off = al(off + sizeof(int) * static_cast<size_t>(b * H * w.nC));
     w.ticket = off;
-    off = al(off + 2 * sizeof(int));
+    off = al(off + 4 * sizeof(int));   // ticket, error word, table entries
+    w.starts = off;
+    off = al(off + sizeof(int) * static_cast<size_t>(nseq > 0 ? nseq + 1 : 0));
+    w.vtab = off;
+    off = al(off + sizeof(int4) * static_cast<size_t>(nseq > 0 ? w.nC : 0));
     w.total = off;
     return w;
 }

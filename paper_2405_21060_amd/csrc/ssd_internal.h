@@ -71,6 +71,17 @@ struct FusedParams {
     int* flags;       // (b, H, nC)      state-published flags
     int* ticket;      // [0] work ticket, [1] wait-timeout error word
     DtTransform dtx;
+    // Packed row (batch 1) with device seq_idx: every sequence is cut into
+    // chunks of its own (the last one partial), listed in token order in a
+    // device table that k_seq_chunks builds; nC is then the table's capacity.
+    // Null seq_idx: plain rows, chunk c of row b at token c Q.
+    const int32_t* seq_idx = nullptr;  // (T)
+    int64_t nseq = 0;
+    int* starts = nullptr;             // (nseq + 1) first token of each sequence, then T
+    int4* vtab = nullptr;              // (nC) {first token, length, sequence, bit 0 first chunk of
+                                       //  its sequence | bit 1 last | ring row << 2}
+    int* vcount = nullptr;             // [0] table entries
+    int64_t ring_rows = 0;             // sequences of more than one chunk that the ring holds
     // gate / per-head normalisation in the output stage (null: none)
     const void* z = nullptr;             // (b, T, H, P) bf16
     const float* norm_weight = nullptr;  // (H * P), with norm_head
@@ -79,12 +90,16 @@ struct FusedParams {
 };
 
 struct FusedLayout {
-    size_t gram, BT, ring, flags, ticket, total;
+    size_t gram, BT, ring, flags, ticket, starts, vtab, total;
+    int64_t nC;          // chunks the layout holds (table capacity for a packed row)
+    int64_t ring_rows;   // rows of the state ring
 };
 
 int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units);
-bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16, bool varlen);
-FusedLayout fused_layout(int64_t b, int64_t H, int64_t N, int64_t G, int64_t nC);
+bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16);
+// nseq > 0: layout for one packed row of nseq sequences (seq_idx); nC is the
+// row's chunk count ceil(T / Q) either way.
+FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, int64_t nC, int64_t nseq);
 hipError_t launch_fused(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin,
                         hipEvent_t ev_end);
 

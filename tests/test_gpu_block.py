@@ -76,6 +76,9 @@ SHAPES = {
     # fused path: bf16, P 64, N 128 / 64, Q 256; ragged T, several chunks and items
     "fused_n128": Problem(2, 600, 8, 64, 128, 1, 256, "bf16", init_states=True),
     "fused_n64_g2": Problem(1, 700, 4, 64, 64, 2, 256, "bf16"),
+    # fused path on a packed row (the device chunk table), short and long sequences
+    "fused_varlen": Problem(1, 1500, 8, 64, 128, 2, 256, "bf16", varlen=True, len_lo=1, len_hi=700,
+                            init_states=True),
     # general path: fp32, and packed variable-length rows
     "general_f32": Problem(1, 200, 4, 16, 16, 2, 64, "f32", init_states=True),
     "general_varlen": Problem(1, 1500, 4, 32, 32, 2, 128, "bf16", varlen=True, len_lo=100,

@@ -100,6 +100,76 @@ def test_varlen_bf16_small():
     check(make_inputs(p, 9), tag="varlen_bf16_small")
 
 
+# ---- packed rows given by the device seq_idx on the fused kernels: every
+# sequence cut into chunks of its own (the last one partial) from a chunk table
+# built on the device
+def _packed(lens, H, N, G, seed, init=True):
+    T = int(sum(lens))
+    p = Problem(1, T, H, 64, N, G, 256, "bf16", varlen=True, init_states=init)
+    inp = make_inputs(p, seed)
+    inp.seq_idx = np.repeat(np.arange(len(lens), dtype=np.int32), lens).reshape(1, T)
+    inp.nseq = len(lens)
+    if init:
+        inp.initial_states = np.random.default_rng(seed + 1).standard_normal(
+            (len(lens), H, 64, N)).astype(np.float32)
+    else:
+        inp.initial_states = None
+    return inp
+
+
+@pytest.mark.parametrize("lens,H,N,G", [
+    # one-token sequences, lengths at and around the chunk length, several
+    # sequences inside one chunk, a sequence over three chunks
+    ([1, 255, 256, 257, 1, 513, 2, 700, 3], 6, 64, 2),
+    ([300, 1, 1, 1, 40, 600, 256], 4, 128, 1),
+    # one sequence only, shorter than a chunk
+    ([200], 2, 128, 1),
+])
+def test_fused_packed_rows(lens, H, N, G):
+    inp = _packed(lens, H, N, G, 31)
+    check(inp, tag="fused_packed")
+    check(inp, use_init=False, tag="fused_packed_noinit")
+
+
+def test_fused_packed_many_sequences():
+    """More sequences than the table kernel's workgroup has lanes (1,024), and
+    more sequences than chunks."""
+    lens = np.random.default_rng(5).integers(1, 4, 1500).tolist() + [600, 900]
+    check(_packed(lens, 2, 64, 1, 17), tag="fused_packed_1502_sequences")
+
+
+@pytest.mark.parametrize("hg", ["1", "4"])
+def test_fused_packed_persistent_items(monkeypatch, hg):
+    """Few persistent workgroups taking many table entries each."""
+    monkeypatch.setenv("SSD_MAX_WORKGROUPS", "3")
+    monkeypatch.setenv("SSD_HEADS_PER_WG", hg)
+    check(_packed([700, 30, 1, 900, 256, 513], 8, 128, 1, 19), tag="fused_packed_persistent_hg" + hg)
+
+
+def test_fused_packed_one_sequence_equals_plain_row():
+    """seq_idx all zero (one sequence) gives exactly the plain row's result:
+    the same chunks, the same arithmetic."""
+    import torch
+
+    inp = _packed([1300], 8, 128, 2, 23)
+    y1, f1 = run_gpu(inp)
+    plain = _packed([1300], 8, 128, 2, 23)
+    plain.seq_idx = None
+    y2, f2 = run_gpu(plain)
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    assert torch.equal(f1, f2)
+
+
+def test_packed_rows_both_device_paths(monkeypatch):
+    """The general kernels (forced) and the fused ones on one packed row, each
+    against the oracle."""
+    inp = _packed([100, 400, 1, 256, 800], 4, 128, 2, 29)
+    monkeypatch.setenv("SSD_PATH", "unfused")
+    check(inp, tag="packed_general_forced")
+    monkeypatch.delenv("SSD_PATH")
+    check(inp, tag="packed_fused")
+
+
 @pytest.mark.parametrize("shape", [
     # (batch, T, H, N, G): ragged last chunk, N = 64, 3 heads per group (1 head per workgroup)
     (2, 700, 6, 64, 2),
