@@ -79,6 +79,9 @@ constexpr int64_t kMaxElemsPublic = kMaxElems;
 // best at the 130M and 2.7B layer shapes), else the largest that leaves one,
 // else 1.  SSD_HEADS_PER_WG overrides it
 // (tuning knob; ignored unless it divides the heads per group).
+// chunks in flight from which a chunk's state flag is set early (see forward_impl)
+constexpr int64_t kEarlyFlagChunks = 8;
+
 int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units)
 {
     if (const char* env = std::getenv("SSD_HEADS_PER_WG")) {
@@ -213,6 +216,12 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
             return SSD_ERR_LAUNCH;
         f.HG = ssd::heads_per_workgroup(s.H / s.G, fw.nC * s.b * s.G, cus);
+        // Chunks of one chain the chip holds at once: with many of them the
+        // chain's latency bounds the launch, and each chunk publishes its state
+        // before its left factor.  SSD_EARLY_FLAG=0/1 overrides (measurement knob).
+        const int64_t per_chunk = s.b * (s.H / f.HG);
+        f.early_flag = cus >= ssd::kEarlyFlagChunks * per_chunk ? 1 : 0;
+        if (const char* ef = std::getenv("SSD_EARLY_FLAG")) f.early_flag = ef[0] == '1' ? 1 : 0;
         f.x = x;
         f.dt = dt;
         f.A_log = A_log;

@@ -260,7 +260,8 @@ __global__ __launch_bounds__(kTabThreads) void k_seq_chunks(const int* __restric
     if (threadIdx.x == 0) *vcount = static_cast<int>(base < cap ? base : cap);
 }
 
-template <int N>
+// PACKED: a packed row, chunk positions from the chunk table.
+template <int N, bool PACKED>
 __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
 {
     constexpr int RS = N + 8;
@@ -277,7 +278,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
     }
     int64_t c0 = static_cast<int64_t>(c) * kQ;
     int L = static_cast<int>(kQ < p.T - c0 ? kQ : p.T - c0);
-    if (p.vtab) {   // packed row: chunk c of the table (entries past its end: nothing to do)
+    if constexpr (PACKED) {   // packed row: chunk c of the table (entries past its end: nothing to do)
         if (c >= *p.vcount) return;
         const int4 e = p.vtab[c];
         c0 = e.x;
@@ -571,6 +572,7 @@ struct Item {
     bool has_prev, has_next;
 };
 
+template <bool PACKED>
 __device__ __forceinline__ Item decode_item(const FusedParams& p, int work, int per_c, int nHG, int N)
 {
     Item it;
@@ -578,7 +580,7 @@ __device__ __forceinline__ Item decode_item(const FusedParams& p, int work, int 
     it.b = (work % per_c) / nHG;
     it.h0 = (work % nHG) * static_cast<int>(p.HG);
     it.g = it.h0 / static_cast<int>(p.H / p.G);
-    if (p.vtab) {   // packed row (batch 1): chunk it.c of the sequence chunk table
+    if constexpr (PACKED) {   // packed row (batch 1): chunk it.c of the sequence chunk table
         const int4 e = p.vtab[it.c];
         it.c0 = e.x;
         it.L = e.y;
@@ -756,7 +758,7 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
 // parameter: the compiler then knows that the asynchronous copies into the
 // next head's buffers (and the next item's Gram tiles) never alias the buffers
 // read here, and does not make those reads wait for the copies.
-template <int N>
+template <int N, bool PACKED, bool EARLY>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
                                           uint2 (&btf)[kQ / 32][2], uint4 (&cf)[2][N / 32],
@@ -805,7 +807,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         dma_head(p, it, h + 1, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, it, h + 1, tid);
     } else if (hk > 0 && next < nwork) {
-        const Item nit = decode_item(p, next, per_c, nHG, N);
+        const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
         dma_head(p, nit, nit.h0, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
     }
@@ -856,7 +858,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // Gram rows it has just finished with (no other wavefront reads them) for
     // the next item, well ahead of that item's diagonal block.
     const bool gram_early = last && hk > 0 && next < nwork;
-    if (gram_early) dma_gram_rows(gr, p, decode_item(p, next, per_c, nHG, N), wave, lane);
+    if (gram_early) dma_gram_rows(gr, p, decode_item<PACKED>(p, next, per_c, nHG, N), wave, lane);
     // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
     // after the right factor)
 #pragma unroll
@@ -991,8 +993,16 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
     // The state stores drain while the left factor runs; the flag is set after
     // the epilogue's barrier, once every wavefront has waited for its stores.
+    // Where the chain of chunks is what bounds the launch (early_flag), every
+    // wavefront waits for its stores here instead and the flag follows this
+    // barrier, so the next chunk need not wait for this one's left factor.
+    // (EARLY: a template parameter, so that the other launches carry none of it.)
     if (norm && tid < kP) wn[tid] = wreg;
+    if constexpr (EARLY) wait_vmem();
     lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
+    if (EARLY && tid == 0 && has_next)
+        __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (hk == 0) next = *tk;
     // The next item's Gram tiles (and, with one head per item, its first head's
     // x): only the bf16 state and z are read from here on.
@@ -1000,7 +1010,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // and its first head's x follow now, by all wavefronts.)
     const bool gram_ahead = last && hk == 0 && next < nwork;
     if (gram_ahead) {
-        const Item nit = decode_item(p, next, per_c, nHG, N);
+        const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
         dma_gram(gr, p, nit, wave, dmo);
         dma_head(p, nit, nit.h0, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
@@ -1090,7 +1100,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             }
         }
         lds_barrier();
-        if (tid == 0 && has_next)
+        if (!EARLY && tid == 0 && has_next)
             __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
@@ -1114,7 +1124,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // behind us), requested after the waits above so that none of those waits
     // for them.
     if (last && next < nwork) {
-        const Item nit = decode_item(p, next, per_c, nHG, N);
+        const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
         load_bt<N>(p, nit, ntw, r, lg, btf);
         load_c<N>(p, nit, strip, r, lg, cf);
     }
@@ -1124,7 +1134,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 
 // A_log, D and the dt bias come as separate read-only arguments so that their per-head values
 // are scalar loads (a vector load would wait behind the outstanding copies).
-template <int N>
+template <int N, bool PACKED, bool EARLY>
 __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, const float* __restrict__ A_logp,
                                                                 const float* __restrict__ Dp,
                                                                 const float* __restrict__ biasp)
@@ -1146,7 +1156,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nHG = static_cast<int>(p.H / p.HG);
     const int per_c = static_cast<int>(p.b) * nHG;
-    const int nwork = (p.vtab ? *p.vcount : static_cast<int>(p.nC)) * per_c;
+    const int nwork = (PACKED ? *p.vcount : static_cast<int>(p.nC)) * per_c;
     const DmaOffsets dmo = dma_offsets(p, wave, lane);
     const int ntw = (PTW == 4) ? wave : (wave & 3);
     const int strip[2] = {wave, kNQ - 1 - wave};
@@ -1161,7 +1171,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     int work = sm.ticket;
     if (work >= nwork) return;
     {
-        const Item it = decode_item(p, work, per_c, nHG, N);
+        const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
         dma_gram(s_gr, p, it, wave, dmo);
         dma_head(p, it, it.h0, sm.XS[0], wave, dmo);
         if (tid < kQ) dtr = load_dt(p, it, it.h0, tid);
@@ -1176,15 +1186,15 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     uint2 btf[kQ / 32][2];
     uint4 cf[2][KN];   // raw bf16 (as a bf16 vector type the compiler merges lanes right at the loads)
     {
-        const Item it = decode_item(p, work, per_c, nHG, N);
+        const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
         load_bt<N>(p, it, ntw, r, lg, btf);
         load_c<N>(p, it, strip, r, lg, cf);
     }
     for (;;) {
-    const Item it = decode_item(p, work, per_c, nHG, N);
+    const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
     int next = nwork;
     for (int hk = 0; hk < p.HG; ++hk) {
-        head_step<N>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
+        head_step<N, PACKED, EARLY>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
                      sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp,
                      biasp, sm.wn);
         q ^= 1;
@@ -1205,7 +1215,10 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
                            static_cast<int>(p.nC), static_cast<int>(p.ring_rows), p.vtab, p.vcount);
     }
     const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), kGramParts);
-    hipLaunchKernelGGL(k_fused_prep<N>, g_prep, dim3(kPrepThreads), 0, stream, p);
+    if (p.vtab)
+        hipLaunchKernelGGL((k_fused_prep<N, true>), g_prep, dim3(kPrepThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL((k_fused_prep<N, false>), g_prep, dim3(kPrepThreads), 0, stream, p);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess && ev_begin) err = hipEventRecord(ev_begin, stream);
     if (err != hipSuccess) return err;
@@ -1221,8 +1234,18 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
         const long v = std::strtol(cap, nullptr, 10);
         if (v >= 1 && v < grid) grid = v;
     }
-    hipLaunchKernelGGL(k_fused_main<N>, dim3(static_cast<unsigned>(grid)), dim3(kMainThreads), 0, stream, p,
-                       p.A_log, p.D, p.dtx.bias);
+    const dim3 g_main(static_cast<unsigned>(grid));
+    const float* A_logp = p.A_log;
+    const float* Dp = p.D;
+    const float* biasp = p.dtx.bias;
+    if (p.vtab && p.early_flag)
+        hipLaunchKernelGGL((k_fused_main<N, true, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+    else if (p.vtab)
+        hipLaunchKernelGGL((k_fused_main<N, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+    else if (p.early_flag)
+        hipLaunchKernelGGL((k_fused_main<N, false, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+    else
+        hipLaunchKernelGGL((k_fused_main<N, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;

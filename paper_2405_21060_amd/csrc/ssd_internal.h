@@ -82,6 +82,9 @@ struct FusedParams {
                                        //  its sequence | bit 1 last | ring row << 2}
     int* vcount = nullptr;             // [0] table entries
     int64_t ring_rows = 0;             // sequences of more than one chunk that the ring holds
+    // nonzero: a chunk's state flag is set as soon as its state is stored
+    // (before its left factor), for launches bound by the chain of chunks
+    int early_flag = 0;
     // gate / per-head normalisation in the output stage (null: none)
     const void* z = nullptr;             // (b, T, H, P) bf16
     const float* norm_weight = nullptr;  // (H * P), with norm_head
