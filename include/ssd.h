@@ -128,10 +128,11 @@ int ssd_forward_timed(const ssd_problem* prob,
  * offsets instead of the device seq_idx: seq_starts (host memory) holds nseq +
  * 1 token offsets, seq_starts[0] = 0, strictly increasing, seq_starts[nseq] =
  * seqlen (else SSD_ERR_BAD_SHAPE); token t belongs to sequence s when
- * seq_starts[s] <= t < seq_starts[s + 1].  Each sequence runs as a problem of
- * its own on its slice of the packed tensors (on the fused chunk kernel where
- * the shape allows), so the result equals ssd_forward with the matching
- * seq_idx.  initial_states / final_states are (nseq, nheads, headdim, dstate)
+ * seq_starts[s] <= t < seq_starts[s + 1].  At the fused kernels' shapes and
+ * up to 511 sequences the offsets are handed to the device by value and the
+ * row runs as one launch, as ssd_forward with seq_idx does; otherwise each
+ * sequence runs as a problem of its own on its slice of the packed tensors.
+ * Either way the result equals ssd_forward with the matching seq_idx.  initial_states / final_states are (nseq, nheads, headdim, dstate)
  * (either may be NULL).  Workspace: ssd_forward_varlen_workspace_bytes().
  * Errors as for ssd_forward. */
 int ssd_forward_varlen_workspace_bytes(const ssd_problem* prob, const int64_t* seq_starts, size_t* bytes);

@@ -177,17 +177,22 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
                  const float* A_log, const void* B, const void* C, const float* D,
                  const float* initial_states, const int32_t* seq_idx, void* y, float* final_states,
                  void* workspace, size_t workspace_bytes, void* stream, hipEvent_t ev_begin,
-                 hipEvent_t ev_end)
+                 hipEvent_t ev_end, const ssd::SeqStartsArg* arg_starts = nullptr)
 {
+    // arg_starts (a packed row by host offsets, instead of seq_idx): only on the
+    // fused path, which the caller has checked; the workspace is its layout
     ssd::Shape s;
-    int rc = ssd::validate(prob, seq_idx != nullptr, &s);
+    int rc = ssd::validate(prob, seq_idx != nullptr || arg_starts != nullptr, &s);
     if (rc != SSD_OK) return rc;
     if (!x || !dt || !A_log || !B || !C || !y) return SSD_ERR_NULL_ARG;
     ssd::DtTransform dtx;
     if (opts && (rc = validate_block(opts, s, y, &dtx)) != SSD_OK) return rc;
     size_t need = 0;
-    if (ssd_workspace_bytes(prob, &need) != SSD_OK || !workspace || workspace_bytes < need)
+    if (arg_starts)
+        need = ssd::fused_layout(1, s.T, s.H, s.N, s.G, s.nC, s.nseq).total;
+    else if (ssd_workspace_bytes(prob, &need) != SSD_OK)
         return SSD_ERR_WORKSPACE;
+    if (!workspace || workspace_bytes < need) return SSD_ERR_WORKSPACE;
     // output side of the block: gate and grouped normalisation
     ssd::GateNormParams gn;
     gn.rows = s.b * s.T;
@@ -200,8 +205,9 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
     const bool post = gn.z || gn.group > 0;
     const char* path = std::getenv("SSD_PATH");  // debug knob: "unfused" forces the step-by-step kernels
     const bool force_unfused = path && path[0] == 'u';
-    if (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16) && (!seq_idx || fused_packed_ok(prob))) {
-        const int64_t nseq = seq_idx ? s.nseq : 0;
+    if (arg_starts ||
+        (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16) && (!seq_idx || fused_packed_ok(prob)))) {
+        const int64_t nseq = seq_idx || arg_starts ? s.nseq : 0;
         const ssd::FusedLayout fw = ssd::fused_layout(s.b, s.T, s.H, s.N, s.G, s.nC, nseq);
         ssd::FusedParams f;
         f.b = s.b;
@@ -238,8 +244,9 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.flags = reinterpret_cast<int*>(base + fw.flags);
         f.ticket = reinterpret_cast<int*>(base + fw.ticket);
         f.ring_rows = fw.ring_rows;
-        if (seq_idx) {
+        if (seq_idx || arg_starts) {
             f.seq_idx = seq_idx;
+            f.arg_starts = arg_starts;
             f.nseq = nseq;
             f.starts = reinterpret_cast<int*>(base + fw.starts);
             f.vtab = reinterpret_cast<int4*>(base + fw.vtab);
@@ -810,15 +817,37 @@ namespace {
 // Packed rows with host offsets: the forward of each sequence on its slice of
 // the packed tensors (the fused kernel where the shape allows), one initial
 // and final state per sequence.
+// One launch over the whole packed row (the fused kernels' chunk table, the
+// offsets handed over by value) where the shape and the number of sequences
+// allow; else one call per sequence.  SSD_VARLEN_PER_SEQUENCE=1 forces the
+// latter (a test and measurement knob).
+bool varlen_one_launch(const ssd_problem* prob)
+{
+    const char* path = std::getenv("SSD_PATH");
+    const char* per = std::getenv("SSD_VARLEN_PER_SEQUENCE");
+    if ((path && path[0] == 'u') || (per && per[0] == '1')) return false;
+    ssd::Shape s;
+    if (ssd::validate(prob, true, &s) != SSD_OK) return false;
+    return ssd::fused_supported(s.P, s.N, s.Q, s.bf16) && fused_packed_ok(prob) && prob->nseq <= ssd::kArgSeqs;
+}
+
 int fwd_varlen_plan(const ssd_problem* prob, const int64_t* seq_starts, size_t* bytes)
 {
     if (!prob || !seq_starts) return SSD_ERR_NULL_ARG;
     if (prob->batch != 1) return SSD_ERR_SEQIDX_BATCH;
     if (prob->nseq < 1 || prob->nseq > prob->seqlen) return SSD_ERR_BAD_SHAPE;
     if (seq_starts[0] != 0 || seq_starts[prob->nseq] != prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    for (int64_t s = 0; s < prob->nseq; ++s)
+        if (seq_starts[s + 1] <= seq_starts[s]) return SSD_ERR_BAD_SHAPE;
+    if (varlen_one_launch(prob)) {
+        ssd::Shape sh;
+        const int rc = ssd::validate(prob, true, &sh);
+        if (rc != SSD_OK) return rc;
+        *bytes = ssd::fused_layout(1, sh.T, sh.H, sh.N, sh.G, sh.nC, sh.nseq).total;
+        return SSD_OK;
+    }
     size_t need = 0;
     for (int64_t s = 0; s < prob->nseq; ++s) {
-        if (seq_starts[s + 1] <= seq_starts[s]) return SSD_ERR_BAD_SHAPE;
         ssd_problem q = *prob;
         q.seqlen = seq_starts[s + 1] - seq_starts[s];
         size_t b = 0;
@@ -851,6 +880,13 @@ extern "C" int ssd_forward_varlen(const ssd_problem* prob, const int64_t* seq_st
     if ((rc = ssd::validate(prob, true, &s)) != SSD_OK) return rc;
     if (!x || !dt || !A_log || !B || !C || !y) return SSD_ERR_NULL_ARG;
     if (!workspace || workspace_bytes < need) return SSD_ERR_WORKSPACE;
+    if (varlen_one_launch(prob)) {
+        ssd::SeqStartsArg a;
+        a.n = static_cast<int>(prob->nseq);
+        for (int64_t q = 0; q <= prob->nseq; ++q) a.v[q] = static_cast<int>(seq_starts[q]);
+        return forward_impl(prob, nullptr, x, dt, A_log, B, C, D, initial_states, nullptr, y, final_states,
+                            workspace, workspace_bytes, stream, nullptr, nullptr, &a);
+    }
     const size_t act = s.bf16 ? 2 : 4;
     const int64_t H = s.H, HP = s.H * s.P, GN = s.G * s.N, HPN = s.H * s.P * s.N;
     for (int64_t q = 0; q < prob->nseq; ++q) {

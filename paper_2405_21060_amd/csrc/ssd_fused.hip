@@ -204,6 +204,12 @@ __global__ __launch_bounds__(256) void k_seq_starts(const int32_t* __restrict__ 
     if ((t == 0 || seq_idx[t - 1] != v) && v >= 0 && v < nseq) starts[v] = t;
 }
 
+// The same from starts given by value (host offsets).
+__global__ __launch_bounds__(256) void k_seq_starts_args(SeqStartsArg a, int* __restrict__ starts)
+{
+    for (int i = threadIdx.x; i <= a.n; i += 256) starts[i] = a.v[i];
+}
+
 constexpr int kTabThreads = 1024;
 
 // Exclusive prefix sum over the workgroup (kTabThreads lanes), plus the total.
@@ -1207,10 +1213,13 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
 template <int N>
 hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
-    if (p.seq_idx) {   // packed row: the chunk table first
+    if (p.vtab) {   // packed row: the chunk table first
         const int T = static_cast<int>(p.T), nseq = static_cast<int>(p.nseq);
-        hipLaunchKernelGGL(k_seq_starts, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream,
-                           p.seq_idx, T, nseq, p.starts);
+        if (p.seq_idx)
+            hipLaunchKernelGGL(k_seq_starts, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream,
+                               p.seq_idx, T, nseq, p.starts);
+        else
+            hipLaunchKernelGGL(k_seq_starts_args, dim3(1), dim3(256), 0, stream, *p.arg_starts, p.starts);
         hipLaunchKernelGGL(k_seq_chunks, dim3(1), dim3(kTabThreads), 0, stream, p.starts, T, nseq,
                            static_cast<int>(p.nC), static_cast<int>(p.ring_rows), p.vtab, p.vcount);
     }

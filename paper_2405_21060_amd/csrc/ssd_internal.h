@@ -53,6 +53,14 @@ hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream,
                           hipEvent_t ev_begin, hipEvent_t ev_end);
 
 // Fused path (bf16, P = 64, N in {64, 128}, Q = 256, no packed rows).
+// Sequence starts of a packed row handed to the device by value (kernel
+// argument) when the caller gives them in host memory: n sequences, v[0..n].
+constexpr int kArgSeqs = 511;
+struct SeqStartsArg {
+    int n;
+    int v[kArgSeqs + 1];
+};
+
 struct FusedParams {
     int64_t b, T, H, P, N, G, nC, HG;
     const void* x;
@@ -76,6 +84,7 @@ struct FusedParams {
     // device table that k_seq_chunks builds; nC is then the table's capacity.
     // Null seq_idx: plain rows, chunk c of row b at token c Q.
     const int32_t* seq_idx = nullptr;  // (T)
+    const SeqStartsArg* arg_starts = nullptr;  // host memory, instead of seq_idx; read at launch
     int64_t nseq = 0;
     int* starts = nullptr;             // (nseq + 1) first token of each sequence, then T
     int4* vtab = nullptr;              // (nC) {first token, length, sequence, bit 0 first chunk of

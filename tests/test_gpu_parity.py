@@ -160,6 +160,18 @@ def test_fused_packed_one_sequence_equals_plain_row():
     assert torch.equal(f1, f2)
 
 
+@pytest.mark.parametrize("early", ["0", "1"])
+def test_fused_state_flag_placement(monkeypatch, early):
+    """Both placements of a chunk's state flag (after its output stage, or
+    right after its state is stored) forced on a plain and a packed row, with
+    few persistent workgroups so that items wait on each other."""
+    monkeypatch.setenv("SSD_EARLY_FLAG", early)
+    monkeypatch.setenv("SSD_MAX_WORKGROUPS", "5")
+    check(make_inputs(Problem(2, 1100, 8, 64, 128, 2, 256, "bf16", init_states=True), 37),
+          tag="flag%s_plain" % early)
+    check(_packed([300, 1, 700, 256, 90], 4, 64, 1, 41), tag="flag%s_packed" % early)
+
+
 def test_packed_rows_both_device_paths(monkeypatch):
     """The general kernels (forced) and the fused ones on one packed row, each
     against the oracle."""
@@ -270,6 +282,17 @@ def test_varlen_host_offsets_small():
     check_varlen_host(make_inputs(p, 9), tag="varlen_bf16_small")
     p = Problem(1, 700, 4, 32, 64, 2, 64, "f32", varlen=True, len_lo=1, len_hi=200, init_states=True)
     check_varlen_host(make_inputs(p, 4), tag="varlen_f32_small")
+
+
+def test_varlen_host_offsets_per_sequence_and_many(monkeypatch):
+    """The per-sequence launches (forced), and more sequences than one launch
+    takes by value (they run per sequence)."""
+    p = Problem(1, 3000, 8, 64, 128, 4, 256, "bf16", varlen=True, len_lo=1, len_hi=700, init_states=True)
+    monkeypatch.setenv("SSD_VARLEN_PER_SEQUENCE", "1")
+    check_varlen_host(make_inputs(p, 9), tag="varlen_per_sequence_forced")
+    monkeypatch.delenv("SSD_VARLEN_PER_SEQUENCE")
+    inp = _packed(np.random.default_rng(7).integers(1, 4, 600).tolist() + [500], 2, 64, 1, 43)
+    check_varlen_host(inp, tag="varlen_601_sequences")
 
 
 def test_varlen_host_offsets_full_size():
