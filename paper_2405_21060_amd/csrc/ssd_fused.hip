@@ -274,11 +274,10 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
     __shared__ __attribute__((aligned(16))) PrepSmem<N> sm;
     const int c = blockIdx.x;
     const int b = static_cast<int>(blockIdx.y / p.G), g = static_cast<int>(blockIdx.y % p.G);
-    const int part = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hpg = static_cast<int>(p.H / p.G);
-    if (part == 0 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
+    if (blockIdx.z == 0 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
         p.ticket[0] = 0;
         p.ticket[1] = 0;  // error word: set when a state wait times out
     }
@@ -291,83 +290,91 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
         L = e.y;
     }
 
-    // ---- flags of this (batch, chunk) and group
-    if (part == 0)
-        for (int hh = tid; hh < hpg; hh += kPrepThreads)
-            p.flags[(static_cast<int64_t>(b) * p.H + g * hpg + hh) * p.nC + c] = 0;
-    // t-tile rows of this part (balanced: 34 tiles)
-    const int rows[4] = {part, 7 - part, 8 + part, kNQ - 1 - part};
+    // A workgroup takes parts z, z + gridDim.z, ... of the chunk (fewer
+    // workgroups per chunk when there are many chunks: the B rows stay in LDS).
+    for (int part = blockIdx.z; part < kGramParts; part += gridDim.z) {
+        const bool first = part == static_cast<int>(blockIdx.z);
+        if (!first) __syncthreads();   // the previous part's LDS reads are done
+        // ---- flags of this (batch, chunk) and group
+        if (part == 0)
+            for (int hh = tid; hh < hpg; hh += kPrepThreads)
+                p.flags[(static_cast<int64_t>(b) * p.H + g * hpg + hh) * p.nC + c] = 0;
+        // t-tile rows of this part (balanced: 34 tiles)
+        const int rows[4] = {part, 7 - part, 8 + part, kNQ - 1 - part};
 
-    // ---- B rows of the chunk and C rows of this part's t-tiles into LDS (rows
-    // past a partial chunk: zeros).  C row tile rows[k] lands at LDS row 16 k.
-    const u16* Bchunk = static_cast<const u16*>(p.B) + ((b * p.T + c0) * p.G + g) * N;
-    const u16* Cchunk = static_cast<const u16*>(p.C) + ((b * p.T + c0) * p.G + g) * N;
-    const int64_t brow = p.G * N;
-    // all loads are issued before any LDS store, so that they are in flight together
-    constexpr int kBPer = kQ * N / 8 / kPrepThreads, kCPer = 64 * N / 8 / kPrepThreads;
-    static_assert(kBPer * kPrepThreads == kQ * N / 8 && kCPer * kPrepThreads == 64 * N / 8, "even split");
-    uint4 vb[kBPer], vc[kCPer];
+        // ---- B rows of the chunk and C rows of this part's t-tiles into LDS (rows
+        // past a partial chunk: zeros).  C row tile rows[k] lands at LDS row 16 k.
+        const u16* Bchunk = static_cast<const u16*>(p.B) + ((b * p.T + c0) * p.G + g) * N;
+        const u16* Cchunk = static_cast<const u16*>(p.C) + ((b * p.T + c0) * p.G + g) * N;
+        const int64_t brow = p.G * N;
+        // all loads are issued before any LDS store, so that they are in flight together
+        constexpr int kBPer = kQ * N / 8 / kPrepThreads, kCPer = 64 * N / 8 / kPrepThreads;
+        static_assert(kBPer * kPrepThreads == kQ * N / 8 && kCPer * kPrepThreads == 64 * N / 8, "even split");
+        uint4 vb[kBPer], vc[kCPer];
+        if (first)
 #pragma unroll
-    for (int k = 0; k < kBPer; ++k) {
-        const int i = tid + kPrepThreads * k;
-        const int s = i / (N / 8), col = 8 * (i % (N / 8));
-        vb[k] = *reinterpret_cast<const uint4*>(Bchunk + (s < L ? s : L - 1) * brow + col);
-    }
-#pragma unroll
-    for (int k = 0; k < kCPer; ++k) {
-        const int i = tid + kPrepThreads * k;
-        const int lr = i / (N / 8), col = 8 * (i % (N / 8));
-        const int t = 16 * rows[lr >> 4] + (lr & 15);
-        vc[k] = *reinterpret_cast<const uint4*>(Cchunk + (t < L ? t : L - 1) * brow + col);
-    }
-#pragma unroll
-    for (int k = 0; k < kBPer; ++k) {
-        const int i = tid + kPrepThreads * k;
-        const int s = i / (N / 8), col = 8 * (i % (N / 8));
-        *reinterpret_cast<uint4*>(&sm.B[s * RS + col]) = (s < L) ? vb[k] : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int k = 0; k < kCPer; ++k) {
-        const int i = tid + kPrepThreads * k;
-        const int lr = i / (N / 8), col = 8 * (i % (N / 8));
-        const int t = 16 * rows[lr >> 4] + (lr & 15);
-        *reinterpret_cast<uint4*>(&sm.C[lr * RS + col]) = (t < L) ? vc[k] : make_uint4(0, 0, 0, 0);
-    }
-    __syncthreads();
-
-    // ---- Gram tiles G^T[s][t] = sum_n B_s[n] C_t[n] (bf16), accumulator layout per lane.
-    // Wavefront w: row rows[w / 2], s-tiles j = w%2, w%2 + 2, ...
-    u16* gram = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
-    {
-        const int i = rows[wave >> 1];
-        uint4 cfr[N / 32];
-#pragma unroll
-        for (int k = 0; k < N / 32; ++k)
-            cfr[k] = *reinterpret_cast<const uint4*>(&sm.C[(16 * (wave >> 1) + r) * RS + 32 * k + 8 * lg]);
-#pragma unroll 1
-        for (int j = wave & 1; j <= i; j += 2) {
-            f32x4_t acc = zero4();
-#pragma unroll
-            for (int k = 0; k < N / 32; ++k) {
-                const uint4 va = *reinterpret_cast<const uint4*>(&sm.B[(16 * j + r) * RS + 32 * k + 8 * lg]);
-                acc = mfma(as_bf16x8(va), as_bf16x8(cfr[k]), acc);
-            }
-            uint2 packed;
-            packed.x = pack_bf16x2(acc[0], acc[1]);
-            packed.y = pack_bf16x2(acc[2], acc[3]);
-            *reinterpret_cast<uint2*>(gram + (static_cast<int64_t>(tile_index(i, j)) * 64 + lane) * 4) = packed;
+        for (int k = 0; k < kBPer; ++k) {
+            const int i = tid + kPrepThreads * k;
+            const int s = i / (N / 8), col = 8 * (i % (N / 8));
+            vb[k] = *reinterpret_cast<const uint4*>(Bchunk + (s < L ? s : L - 1) * brow + col);
         }
-    }
-
-    // ---- this part's quarter of B^T from LDS: item (n, 8 tokens), 16-byte stores along s
-    u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
-    constexpr int kBtItems = N * (kQ / 8) / kGramParts;
-    for (int i = part * kBtItems + tid; i < (part + 1) * kBtItems; i += kPrepThreads) {
-        const int n = i % N, so = i / N;
-        U16x8 v;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v.v[e] = sm.B[(8 * so + e) * RS + n];
-        *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
+        for (int k = 0; k < kCPer; ++k) {
+            const int i = tid + kPrepThreads * k;
+            const int lr = i / (N / 8), col = 8 * (i % (N / 8));
+            const int t = 16 * rows[lr >> 4] + (lr & 15);
+            vc[k] = *reinterpret_cast<const uint4*>(Cchunk + (t < L ? t : L - 1) * brow + col);
+        }
+        if (first)
+#pragma unroll
+        for (int k = 0; k < kBPer; ++k) {
+            const int i = tid + kPrepThreads * k;
+            const int s = i / (N / 8), col = 8 * (i % (N / 8));
+            *reinterpret_cast<uint4*>(&sm.B[s * RS + col]) = (s < L) ? vb[k] : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int k = 0; k < kCPer; ++k) {
+            const int i = tid + kPrepThreads * k;
+            const int lr = i / (N / 8), col = 8 * (i % (N / 8));
+            const int t = 16 * rows[lr >> 4] + (lr & 15);
+            *reinterpret_cast<uint4*>(&sm.C[lr * RS + col]) = (t < L) ? vc[k] : make_uint4(0, 0, 0, 0);
+        }
+        __syncthreads();
+
+        // ---- Gram tiles G^T[s][t] = sum_n B_s[n] C_t[n] (bf16), accumulator layout per lane.
+        // Wavefront w: row rows[w / 2], s-tiles j = w%2, w%2 + 2, ...
+        u16* gram = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
+        {
+            const int i = rows[wave >> 1];
+            uint4 cfr[N / 32];
+#pragma unroll
+            for (int k = 0; k < N / 32; ++k)
+                cfr[k] = *reinterpret_cast<const uint4*>(&sm.C[(16 * (wave >> 1) + r) * RS + 32 * k + 8 * lg]);
+#pragma unroll 1
+            for (int j = wave & 1; j <= i; j += 2) {
+                f32x4_t acc = zero4();
+#pragma unroll
+                for (int k = 0; k < N / 32; ++k) {
+                    const uint4 va = *reinterpret_cast<const uint4*>(&sm.B[(16 * j + r) * RS + 32 * k + 8 * lg]);
+                    acc = mfma(as_bf16x8(va), as_bf16x8(cfr[k]), acc);
+                }
+                uint2 packed;
+                packed.x = pack_bf16x2(acc[0], acc[1]);
+                packed.y = pack_bf16x2(acc[2], acc[3]);
+                *reinterpret_cast<uint2*>(gram + (static_cast<int64_t>(tile_index(i, j)) * 64 + lane) * 4) = packed;
+            }
+        }
+
+        // ---- this part's quarter of B^T from LDS: item (n, 8 tokens), 16-byte stores along s
+        u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
+        constexpr int kBtItems = N * (kQ / 8) / kGramParts;
+        for (int i = part * kBtItems + tid; i < (part + 1) * kBtItems; i += kPrepThreads) {
+            const int n = i % N, so = i / N;
+            U16x8 v;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v.v[e] = sm.B[(8 * so + e) * RS + n];
+            *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
+        }
     }
 }
 
@@ -1223,19 +1230,23 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
         hipLaunchKernelGGL(k_seq_chunks, dim3(1), dim3(kTabThreads), 0, stream, p.starts, T, nseq,
                            static_cast<int>(p.nC), static_cast<int>(p.ring_rows), p.vtab, p.vcount);
     }
-    const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), kGramParts);
+    int dev = 0, cus = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    // four prep workgroups per (chunk, group) while that fills the chip at most
+    // twice over; else two or one, each taking several parts with B loaded once
+    const int64_t pairs = p.nC * p.b * p.G;
+    const unsigned gz = pairs * kGramParts <= 2 * cus ? kGramParts : (pairs * 2 <= 2 * cus ? 2 : 1);
+    const dim3 g_prep(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b * p.G), gz);
     if (p.vtab)
         hipLaunchKernelGGL((k_fused_prep<N, true>), g_prep, dim3(kPrepThreads), 0, stream, p);
     else
         hipLaunchKernelGGL((k_fused_prep<N, false>), g_prep, dim3(kPrepThreads), 0, stream, p);
-    hipError_t err = hipGetLastError();
+    err = hipGetLastError();
     if (err == hipSuccess && ev_begin) err = hipEventRecord(ev_begin, stream);
     if (err != hipSuccess) return err;
     const int64_t nwork = p.nC * p.b * (p.H / p.HG);
-    int dev = 0, cus = 0;
-    err = hipGetDevice(&dev);
-    if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (err != hipSuccess) return err;
     // one persistent workgroup per compute unit (the LDS footprint allows one);
     // SSD_MAX_WORKGROUPS caps it (a test knob: few workgroups, many items each)
     int64_t grid = nwork < cus ? nwork : cus;
