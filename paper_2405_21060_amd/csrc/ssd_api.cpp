@@ -76,8 +76,9 @@ constexpr int64_t kMaxElemsPublic = kMaxElems;
 // item's heads share B and C).  More heads per item share more of the item's
 // set-up (Gram tiles, B^T and C fragments); fewer give more items.  The
 // largest of 4, 2 that leaves at least two items per compute unit (measured
-// best at the 130M and 2.7B layer shapes), else the largest that leaves one,
-// else 1.  SSD_HEADS_PER_WG overrides it
+// best at the 2.7B layer shape), else the largest that leaves one, else 1;
+// then a divisor up to 6 that fills whole rounds where that is clearly cheaper
+// (below).  SSD_HEADS_PER_WG overrides it
 // (tuning knob; ignored unless it divides the heads per group).
 // chunks in flight from which a chunk's state flag is set early (see forward_impl)
 constexpr int64_t kEarlyFlagChunks = 8;
@@ -89,11 +90,34 @@ int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int
         if (v >= 1 && heads_per_group % v == 0) return v;
     }
     // items_per_head: chunks x batch rows x groups, the items at one head per item
-    for (int64_t need : {2, 1})
-        for (int64_t hg : {4, 2})
-            if (heads_per_group % hg == 0 && items_per_head * (heads_per_group / hg) >= need * compute_units)
-                return hg;
-    return 1;
+    int64_t hg = 1;
+    bool found = false;
+    for (int64_t need : {2, 1}) {
+        for (int64_t h : {4, 2})
+            if (heads_per_group % h == 0 && items_per_head * (heads_per_group / h) >= need * compute_units) {
+                hg = h;
+                found = true;
+                break;
+            }
+        if (found) break;
+    }
+    // A divisor up to 6 whose items fill whole rounds of the compute units
+    // replaces that choice when it is clearly cheaper by rounds x (heads per item
+    // + 1/2 of a head for the item's set-up): at the 130M layer shape, 6 heads
+    // give 256 items (one round) where 2 give 768 (three).
+    const auto cost = [&](int64_t h) {
+        const int64_t items = items_per_head * (heads_per_group / h);
+        return static_cast<double>((items + compute_units - 1) / compute_units) * (h + 0.5);
+    };
+    double best = cost(hg);
+    const double base = best;
+    int64_t pick = hg;
+    for (int64_t h = 1; h <= 6; ++h)
+        if (heads_per_group % h == 0 && cost(h) < best) {
+            best = cost(h);
+            pick = h;
+        }
+    return best < 0.9 * base ? pick : hg;
 }
 
 WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int64_t G,
