@@ -759,15 +759,78 @@ namespace {
 // packed tensors; one state per sequence), and the per-sequence dA_log and dD
 // are summed at the end.  seq_starts (host): nseq + 1 offsets, 0 = first <
 // ... < last = seqlen.
+// Packed-row backward in one launch (matrix-core path): every sequence cut
+// into 64-token chunks of its own from a chunk table built on the device from
+// the offsets handed over by value; b = 1 and nC = the table's capacity.
+struct PackedBwdLayout {
+    ssd::BwdLayout l;
+    size_t starts, vtab, seq_first, vcount, total;
+};
+
+bool packed_backward_ok(const ssd_problem* prob)
+{
+    const char* per = std::getenv("SSD_VARLEN_PER_SEQUENCE");
+    const char* path = std::getenv("SSD_PATH");
+    if ((per && per[0] == '1') || (path && path[0] == 'u')) return false;
+    ssd_problem q = *prob;
+    q.chunk_size = 256;
+    ssd::Shape s;
+    if (ssd::validate(&q, true, &s) != SSD_OK) return false;
+    return backward_fast(s) && prob->batch == 1 && prob->nseq <= ssd::kArgSeqs && prob->seqlen <= INT32_MAX;
+}
+
+int packed_backward_plan(const ssd_problem* prob, ssd::BwdParams* p, PackedBwdLayout* pl)
+{
+    ssd_problem q = *prob;
+    q.chunk_size = 256;
+    ssd::Shape s;
+    const int rc = ssd::validate(&q, true, &s);
+    if (rc != SSD_OK) return rc;
+    const int64_t Q = ssd::kBwdQFast;
+    p->b = 1;
+    p->T = s.T;
+    p->H = s.H;
+    p->P = s.P;
+    p->N = s.N;
+    p->G = s.G;
+    p->nseq = s.nseq;
+    const int64_t nCd = (s.T + Q - 1) / Q;
+    p->nC = std::min(nCd + s.nseq - 1, s.T);   // at most this many per-sequence chunks
+    if (static_cast<double>(p->nC) * p->H * p->P * p->N > 16.0 * ssd::kMaxElemsPublic) return SSD_ERR_TOO_LARGE;
+    ssd::bwd_slices(1, p->nC, p->G, p->H / p->G, &p->S, &p->hs);
+    pl->l = ssd::bwd_layout(1, p->T, p->H, p->P, p->N, p->G, p->nC, p->S, true);
+    size_t off = pl->l.total;
+    pl->starts = off;
+    off = ssd::align_up(off + sizeof(int) * static_cast<size_t>(s.nseq + 1));
+    pl->vtab = off;
+    off = ssd::align_up(off + sizeof(int4) * static_cast<size_t>(p->nC));
+    pl->seq_first = off;
+    off = ssd::align_up(off + sizeof(int) * static_cast<size_t>(s.nseq + 1));
+    pl->vcount = off;
+    off = ssd::align_up(off + sizeof(int));
+    pl->total = off;
+    return SSD_OK;
+}
+
 int varlen_plan(const ssd_problem* prob, const int64_t* seq_starts, size_t* sub_bytes, size_t* total)
 {
     if (!prob || !seq_starts) return SSD_ERR_NULL_ARG;
     if (prob->batch != 1) return SSD_ERR_SEQIDX_BATCH;
     if (prob->nseq < 1 || prob->nseq > prob->seqlen) return SSD_ERR_BAD_SHAPE;
     if (seq_starts[0] != 0 || seq_starts[prob->nseq] != prob->seqlen) return SSD_ERR_BAD_SHAPE;
+    for (int64_t s = 0; s < prob->nseq; ++s)
+        if (seq_starts[s + 1] <= seq_starts[s]) return SSD_ERR_BAD_SHAPE;
+    if (packed_backward_ok(prob)) {
+        ssd::BwdParams p{};
+        PackedBwdLayout pl{};
+        const int rc = packed_backward_plan(prob, &p, &pl);
+        if (rc != SSD_OK) return rc;
+        *sub_bytes = 0;
+        *total = pl.total;
+        return SSD_OK;
+    }
     size_t need = 0;
     for (int64_t s = 0; s < prob->nseq; ++s) {
-        if (seq_starts[s + 1] <= seq_starts[s]) return SSD_ERR_BAD_SHAPE;
         ssd_problem q = *prob;
         q.seqlen = seq_starts[s + 1] - seq_starts[s];
         size_t b = 0;
@@ -810,6 +873,49 @@ extern "C" int ssd_backward_varlen(const ssd_problem* prob, const int64_t* seq_s
         !aligned16(x) || !aligned16(B) || !aligned16(C) || !aligned16(dy) || !aligned16(dx))
         return SSD_ERR_UNSUPPORTED_DIMS;   // (every slice below keeps the alignment: rows are multiples of 32 bytes)
     if (!workspace || workspace_bytes < total) return SSD_ERR_WORKSPACE;
+    if (packed_backward_ok(prob)) {
+        ssd::BwdParams p{};
+        PackedBwdLayout pl{};
+        if ((rc = packed_backward_plan(prob, &p, &pl)) != SSD_OK) return rc;
+        char* ws = static_cast<char*>(workspace);
+        p.x = x;
+        p.dt = dt;
+        p.A_log = A_log;
+        p.B = B;
+        p.C = C;
+        p.D = D;
+        p.init = initial_states;
+        p.dy = dy;
+        p.dfinal = dfinal_states;
+        p.dx = dx;
+        p.ddt = ddt;
+        p.dA_log = dA_log;
+        p.dB = dB;
+        p.dC = dC;
+        p.dD = D ? dD : nullptr;
+        p.dinit = dinitial_states;
+        p.hin = reinterpret_cast<float*>(ws + pl.l.hin);
+        p.gnT = reinterpret_cast<float*>(ws + pl.l.gnT);
+        p.dBp = reinterpret_cast<float*>(ws + pl.l.dBp);
+        p.dCp = reinterpret_cast<float*>(ws + pl.l.dCp);
+        p.dAp = reinterpret_cast<float*>(ws + pl.l.dAp);
+        p.dDp = reinterpret_cast<float*>(ws + pl.l.dDp);
+        int* starts = reinterpret_cast<int*>(ws + pl.starts);
+        int4* vtab = reinterpret_cast<int4*>(ws + pl.vtab);
+        int* seq_first = reinterpret_cast<int*>(ws + pl.seq_first);
+        int* vcount = reinterpret_cast<int*>(ws + pl.vcount);
+        p.vtab = vtab;
+        p.seq_first = seq_first;
+        p.vcount = vcount;
+        ssd::SeqStartsArg arg;
+        arg.n = static_cast<int>(prob->nseq);
+        for (int64_t q = 0; q <= prob->nseq; ++q) arg.v[q] = static_cast<int>(seq_starts[q]);
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        hipError_t err = ssd::launch_seq_table(nullptr, &arg, p.T, p.nseq, static_cast<int>(ssd::kBwdQFast), p.nC, 1,
+                                               starts, vtab, seq_first, vcount, st);
+        if (err == hipSuccess) err = ssd::launch_backward_fast(p, st, nullptr, nullptr);
+        return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+    }
     const size_t act = s.bf16 ? 2 : 4;
     const int64_t H = s.H, HP = s.H * s.P, GN = s.G * s.N, HPN = s.H * s.P * s.N;
     float* partA = static_cast<float*>(workspace);
@@ -838,9 +944,6 @@ extern "C" int ssd_backward_varlen(const ssd_problem* prob, const int64_t* seq_s
 
 namespace {
 
-// Packed rows with host offsets: the forward of each sequence on its slice of
-// the packed tensors (the fused kernel where the shape allows), one initial
-// and final state per sequence.
 // One launch over the whole packed row (the fused kernels' chunk table, the
 // offsets handed over by value) where the shape and the number of sequences
 // allow; else one call per sequence.  SSD_VARLEN_PER_SEQUENCE=1 forces the

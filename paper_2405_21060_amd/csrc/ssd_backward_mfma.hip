@@ -185,7 +185,9 @@ __device__ __forceinline__ uint4 tr_frag(const u16* buf, int m, int f0, int lane
     return make_uint4(lo.x, lo.y, hi.x, hi.y);
 }
 
-template <int N>
+// PACKED: a packed row; workgroup (sequence, head) walks that sequence's
+// chunks of the chunk table.
+template <int N, bool PACKED>
 __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
 {
     __shared__ __attribute__((aligned(16))) u16 XS[kQ2 * kP2];   // weighted x (or dy), token-major
@@ -221,12 +223,25 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         float dt;
         uint4 x[kXK], y[kYK];
     };
-    const auto chunk_at = [&](int64_t k) { return dir == 0 ? k : p.nC - 1 - k; };
+    int64_t first = 0, nch = p.nC;   // this row's (or sequence's) chunks
+    if constexpr (PACKED) {
+        first = p.seq_first[b];
+        nch = p.seq_first[b + 1] - first;
+    }
+    const auto chunk_at = [&](int64_t k) { return first + (dir == 0 ? k : nch - 1 - k); };
     const auto fetch = [&](Stage& st, int64_t k) {
-        if (k >= p.nC) return;
+        if (k >= nch) return;
         const int64_t c = chunk_at(k);
-        const int L = chunk_len2(p.T, c);
-        const int64_t t0 = b * p.T + c * kQ2;
+        int L;
+        int64_t t0;
+        if constexpr (PACKED) {
+            const int4 e = p.vtab[c];
+            L = e.y;
+            t0 = e.x;
+        } else {
+            L = chunk_len2(p.T, c);
+            t0 = b * p.T + c * kQ2;
+        }
         st.dt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
 #pragma unroll
         for (int kk = 0; kk < kXK; ++kk) {
@@ -243,7 +258,7 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     };
     const auto step = [&](Stage& st, int64_t k) {
         const int64_t c = chunk_at(k);
-        const int L = chunk_len2(p.T, c);
+        const int L = PACKED ? p.vtab[c].y : chunk_len2(p.T, c);
         // token weights: cumsum with lane = token, then each piece's token's weight
         const float cs = wave_scan(st.dt * A2);
         const float csend = lane_value(cs, L - 1);
@@ -267,7 +282,7 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         fetch(st, k + 2);
 
         // S before this chunk's term -> out(c), bf16 (n x p)
-        u16* o = out + ((b * p.nC + c) * p.H + h) * kP2 * N;
+        u16* o = out + ((PACKED ? c : b * p.nC + c) * p.H + h) * kP2 * N;
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
             *reinterpret_cast<uint2*>(o + (16 * nt + r) * kP2 + 16 * w + 4 * q) =
@@ -288,9 +303,9 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     Stage s0st, s1st;
     fetch(s0st, 0);
     fetch(s1st, 1);
-    for (int64_t k = 0; k < p.nC; k += 2) {
+    for (int64_t k = 0; k < nch; k += 2) {
         step(s0st, k);
-        if (k + 1 < p.nC) step(s1st, k + 1);
+        if (k + 1 < nch) step(s1st, k + 1);
     }
     if (dir == 1 && p.dinit) {
 #pragma unroll
@@ -315,7 +330,7 @@ struct ChunkSmem {
 __constant__ int2 kLowerTile[10] = {{0, 0}, {1, 0}, {1, 1}, {2, 0}, {2, 1}, {2, 2}, {3, 0}, {3, 1}, {3, 2}, {3, 3}};
 __constant__ int2 kUpperTile[6] = {{0, 1}, {0, 2}, {0, 3}, {1, 2}, {1, 3}, {2, 3}};
 
-template <int N>
+template <int N, bool PACKED>
 __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 {
     constexpr int kLdN = ChunkSmem<N>::kLdN;
@@ -340,10 +355,27 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 
     const int64_t c = blockIdx.x, b = blockIdx.y;
     const HeadRange hr = head_range(p);
-    const int L = chunk_len2(p.T, c);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, q = lane >> 4;
-    const int64_t t0 = b * p.T + c * kQ2;
+    int L0 = 0;
+    int64_t t00 = 0;
+    if constexpr (PACKED) {   // chunk c of the table; entries past its end add nothing to dA, dD
+        if (c >= *p.vcount) {
+            for (int64_t hh = hr.lo + tid; hh < hr.hi; hh += kT2) {
+                p.dAp[hh * p.nC + c] = 0.f;
+                p.dDp[hh * p.nC + c] = 0.f;
+            }
+            return;
+        }
+        const int4 e = p.vtab[c];
+        L0 = e.y;
+        t00 = e.x;
+    } else {
+        L0 = chunk_len2(p.T, c);
+        t00 = b * p.T + c * kQ2;
+    }
+    const int L = L0;
+    const int64_t t0 = t00;
     const u16* Bg = static_cast<const u16*>(p.B);
     const u16* Cg = static_cast<const u16*>(p.C);
     const u16* xg = static_cast<const u16*>(p.x);
@@ -680,15 +712,24 @@ hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEv
 {
     const size_t sm_chunk = ChunkSmem<N>::kBytes;
     hipError_t e;
-    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bwd2_chunk<N>),
-                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
+    const bool packed = p.vtab != nullptr;
+    const void* chunk_fn = packed ? reinterpret_cast<const void*>(&k_bwd2_chunk<N, true>)
+                                  : reinterpret_cast<const void*>(&k_bwd2_chunk<N, false>);
+    if ((e = hipFuncSetAttribute(chunk_fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
         hipSuccess)
         return e;
-    hipLaunchKernelGGL(k_bwd2_pass<N>, dim3(static_cast<unsigned>(p.b * p.H), 2), dim3(kPassT), 0, st, p);
+    if (packed)   // one workgroup per (sequence, head) and direction
+        hipLaunchKernelGGL((k_bwd2_pass<N, true>), dim3(static_cast<unsigned>(p.nseq * p.H), 2), dim3(kPassT), 0,
+                           st, p);
+    else
+        hipLaunchKernelGGL((k_bwd2_pass<N, false>), dim3(static_cast<unsigned>(p.b * p.H), 2), dim3(kPassT), 0, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
-    hipLaunchKernelGGL(k_bwd2_chunk<N>, grid, dim3(kT2), sm_chunk, st, p);
+    if (packed)
+        hipLaunchKernelGGL((k_bwd2_chunk<N, true>), grid, dim3(kT2), sm_chunk, st, p);
+    else
+        hipLaunchKernelGGL((k_bwd2_chunk<N, false>), grid, dim3(kT2), sm_chunk, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
     return launch_backward_reduce(p, true, st);

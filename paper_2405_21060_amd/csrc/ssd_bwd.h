@@ -45,6 +45,12 @@ struct BwdParams {
     float* dCp;    // (S, b, T, G, N)
     float* dAp;    // (b, H, nC)          per-chunk terms of dA
     float* dDp;    // (b, H, nC)          per-chunk terms of dD
+    // Packed row (b = 1, matrix-core path): every sequence cut into chunks of
+    // its own; nC is then the chunk table's capacity.  Null vtab: plain rows.
+    int64_t nseq = 0;
+    const int4* vtab = nullptr;     // (nC) {first token, length, sequence, flags}
+    const int* seq_first = nullptr; // (nseq + 1) first table entry of each sequence, then the count
+    const int* vcount = nullptr;    // [0] table entries
 };
 
 struct BwdLayout {

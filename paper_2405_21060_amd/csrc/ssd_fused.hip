@@ -237,9 +237,12 @@ __device__ long long block_exclusive_sum(long long v, long long* s_w, long long*
 // The chunks of every sequence, in token order (one workgroup): sequence r
 // of length len gives ceil(len / Q) chunks from its first token on.  Every
 // entry stays inside [0, T) and the table's capacity whatever the ids hold.
+// seq_first (may be null): the table index of each sequence's first chunk,
+// then the number of entries.
+template <int Q>
 __global__ __launch_bounds__(kTabThreads) void k_seq_chunks(const int* __restrict__ starts, int T, int nseq,
                                                             int cap, int ring_cap, int4* __restrict__ vtab,
-                                                            int* __restrict__ vcount)
+                                                            int* __restrict__ seq_first, int* __restrict__ vcount)
 {
     __shared__ long long s_w[kTabThreads / 64];
     // 64-bit sums: ids that break the contract may describe more chunks than T
@@ -251,19 +254,23 @@ __global__ __launch_bounds__(kTabThreads) void k_seq_chunks(const int* __restric
             st = min(max(starts[r], 0), T);
             len = min(max(starts[r + 1], st), T) - st;
         }
-        const int nch = len / kQ + (len % kQ != 0 ? 1 : 0);
+        const int nch = len / Q + (len % Q != 0 ? 1 : 0);
         long long tot = 0, rtot = 0;
         const long long v0 = base + block_exclusive_sum(nch, s_w, &tot);
         const long long rr = rbase + block_exclusive_sum(nch > 1 ? 1 : 0, s_w, &rtot);
         const int ring = static_cast<int>(rr < ring_cap ? rr : ring_cap - 1);
         for (int k = 0; k < nch && v0 + k < cap; ++k) {
             const int flags = (k == 0 ? 1 : 0) | (k == nch - 1 ? 2 : 0) | (ring << 2);
-            vtab[v0 + k] = make_int4(st + k * kQ, min(kQ, len - k * kQ), r, flags);
+            vtab[v0 + k] = make_int4(st + k * Q, min(Q, len - k * Q), r, flags);
         }
+        if (seq_first && r < nseq) seq_first[r] = static_cast<int>(v0 < cap ? v0 : cap);
         base += tot;
         rbase += rtot;
     }
-    if (threadIdx.x == 0) *vcount = static_cast<int>(base < cap ? base : cap);
+    if (threadIdx.x == 0) {
+        *vcount = static_cast<int>(base < cap ? base : cap);
+        if (seq_first) seq_first[nseq] = *vcount;
+    }
 }
 
 // PACKED: a packed row, chunk positions from the chunk table.
@@ -1221,14 +1228,9 @@ template <int N>
 hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
     if (p.vtab) {   // packed row: the chunk table first
-        const int T = static_cast<int>(p.T), nseq = static_cast<int>(p.nseq);
-        if (p.seq_idx)
-            hipLaunchKernelGGL(k_seq_starts, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream,
-                               p.seq_idx, T, nseq, p.starts);
-        else
-            hipLaunchKernelGGL(k_seq_starts_args, dim3(1), dim3(256), 0, stream, *p.arg_starts, p.starts);
-        hipLaunchKernelGGL(k_seq_chunks, dim3(1), dim3(kTabThreads), 0, stream, p.starts, T, nseq,
-                           static_cast<int>(p.nC), static_cast<int>(p.ring_rows), p.vtab, p.vcount);
+        const hipError_t e = launch_seq_table(p.seq_idx, p.arg_starts, p.T, p.nseq, kQ, p.nC, p.ring_rows, p.starts,
+                                              p.vtab, nullptr, p.vcount, stream);
+        if (e != hipSuccess) return e;
     }
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
@@ -1272,6 +1274,28 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
 }
 
 }  // namespace
+
+hipError_t launch_seq_table(const int32_t* seq_idx, const SeqStartsArg* arg_starts, int64_t T, int64_t nseq, int Q,
+                            int64_t cap, int64_t ring_rows, int* starts, int4* vtab, int* seq_first, int* vcount,
+                            hipStream_t stream)
+{
+    const int Ti = static_cast<int>(T), ns = static_cast<int>(nseq);
+    if (seq_idx)
+        hipLaunchKernelGGL(k_seq_starts, dim3(static_cast<unsigned>((Ti + 255) / 256)), dim3(256), 0, stream,
+                           seq_idx, Ti, ns, starts);
+    else
+        hipLaunchKernelGGL(k_seq_starts_args, dim3(1), dim3(256), 0, stream, *arg_starts, starts);
+    const int capi = static_cast<int>(cap), ring = static_cast<int>(ring_rows < 1 ? 1 : ring_rows);
+    if (Q == kQ)
+        hipLaunchKernelGGL((k_seq_chunks<kQ>), dim3(1), dim3(kTabThreads), 0, stream, starts, Ti, ns, capi, ring,
+                           vtab, seq_first, vcount);
+    else if (Q == 64)
+        hipLaunchKernelGGL((k_seq_chunks<64>), dim3(1), dim3(kTabThreads), 0, stream, starts, Ti, ns, capi, ring,
+                           vtab, seq_first, vcount);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
 
 bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16)
 {

@@ -109,6 +109,14 @@ struct FusedLayout {
 
 int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units);
 bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16);
+// The chunk table of a packed row of T tokens and nseq sequences, from the
+// device seq_idx or, when it is null, from starts handed over by value: every
+// sequence cut into chunks of Q tokens (256 or 64) from its first token on,
+// at most `cap` entries; seq_first (may be null) gets each sequence's first
+// entry and then the entry count.  `starts` is (nseq + 1) ints of workspace.
+hipError_t launch_seq_table(const int32_t* seq_idx, const SeqStartsArg* arg_starts, int64_t T, int64_t nseq, int Q,
+                            int64_t cap, int64_t ring_rows, int* starts, int4* vtab, int* seq_first, int* vcount,
+                            hipStream_t stream);
 // nseq > 0: layout for one packed row of nseq sequences (seq_idx); nC is the
 // row's chunk count ceil(T / Q) either way.
 FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, int64_t nC, int64_t nseq);

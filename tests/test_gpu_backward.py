@@ -199,6 +199,10 @@ VARLEN_CASES = [
     ("bf16", (300, 3, 64, 64, 1), [64, 64, 1, 171], False, True, False),
     ("f32", (300, 3, 32, 16, 1), [100, 64, 136], False, True, True),
     ("f32", (97, 2, 16, 32, 2), [5, 3, 1, 40, 48], True, False, True),
+    # one launch over the row (matrix-core path): lengths around its 64-token
+    # chunks, and many one-token sequences (more sequences than chunks)
+    ("bf16", (1000, 8, 64, 128, 4), [64, 65, 63, 128, 300, 380], True, True, True),
+    ("bf16", (700, 2, 64, 64, 1), [1] * 100 + [600], True, True, True),
 ]
 
 
@@ -244,3 +248,10 @@ def test_backward_packed_rows_full_size_head_subset():
     check("dx", got["dx"][:, :, heads], ref["dx"], tol)
     check("ddt", got["ddt"][:, :, heads], ref["ddt"], tol)
     check("dinit", got["dinit"][:, heads], ref["dinit"], tol)
+
+
+def test_backward_packed_rows_per_sequence_forced(monkeypatch):
+    """The per-sequence launches (forced) at a shape that otherwise runs as
+    one launch over the row."""
+    monkeypatch.setenv("SSD_VARLEN_PER_SEQUENCE", "1")
+    test_backward_packed_rows_match_oracle(VARLEN_CASES[0])
