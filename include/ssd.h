@@ -319,8 +319,11 @@ int ssd_backward_timed(const ssd_problem* prob,
  * belongs to sequence s when seq_starts[s] <= t < seq_starts[s + 1] (the
  * seq_idx of ssd_forward).  initial_states, dfinal_states and
  * dinitial_states are (nseq, nheads, headdim, dstate).  The sequences do not
- * interact: each runs as a problem of its own on its slice of the packed
- * tensors, and dA_log and dD are summed over the sequences in order.
+ * interact.  On the matrix-core path (bf16, headdim 64, dstate 64 or 128) and
+ * up to 511 sequences the offsets are handed to the device by value and the
+ * row runs as one backward over per-sequence chunks; otherwise each sequence
+ * runs as a problem of its own on its slice of the packed tensors and dA_log
+ * and dD are summed over the sequences in order.
  * Workspace: ssd_backward_varlen_workspace_bytes() bytes.  Otherwise as
  * ssd_backward (every check is made before any work is enqueued). */
 int ssd_backward_varlen_workspace_bytes(const ssd_problem* prob, const int64_t* seq_starts, size_t* bytes);
