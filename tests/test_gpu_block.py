@@ -111,6 +111,17 @@ def test_block_matches_oracle(sname, oname):
     check_block(make_block_inputs(p, 11), resolve(OPTS[oname], p), "%s/%s" % (sname, oname))
 
 
+@pytest.mark.parametrize("early", ["0", "1"])
+@pytest.mark.parametrize("sname", ["fused_n128", "fused_varlen"])
+def test_block_state_flag_placement(sname, early, monkeypatch):
+    # the gate and per-head normalisation in the chunk kernel's output stage with
+    # either placement of the state flag, few persistent workgroups
+    monkeypatch.setenv("SSD_EARLY_FLAG", early)
+    monkeypatch.setenv("SSD_MAX_WORKGROUPS", "4")
+    p = SHAPES[sname]
+    check_block(make_block_inputs(p, 14), resolve(OPTS["gate_headnorm"], p), "flag%s/%s" % (early, sname))
+
+
 @pytest.mark.parametrize("oname", ["gate_headnorm", "gate_norm2heads", "rownorm_clamp"])
 def test_block_output_pass_separate(oname, monkeypatch):
     # the fused chunk kernel with gate and normalisation left to the output pass
