@@ -189,19 +189,14 @@ struct Piece {
 // (sum of squares; sum of dn n; the gradients), or re-reads them when the
 // group is wider (MAXP == 0).  Records 1 / r per (row, group) for the weight
 // gradient.
+// The gradients of one (row, group), by the `seg` lanes that hold it.  acc
+// (may be null): this lane's pieces' dout n added to it, for the weight
+// gradient.  Every lane of the wavefront takes part (cross-lane sums); lanes of
+// an inactive group load and store nothing.
 template <typename T, int MAXP>
-__global__ __launch_bounds__(kBT) void k_norm_bwd(BlockBwdParams p, int seg, int log2seg)
+__device__ __forceinline__ void norm_group_bwd(const BlockBwdParams& p, bool active, int64_t gid, int64_t row,
+                                               int64_t c0, int li, int seg, float* acc)
 {
-    const int lane = threadIdx.x & 63;
-    const int per_wave = 64 >> log2seg;
-    const int64_t gpr = p.C / p.group;
-    const int64_t ngroups = p.rows * gpr;
-    const int64_t gid = (static_cast<int64_t>(blockIdx.x) * (kBT / 64) + (threadIdx.x >> 6)) * per_wave +
-                        (lane >> log2seg);
-    const int li = lane & (seg - 1);
-    const bool active = gid < ngroups;
-    const int64_t row = active ? gid / gpr : 0;
-    const int64_t c0 = active ? (gid - row * gpr) * p.group : 0;
     const int64_t base = row * p.C + c0;
     const int pieces = static_cast<int>(p.group / 8);
     Piece<T> pc[MAXP > 0 ? MAXP : 1];
@@ -275,6 +270,67 @@ __global__ __launch_bounds__(kBT) void k_norm_bwd(BlockBwdParams p, int seg, int
         if (p.z) store8<T>(p.dz, base + 8 * j, dz);
     });
     if (li == 0 && p.inv_rms) p.inv_rms[gid] = inv;
+    if constexpr (MAXP > 0) {
+        if (acc) {
+#pragma unroll
+            for (int k = 0; k < MAXP; ++k)
+                if (k < mine)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[8 * k + e] += pc[k].d[e] * pc[k].g(p, e) * inv;
+        }
+    }
+}
+
+template <typename T, int MAXP>
+__global__ __launch_bounds__(kBT) void k_norm_bwd(BlockBwdParams p, int seg, int log2seg)
+{
+    const int lane = threadIdx.x & 63;
+    const int per_wave = 64 >> log2seg;
+    const int64_t gpr = p.C / p.group;
+    const int64_t ngroups = p.rows * gpr;
+    const int64_t gid = (static_cast<int64_t>(blockIdx.x) * (kBT / 64) + (threadIdx.x >> 6)) * per_wave +
+                        (lane >> log2seg);
+    const int li = lane & (seg - 1);
+    const bool active = gid < ngroups;
+    const int64_t row = active ? gid / gpr : 0;
+    const int64_t c0 = active ? (gid - row * gpr) * p.group : 0;
+    norm_group_bwd<T, MAXP>(p, active, gid, row, c0, li, seg, nullptr);
+}
+
+// The same with the weight gradient's per-chunk partial sums folded in (groups
+// of at most 2 pieces per lane): workgroup (x, y) = (a run of groups of a row,
+// chunk of kRowsPerChunk rows); each segment keeps its group over the chunk's
+// rows and adds dout n in registers, so y, z and dout are read once.
+template <typename T, int MAXP>
+__global__ __launch_bounds__(kBT) void k_norm_bwd_rows(BlockBwdParams p, int seg, int log2seg)
+{
+    static_assert(MAXP > 0, "pieces kept in registers");
+    const int lane = threadIdx.x & 63;
+    const int per_wave = 64 >> log2seg;
+    const int64_t gpr = p.C / p.group;
+    const int64_t g = (static_cast<int64_t>(blockIdx.x) * (kBT / 64) + (threadIdx.x >> 6)) * per_wave +
+                      (lane >> log2seg);
+    const int li = lane & (seg - 1);
+    const bool active = g < gpr;
+    const int64_t c0 = active ? g * p.group : 0;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kRowsPerChunk;
+    const int64_t r1 = r0 + kRowsPerChunk < p.rows ? r0 + kRowsPerChunk : p.rows;
+    float acc[8 * MAXP];
+#pragma unroll
+    for (int k = 0; k < 8 * MAXP; ++k) acc[k] = 0.f;
+    for (int64_t r = r0; r < r1; ++r) norm_group_bwd<T, MAXP>(p, active, r * gpr + g, r, c0, li, seg, acc);
+    if (!active) return;
+    const int pieces = static_cast<int>(p.group / 8);
+    const int mine = (pieces - li + seg - 1) / seg;
+    float* o = p.dw_part + static_cast<int64_t>(blockIdx.y) * p.C + c0;
+#pragma unroll
+    for (int k = 0; k < MAXP; ++k)
+        if (k < mine) {
+            const int j = li + k * seg;
+            *reinterpret_cast<float4*>(o + 8 * j) = make_float4(acc[8 * k], acc[8 * k + 1], acc[8 * k + 2], acc[8 * k + 3]);
+            *reinterpret_cast<float4*>(o + 8 * j + 4) =
+                make_float4(acc[8 * k + 4], acc[8 * k + 5], acc[8 * k + 6], acc[8 * k + 7]);
+        }
 }
 
 // Per-chunk partial sums over rows of dout n for the weight gradient.  Thread =
@@ -340,6 +396,20 @@ hipError_t out_side(const BlockBwdParams& p, hipStream_t st)
     const int64_t ngroups = p.rows * (p.C / p.group);
     const dim3 grid(static_cast<unsigned>((ngroups + per_block - 1) / per_block));
     const int64_t per_lane = (pieces + seg - 1) / seg;
+    const int64_t nch = (p.rows + kRowsPerChunk - 1) / kRowsPerChunk;
+    if (p.dw && per_lane <= 2) {   // weight gradient folded in: y, z, dout read once
+        const int64_t gpr = p.C / p.group;
+        const dim3 g2(static_cast<unsigned>((gpr + per_block - 1) / per_block), static_cast<unsigned>(nch));
+        if (per_lane <= 1)
+            hipLaunchKernelGGL((k_norm_bwd_rows<T, 1>), g2, dim3(kBT), 0, st, p, seg, log2seg);
+        else
+            hipLaunchKernelGGL((k_norm_bwd_rows<T, 2>), g2, dim3(kBT), 0, st, p, seg, log2seg);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_sum_chunks, dim3(static_cast<unsigned>(p.C)), dim3(kBT), 0, st, p.dw_part, nch, p.C,
+                           p.dw);
+        return hipGetLastError();
+    }
     if (per_lane <= 1)
         hipLaunchKernelGGL((k_norm_bwd<T, 1>), grid, dim3(kBT), 0, st, p, seg, log2seg);
     else if (per_lane <= 2)
@@ -348,7 +418,6 @@ hipError_t out_side(const BlockBwdParams& p, hipStream_t st)
         hipLaunchKernelGGL((k_norm_bwd<T, 0>), grid, dim3(kBT), 0, st, p, seg, log2seg);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !p.dw) return e;
-    const int64_t nch = (p.rows + kRowsPerChunk - 1) / kRowsPerChunk;
     hipLaunchKernelGGL(k_norm_dw<T>, dim3(blocks(p.C / 8), static_cast<unsigned>(nch)), dim3(kBT), 0, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_sum_chunks, dim3(static_cast<unsigned>(p.C)), dim3(kBT), 0, st, p.dw_part, nch, p.C, p.dw);
