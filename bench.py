@@ -222,7 +222,7 @@ def block_bench(args, torch, ssd):
 
     def timed(mode, with_events=False):
         if mode == "separate":
-            os.environ["SSD_BLOCK_POST"] = "separate"
+            ssd.ssd_set_tuning("separate_block_post", 1)
         try:
             for i in range(args.warmup):
                 call(i, mode)
@@ -234,7 +234,7 @@ def block_bench(args, torch, ssd):
             t1.record(stream)
             torch.cuda.synchronize()
         finally:
-            os.environ.pop("SSD_BLOCK_POST", None)
+            ssd.ssd_set_tuning("separate_block_post", 0)
         return t0.elapsed_time(t1) / args.steps
 
     ms = timed("block")
@@ -280,9 +280,13 @@ def backward_counts(p):
       state dimension), C B^T once per group, and three state-sized products
       per token (Gn B, Gn^T x~, h_in^T dy);
     * bytes: the backward's compulsory bytes (x, dt, B, C, dy read; dx, ddt,
-      dB, dC written; A_log, D and their gradients) plus the two chunk-state
-      arrays the kernel reads (h_in and Gn per chunk and head, P x N each, bf16
-      on the matrix-core path, float32 otherwise)."""
+      dB, dC written; A_log, D and their gradients).  The two chunk-state
+      arrays the kernel also reads (h_in and Gn per chunk and head, P x N each,
+      bf16 on the matrix-core path, float32 otherwise) are intermediates of
+      this design, not of the problem: returned separately, never counted as
+      algorithmic bytes.
+
+    Returns (flops, algorithmic bytes, chunk-state bytes, Qb)."""
     b, T, H, P, N, G = p.batch, p.seqlen, p.nheads, p.headdim, p.dstate, p.ngroups
     fast = backward_fast(p)
     Qb = 64 if fast else 32
@@ -292,7 +296,7 @@ def backward_counts(p):
     act = 2 if p.dtype == "bf16" else 4
     compulsory = act * (3 * b * T * H * P + 2 * b * T * H + 4 * b * T * G * N) + 4 * 4 * H
     states = 2 * b * nC * H * P * N * (2 if fast else 4)
-    return flops, compulsory + states, compulsory, Qb
+    return flops, compulsory, states, Qb
 
 
 def backward_bench(args, torch, ssd):
@@ -301,7 +305,7 @@ def backward_bench(args, torch, ssd):
     import numpy as np
 
     from paper_2405_21060_amd.inputs import WORKLOADS, make_grad_inputs, make_inputs
-    from tests.ssd_harness import act_to_device, to_device
+    from paper_2405_21060_amd.device import act_to_device, to_device
 
     p = WORKLOADS[args.workload]
     inp = make_inputs(p, args.seed)
@@ -373,7 +377,8 @@ def backward_bench(args, torch, ssd):
                "p90": ks[(9 * len(ks)) // 10]}
     else:   # one call per sequence inside: no single chunk kernel to bracket; whole-call time
         kms = {"mean": ms, "p10": ms, "p50": ms, "p90": ms}
-    flops, kbytes, compulsory, Qb = backward_counts(p)
+    flops, kbytes, state_bytes, Qb = backward_counts(p)
+    compulsory = kbytes
     ksec = kms["mean"] * 1e-3
     tokens = p.batch * p.seqlen
     fast = backward_fast(p)
@@ -395,6 +400,7 @@ def backward_bench(args, torch, ssd):
     roof["kernel_ms"] = kms
     roof["algorithmic_bytes"] = kbytes
     roof["algorithmic_flops"] = flops
+    roof["chunk_state_bytes"] = state_bytes   # design intermediates: in traffic, not in achieved
     print(json.dumps({
         "metric": "SSD bwd tokens/s (gradients of the %s, 1 GPU)" % (
             "2.7B-layer shape" if args.workload == "mamba2_2p7b" else args.workload + " workload"),
@@ -418,7 +424,7 @@ def block_backward_bench(args, torch, ssd):
     normalisation groups with weight; dout seeded, no initial state, no
     final-state gradient."""
     from paper_2405_21060_amd.inputs import WORKLOADS, make_block_inputs, make_grad_inputs
-    from tests.ssd_harness import act_to_device
+    from paper_2405_21060_amd.device import act_to_device
 
     p = WORKLOADS[args.workload]
     bi = make_block_inputs(p, args.seed)
@@ -465,7 +471,7 @@ def block_backward_bench(args, torch, ssd):
     t1.record(stream)
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / args.steps
-    _, _, compulsory, Qb = backward_counts(p)
+    _, compulsory, _, Qb = backward_counts(p)
     tokens = p.batch * p.seqlen
     act = 2 if p.dtype == "bf16" else 4
     byts = compulsory + 2 * act * tokens * p.nheads * p.headdim + 8 * p.nheads * p.headdim   # z, dz, w, dw
@@ -493,7 +499,7 @@ def cp_bench(args, torch, ssd):
     exchange of (decay, state) pairs between GPUs is not implemented here;
     the combine of all 8 pairs runs here on one GPU and is timed apart)."""
     from paper_2405_21060_amd.inputs import Problem, make_inputs
-    from tests.ssd_harness import to_device
+    from paper_2405_21060_amd.device import to_device
 
     R = 8
     p = Problem(4, 4096 // R, 80, 64, 128, 1, 256, "bf16", init_states=True)
@@ -617,7 +623,7 @@ def main():
 
     from paper_2405_21060_amd import ssd
     from paper_2405_21060_amd.inputs import WORKLOADS, make_inputs
-    from tests.ssd_harness import to_device
+    from paper_2405_21060_amd.device import to_device
 
     if args.decode:
         return decode_bench(args, torch, ssd)

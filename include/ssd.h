@@ -40,9 +40,11 @@
  * Ownership: every pointer is device memory owned by the caller; the library
  * allocates nothing on the call path.  `workspace` is caller-provided device
  * memory of at least ssd_workspace_bytes() bytes; its contents on entry do not
- * matter and on exit are unspecified.  The call is asynchronous on `stream`
- * (a hipStream_t; NULL = the null stream); it keeps no global mutable state, so
- * concurrent calls with distinct workspaces are safe.  Results are
+ * matter, and on exit only its first int is specified: the status word that
+ * ssd_workspace_status() reads.  The call is asynchronous on `stream`
+ * (a hipStream_t; NULL = the null stream); it keeps no global mutable state
+ * (apart from the test settings of ssd_set_tuning), so concurrent calls with
+ * distinct workspaces are safe.  Results are
  * deterministic (no floating-point atomics).
  *
  * Errors: functions return SSD_OK (0) or a negative ssd_status.  On error no
@@ -77,7 +79,12 @@ typedef enum {
     SSD_ERR_WORKSPACE = -7,        /* workspace NULL or smaller than required        */
     SSD_ERR_LAUNCH = -8,           /* a kernel launch failed                         */
     SSD_ERR_TOO_LARGE = -9,        /* a tensor exceeds the supported index range     */
-    SSD_ERR_BAD_OPTION = -10       /* an ssd_block_opts field out of range           */
+    SSD_ERR_BAD_OPTION = -10,      /* an ssd_block_opts field out of range, or an
+                                      unknown ssd_set_tuning name or value           */
+    SSD_ERR_STATE_TIMEOUT = -11    /* reported by ssd_workspace_status only: a chunk
+                                      kernel's wait for the state of the chunk before
+                                      it gave up; that call's y and final_states are
+                                      wrong                                          */
 } ssd_status;
 
 typedef struct {
@@ -362,6 +369,53 @@ int ssd_backward_block(const ssd_problem* prob, const ssd_block_opts* opts,
                        float* dD, float* dinitial_states,
                        float* ddt_bias, void* dz, float* dnorm_weight,
                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Status of the state passing of the last call that used `workspace`.
+ *
+ * On the fused path the chunk kernel passes each chunk's final state to the
+ * next chunk's workgroup through device memory (the centre factors of
+ * Section 6, as the sequential scan of Appendix B): a workgroup waits for the
+ * state of the chunk before it.  That wait is bounded (2^22 polls with a short
+ * sleep in between, far beyond any normal wait) so that a fault can never hang
+ * the GPU; when it gives up, the kernel sets the status word, the first int of
+ * the workspace, and finishes with a wrong entering state.  Every call of
+ * ssd_forward, ssd_forward_timed, ssd_forward_block(_timed),
+ * ssd_forward_varlen and ssd_backward_block writes that word (0 when no wait
+ * gave up); the general path, which has no such wait, writes 0.
+ *
+ * ssd_workspace_status waits for `stream` (a hipStream_t) to finish, then
+ * reads the word: SSD_OK, SSD_ERR_STATE_TIMEOUT, SSD_ERR_NULL_ARG (workspace
+ * NULL) or SSD_ERR_LAUNCH (the synchronisation or the read failed).  After any
+ * other call on the workspace the result is unspecified. */
+int ssd_workspace_status(const void* workspace, void* stream);
+
+/* Testing and measurement hook; normal use never needs it.  Overrides one of
+ * the library's internal choices for every later call in this process, until
+ * it is set back to 0 (each choice's default: the library decides).  The
+ * results stay within the stated tolerances whatever the setting; only the
+ * kernels and launch shapes that compute them change.
+ *   "force_general_path"   1: every call takes the general kernels (one
+ *                          launch per step of Section 6), also where the
+ *                          fused or matrix-core kernels apply
+ *   "heads_per_item"       k >= 1: heads per work item of the fused chunk
+ *                          kernel (ignored unless k divides nheads/ngroups)
+ *   "early_state_flag"     1: a chunk's state flag is set after its output
+ *                          stage, 2: right after its state is stored
+ *   "max_workgroups"       k >= 1: at most k persistent workgroups of the
+ *                          fused chunk kernel
+ *   "separate_block_post"  1: the block's gate and normalisation always run
+ *                          as their own pass over y
+ *   "bwd_heads_per_slice"  k >= 1: heads per workgroup of the backward's
+ *                          per-chunk gradient kernel
+ *   "varlen_per_sequence"  1: ssd_forward_varlen and ssd_backward_varlen run
+ *                          one problem per sequence
+ *   "state_wait_limit"     k >= 1: polls before a state wait gives up (see
+ *                          ssd_workspace_status; 1 gives up at the first
+ *                          poll that finds the state missing)
+ * Returns SSD_OK, SSD_ERR_NULL_ARG, or SSD_ERR_BAD_OPTION (unknown name, or a
+ * value out of range).  The settings are process-wide and not ordered with
+ * calls made concurrently on other host threads. */
+int ssd_set_tuning(const char* name, int64_t value);
 
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);

@@ -121,22 +121,29 @@ def forward_inputs(inp, heads=None, nthreads=None):
 
     ``heads`` optionally selects a subset of heads (the result then covers
     only those heads, in that order).  Heads of one group share B and C, so a
-    subset is computed exactly as in the full run.
+    subset is computed exactly as in the full run: each selected head gets
+    its own copy of its group's B and C.  Only the selected slices are
+    widened to float64.
     """
+    from paper_2405_21060_amd.inputs import bf16_bits_to_f32
+
+    def f64(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return bf16_bits_to_f32(a).astype(np.float64)
+        return a.astype(np.float64)
+
     p = inp.problem
-    x, dt, B, C = (inp.as_f64(n) for n in ("x", "dt", "B", "C"))
-    A_log = inp.A_log.astype(np.float64)
-    D = inp.D.astype(np.float64)
-    init = inp.initial_states
+    x, dt, B, C = inp.x, inp.dt, inp.B, inp.C
+    A_log, D, init = inp.A_log, inp.D, inp.initial_states
     if heads is not None:
         heads = np.asarray(heads)
-        hpg = p.nheads // p.ngroups
-        groups = heads // hpg
-        # give every selected head its own group so the mapping stays exact
+        groups = heads // (p.nheads // p.ngroups)
         x, dt = x[:, :, heads], dt[:, :, heads]
         B, C = B[:, :, groups], C[:, :, groups]
         A_log, D = A_log[heads], D[heads]
         if init is not None:
             init = init[:, heads]
-    return forward(x, dt, A_log, B, C, D, init, inp.seq_idx, nseq=inp.nseq,
-                   nthreads=nthreads)
+    return forward(f64(x), f64(dt), f64(A_log), f64(B), f64(C), f64(D), f64(init), inp.seq_idx,
+                   nseq=inp.nseq, nthreads=nthreads)

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -72,23 +73,28 @@ int validate(const ssd_problem* prob, bool has_seq_idx, Shape* s)
 
 constexpr int64_t kMaxElemsPublic = kMaxElems;
 
+// Process-wide overrides of internal choices (ssd_set_tuning); 0 = automatic.
+namespace {
+std::atomic<int64_t> g_tuning[kTuneCount];
+}
+
+int64_t tuning(Tuning k) { return g_tuning[k].load(std::memory_order_relaxed); }
+
+
 // Heads per work item of the fused path: a divisor of the heads per group (an
 // item's heads share B and C).  More heads per item share more of the item's
 // set-up (Gram tiles, B^T and C fragments); fewer give more items.  The
 // largest of 4, 2 that leaves at least two items per compute unit (measured
 // best at the 2.7B layer shape), else the largest that leaves one, else 1;
 // then a divisor up to 6 that fills whole rounds where that is clearly cheaper
-// (below).  SSD_HEADS_PER_WG overrides it
-// (tuning knob; ignored unless it divides the heads per group).
+// (below).  The heads_per_item tuning overrides it (ignored unless it divides
+// the heads per group).
 // chunks in flight from which a chunk's state flag is set early (see forward_impl)
 constexpr int64_t kEarlyFlagChunks = 8;
 
 int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units)
 {
-    if (const char* env = std::getenv("SSD_HEADS_PER_WG")) {
-        const long v = std::strtol(env, nullptr, 10);
-        if (v >= 1 && heads_per_group % v == 0) return v;
-    }
+    if (const int64_t v = tuning(kTuneHeadsPerItem); v >= 1 && heads_per_group % v == 0) return v;
     // items_per_head: chunks x batch rows x groups, the items at one head per item
     int64_t hg = 1;
     bool found = false;
@@ -124,7 +130,7 @@ WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int
                                  int64_t Q, int64_t nC)
 {
     WorkspaceLayout w;
-    size_t off = 0;
+    size_t off = kWorkspaceHeader;   // the status word sits in the header
     w.cs = off;
     off = align_up(off + sizeof(float) * static_cast<size_t>(b * H * nC * Q));
     w.info = off;
@@ -201,7 +207,8 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
                  const float* A_log, const void* B, const void* C, const float* D,
                  const float* initial_states, const int32_t* seq_idx, void* y, float* final_states,
                  void* workspace, size_t workspace_bytes, void* stream, hipEvent_t ev_begin,
-                 hipEvent_t ev_end, const ssd::SeqStartsArg* arg_starts = nullptr)
+                 hipEvent_t ev_end, const ssd::SeqStartsArg* arg_starts = nullptr, int* status = nullptr,
+                 bool reset_status = true)
 {
     // arg_starts (a packed row by host offsets, instead of seq_idx): only on the
     // fused path, which the caller has checked; the workspace is its layout
@@ -227,8 +234,9 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
     gn.weight = opts ? opts->norm_weight : nullptr;
     gn.eps = opts ? opts->norm_eps : 0.f;
     const bool post = gn.z || gn.group > 0;
-    const char* path = std::getenv("SSD_PATH");  // debug knob: "unfused" forces the step-by-step kernels
-    const bool force_unfused = path && path[0] == 'u';
+    const bool force_unfused = ssd::tuning(ssd::kTuneForceGeneral) == 1;
+    // status word: in the workspace's header unless the caller keeps it elsewhere
+    if (!status) status = static_cast<int*>(workspace);
     if (arg_starts ||
         (!force_unfused && ssd::fused_supported(s.P, s.N, s.Q, s.bf16) && (!seq_idx || fused_packed_ok(prob)))) {
         const int64_t nseq = seq_idx || arg_starts ? s.nseq : 0;
@@ -248,10 +256,14 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.HG = ssd::heads_per_workgroup(s.H / s.G, fw.nC * s.b * s.G, cus);
         // Chunks of one chain the chip holds at once: with many of them the
         // chain's latency bounds the launch, and each chunk publishes its state
-        // before its left factor.  SSD_EARLY_FLAG=0/1 overrides (measurement knob).
+        // before its left factor.  The early_state_flag tuning overrides it.
         const int64_t per_chunk = s.b * (s.H / f.HG);
         f.early_flag = cus >= ssd::kEarlyFlagChunks * per_chunk ? 1 : 0;
-        if (const char* ef = std::getenv("SSD_EARLY_FLAG")) f.early_flag = ef[0] == '1' ? 1 : 0;
+        if (const int64_t ef = ssd::tuning(ssd::kTuneEarlyFlag); ef == 1 || ef == 2) f.early_flag = ef == 2;
+        f.status = status;
+        f.reset_status = reset_status ? 1 : 0;
+        if (const int64_t sl = ssd::tuning(ssd::kTuneStateWaitLimit); sl >= 1) f.spin_limit = sl;
+        f.max_workgroups = static_cast<int>(ssd::tuning(ssd::kTuneMaxWorkgroups));
         f.x = x;
         f.dt = dt;
         f.A_log = A_log;
@@ -280,10 +292,9 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         // The chunk kernel gates, and normalises one-head groups, in its output
         // stage.  Wider groups take one more pass, which then also gates (z is
         // read once either way, and gating in that pass measured faster than in
-        // the chunk kernel).  SSD_BLOCK_POST=separate (a measurement knob) leaves
-        // gate and normalisation to that pass in every case.
-        const char* bp = std::getenv("SSD_BLOCK_POST");
-        const bool separate = bp && bp[0] == 's';
+        // the chunk kernel).  The separate_block_post tuning leaves gate and
+        // normalisation to that pass in every case.
+        const bool separate = ssd::tuning(ssd::kTuneSeparatePost) == 1;
         if (post && !separate && (gn.group == 0 || gn.group == s.P)) {
             f.z = gn.z;
             if (gn.group == s.P) {
@@ -327,6 +338,7 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
     p.gram = reinterpret_cast<float*>(ws + w.gram);
     p.states = reinterpret_cast<float*>(ws + w.states);
     p.dtx = dtx;
+    p.status = reset_status ? status : nullptr;
     hipError_t err = ssd::launch_unfused(p, s.bf16, static_cast<hipStream_t>(stream), ev_begin, ev_end);
     if (err == hipSuccess && post) err = ssd::launch_gate_norm(gn, s.bf16, static_cast<hipStream_t>(stream));
     return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
@@ -503,12 +515,11 @@ namespace {
 
 // Shape checks of the backward: those of ssd_forward without packed rows; the
 // chunk size is not used (the backward has its own decomposition).
-// The matrix-core path where it applies; SSD_PATH=unfused (a debug knob, as
+// The matrix-core path where it applies; the force_general_path tuning (as
 // for the forward) forces the general one.
 bool backward_fast(const ssd::Shape& s)
 {
-    const char* path = std::getenv("SSD_PATH");
-    if (path && std::strcmp(path, "unfused") == 0) return false;
+    if (ssd::tuning(ssd::kTuneForceGeneral) == 1) return false;
     return ssd::bwd_fast_supported(s.bf16, s.P, s.N);
 }
 
@@ -532,12 +543,9 @@ int backward_plan(const ssd_problem* prob, ssd::BwdParams* p, ssd::BwdLayout* l,
     if (static_cast<double>(p->b) * p->nC * p->H * p->P * p->N > 16.0 * ssd::kMaxElemsPublic)
         return SSD_ERR_TOO_LARGE;
     ssd::bwd_slices(p->b, p->nC, p->G, p->H / p->G, &p->S, &p->hs);
-    if (const char* env = std::getenv("SSD_BWD_HEADS_PER_SLICE")) {   // debug knob
-        const long v = std::strtol(env, nullptr, 10);
-        if (v >= 1) {
-            p->hs = v < p->H / p->G ? v : p->H / p->G;
-            p->S = (p->H / p->G + p->hs - 1) / p->hs;
-        }
+    if (const int64_t v = ssd::tuning(ssd::kTuneBwdHeadsPerSlice); v >= 1) {
+        p->hs = v < p->H / p->G ? v : p->H / p->G;
+        p->S = (p->H / p->G + p->hs - 1) / p->hs;
     }
     *l = ssd::bwd_layout(p->b, p->T, p->H, p->P, p->N, p->G, p->nC, p->S, *fast);
     return SSD_OK;
@@ -651,7 +659,7 @@ int block_backward_plan(const ssd_problem* prob, const ssd_block_opts* opts, Blo
     const size_t nch = static_cast<size_t>(ssd::block_bwd_row_chunks(static_cast<int64_t>(rows)));
     if (nch > 65535) return SSD_ERR_TOO_LARGE;   // row chunks on grid y
     const size_t groups = opts->norm_group_size > 0 ? Cc / static_cast<size_t>(opts->norm_group_size) : 0;
-    size_t off = 0;
+    size_t off = ssd::kWorkspaceHeader;   // the recomputed forward's status word sits in the header
     const auto take = [&](size_t bytes) {
         const size_t o = off;
         off += ssd::align_up(bytes);
@@ -738,7 +746,7 @@ extern "C" int ssd_backward_block(const ssd_problem* prob, const ssd_block_opts*
     // 1. the dt step; 2. the layer's output, recomputed
     if (ssd::launch_block_dt_apply(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
     rc = forward_impl(prob, nullptr, x, p.dt, A_log, B, C, D, initial_states, nullptr, ws + l.y, nullptr,
-                      ws + l.shared, shared_bytes, stream, nullptr, nullptr);
+                      ws + l.shared, shared_bytes, stream, nullptr, nullptr, nullptr, reinterpret_cast<int*>(ws));
     if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
     // 3. gate and normalisation: dy (the block's output gradient when neither is on)
     const bool post = opts->z || opts->norm_group_size > 0;
@@ -769,9 +777,7 @@ struct PackedBwdLayout {
 
 bool packed_backward_ok(const ssd_problem* prob)
 {
-    const char* per = std::getenv("SSD_VARLEN_PER_SEQUENCE");
-    const char* path = std::getenv("SSD_PATH");
-    if ((per && per[0] == '1') || (path && path[0] == 'u')) return false;
+    if (ssd::tuning(ssd::kTuneVarlenPerSequence) == 1 || ssd::tuning(ssd::kTuneForceGeneral) == 1) return false;
     ssd_problem q = *prob;
     q.chunk_size = 256;
     ssd::Shape s;
@@ -946,13 +952,11 @@ namespace {
 
 // One launch over the whole packed row (the fused kernels' chunk table, the
 // offsets handed over by value) where the shape and the number of sequences
-// allow; else one call per sequence.  SSD_VARLEN_PER_SEQUENCE=1 forces the
-// latter (a test and measurement knob).
+// allow; else one call per sequence.  The varlen_per_sequence tuning forces
+// the latter.
 bool varlen_one_launch(const ssd_problem* prob)
 {
-    const char* path = std::getenv("SSD_PATH");
-    const char* per = std::getenv("SSD_VARLEN_PER_SEQUENCE");
-    if ((path && path[0] == 'u') || (per && per[0] == '1')) return false;
+    if (ssd::tuning(ssd::kTuneForceGeneral) == 1 || ssd::tuning(ssd::kTuneVarlenPerSequence) == 1) return false;
     ssd::Shape s;
     if (ssd::validate(prob, true, &s) != SSD_OK) return false;
     return ssd::fused_supported(s.P, s.N, s.Q, s.bf16) && fused_packed_ok(prob) && prob->nseq <= ssd::kArgSeqs;
@@ -1025,7 +1029,8 @@ extern "C" int ssd_forward_varlen(const ssd_problem* prob, const int64_t* seq_st
                           static_cast<const char*>(B) + t0 * GN * act, static_cast<const char*>(C) + t0 * GN * act,
                           D, initial_states ? initial_states + q * HPN : nullptr, nullptr,
                           static_cast<char*>(y) + t0 * HP * act, final_states ? final_states + q * HPN : nullptr,
-                          workspace, workspace_bytes, stream, nullptr, nullptr);
+                          workspace, workspace_bytes, stream, nullptr, nullptr, nullptr, nullptr,
+                          /*reset_status=*/q == 0);
         // the first call validates everything the later ones check (same shapes
         // but for seqlen): an error after it is a launch failure
         if (rc != SSD_OK) return q == 0 ? rc : SSD_ERR_LAUNCH;
@@ -1047,7 +1052,46 @@ extern "C" const char* ssd_error_string(int code)
     case SSD_ERR_WORKSPACE: return "workspace missing or smaller than ssd_workspace_bytes()";
     case SSD_ERR_LAUNCH: return "kernel launch failed";
     case SSD_ERR_TOO_LARGE: return "problem exceeds the supported index range";
-    case SSD_ERR_BAD_OPTION: return "block option out of range (dt clamp, norm group size or eps)";
+    case SSD_ERR_BAD_OPTION: return "option out of range (block option, or unknown tuning name or value)";
+    case SSD_ERR_STATE_TIMEOUT:
+        return "a chunk's wait for the state of the chunk before it gave up: y and final_states are wrong";
     default: return "unknown ssd status";
     }
+}
+
+extern "C" int ssd_workspace_status(const void* workspace, void* stream)
+{
+    if (!workspace) return SSD_ERR_NULL_ARG;
+    int word = 0;
+    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess ||
+        hipMemcpy(&word, workspace, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+        return SSD_ERR_LAUNCH;
+    return word == 0 ? SSD_OK : SSD_ERR_STATE_TIMEOUT;
+}
+
+extern "C" int ssd_set_tuning(const char* name, int64_t value)
+{
+    if (!name) return SSD_ERR_NULL_ARG;
+    struct Entry {
+        const char* name;
+        ssd::Tuning k;
+        int64_t lo, hi;
+    };
+    static const Entry table[] = {
+        {"force_general_path", ssd::kTuneForceGeneral, 0, 1},
+        {"heads_per_item", ssd::kTuneHeadsPerItem, 0, 1 << 16},
+        {"early_state_flag", ssd::kTuneEarlyFlag, 0, 2},
+        {"max_workgroups", ssd::kTuneMaxWorkgroups, 0, 1 << 20},
+        {"separate_block_post", ssd::kTuneSeparatePost, 0, 1},
+        {"bwd_heads_per_slice", ssd::kTuneBwdHeadsPerSlice, 0, 1 << 16},
+        {"varlen_per_sequence", ssd::kTuneVarlenPerSequence, 0, 1},
+        {"state_wait_limit", ssd::kTuneStateWaitLimit, 0, INT64_MAX},
+    };
+    for (const Entry& e : table)
+        if (std::strcmp(name, e.name) == 0) {
+            if (value < e.lo || value > e.hi) return SSD_ERR_BAD_OPTION;
+            ssd::g_tuning[e.k].store(value, std::memory_order_relaxed);
+            return SSD_OK;
+        }
+    return SSD_ERR_BAD_OPTION;
 }

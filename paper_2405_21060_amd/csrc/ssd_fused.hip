@@ -1,5 +1,7 @@
 // Fused SSD forward for the Mamba-2 layer shapes: bf16 activations, head
-// dimension P = 64, state N in {64, 128}, chunk Q = 256, no packed rows.
+// dimension P = 64, state N in {64, 128}, chunk Q = 256; plain rows, or one
+// packed row of sequences (Section 8.3) through a chunk table built on the
+// device.
 //
 // Two launches per call.
 //
@@ -41,7 +43,9 @@
 // needed because every access to shared data is device-coherent.  Workgroups
 // take their work item from a ticket counter in dispatch order, so a
 // workgroup only ever waits on an item already owned by a running or finished
-// workgroup; the wait is additionally bounded (a timeout sets an error word).
+// workgroup; the wait is additionally bounded: when it gives up it sets the
+// call's status word (which the host reads back as SSD_ERR_STATE_TIMEOUT)
+// and goes on, so that every wavefront still exits.
 // Two ring slots suffice: chunk c+2 overwrites the slot of chunk c only after
 // reading the state of chunk c+1, which chunk c+1 published only after it had
 // read (consumed) the state of chunk c.
@@ -62,7 +66,6 @@ constexpr int kP = 64;                        // head dimension
 constexpr int kWaves = 8;
 constexpr int kMainThreads = kWaves * 64;
 constexpr int kPrepThreads = 512;
-constexpr long long kSpinLimit = 1LL << 22;   // polls (with s_sleep) before giving up
 
 typedef unsigned short u16;
 typedef uint32_t u32;
@@ -286,7 +289,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
     const int hpg = static_cast<int>(p.H / p.G);
     if (blockIdx.z == 0 && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
         p.ticket[0] = 0;
-        p.ticket[1] = 0;  // error word: set when a state wait times out
+        if (p.reset_status) *p.status = 0;   // set by the chunk kernel when a state wait gives up
     }
     int64_t c0 = static_cast<int64_t>(c) * kQ;
     int L = static_cast<int>(kQ < p.T - c0 ? kQ : p.T - c0);
@@ -942,11 +945,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         const int* flag = p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + (c - 1);
         long long spins = 0;
         while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-            __builtin_amdgcn_s_sleep(2);
-            if (++spins > kSpinLimit) {
-                __hip_atomic_store(p.ticket + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (++spins >= p.spin_limit) {   // give up: report it, never hang
+                __hip_atomic_store(p.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 break;
             }
+            __builtin_amdgcn_s_sleep(2);
         }
     }
     lds_barrier();   // flag seen by tid 0
@@ -1250,12 +1253,9 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     if (err != hipSuccess) return err;
     const int64_t nwork = p.nC * p.b * (p.H / p.HG);
     // one persistent workgroup per compute unit (the LDS footprint allows one);
-    // SSD_MAX_WORKGROUPS caps it (a test knob: few workgroups, many items each)
+    // p.max_workgroups caps it (a test setting: few workgroups, many items each)
     int64_t grid = nwork < cus ? nwork : cus;
-    if (const char* cap = std::getenv("SSD_MAX_WORKGROUPS")) {
-        const long v = std::strtol(cap, nullptr, 10);
-        if (v >= 1 && v < grid) grid = v;
-    }
+    if (p.max_workgroups >= 1 && p.max_workgroups < grid) grid = p.max_workgroups;
     const dim3 g_main(static_cast<unsigned>(grid));
     const float* A_logp = p.A_log;
     const float* Dp = p.D;
@@ -1311,7 +1311,7 @@ FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, 
     // between chunks, and there are fewer of them than chunks.
     w.nC = nseq > 0 ? std::min(nC + nseq - 1, T) : nC;
     w.ring_rows = nseq > 0 ? std::min(nseq, nC) : b;
-    size_t off = 0;
+    size_t off = kWorkspaceHeader;   // the status word sits in the header
     w.gram = off;
     off = al(off + sizeof(u16) * static_cast<size_t>(b * G * w.nC) * kTiles * 256);
     w.BT = off;
@@ -1321,7 +1321,7 @@ FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, 
     w.flags = off;
     off = al(off + sizeof(int) * static_cast<size_t>(b * H * w.nC));
     w.ticket = off;
-    off = al(off + 4 * sizeof(int));   // ticket, error word, table entries
+    off = al(off + 4 * sizeof(int));   // ticket, (unused), table entries
     w.starts = off;
     off = al(off + sizeof(int) * static_cast<size_t>(nseq > 0 ? nseq + 1 : 0));
     w.vtab = off;

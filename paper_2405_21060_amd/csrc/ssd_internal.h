@@ -8,6 +8,29 @@
 
 namespace ssd {
 
+// Internal choices a test or a measurement may override for the whole process
+// (ssd_set_tuning in the C ABI; every value 0 = the library's own choice).
+enum Tuning {
+    kTuneForceGeneral = 0,   // 1: the general step-by-step kernels for every call
+    kTuneHeadsPerItem,       // heads per work item of the fused chunk kernel
+    kTuneEarlyFlag,          // 1: state flag after the output stage, 2: right after the state store
+    kTuneMaxWorkgroups,      // cap on the fused chunk kernel's persistent workgroups
+    kTuneSeparatePost,       // 1: gate and normalisation always in their own output pass
+    kTuneBwdHeadsPerSlice,   // heads per workgroup of the backward's chunk kernel
+    kTuneVarlenPerSequence,  // 1: packed rows by host offsets run one call per sequence
+    kTuneStateWaitLimit,     // polls before a chunk's wait for the state before it gives up
+    kTuneCount
+};
+int64_t tuning(Tuning k);
+
+// Polls (each followed by a short sleep) before a chunk kernel's wait for the
+// state of the chunk before it gives up and reports SSD_ERR_STATE_TIMEOUT.
+constexpr int64_t kDefaultSpinLimit = 1LL << 22;
+
+// Every workspace begins with a 256-byte header; its first int is the status
+// word of the last forward that used it (0 = fine, 1 = a state wait gave up).
+constexpr size_t kWorkspaceHeader = 256;
+
 // dt parameterisation of the block path: dt = clamp(softplus?(dt_in + bias)).
 // `active` false = dt is used as given (the plain layer).
 struct DtTransform {
@@ -36,6 +59,7 @@ struct Params {
     float* gram;     // (b, G, nC, Q, Q) C B^T per chunk (lower block triangle only)
     float* states;   // (b, nC, H, P, N) chunk states, then states entering each chunk
     DtTransform dtx;
+    int* status = nullptr;   // status word, zeroed by the first kernel when not null
 };
 
 struct WorkspaceLayout {
@@ -52,7 +76,7 @@ WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int
 hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream,
                           hipEvent_t ev_begin, hipEvent_t ev_end);
 
-// Fused path (bf16, P = 64, N in {64, 128}, Q = 256, no packed rows).
+// Fused path (bf16, P = 64, N in {64, 128}, Q = 256; plain rows or one packed row).
 // Sequence starts of a packed row handed to the device by value (kernel
 // argument) when the caller gives them in host memory: n sequences, v[0..n].
 constexpr int kArgSeqs = 511;
@@ -77,7 +101,11 @@ struct FusedParams {
     uint16_t* BT;     // (b, G, nC, N, Q) B^T per chunk, bf16
     float* ring;      // (b, H, 2, P, N) chunk-state ring
     int* flags;       // (b, H, nC)      state-published flags
-    int* ticket;      // [0] work ticket, [1] wait-timeout error word
+    int* ticket;      // [0] work ticket, [2] chunk table entries of a packed row
+    int* status;      // set to 1 when a state wait gives up (zeroed first when reset_status)
+    int reset_status = 1;
+    int64_t spin_limit = kDefaultSpinLimit;
+    int max_workgroups = 0;   // > 0: cap on the chunk kernel's persistent workgroups
     DtTransform dtx;
     // Packed row (batch 1) with device seq_idx: every sequence is cut into
     // chunks of its own (the last one partial), listed in token order in a

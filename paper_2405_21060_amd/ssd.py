@@ -34,6 +34,7 @@ SSD_ERR_WORKSPACE = -7
 SSD_ERR_LAUNCH = -8
 SSD_ERR_TOO_LARGE = -9
 SSD_ERR_BAD_OPTION = -10
+SSD_ERR_STATE_TIMEOUT = -11
 
 EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
             "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
@@ -41,7 +42,8 @@ EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_deco
             "ssd_backward_workspace_bytes", "ssd_backward", "ssd_backward_timed",
             "ssd_backward_varlen_workspace_bytes", "ssd_backward_varlen",
             "ssd_forward_varlen_workspace_bytes", "ssd_forward_varlen",
-            "ssd_backward_block_workspace_bytes", "ssd_backward_block", "ssd_error_string")
+            "ssd_backward_block_workspace_bytes", "ssd_backward_block", "ssd_workspace_status",
+            "ssd_set_tuning", "ssd_error_string")
 
 
 class SsdProblem(ctypes.Structure):
@@ -138,6 +140,10 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_backward_block.argtypes = [pp, ctypes.POINTER(SsdBlockOpts)] + [vp] * 19 + [vp, ctypes.c_size_t, vp]
     lib.ssd_backward_block.restype = ctypes.c_int
     lib.ssd_error_string.argtypes = [ctypes.c_int]
+    lib.ssd_workspace_status.argtypes = [vp, vp]
+    lib.ssd_workspace_status.restype = ctypes.c_int
+    lib.ssd_set_tuning.argtypes = [ctypes.c_char_p, ctypes.c_int64]
+    lib.ssd_set_tuning.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -156,6 +162,50 @@ def ssd_workspace_bytes(prob: SsdProblem) -> int:
 
 def ssd_error_string(code: int) -> str:
     return load_library().ssd_error_string(int(code)).decode()
+
+
+def ssd_workspace_status(workspace, stream) -> int:
+    """Raw ABI call (integer device address and hipStream_t); returns the status."""
+    return load_library().ssd_workspace_status(workspace, stream or None)
+
+
+def ssd_set_tuning(name: str, value: int) -> int:
+    """Raw ABI call; returns the status."""
+    return load_library().ssd_set_tuning(name.encode(), int(value))
+
+
+def workspace_status(workspace) -> int:
+    """Status word of the last forward that used ``workspace`` (a device
+    tensor), read after torch's current stream of its device has finished:
+    ``SSD_OK`` or ``SSD_ERR_STATE_TIMEOUT``."""
+    import torch
+
+    stream = torch.cuda.current_stream(workspace.device).cuda_stream
+    rc = ssd_workspace_status(workspace.data_ptr(), stream)
+    if rc not in (SSD_OK, SSD_ERR_STATE_TIMEOUT):
+        raise SsdError(rc, "ssd_workspace_status")
+    return rc
+
+
+class tuning:
+    """Context manager over :func:`ssd_set_tuning`: ``with tuning(max_workgroups=3):``
+    sets the given settings and puts each back to 0 (the library's own
+    choice) on exit."""
+
+    def __init__(self, **settings):
+        self.settings = settings
+
+    def __enter__(self):
+        for k, v in self.settings.items():
+            rc = ssd_set_tuning(k, v)
+            if rc != SSD_OK:
+                raise SsdError(rc, "ssd_set_tuning(%s)" % k)
+        return self
+
+    def __exit__(self, *exc):
+        for k in self.settings:
+            ssd_set_tuning(k, 0)
+        return False
 
 
 def ssd_forward(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx, y,
@@ -180,6 +230,20 @@ def ssd_forward_timed(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, s
 
 def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
+
+
+def _workspace(workspace, need: int, dev):
+    """The caller's workspace (a uint8 device tensor of at least ``need``
+    bytes; a smaller one is an error, so that its status word is the one the
+    call writes), or a new one."""
+    import torch
+
+    if workspace is None:
+        return torch.empty(max(int(need), 1), dtype=torch.uint8, device=dev)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError("workspace holds %d bytes, the call needs %d"
+                         % (workspace.numel() * workspace.element_size(), need))
+    return workspace
 
 
 def ssd_forward_block(prob: SsdProblem, opts: SsdBlockOpts, x, dt, A_log, B, C, D, initial_states,
@@ -242,8 +306,7 @@ def _call(opts, x, dt, A_log, B, C, D, chunk_size, initial_states, seq_idx, nseq
         nseq = int(seq_idx[0, -1].item()) + 1
     prob = make_problem(b, T, H, P, N, G, chunk_size, dtype, nseq or 0)
     wsb = ssd_workspace_bytes(prob)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, wsb, dev)
     y = out if out is not None else torch.empty_like(x)
     units = nseq if seq_idx is not None else b
     fin = None
@@ -391,8 +454,7 @@ def span_correct(dt, A_log, C, entering, y, workspace=None):
     rc = load_library().ssd_span_correct_workspace_bytes(ctypes.byref(prob), ctypes.byref(need))
     if rc != SSD_OK:
         raise SsdError(rc, "ssd_span_correct_workspace_bytes")
-    if workspace is None or workspace.numel() < need.value:
-        workspace = torch.empty(max(int(need.value), 1), dtype=torch.uint8, device=y.device)
+    workspace = _workspace(workspace, int(need.value), y.device)
     rc = load_library().ssd_span_correct(ctypes.byref(prob), _ptr(dt), _ptr(A_log), _ptr(C), _ptr(entering),
                                          _ptr(y), _ptr(workspace), int(need.value),
                                          torch.cuda.current_stream(y.device).cuda_stream)
@@ -454,8 +516,7 @@ def backward(x, dt, A_log, B, C, dy, D=None, initial_states=None, dfinal_states=
     G, N = B.shape[2], B.shape[3]
     prob = make_problem(b, T, H, P, N, G, 256, dtype)
     wsb = ssd_backward_workspace_bytes(prob)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, wsb, dev)
     g = {"dx": torch.empty_like(x), "ddt": torch.empty_like(dt), "dB": torch.empty_like(B),
          "dC": torch.empty_like(C), "dA_log": torch.empty_like(A_log),
          "dD": torch.empty_like(D) if D is not None else None,
@@ -518,8 +579,7 @@ def backward_block(x, dt, A_log, B, C, dout, D=None, initial_states=None, dfinal
     prob = make_problem(b, T, H, P, N, G, 256, SSD_DTYPE_BF16 if x.dtype == torch.bfloat16 else SSD_DTYPE_F32)
     opts = make_block_opts(dt_bias, dt_softplus, dt_min, dt_max, z, norm_weight, norm_group_size, norm_eps)
     wsb = ssd_backward_block_workspace_bytes(prob, opts)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, wsb, dev)
     g = {"dx": torch.empty_like(x), "ddt": torch.empty_like(dt), "dB": torch.empty_like(B),
          "dC": torch.empty_like(C), "dA_log": torch.empty_like(A_log),
          "dD": torch.empty_like(D) if D is not None else None,
@@ -586,8 +646,7 @@ def backward_varlen(x, dt, A_log, B, C, dy, seq_starts, D=None, initial_states=N
     prob = make_problem(1, T, H, P, N, G, 256, SSD_DTYPE_BF16 if x.dtype == torch.bfloat16 else SSD_DTYPE_F32,
                         nseq)
     wsb = ssd_backward_varlen_workspace_bytes(prob, seq_starts)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, wsb, dev)
     g = {"dx": torch.empty_like(x), "ddt": torch.empty_like(dt), "dB": torch.empty_like(B),
          "dC": torch.empty_like(C), "dA_log": torch.empty_like(A_log),
          "dD": torch.empty_like(D) if D is not None else None,
@@ -634,8 +693,7 @@ def forward_varlen(x, dt, A_log, B, C, seq_starts, D=None, chunk_size: int = 256
     prob = make_problem(1, T, H, P, N, G, chunk_size,
                         SSD_DTYPE_BF16 if x.dtype == torch.bfloat16 else SSD_DTYPE_F32, nseq)
     wsb = ssd_forward_varlen_workspace_bytes(prob, seq_starts)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, wsb, dev)
     y = out if out is not None else torch.empty_like(x)
     fin = torch.empty((nseq, H, P, N), dtype=torch.float32, device=dev) if return_final_states else None
     rc = ssd_forward_varlen(prob, seq_starts, _ptr(x), _ptr(dt), _ptr(A_log), _ptr(B), _ptr(C), _ptr(D),

@@ -281,3 +281,20 @@ def test_error_strings(lib):
         s = ssd.ssd_error_string(code)
         assert s and s != "unknown ssd status"
     assert ssd.ssd_error_string(-100) == "unknown ssd status"
+
+
+def test_tuning_hook_validates_names_and_values(lib):
+    assert ssd.ssd_set_tuning("no_such_setting", 1) == ssd.SSD_ERR_BAD_OPTION
+    assert ssd.ssd_set_tuning("force_general_path", 2) == ssd.SSD_ERR_BAD_OPTION
+    assert ssd.ssd_set_tuning("early_state_flag", -1) == ssd.SSD_ERR_BAD_OPTION
+    assert lib.ssd_set_tuning(None, 1) == ssd.SSD_ERR_NULL_ARG
+    for name in ("force_general_path", "heads_per_item", "early_state_flag", "max_workgroups",
+                 "separate_block_post", "bwd_heads_per_slice", "varlen_per_sequence",
+                 "state_wait_limit"):
+        assert ssd.ssd_set_tuning(name, 1) == ssd.SSD_OK, name
+        assert ssd.ssd_set_tuning(name, 0) == ssd.SSD_OK, name
+
+
+def test_workspace_status_null(lib):
+    assert ssd.ssd_workspace_status(0, 0) == ssd.SSD_ERR_NULL_ARG
+    assert "state" in ssd.ssd_error_string(ssd.SSD_ERR_STATE_TIMEOUT)

@@ -89,8 +89,8 @@ CASES = [
     (1, 63, 2, 64, 128, 1, "bf16", True, True, False),
 ]
 
-# shapes of the matrix-core path, also run on the general path (SSD_PATH=unfused),
-# and with heads split into slices of 3 per workgroup (SSD_BWD_HEADS_PER_SLICE)
+# shapes of the matrix-core path, also run on the general path (force_general_path),
+# and with heads split into slices of 3 per workgroup (bwd_heads_per_slice)
 FAST_SHAPES = [
     (2, 257, 6, 64, 128, 2, "bf16", True, True, True),
     (3, 96, 8, 64, 64, 1, "bf16", True, False, True),
@@ -117,11 +117,11 @@ def test_backward_matches_oracle(case):
         assert got["dD"] is None
 
 
-@pytest.mark.parametrize("knob", ["SSD_PATH=unfused", "SSD_BWD_HEADS_PER_SLICE=3"])
+@pytest.mark.parametrize("knob", ["force_general_path=1", "bwd_heads_per_slice=3"])
 @pytest.mark.parametrize("case", FAST_SHAPES, ids=lambda c: "b%d_T%d_H%d_P%d_N%d_G%d_%s_D%d_i%d_f%d" % c)
-def test_backward_knobs_match_oracle(case, knob, monkeypatch):
+def test_backward_knobs_match_oracle(case, knob, tune):
     name, value = knob.split("=")
-    monkeypatch.setenv(name, value)
+    tune(name, int(value))
     test_backward_matches_oracle(case)
 
 
@@ -250,8 +250,8 @@ def test_backward_packed_rows_full_size_head_subset():
     check("dinit", got["dinit"][:, heads], ref["dinit"], tol)
 
 
-def test_backward_packed_rows_per_sequence_forced(monkeypatch):
+def test_backward_packed_rows_per_sequence_forced(tune):
     """The per-sequence launches (forced) at a shape that otherwise runs as
     one launch over the row."""
-    monkeypatch.setenv("SSD_VARLEN_PER_SEQUENCE", "1")
+    tune("varlen_per_sequence", 1)
     test_backward_packed_rows_match_oracle(VARLEN_CASES[0])

@@ -12,7 +12,7 @@ import pytest
 import oracle
 import oracle.block as ob
 from paper_2405_21060_amd.inputs import Problem, make_block_inputs
-from tests.ssd_harness import TOL, announce, rel_err, to_device, to_f64
+from tests.ssd_harness import TOL, announce, forward_workspace, rel_err, to_device, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -43,10 +43,11 @@ def run_block(bi, opts):
     b = bi.base
     p = b.problem
     d = to_device(b)
+    ws = forward_workspace(b)   # the block steps need no workspace of their own
     y, fin = ssd.forward_block(
         d["x"], _act(bi.dt_raw), d["A_log"], d["B"], d["C"], d["D"], chunk_size=p.chunk_size,
         initial_states=d["initial_states"], seq_idx=d["seq_idx"],
-        nseq=b.nseq if b.seq_idx is not None else None,
+        nseq=b.nseq if b.seq_idx is not None else None, workspace=ws,
         dt_bias=torch.from_numpy(bi.dt_bias).cuda() if opts.get("dt_bias", True) else None,
         dt_softplus=opts.get("dt_softplus", True), dt_min=opts.get("dt_lo", 0.0),
         dt_max=opts.get("dt_hi", float("inf")),
@@ -54,6 +55,7 @@ def run_block(bi, opts):
         norm_weight=torch.from_numpy(bi.norm_weight).cuda() if opts.get("norm_weight", True) else None,
         norm_group_size=opts.get("norm_group_size", 0), norm_eps=opts.get("norm_eps", 1e-5))
     torch.cuda.synchronize()
+    assert ssd.workspace_status(ws) == ssd.SSD_OK, "a chunk's state wait gave up"
     return y, fin
 
 
@@ -113,31 +115,31 @@ def test_block_matches_oracle(sname, oname):
 
 @pytest.mark.parametrize("early", ["0", "1"])
 @pytest.mark.parametrize("sname", ["fused_n128", "fused_varlen"])
-def test_block_state_flag_placement(sname, early, monkeypatch):
+def test_block_state_flag_placement(sname, early, tune):
     # the gate and per-head normalisation in the chunk kernel's output stage with
     # either placement of the state flag, few persistent workgroups
-    monkeypatch.setenv("SSD_EARLY_FLAG", early)
-    monkeypatch.setenv("SSD_MAX_WORKGROUPS", "4")
+    tune("early_state_flag", 2 if early == "1" else 1)
+    tune("max_workgroups", 4)
     p = SHAPES[sname]
     check_block(make_block_inputs(p, 14), resolve(OPTS["gate_headnorm"], p), "flag%s/%s" % (early, sname))
 
 
 @pytest.mark.parametrize("oname", ["gate_headnorm", "gate_norm2heads", "rownorm_clamp"])
-def test_block_output_pass_separate(oname, monkeypatch):
+def test_block_output_pass_separate(oname, tune):
     # the fused chunk kernel with gate and normalisation left to the output pass
-    monkeypatch.setenv("SSD_BLOCK_POST", "separate")
+    tune("separate_block_post", 1)
     p = SHAPES["fused_n128"]
     check_block(make_block_inputs(p, 12), resolve(OPTS[oname], p), "separate/" + oname)
 
 
 @pytest.mark.parametrize("oname", ["gate_headnorm", "rownorm_clamp"])
-def test_block_general_path_at_fused_shape(oname, monkeypatch):
-    monkeypatch.setenv("SSD_PATH", "unfused")
+def test_block_general_path_at_fused_shape(oname, tune):
+    tune("force_general_path", 1)
     p = SHAPES["fused_n128"]
     check_block(make_block_inputs(p, 13), resolve(OPTS[oname], p), "unfused/" + oname)
 
 
-def test_block_fused_equals_separate_output_pass(monkeypatch):
+def test_block_fused_equals_separate_output_pass(tune):
     # same inputs through the in-kernel gate/norm and through the output pass:
     # both within bf16 rounding of each other (one extra rounding of y)
     import torch
@@ -147,7 +149,7 @@ def test_block_fused_equals_separate_output_pass(monkeypatch):
     o = resolve(OPTS["gate_headnorm"], p)
     announce("block fused vs separate output pass")
     y1, f1 = run_block(bi, o)
-    monkeypatch.setenv("SSD_BLOCK_POST", "separate")
+    tune("separate_block_post", 1)
     y2, f2 = run_block(bi, o)
     assert torch.equal(f1, f2)   # the states do not depend on the output side
     e = rel_err(to_f64(y1), to_f64(y2))

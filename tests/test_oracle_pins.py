@@ -316,3 +316,21 @@ def test_inputs_are_deterministic_and_in_range():
     lens = np.bincount(v.seq_idx[0])
     assert lens.sum() == 32768 and np.all(lens[:-1] >= 256) and np.all(lens <= 4096)
     assert v.initial_states.shape == (v.nseq, 2, 4, 4)
+
+
+@pytest.mark.parametrize("varlen", [False, True])
+def test_head_subset_equals_all_heads(varlen):
+    """The oracle on a subset of heads (every selected head with its own copy
+    of its group's B and C), in any order, gives exactly the all-heads run's
+    values for those heads: the GPU tests compare full-size workloads head
+    batch by head batch through this path.  With 3 groups of 2 heads, a wrong
+    head -> group map (interleaved, or the subset's own index) would change
+    the result."""
+    p = Problem(1 if varlen else 2, 300, 6, 8, 16, 3, 64, "bf16", varlen=varlen, len_lo=20, len_hi=120,
+                init_states=True)
+    inp = make_inputs(p, 21)
+    y_all, f_all = oracle.forward_inputs(inp)
+    for heads in ([5, 0, 3, 2], [4], list(range(6))):
+        y_sub, f_sub = oracle.forward_inputs(inp, heads=heads)
+        assert np.array_equal(y_sub, y_all[:, :, heads])
+        assert np.array_equal(f_sub, f_all[:, heads])
