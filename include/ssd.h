@@ -349,8 +349,14 @@ int ssd_backward_varlen(const ssd_problem* prob, const int64_t* seq_starts,
  * dfinal_states (NULL = 0).  The paper gives no backward; this is the chain
  * rule through the normalisation, the gate (Section 8.1), the layer
  * (ssd_backward) and the dt step, with the layer's output recomputed from the
- * inputs.  Outputs as for ssd_backward with `ddt` the gradient of `dt` as
- * given (before bias, softplus and clamp), plus
+ * inputs.  What the steps exchange with the layer -- dt after the dt step, the
+ * layer's output, its gradient and the layer's dt gradient -- stays float32
+ * (as in ssd_forward_block), with bf16 activations too: only inputs and
+ * outputs have the activation dtype, and the result is the gradient of
+ * ssd_forward_block itself.  (bf16 at headdim 64 and dstate 64 or 128 runs on
+ * the matrix cores; other bf16 shapes run in float32 on widened copies of the
+ * activations.)  Outputs as for ssd_backward with `ddt` the gradient of `dt`
+ * as given (before bias, softplus and clamp), plus
  *   ddt_bias      (nheads) float32, written when opts->dt_bias (may be NULL)
  *   dz            like y, dtype; required when opts->z
  *   dnorm_weight  (nheads * headdim) float32, written when the normalisation

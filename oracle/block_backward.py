@@ -34,31 +34,16 @@ def sigmoid(v):
     return np.where(v >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
 
 
-def round_bf16(a):
-    """Nearest-even rounding to bfloat16 (of the float32 nearest to ``a``),
-    returned as float64."""
-    u = np.asarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
-
-
 def block_backward(x, dt_raw, A_log, B, C, dout, D=None, initial_states=None, dfinal=None,
                    dt_bias=None, dt_softplus=True, dt_lo=0.0, dt_hi=np.inf, z=None,
-                   norm_weight=None, norm_group_size=0, norm_eps=1e-5, handoff=None):
+                   norm_weight=None, norm_group_size=0, norm_eps=1e-5):
     """Gradients of the block (no packed rows).  Shapes as for
     :func:`oracle.block.block_forward`; ``dout`` (b, T, H, P), ``dfinal``
     (b, H, P, N) or None.  Returns a dict with the layer's gradients (``dx``,
     ``ddt`` is replaced by ``ddt_raw``, ``dA_log``, ``dB``, ``dC``, ``dD``,
     ``dinit``) and ``ddt_bias`` (or None), ``dz`` (or None), ``dnorm_weight``
-    (or None).
-
-    ``handoff="bf16"`` rounds, to bfloat16, the four tensors the block steps
-    exchange with the layer in the activation dtype when the layer runs on
-    bf16 activations (its interface takes dt and dy and returns y and ddt in
-    that dtype): dt after the dt step, the layer's output y, the gradient dy
-    handed to the layer, and the layer's ddt.  Everything else stays
-    float64."""
-    rnd = round_bf16 if handoff == "bf16" else (lambda a: a)
+    (or None).  Float64 throughout, from the given (possibly bf16-valued)
+    inputs: nothing in between is rounded."""
     f = lambda a: None if a is None else np.asarray(a, dtype=np.float64)
     x, dt_raw, A_log, B, C, dout, D, init, dfinal = map(f, (x, dt_raw, A_log, B, C, dout, D,
                                                            initial_states, dfinal))
@@ -68,9 +53,8 @@ def block_backward(x, dt_raw, A_log, B, C, dout, D=None, initial_states=None, df
     # forward, keeping what the backward needs
     v = dt_raw + (bias if bias is not None else 0.0)
     sp = _blk.softplus(v) if dt_softplus else v
-    dt = rnd(np.minimum(np.maximum(sp, dt_lo), dt_hi))
+    dt = np.minimum(np.maximum(sp, dt_lo), dt_hi)
     y, _ = _oracle.forward(x, dt, A_log, B, C, D, init)
-    y = rnd(y)
     g = y * _blk.silu(z) if z is not None else y
 
     # normalisation
@@ -100,11 +84,11 @@ def block_backward(x, dt_raw, A_log, B, C, dout, D=None, initial_states=None, df
         dz = None
 
     # the layer
-    gr = _bwd.backward(x, dt, A_log, B, C, rnd(dy), D=D, initial_states=init, dfinal=dfinal)
+    gr = _bwd.backward(x, dt, A_log, B, C, dy, D=D, initial_states=init, dfinal=dfinal)
 
     # dt step
     mask = (sp > dt_lo) & (sp < dt_hi)
-    dv = rnd(gr["ddt"]) * mask * (sigmoid(v) if dt_softplus else 1.0)
+    dv = gr["ddt"] * mask * (sigmoid(v) if dt_softplus else 1.0)
     out = {k: gr[k] for k in ("dx", "dA_log", "dB", "dC", "dD", "dinit")}
     out["ddt_raw"] = dv
     out["ddt_bias"] = np.sum(dv, axis=(0, 1)) if bias is not None else None

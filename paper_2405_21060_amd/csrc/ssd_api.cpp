@@ -208,8 +208,10 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
                  const float* initial_states, const int32_t* seq_idx, void* y, float* final_states,
                  void* workspace, size_t workspace_bytes, void* stream, hipEvent_t ev_begin,
                  hipEvent_t ev_end, const ssd::SeqStartsArg* arg_starts = nullptr, int* status = nullptr,
-                 bool reset_status = true)
+                 bool reset_status = true, bool y32 = false)
 {
+    // y32 (the layer recomputed for the block gradients): y in float32, on the
+    // fused kernels only (plain rows, chunk 256, no gate or normalisation)
     // arg_starts (a packed row by host offsets, instead of seq_idx): only on the
     // fused path, which the caller has checked; the workspace is its layout
     ssd::Shape s;
@@ -264,6 +266,7 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.reset_status = reset_status ? 1 : 0;
         if (const int64_t sl = ssd::tuning(ssd::kTuneStateWaitLimit); sl >= 1) f.spin_limit = sl;
         f.max_workgroups = static_cast<int>(ssd::tuning(ssd::kTuneMaxWorkgroups));
+        f.y32 = y32 ? 1 : 0;
         f.x = x;
         f.dt = dt;
         f.A_log = A_log;
@@ -310,6 +313,7 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
             err = ssd::launch_gate_norm(gn, s.bf16, static_cast<hipStream_t>(stream));
         return err == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
     }
+    if (y32) return SSD_ERR_UNSUPPORTED_DIMS;   // float32 y only from the fused kernels
     const ssd::WorkspaceLayout w = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC);
 
     ssd::Params p;
@@ -555,13 +559,17 @@ int backward_impl(const ssd_problem* prob, const void* x, const void* dt, const 
                   const void* C, const float* D, const float* initial_states, const void* dy,
                   const float* dfinal_states, void* dx, void* ddt, float* dA_log, void* dB, void* dC, float* dD,
                   float* dinitial_states, void* workspace, size_t workspace_bytes, void* stream,
-                  void* ev_begin, void* ev_end)
+                  void* ev_begin, void* ev_end, bool h32 = false)
 {
+    // h32 (the block gradients): dt, dy float32 in, ddt float32 out, on the
+    // matrix-core path only
     ssd::BwdParams p{};
     ssd::BwdLayout l{};
     bool fast = false;
     const int rc = backward_plan(prob, &p, &l, &fast);
     if (rc != SSD_OK) return rc;
+    if (h32 && !fast) return SSD_ERR_UNSUPPORTED_DIMS;
+    p.h32 = h32 ? 1 : 0;
     if (!x || !dt || !A_log || !B || !C || !dy || !dx || !ddt || !dA_log || !dB || !dC)
         return SSD_ERR_NULL_ARG;
     if (!aligned16(initial_states) || !aligned16(dfinal_states) || !aligned16(dinitial_states) ||
@@ -638,43 +646,173 @@ extern "C" int ssd_backward_timed(const ssd_problem* prob, const void* x, const 
 namespace {
 
 // Workspace of the block backward: the dt step's output, the layer's output
-// (recomputed), its gradient, the layer's dt gradient, the normalisation's
-// 1 / r per (row, group), the row-chunk partials of d weight and d bias, and
-// one region shared by the forward and the layer backward (they run one after
-// the other).
+// (recomputed), its gradient, the layer's dt gradient -- all four float32 --
+// the normalisation's 1 / r per (row, group), the row-chunk partials of
+// d weight and d bias, and one region shared by the forward and the layer
+// backward (they run one after the other).
+//
+// Three ways to run it:
+//   kF32      float32 activations: every kernel in float32;
+//   kMatrix   bf16 activations at the matrix-core shapes (headdim 64, dstate
+//             64 or 128): the layer recomputed by the fused kernels with y in
+//             float32, the layer backward on the matrix cores with float32
+//             dt, dy and ddt;
+//   kWidened  bf16 activations at any other shape: the activations widened to
+//             float32 (exactly), the call run as kF32 on the copies, and the
+//             activation-dtype gradients rounded back to bf16.
+enum BlockMode { kF32, kMatrix, kWidened };
+
 struct BlockBwdLayout {
+    BlockMode mode;
     size_t dt, y, dy, ddt, inv_rms, dw_part, db_part, shared, total;
+    // kWidened: float32 copies of the inputs and float32 gradients, then the
+    // float32 call's own workspace at `inner`
+    size_t wx, wdt, wB, wC, wdout, wz, gx, gdt, gB, gC, gz, inner;
 };
+
+BlockMode block_mode(const ssd::Shape& s)
+{
+    if (!s.bf16) return kF32;
+    if (ssd::tuning(ssd::kTuneForceGeneral) != 1 && ssd::fused_supported(s.P, s.N, 256, true) &&
+        ssd::bwd_fast_supported(true, s.P, s.N))
+        return kMatrix;
+    return kWidened;
+}
 
 int block_backward_plan(const ssd_problem* prob, const ssd_block_opts* opts, BlockBwdLayout* l)
 {
     if (!prob || !opts) return SSD_ERR_NULL_ARG;
-    size_t fwd = 0, bwd = 0;
-    int rc = ssd_workspace_bytes(prob, &fwd);
+    ssd::Shape s;
+    int rc = ssd::validate(prob, false, &s);
     if (rc != SSD_OK) return rc;
-    if ((rc = ssd_backward_workspace_bytes(prob, &bwd)) != SSD_OK) return rc;
-    const size_t act = prob->dtype == SSD_DTYPE_BF16 ? 2 : 4;
-    const size_t rows = static_cast<size_t>(prob->batch * prob->seqlen);
-    const size_t H = static_cast<size_t>(prob->nheads), Cc = H * static_cast<size_t>(prob->headdim);
-    const size_t nch = static_cast<size_t>(ssd::block_bwd_row_chunks(static_cast<int64_t>(rows)));
-    if (nch > 65535) return SSD_ERR_TOO_LARGE;   // row chunks on grid y
-    const size_t groups = opts->norm_group_size > 0 ? Cc / static_cast<size_t>(opts->norm_group_size) : 0;
+    l->mode = block_mode(s);
     size_t off = ssd::kWorkspaceHeader;   // the recomputed forward's status word sits in the header
     const auto take = [&](size_t bytes) {
         const size_t o = off;
         off += ssd::align_up(bytes);
         return o;
     };
-    l->dt = take(rows * H * act);
-    l->y = take(rows * Cc * act);
-    l->dy = take(rows * Cc * act);
-    l->ddt = take(rows * H * act);
+    const size_t rows = static_cast<size_t>(prob->batch * prob->seqlen);
+    const size_t H = static_cast<size_t>(prob->nheads), Cc = H * static_cast<size_t>(prob->headdim);
+    if (l->mode == kWidened) {
+        const size_t GN = static_cast<size_t>(prob->ngroups * prob->dstate);
+        l->wx = take(rows * Cc * 4);
+        l->wdt = take(rows * H * 4);
+        l->wB = take(rows * GN * 4);
+        l->wC = take(rows * GN * 4);
+        l->wdout = take(rows * Cc * 4);
+        l->wz = take(opts->z ? rows * Cc * 4 : 0);
+        l->gx = take(rows * Cc * 4);
+        l->gdt = take(rows * H * 4);
+        l->gB = take(rows * GN * 4);
+        l->gC = take(rows * GN * 4);
+        l->gz = take(opts->z ? rows * Cc * 4 : 0);
+        ssd_problem q = *prob;
+        q.dtype = SSD_DTYPE_F32;
+        BlockBwdLayout inner{};
+        if ((rc = block_backward_plan(&q, opts, &inner)) != SSD_OK) return rc;
+        l->inner = take(inner.total);
+        l->total = off;
+        return SSD_OK;
+    }
+    size_t fwd = 0, bwd = 0;
+    ssd_problem qf = *prob;
+    if (l->mode == kMatrix) qf.chunk_size = 256;   // the fused kernels' chunk (the result does not depend on it)
+    if ((rc = ssd_workspace_bytes(&qf, &fwd)) != SSD_OK) return rc;
+    if ((rc = ssd_backward_workspace_bytes(prob, &bwd)) != SSD_OK) return rc;
+    const size_t nch = static_cast<size_t>(ssd::block_bwd_row_chunks(static_cast<int64_t>(rows)));
+    if (nch > 65535) return SSD_ERR_TOO_LARGE;   // row chunks on grid y
+    const size_t groups = opts->norm_group_size > 0 ? Cc / static_cast<size_t>(opts->norm_group_size) : 0;
+    l->dt = take(rows * H * 4);
+    l->y = take(rows * Cc * 4);
+    l->dy = take(rows * Cc * 4);
+    l->ddt = take(rows * H * 4);
     l->inv_rms = take(rows * groups * 4);
     l->dw_part = take(opts->norm_weight && groups ? nch * Cc * 4 : 0);
     l->db_part = take(opts->dt_bias ? nch * H * 4 : 0);
     l->shared = take(fwd > bwd ? fwd : bwd);
     l->total = off;
     return SSD_OK;
+}
+
+// The block backward on validated arguments (kF32 or kMatrix); `status` is
+// where the recomputed forward leaves its status word.
+int block_backward_run(const ssd_problem* prob, const ssd_block_opts* opts, const BlockBwdLayout& l,
+                       const ssd::Shape& s, const void* x, const void* dt, const float* A_log, const void* B,
+                       const void* C, const float* D, const float* initial_states, const void* dout,
+                       const float* dfinal_states, void* dx, void* ddt, float* dA_log, void* dB, void* dC,
+                       float* dD, float* dinitial_states, float* ddt_bias, void* dz, float* dnorm_weight, char* ws,
+                       int* status, void* stream)
+{
+    const bool bf16 = s.bf16;
+    const bool matrix = l.mode == kMatrix;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    const size_t shared_bytes = l.total - l.shared;
+
+    ssd::BlockBwdParams p{};
+    p.rows = s.b * s.T;
+    p.H = s.H;
+    p.C = s.H * s.P;
+    p.group = opts->norm_group_size;
+    p.dt_raw = dt;
+    p.bias = opts->dt_bias;
+    p.softplus = opts->dt_softplus != 0;
+    p.lo = opts->dt_min;
+    p.hi = opts->dt_max;
+    p.dt = ws + l.dt;
+    p.ddt = ws + l.ddt;
+    p.ddt_raw = ddt;
+    p.dbias_part = opts->dt_bias ? reinterpret_cast<float*>(ws + l.db_part) : nullptr;
+    p.ddt_bias = opts->dt_bias ? ddt_bias : nullptr;
+    p.y = ws + l.y;
+    p.z = opts->z;
+    p.w = opts->norm_group_size > 0 ? opts->norm_weight : nullptr;
+    p.eps = opts->norm_eps;
+    p.dout = dout;
+    p.dy = ws + l.dy;
+    p.dz = dz;
+    p.inv_rms = opts->norm_group_size > 0 ? reinterpret_cast<float*>(ws + l.inv_rms) : nullptr;
+    p.dw_part = reinterpret_cast<float*>(ws + l.dw_part);
+    p.dw = p.w ? dnorm_weight : nullptr;
+
+    // 1. the dt step (float32); 2. the layer's output, recomputed in float32:
+    // with bf16 activations the fused kernels apply the dt step themselves, to
+    // the raw dt, exactly as the block forward does
+    if (ssd::launch_block_dt_apply(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
+    int rc;
+    if (matrix) {
+        ssd_problem q = *prob;
+        q.chunk_size = 256;
+        ssd_block_opts dto = *opts;   // the dt step only
+        dto.z = nullptr;
+        dto.norm_weight = nullptr;
+        dto.norm_group_size = 0;
+        rc = forward_impl(&q, &dto, x, dt, A_log, B, C, D, initial_states, nullptr, ws + l.y, nullptr,
+                          ws + l.shared, shared_bytes, stream, nullptr, nullptr, nullptr, status, true,
+                          /*y32=*/true);
+    } else {
+        rc = forward_impl(prob, nullptr, x, p.dt, A_log, B, C, D, initial_states, nullptr, ws + l.y, nullptr,
+                          ws + l.shared, shared_bytes, stream, nullptr, nullptr, nullptr, status);
+    }
+    if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
+    // 3. gate and normalisation: dy (the block's output gradient when neither is on)
+    const bool post = opts->z || opts->norm_group_size > 0;
+    const void* dy = dout;
+    if (post) {
+        if (ssd::launch_block_out_bwd(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
+        dy = p.dy;
+    } else if (matrix) {   // the layer takes dy in float32
+        if (ssd::launch_widen(dout, reinterpret_cast<float*>(p.dy), p.rows * p.C, st) != hipSuccess)
+            return SSD_ERR_LAUNCH;
+        dy = p.dy;
+    }
+    // 4. the layer
+    rc = backward_impl(prob, x, p.dt, A_log, B, C, D, initial_states, dy, dfinal_states, dx, ws + l.ddt, dA_log,
+                       dB, dC, dD, dinitial_states, ws + l.shared, shared_bytes, stream, nullptr, nullptr,
+                       /*h32=*/matrix);
+    if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
+    // 5. the dt step
+    return ssd::launch_block_dt_bwd(p, bf16, st) == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
 }
 
 }  // namespace
@@ -713,51 +851,48 @@ extern "C" int ssd_backward_block(const ssd_problem* prob, const ssd_block_opts*
         return SSD_ERR_UNSUPPORTED_DIMS;
     if (!workspace || workspace_bytes < l.total) return SSD_ERR_WORKSPACE;
     char* ws = static_cast<char*>(workspace);
-    const bool bf16 = s.bf16;
+    int* status = reinterpret_cast<int*>(ws);
+    if (l.mode != kWidened)
+        return block_backward_run(prob, opts, l, s, x, dt, A_log, B, C, D, initial_states, dout, dfinal_states, dx,
+                                  ddt, dA_log, dB, dC, dD, dinitial_states, ddt_bias, dz, dnorm_weight, ws, status,
+                                  stream);
+    // bf16 activations outside the matrix-core shapes: the float32 call on
+    // widened copies, its activation-dtype gradients rounded back to bf16
     const hipStream_t st = static_cast<hipStream_t>(stream);
-    const size_t shared_bytes = l.total - l.shared;
-
-    ssd::BlockBwdParams p{};
-    p.rows = s.b * s.T;
-    p.H = s.H;
-    p.C = s.H * s.P;
-    p.group = opts->norm_group_size;
-    p.dt_raw = dt;
-    p.bias = opts->dt_bias;
-    p.softplus = opts->dt_softplus != 0;
-    p.lo = opts->dt_min;
-    p.hi = opts->dt_max;
-    p.dt = ws + l.dt;
-    p.ddt = ws + l.ddt;
-    p.ddt_raw = ddt;
-    p.dbias_part = opts->dt_bias ? reinterpret_cast<float*>(ws + l.db_part) : nullptr;
-    p.ddt_bias = opts->dt_bias ? ddt_bias : nullptr;
-    p.y = ws + l.y;
-    p.z = opts->z;
-    p.w = opts->norm_group_size > 0 ? opts->norm_weight : nullptr;
-    p.eps = opts->norm_eps;
-    p.dout = dout;
-    p.dy = ws + l.dy;
-    p.dz = dz;
-    p.inv_rms = opts->norm_group_size > 0 ? reinterpret_cast<float*>(ws + l.inv_rms) : nullptr;
-    p.dw_part = reinterpret_cast<float*>(ws + l.dw_part);
-    p.dw = p.w ? dnorm_weight : nullptr;
-
-    // 1. the dt step; 2. the layer's output, recomputed
-    if (ssd::launch_block_dt_apply(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
-    rc = forward_impl(prob, nullptr, x, p.dt, A_log, B, C, D, initial_states, nullptr, ws + l.y, nullptr,
-                      ws + l.shared, shared_bytes, stream, nullptr, nullptr, nullptr, reinterpret_cast<int*>(ws));
-    if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
-    // 3. gate and normalisation: dy (the block's output gradient when neither is on)
-    const bool post = opts->z || opts->norm_group_size > 0;
-    if (post && ssd::launch_block_out_bwd(p, bf16, st) != hipSuccess) return SSD_ERR_LAUNCH;
-    // 4. the layer
-    rc = backward_impl(prob, x, p.dt, A_log, B, C, D, initial_states, post ? p.dy : dout, dfinal_states, dx,
-                       ws + l.ddt, dA_log, dB, dC, dD, dinitial_states, ws + l.shared, shared_bytes, stream,
-                       nullptr, nullptr);
-    if (rc != SSD_OK) return rc == SSD_ERR_LAUNCH ? rc : SSD_ERR_LAUNCH;
-    // 5. the dt step
-    return ssd::launch_block_dt_bwd(p, bf16, st) == hipSuccess ? SSD_OK : SSD_ERR_LAUNCH;
+    const int64_t rows = s.b * s.T, HP = s.H * s.P, GN = s.G * s.N;
+    float* wx = reinterpret_cast<float*>(ws + l.wx);
+    float* wdt = reinterpret_cast<float*>(ws + l.wdt);
+    float* wB = reinterpret_cast<float*>(ws + l.wB);
+    float* wC = reinterpret_cast<float*>(ws + l.wC);
+    float* wdout = reinterpret_cast<float*>(ws + l.wdout);
+    float* wz = opts->z ? reinterpret_cast<float*>(ws + l.wz) : nullptr;
+    if (ssd::launch_widen(x, wx, rows * HP, st) != hipSuccess || ssd::launch_widen(dt, wdt, rows * s.H, st) != hipSuccess ||
+        ssd::launch_widen(B, wB, rows * GN, st) != hipSuccess || ssd::launch_widen(C, wC, rows * GN, st) != hipSuccess ||
+        ssd::launch_widen(dout, wdout, rows * HP, st) != hipSuccess ||
+        (wz && ssd::launch_widen(opts->z, wz, rows * HP, st) != hipSuccess))
+        return SSD_ERR_LAUNCH;
+    ssd_problem q = *prob;
+    q.dtype = SSD_DTYPE_F32;
+    ssd_block_opts o32 = *opts;
+    o32.z = wz;
+    BlockBwdLayout inner{};
+    ssd::Shape s32;
+    if (block_backward_plan(&q, &o32, &inner) != SSD_OK || ssd::validate(&q, false, &s32) != SSD_OK)
+        return SSD_ERR_LAUNCH;   // cannot happen: the same shape validated above
+    float* gx = reinterpret_cast<float*>(ws + l.gx);
+    float* gdt = reinterpret_cast<float*>(ws + l.gdt);
+    float* gB = reinterpret_cast<float*>(ws + l.gB);
+    float* gC = reinterpret_cast<float*>(ws + l.gC);
+    float* gz = wz ? reinterpret_cast<float*>(ws + l.gz) : nullptr;
+    rc = block_backward_run(&q, &o32, inner, s32, wx, wdt, A_log, wB, wC, D, initial_states, wdout, dfinal_states,
+                            gx, gdt, dA_log, gB, gC, dD, dinitial_states, ddt_bias, gz, dnorm_weight, ws + l.inner,
+                            status, stream);
+    if (rc != SSD_OK) return rc;
+    if (ssd::launch_narrow(gx, dx, rows * HP, st) != hipSuccess || ssd::launch_narrow(gdt, ddt, rows * s.H, st) != hipSuccess ||
+        ssd::launch_narrow(gB, dB, rows * GN, st) != hipSuccess || ssd::launch_narrow(gC, dC, rows * GN, st) != hipSuccess ||
+        (gz && ssd::launch_narrow(gz, dz, rows * HP, st) != hipSuccess))
+        return SSD_ERR_LAUNCH;
+    return SSD_OK;
 }
 
 namespace {

@@ -16,6 +16,10 @@
 //                  (B, B^T, C^T, x, dy, dy^T, the score tiles and Gn, transposed
 //                  there from Gn^T), or straight from global memory (Gn^T, h_in^T).
 //
+// H32 (a template flag; the block gradients use it): dt and dy come in as
+// float32 and ddt goes out as float32.  dy is rounded to bf16 only where it is
+// a matrix-core operand; the skip term of dx and the dD sums take it in float32.
+//
 // An MFMA operand row holds the contraction index contiguously; a lane
 // (row r = lane % 16, group q = lane / 16) reads 8 of them (k = 32 s + 8 q ..
 // + 7) as one 16-byte load, and the result tile D[4 q + v][r] lands in its
@@ -50,6 +54,16 @@ __device__ __forceinline__ uint32_t bf16_bits(float f)
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_bits(lo) | (bf16_bits(hi) << 16); }
 
 __device__ __forceinline__ float bf(u16 v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
+
+// dt of token row i (bf16 bits, or float32 with H32).
+template <bool H32>
+__device__ __forceinline__ float load_dt(const void* dt, int64_t i)
+{
+    if constexpr (H32)
+        return static_cast<const float*>(dt)[i];
+    else
+        return bf(static_cast<const u16*>(dt)[i]);
+}
 
 __device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -187,7 +201,7 @@ __device__ __forceinline__ uint4 tr_frag(const u16* buf, int m, int f0, int lane
 
 // PACKED: a packed row; workgroup (sequence, head) walks that sequence's
 // chunks of the chunk table.
-template <int N, bool PACKED>
+template <int N, bool PACKED, bool H32>
 __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
 {
     __shared__ __attribute__((aligned(16))) u16 XS[kQ2 * kP2];   // weighted x (or dy), token-major
@@ -199,8 +213,9 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = lane & 15, q = lane >> 4;
     const u16* src = static_cast<const u16*>(dir == 0 ? p.x : p.dy);
+    const float* dyf = static_cast<const float*>(p.dy);   // H32, dir 1
+    const bool src32 = H32 && dir == 1;
     const u16* bc = static_cast<const u16*>(dir == 0 ? p.B : p.C);
-    const u16* dtg = static_cast<const u16*>(p.dt);
     u16* out = reinterpret_cast<u16*>(dir == 0 ? p.hin : p.gnT);
     const float A2 = -expf(p.A_log[h]) * kLog2e;
 
@@ -222,6 +237,7 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     struct Stage {
         float dt;
         uint4 x[kXK], y[kYK];
+        float4 xf[H32 ? 2 * kXK : 1];   // H32, dir 1: dy in float32
     };
     int64_t first = 0, nch = p.nC;   // this row's (or sequence's) chunks
     if constexpr (PACKED) {
@@ -242,12 +258,19 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
             L = chunk_len2(p.T, c);
             t0 = b * p.T + c * kQ2;
         }
-        st.dt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
+        st.dt = lane < L ? load_dt<H32>(p.dt, (t0 + lane) * p.H + h) : 0.f;
 #pragma unroll
         for (int kk = 0; kk < kXK; ++kk) {
             const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
-            st.x[kk] = s < L ? *reinterpret_cast<const uint4*>(src + ((t0 + s) * p.H + h) * kP2 + f)
-                             : make_uint4(0, 0, 0, 0);
+            if (src32) {
+                const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+                const float* a = dyf + ((t0 + s) * p.H + h) * kP2 + f;
+                st.xf[2 * kk] = s < L ? *reinterpret_cast<const float4*>(a) : z;
+                st.xf[2 * kk + 1] = s < L ? *reinterpret_cast<const float4*>(a + 4) : z;
+            } else {
+                st.x[kk] = s < L ? *reinterpret_cast<const uint4*>(src + ((t0 + s) * p.H + h) * kP2 + f)
+                                 : make_uint4(0, 0, 0, 0);
+            }
         }
 #pragma unroll
         for (int kk = 0; kk < kYK; ++kk) {
@@ -268,10 +291,18 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         for (int kk = 0; kk < kXK; ++kk) {
             const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
             const float ws = __shfl(wt, s, 64);
-            const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
             uint32_t o[4];
+            if (src32) {
+                const float4 a = st.xf[2 * kk], c2 = st.xf[2 * kk + 1];
+                o[0] = pack2(ws * a.x, ws * a.y);
+                o[1] = pack2(ws * a.z, ws * a.w);
+                o[2] = pack2(ws * c2.x, ws * c2.y);
+                o[3] = pack2(ws * c2.z, ws * c2.w);
+            } else {
+                const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = pack2(ws * lo_f(ex[e]), ws * hi_f(ex[e]));
+                for (int e = 0; e < 4; ++e) o[e] = pack2(ws * lo_f(ex[e]), ws * hi_f(ex[e]));
+            }
             *reinterpret_cast<uint4*>(XS + tok_off<kP2>(s, f)) = make_uint4(o[0], o[1], o[2], o[3]);
         }
 #pragma unroll
@@ -317,11 +348,13 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
 
 // ---------------------------------------------------------------------------
 // Chunk gradients.
-template <int N>
+template <int N, bool H32 = false>
 struct ChunkSmem {
     static constexpr int kLdN = N + 8;
+    static constexpr int kLdF = kP2 + 4;   // row stride (floats) of the float32 dy copy (H32)
     static constexpr size_t kBytes =
-        sizeof(u16) * (2 * static_cast<size_t>(kQ2) * kLdN + 2 * N * kLd + 6 * kQ2 * kLd);
+        sizeof(u16) * (2 * static_cast<size_t>(kQ2) * kLdN + 2 * N * kLd + 6 * kQ2 * kLd) +
+        (H32 ? sizeof(float) * kQ2 * kLdF : 0);
 };
 
 // The score tiles (u-tile, t-tile) with u >= t, and those above the diagonal,
@@ -330,10 +363,11 @@ struct ChunkSmem {
 __constant__ int2 kLowerTile[10] = {{0, 0}, {1, 0}, {1, 1}, {2, 0}, {2, 1}, {2, 2}, {3, 0}, {3, 1}, {3, 2}, {3, 3}};
 __constant__ int2 kUpperTile[6] = {{0, 1}, {0, 2}, {0, 3}, {1, 2}, {1, 3}, {2, 3}};
 
-template <int N, bool PACKED>
+template <int N, bool PACKED, bool H32>
 __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 {
     constexpr int kLdN = ChunkSmem<N>::kLdN;
+    constexpr int kLdF = ChunkSmem<N, H32>::kLdF;
     constexpr int kNT = N / 16;             // n-tiles
     constexpr int kBW = N / 32;             // dB / dC tiles per wavefront
     extern __shared__ __attribute__((aligned(16))) u16 sm2[];
@@ -347,6 +381,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     u16* Rs = GsT + kQ2 * kLd;          // 64 x kLd   Rs  (row u, k = t)
     u16* RsT = Rs + kQ2 * kLd;          // 64 x kLd   Rs^T (row t, k = u)
     u16* GnS = RsT + kQ2 * kLd;         // 64 x kLdN  Gn  (row p, k = n), from Gn^T
+    float* dyF = reinterpret_cast<float*>(GnS + kQ2 * kLdN);   // H32: 64 x kLdF dy in float32 (row u)
     // per-token factors, double-buffered by head parity (the per-token phase of
     // one head overlaps the next head's set-up)
     __shared__ float scs2[2][kQ2], sdt2[2][kQ2], seend2[2][kQ2], secs2[2][kQ2];
@@ -380,9 +415,8 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     const u16* Cg = static_cast<const u16*>(p.C);
     const u16* xg = static_cast<const u16*>(p.x);
     const u16* dyg = static_cast<const u16*>(p.dy);
-    const u16* dtg = static_cast<const u16*>(p.dt);
+    const float* dyg32 = static_cast<const float*>(p.dy);   // H32
     u16* dxg = static_cast<u16*>(p.dx);
-    u16* ddtg = static_cast<u16*>(p.ddt);
 
     // B, B^T, C^T of the chunk
     for (int i = tid; i < kQ2 * N / 8; i += kT2) {
@@ -433,13 +467,20 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     const int s_me = lane, p0_me = 8 * w;   // token = lane, 8 p values per wavefront
     float pdt = 0.f;
     uint4 px = make_uint4(0, 0, 0, 0), pd = px;
+    float4 pf0 = make_float4(0.f, 0.f, 0.f, 0.f), pf1 = pf0;   // H32: dy in float32
     const auto fetch = [&](int64_t h) {
-        if (w == 0) pdt = lane < L ? bf(dtg[(t0 + lane) * p.H + h]) : 0.f;
+        if (w == 0) pdt = lane < L ? load_dt<H32>(p.dt, (t0 + lane) * p.H + h) : 0.f;
         px = pd = make_uint4(0, 0, 0, 0);
+        pf0 = pf1 = make_float4(0.f, 0.f, 0.f, 0.f);
         if (s_me < L) {
             const int64_t gi = ((t0 + s_me) * p.H + h) * kP2 + p0_me;
             px = *reinterpret_cast<const uint4*>(xg + gi);
-            pd = *reinterpret_cast<const uint4*>(dyg + gi);
+            if constexpr (H32) {
+                pf0 = *reinterpret_cast<const float4*>(dyg32 + gi);
+                pf1 = *reinterpret_cast<const float4*>(dyg32 + gi + 4);
+            } else {
+                pd = *reinterpret_cast<const uint4*>(dyg + gi);
+            }
         }
     };
     fetch(hr.lo);
@@ -475,6 +516,11 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             }
         }
         // this head's x, dy (fetched during the previous head) into shared memory
+        if constexpr (H32) {   // the operand copies in bf16, dy also kept in float32
+            pd = make_uint4(pack2(pf0.x, pf0.y), pack2(pf0.z, pf0.w), pack2(pf1.x, pf1.y), pack2(pf1.z, pf1.w));
+            *reinterpret_cast<float4*>(dyF + s_me * kLdF + p0_me) = pf0;
+            *reinterpret_cast<float4*>(dyF + s_me * kLdF + p0_me + 4) = pf1;
+        }
         *reinterpret_cast<uint4*>(xs + s_me * kLd + p0_me) = px;
         *reinterpret_cast<uint4*>(dys + s_me * kLd + p0_me) = pd;
         {
@@ -577,9 +623,15 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             const int t = 16 * tt + r, p0 = 16 * pw + 4 * q;
             const float ee = seend[t], dtt = sdt[t];
             const uint2 xv = *reinterpret_cast<const uint2*>(xs + t * kLd + p0);
-            const uint2 dv = *reinterpret_cast<const uint2*>(dys + t * kLd + p0);
             const float xf[4] = {lo_f(xv.x), hi_f(xv.x), lo_f(xv.y), hi_f(xv.y)};
-            const float df[4] = {lo_f(dv.x), hi_f(dv.x), lo_f(dv.y), hi_f(dv.y)};
+            float df[4];
+            if constexpr (H32) {
+                const float4 d4 = *reinterpret_cast<const float4*>(dyF + t * kLdF + p0);
+                df[0] = d4.x; df[1] = d4.y; df[2] = d4.z; df[3] = d4.w;
+            } else {
+                const uint2 dv = *reinterpret_cast<const uint2*>(dys + t * kLd + p0);
+                df[0] = lo_f(dv.x); df[1] = hi_f(dv.x); df[2] = lo_f(dv.y); df[3] = hi_f(dv.y);
+            }
             float dx[4], sxd = 0.f, sxg = 0.f, sdx = 0.f;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
@@ -684,7 +736,13 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
             float dcs = in ? row - col + secs[t] * s1 - seend[t] * q2 : 0.f;
             if (t == L - 1) dcs += secs[t] * ghs + hsum;   // <Gn, h_out>
             const float da = wave_scan(dcs);   // over tokens t' >= t
-            if (in) ddtg[(t0 + t) * p.H + h] = static_cast<u16>(bf16_bits(fmaf(Ah, da, xd)));
+            if (in) {
+                const float g = fmaf(Ah, da, xd);
+                if constexpr (H32)
+                    static_cast<float*>(p.ddt)[(t0 + t) * p.H + h] = g;
+                else
+                    static_cast<u16*>(p.ddt)[(t0 + t) * p.H + h] = static_cast<u16>(bf16_bits(g));
+            }
             const float sa = wave_sum(in ? sdt[t] * da : 0.f);
             const float sd = wave_sum(in ? dyx : 0.f);
             if (lane == 0) {
@@ -710,26 +768,34 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 template <int N>
 hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
 {
-    const size_t sm_chunk = ChunkSmem<N>::kBytes;
+    const bool packed = p.vtab != nullptr, h32 = p.h32 != 0;
+    if (packed && h32) return hipErrorInvalidValue;   // float32 handoffs: plain rows only
+    const size_t sm_chunk = h32 ? ChunkSmem<N, true>::kBytes : ChunkSmem<N>::kBytes;
     hipError_t e;
-    const bool packed = p.vtab != nullptr;
-    const void* chunk_fn = packed ? reinterpret_cast<const void*>(&k_bwd2_chunk<N, true>)
-                                  : reinterpret_cast<const void*>(&k_bwd2_chunk<N, false>);
+    const void* chunk_fn = packed ? reinterpret_cast<const void*>(&k_bwd2_chunk<N, true, false>)
+                           : h32  ? reinterpret_cast<const void*>(&k_bwd2_chunk<N, false, true>)
+                                  : reinterpret_cast<const void*>(&k_bwd2_chunk<N, false, false>);
     if ((e = hipFuncSetAttribute(chunk_fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
         hipSuccess)
         return e;
     if (packed)   // one workgroup per (sequence, head) and direction
-        hipLaunchKernelGGL((k_bwd2_pass<N, true>), dim3(static_cast<unsigned>(p.nseq * p.H), 2), dim3(kPassT), 0,
+        hipLaunchKernelGGL((k_bwd2_pass<N, true, false>), dim3(static_cast<unsigned>(p.nseq * p.H), 2), dim3(kPassT),
+                           0, st, p);
+    else if (h32)
+        hipLaunchKernelGGL((k_bwd2_pass<N, false, true>), dim3(static_cast<unsigned>(p.b * p.H), 2), dim3(kPassT), 0,
                            st, p);
     else
-        hipLaunchKernelGGL((k_bwd2_pass<N, false>), dim3(static_cast<unsigned>(p.b * p.H), 2), dim3(kPassT), 0, st, p);
+        hipLaunchKernelGGL((k_bwd2_pass<N, false, false>), dim3(static_cast<unsigned>(p.b * p.H), 2), dim3(kPassT), 0,
+                           st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
     if (packed)
-        hipLaunchKernelGGL((k_bwd2_chunk<N, true>), grid, dim3(kT2), sm_chunk, st, p);
+        hipLaunchKernelGGL((k_bwd2_chunk<N, true, false>), grid, dim3(kT2), sm_chunk, st, p);
+    else if (h32)
+        hipLaunchKernelGGL((k_bwd2_chunk<N, false, true>), grid, dim3(kT2), sm_chunk, st, p);
     else
-        hipLaunchKernelGGL((k_bwd2_chunk<N, false>), grid, dim3(kT2), sm_chunk, st, p);
+        hipLaunchKernelGGL((k_bwd2_chunk<N, false, false>), grid, dim3(kT2), sm_chunk, st, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
     return launch_backward_reduce(p, true, st);

@@ -16,18 +16,18 @@ struct BlockBwdParams {
     const float* bias;     // (H) or null
     int softplus;
     float lo, hi;
-    void* dt;              // (rows, H) dtype: the step's output (workspace)
-    const void* ddt;       // (rows, H) dtype: gradient of the layer's dt
+    void* dt;              // (rows, H) float32: the step's output (workspace)
+    const void* ddt;       // (rows, H) float32: gradient of the layer's dt
     void* ddt_raw;         // (rows, H) dtype: output
     float* dbias_part;     // (row chunks, H) workspace, or null
     float* ddt_bias;       // (H) output, or null
     // gate and normalisation
-    const void* y;         // (rows, C) dtype: the layer's output (workspace)
+    const void* y;         // (rows, C) float32: the layer's output (workspace)
     const void* z;         // (rows, C) dtype, or null
     const float* w;        // (C), or null
     float eps;
     const void* dout;      // (rows, C) dtype: gradient of the block's output
-    void* dy;              // (rows, C) dtype: gradient of the layer's output (workspace)
+    void* dy;              // (rows, C) float32: gradient of the layer's output (workspace)
     void* dz;              // (rows, C) dtype output, or null
     float* inv_rms;        // (rows, C / group) workspace
     float* dw_part;        // (row chunks, C) workspace
@@ -42,5 +42,9 @@ hipError_t launch_block_dt_apply(const BlockBwdParams& p, bool bf16, hipStream_t
 hipError_t launch_block_out_bwd(const BlockBwdParams& p, bool bf16, hipStream_t stream);
 // ddt_raw (and ddt_bias) from ddt.
 hipError_t launch_block_dt_bwd(const BlockBwdParams& p, bool bf16, hipStream_t stream);
+
+// n bf16 values to float32 (exact), and float32 to bf16 (nearest even).
+hipError_t launch_widen(const void* src, float* dst, int64_t n, hipStream_t stream);
+hipError_t launch_narrow(const float* src, void* dst, int64_t n, hipStream_t stream);
 
 }  // namespace ssd

@@ -14,6 +14,12 @@
 //
 // The layer's own gradient in between is ssd_backward.  Sums over rows go
 // through per-chunk partials and a fixed-order sum (deterministic).
+//
+// What the block steps exchange with the layer -- dt after the dt step, the
+// layer's output y, its gradient dy and the layer's ddt -- is float32 in every
+// case (with bf16 activations too): only the block's own inputs and outputs
+// (dt_raw, z, dout, dz, d dt_raw) have the activation dtype, so the result is
+// the gradient of the block forward, which keeps dt and y in float32 as well.
 #include "ssd_block_bwd.h"
 #include "ssd_device.h"
 
@@ -102,7 +108,7 @@ __device__ __forceinline__ float segment_sum(float v, int seg)
     return v;
 }
 
-// The dt step of the forward, into a buffer of the activation dtype.
+// The dt step of the forward, into a float32 buffer.
 template <typename T>
 __global__ __launch_bounds__(kBT) void k_dt_apply(BlockBwdParams p)
 {
@@ -111,7 +117,21 @@ __global__ __launch_bounds__(kBT) void k_dt_apply(BlockBwdParams p)
     const int64_t h = i % p.H;
     float v = ldv<T>(p.dt_raw, i) + (p.bias ? p.bias[h] : 0.f);
     if (p.softplus) v = softplus_f(v);
-    stv<T>(p.dt, i, fminf(fmaxf(v, p.lo), p.hi));
+    static_cast<float*>(p.dt)[i] = fminf(fmaxf(v, p.lo), p.hi);
+}
+
+// bf16 -> float32 (exact) and float32 -> bf16 (nearest even), one element
+// per thread (any length and alignment).
+__global__ __launch_bounds__(kBT) void k_widen(const void* src, float* dst, int64_t n)
+{
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBT + threadIdx.x;
+    if (i < n) dst[i] = ldv<uint16_t>(src, i);
+}
+
+__global__ __launch_bounds__(kBT) void k_narrow(const float* src, void* dst, int64_t n)
+{
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBT + threadIdx.x;
+    if (i < n) stv<uint16_t>(dst, i, src[i]);
 }
 
 // d dt_raw, and per-chunk partial sums over rows for d bias.  Thread = head,
@@ -132,7 +152,7 @@ __global__ __launch_bounds__(kBT) void k_dt_bwd(BlockBwdParams p)
         const float v = ldv<T>(p.dt_raw, i) + bias;
         const float sp = p.softplus ? softplus_f(v) : v;
         const bool in = sp > p.lo && sp < p.hi;
-        const float dv = in ? ldv<T>(p.ddt, i) * (p.softplus ? sigmoid_f(v) : 1.f) : 0.f;
+        const float dv = in ? static_cast<const float*>(p.ddt)[i] * (p.softplus ? sigmoid_f(v) : 1.f) : 0.f;
         stv<T>(p.ddt_raw, i, dv);
         acc += dv;
     }
@@ -146,7 +166,7 @@ __global__ __launch_bounds__(kBT) void k_gate_bwd(BlockBwdParams p)
     const int64_t i = static_cast<int64_t>(blockIdx.x) * kBT + threadIdx.x;
     if (i >= p.rows * p.C / 8) return;
     float y[8], z[8], d[8], dy[8], dz[8];
-    load8<T>(p.y, 8 * i, y);
+    load8<float>(p.y, 8 * i, y);
     load8<T>(p.z, 8 * i, z);
     load8<T>(p.dout, 8 * i, d);
 #pragma unroll
@@ -155,7 +175,7 @@ __global__ __launch_bounds__(kBT) void k_gate_bwd(BlockBwdParams p)
         dy[e] = d[e] * z[e] * s;
         dz[e] = d[e] * y[e] * s * (1.f + z[e] * (1.f - s));
     }
-    store8<T>(p.dy, 8 * i, dy);
+    store8<float>(p.dy, 8 * i, dy);
     store8<T>(p.dz, 8 * i, dz);
 }
 
@@ -166,7 +186,7 @@ struct Piece {
     float y[8], z[8], s[8], gv[8], d[8];
     __device__ __forceinline__ void load(const BlockBwdParams& p, int64_t e)
     {
-        load8<T>(p.y, e, y);
+        load8<float>(p.y, e, y);
         load8<T>(p.dout, e, d);
         if (p.z) {
             load8<T>(p.z, e, z);
@@ -266,7 +286,7 @@ __device__ __forceinline__ void norm_group_bwd(const BlockBwdParams& p, bool act
                 dy[e] = dg;
             }
         }
-        store8<T>(p.dy, base + 8 * j, dy);
+        store8<float>(p.dy, base + 8 * j, dy);
         if (p.z) store8<T>(p.dz, base + 8 * j, dz);
     });
     if (li == 0 && p.inv_rms) p.inv_rms[gid] = inv;
@@ -453,6 +473,20 @@ hipError_t launch_block_out_bwd(const BlockBwdParams& p, bool bf16, hipStream_t 
 hipError_t launch_block_dt_bwd(const BlockBwdParams& p, bool bf16, hipStream_t st)
 {
     return bf16 ? dt_side<uint16_t>(p, st) : dt_side<float>(p, st);
+}
+
+hipError_t launch_widen(const void* src, float* dst, int64_t n, hipStream_t st)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_widen, dim3(blocks(n)), dim3(kBT), 0, st, src, dst, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_narrow(const float* src, void* dst, int64_t n, hipStream_t st)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_narrow, dim3(blocks(n)), dim3(kBT), 0, st, src, dst, n);
+    return hipGetLastError();
 }
 
 }  // namespace ssd

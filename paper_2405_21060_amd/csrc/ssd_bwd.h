@@ -51,6 +51,10 @@ struct BwdParams {
     const int4* vtab = nullptr;     // (nC) {first token, length, sequence, flags}
     const int* seq_first = nullptr; // (nseq + 1) first table entry of each sequence, then the count
     const int* vcount = nullptr;    // [0] table entries
+    // Matrix-core path, plain rows: nonzero = dt and dy are float32 and ddt is
+    // written in float32 (the block gradients' handoffs); x, B, C, dx, dB, dC
+    // keep the bf16 activation dtype.
+    int h32 = 0;
 };
 
 struct BwdLayout {

@@ -781,7 +781,9 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
 // parameter: the compiler then knows that the asynchronous copies into the
 // next head's buffers (and the next item's Gram tiles) never alias the buffers
 // read here, and does not make those reads wait for the copies.
-template <int N, bool PACKED, bool EARLY>
+// Y32: y is written in float32 straight from the accumulators (the layer
+// recomputed for the block gradients, whose dy and dz need y before rounding).
+template <int N, bool PACKED, bool EARLY, bool Y32>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
                                           uint2 (&btf)[kQ / 32][2], uint4 (&cf)[2][N / 32],
@@ -1126,6 +1128,24 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         if (!EARLY && tid == 0 && has_next)
             __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (Y32) {
+            // lane: token 16 strip + r, features 16 pt + 4 lg .. + 3 (16 bytes)
+            float* y32 = static_cast<float*>(p.y) + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
+#pragma unroll
+            for (int k4 = 0; k4 < 2; ++k4) {
+                const int t = 16 * strip[k4] + r;
+                if (t < L)
+#pragma unroll
+                    for (int pt = 0; pt < 4; ++pt)
+                        *reinterpret_cast<float4*>(y32 + static_cast<unsigned>(t) * xrow + 16 * pt + 4 * lg) =
+                            make_float4(y[k4][pt][0], y[k4][pt][1], y[k4][pt][2], y[k4][pt][3]);
+            }
+            lds_barrier();
+            if (!EARLY && tid == 0 && has_next)
+                __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (gram_ahead) wait_vmem();   // the next item's Gram tiles have landed
+        } else {
         u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
         constexpr int kPieces = kQ * kP / 8 / kMainThreads;   // 16-byte pieces per thread
         uint4 v[kPieces];
@@ -1142,6 +1162,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             // streaming (non-temporal) stores: y is not read again by this kernel
             if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
         }
+        }
     }
     // The next item's B^T and C fragments (their last uses in this item are
     // behind us), requested after the waits above so that none of those waits
@@ -1157,7 +1178,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 
 // A_log, D and the dt bias come as separate read-only arguments so that their per-head values
 // are scalar loads (a vector load would wait behind the outstanding copies).
-template <int N, bool PACKED, bool EARLY>
+template <int N, bool PACKED, bool EARLY, bool Y32>
 __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, const float* __restrict__ A_logp,
                                                                 const float* __restrict__ Dp,
                                                                 const float* __restrict__ biasp)
@@ -1217,7 +1238,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
     int next = nwork;
     for (int hk = 0; hk < p.HG; ++hk) {
-        head_step<N, PACKED, EARLY>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
+        head_step<N, PACKED, EARLY, Y32>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
                      sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp,
                      biasp, sm.wn);
         q ^= 1;
@@ -1230,6 +1251,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
 template <int N>
 hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end)
 {
+    if (p.y32 && (p.vtab || p.z || p.norm_head)) return hipErrorInvalidValue;   // plain rows, no gate/norm
     if (p.vtab) {   // packed row: the chunk table first
         const hipError_t e = launch_seq_table(p.seq_idx, p.arg_starts, p.T, p.nseq, kQ, p.nC, p.ring_rows, p.starts,
                                               p.vtab, nullptr, p.vcount, stream);
@@ -1260,14 +1282,24 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     const float* A_logp = p.A_log;
     const float* Dp = p.D;
     const float* biasp = p.dtx.bias;
-    if (p.vtab && p.early_flag)
-        hipLaunchKernelGGL((k_fused_main<N, true, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+    if (p.y32 && p.early_flag)
+        hipLaunchKernelGGL((k_fused_main<N, false, true, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
+                           biasp);
+    else if (p.y32)
+        hipLaunchKernelGGL((k_fused_main<N, false, false, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+                           Dp, biasp);
+    else if (p.vtab && p.early_flag)
+        hipLaunchKernelGGL((k_fused_main<N, true, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
+                           biasp);
     else if (p.vtab)
-        hipLaunchKernelGGL((k_fused_main<N, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+        hipLaunchKernelGGL((k_fused_main<N, true, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+                           Dp, biasp);
     else if (p.early_flag)
-        hipLaunchKernelGGL((k_fused_main<N, false, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+        hipLaunchKernelGGL((k_fused_main<N, false, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+                           Dp, biasp);
     else
-        hipLaunchKernelGGL((k_fused_main<N, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp, biasp);
+        hipLaunchKernelGGL((k_fused_main<N, false, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+                           Dp, biasp);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;

@@ -127,6 +127,8 @@ struct FusedParams {
     const float* norm_weight = nullptr;  // (H * P), with norm_head
     int norm_head = 0;                   // nonzero: RMS-normalise each head's P channels
     float norm_eps = 0.f;
+    // nonzero: y is float32 (plain rows, no gate or normalisation)
+    int y32 = 0;
 };
 
 struct FusedLayout {

@@ -121,27 +121,3 @@ def _mutant(name):
 def test_block_backward_mutant_is_caught(name):
     kw = dict(lo=0.12, hi=0.45) if name == "no_clamp_mask" else {}
     assert not finite_difference_ok(_mutant(name), **kw)
-
-
-def test_round_bf16_is_nearest_even():
-    # exact bf16 values stay; halfway cases go to the even neighbour; others to the nearest
-    one_ulp = 2.0 ** -7                                   # bf16 spacing in [1, 2)
-    assert obb.round_bf16(np.array([1.0, 1.0 + one_ulp]))[1] == 1.0 + one_ulp
-    assert obb.round_bf16(np.array([1.0 + one_ulp / 2]))[0] == 1.0              # tie -> even (1.0)
-    assert obb.round_bf16(np.array([1.0 + 3 * one_ulp / 2]))[0] == 1.0 + 2 * one_ulp   # tie -> even
-    assert obb.round_bf16(np.array([1.0 + 0.6 * one_ulp]))[0] == 1.0 + one_ulp
-    v = np.random.default_rng(0).standard_normal(1000)
-    r = obb.round_bf16(v)
-    assert np.all(np.abs(r - v) <= np.abs(v) * 2.0 ** -8 + 1e-30)
-
-
-def test_handoff_rounding_stays_close():
-    # rounding the four handoffs moves the gradients by bf16-sized amounts only
-    inp, opts, W, V = _problem(4)
-    kw = dict(D=inp["D"], initial_states=inp["init"], dfinal=V, dt_bias=inp["bias"], z=inp["z"],
-              norm_weight=inp["w"], norm_group_size=opts["group"])
-    a = obb.block_backward(inp["x"], inp["dt_raw"], inp["A_log"], inp["B"], inp["C"], W, **kw)
-    b = obb.block_backward(inp["x"], inp["dt_raw"], inp["A_log"], inp["B"], inp["C"], W, handoff="bf16", **kw)
-    for k in ("dx", "ddt_raw", "dB", "dC", "dz", "dnorm_weight"):
-        assert np.abs(a[k] - b[k]).max() <= 0.05 * np.abs(a[k]).max(), k
-        assert np.abs(a[k] - b[k]).max() > 0, k
