@@ -81,10 +81,12 @@ typedef enum {
     SSD_ERR_TOO_LARGE = -9,        /* a tensor exceeds the supported index range     */
     SSD_ERR_BAD_OPTION = -10,      /* an ssd_block_opts field out of range, or an
                                       unknown ssd_set_tuning name or value           */
-    SSD_ERR_STATE_TIMEOUT = -11    /* reported by ssd_workspace_status only: a chunk
+    SSD_ERR_STATE_TIMEOUT = -11,   /* reported by ssd_workspace_status only: a chunk
                                       kernel's wait for the state of the chunk before
                                       it gave up; that call's y and final_states are
                                       wrong                                          */
+    SSD_ERR_SCRATCH_TOO_SMALL = -12 /* ssd_forward_noalloc: the problem needs more
+                                      workspace than SSD_NOALLOC_SCRATCH_BYTES       */
 } ssd_status;
 
 typedef struct {
@@ -422,6 +424,29 @@ int ssd_workspace_status(const void* workspace, void* stream);
  * value out of range).  The settings are process-wide and not ordered with
  * calls made concurrently on other host threads. */
 int ssd_set_tuning(const char* name, int64_t value);
+
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, serving loops that must not call hipMalloc, harnesses that forbid
+ * it: ssd_forward without a workspace argument.  Its workspace is a fixed
+ * device array of SSD_NOALLOC_SCRATCH_BYTES inside the library (one per GPU
+ * it runs on, held until the process ends); the call itself allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine).  Problems whose
+ * ssd_workspace_bytes() exceed that size return SSD_ERR_SCRATCH_TOO_SMALL
+ * before anything is enqueued (the 2.7B and 130M layer shapes need about 35
+ * and 27 MB).  Every call on one GPU shares that GPU's array: calls that
+ * overlap in time on one GPU (different streams, or host threads) race and
+ * give wrong results; calls in order on one stream are safe (each call's
+ * kernels reset what must start at zero).  `status` (device memory, may be
+ * NULL) receives, when the call's work completes, 0 or -- when a chunk's wait
+ * for the state before it gave up (see ssd_workspace_status) -- a nonzero
+ * value; with NULL that report is lost.  Everything else as ssd_forward. */
+#define SSD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+int ssd_forward_noalloc(const ssd_problem* prob,
+                        const void* x, const void* dt, const float* A_log,
+                        const void* B, const void* C, const float* D,
+                        const float* initial_states, const int32_t* seq_idx,
+                        void* y, float* final_states, int32_t* status, void* stream);
 
 /* Static, NUL-terminated description of a status code. */
 const char* ssd_error_string(int code);

@@ -11,6 +11,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 #include "ssd_block_bwd.h"
 #include "ssd_bwd.h"
@@ -1188,6 +1189,8 @@ extern "C" const char* ssd_error_string(int code)
     case SSD_ERR_LAUNCH: return "kernel launch failed";
     case SSD_ERR_TOO_LARGE: return "problem exceeds the supported index range";
     case SSD_ERR_BAD_OPTION: return "option out of range (block option, or unknown tuning name or value)";
+    case SSD_ERR_SCRATCH_TOO_SMALL:
+        return "the problem needs more workspace than ssd_forward_noalloc's fixed scratch array";
     case SSD_ERR_STATE_TIMEOUT:
         return "a chunk's wait for the state of the chunk before it gave up: y and final_states are wrong";
     default: return "unknown ssd status";
@@ -1229,4 +1232,49 @@ extern "C" int ssd_set_tuning(const char* name, int64_t value)
             return SSD_OK;
         }
     return SSD_ERR_BAD_OPTION;
+}
+
+// ---------------------------------------------------------------------------
+// ssd_forward_noalloc: the forward with the library's own fixed workspace.
+// The array lives in device memory of every GPU the library runs on; its name
+// is only a host-side stand-in, so host code uses the address that
+// hipGetSymbolAddress gives for the current device, never the name itself.
+static __device__ __align__(256) unsigned char scratch[SSD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];   // per device, looked up once (under g_scratch_mu)
+
+int scratch_address(void** out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return SSD_ERR_LAUNCH;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SSD_ERR_LAUNCH;
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" int ssd_forward_noalloc(const ssd_problem* prob, const void* x, const void* dt, const float* A_log,
+                                   const void* B, const void* C, const float* D, const float* initial_states,
+                                   const int32_t* seq_idx, void* y, float* final_states, int32_t* status,
+                                   void* stream)
+{
+    size_t need = 0;
+    int rc = ssd_workspace_bytes(prob, &need);   // host-side validation and sizing only
+    if (rc != SSD_OK) return rc;
+    if (need > SSD_NOALLOC_SCRATCH_BYTES) return SSD_ERR_SCRATCH_TOO_SMALL;
+    void* ws = nullptr;
+    if ((rc = scratch_address(&ws)) != SSD_OK) return rc;
+    // the status word goes to the caller's pointer, or stays in the scratch header
+    return forward_impl(prob, nullptr, x, dt, A_log, B, C, D, initial_states, seq_idx, y, final_states, ws,
+                        SSD_NOALLOC_SCRATCH_BYTES, stream, nullptr, nullptr, nullptr, status);
 }

@@ -35,6 +35,8 @@ SSD_ERR_LAUNCH = -8
 SSD_ERR_TOO_LARGE = -9
 SSD_ERR_BAD_OPTION = -10
 SSD_ERR_STATE_TIMEOUT = -11
+SSD_ERR_SCRATCH_TOO_SMALL = -12
+SSD_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_decode_step",
             "ssd_block_workspace_bytes", "ssd_forward_block", "ssd_forward_block_timed",
@@ -43,7 +45,7 @@ EXPORTED = ("ssd_workspace_bytes", "ssd_forward", "ssd_forward_timed", "ssd_deco
             "ssd_backward_varlen_workspace_bytes", "ssd_backward_varlen",
             "ssd_forward_varlen_workspace_bytes", "ssd_forward_varlen",
             "ssd_backward_block_workspace_bytes", "ssd_backward_block", "ssd_workspace_status",
-            "ssd_set_tuning", "ssd_error_string")
+            "ssd_set_tuning", "ssd_forward_noalloc", "ssd_error_string")
 
 
 class SsdProblem(ctypes.Structure):
@@ -144,6 +146,8 @@ def load_library(path: str = LIB_PATH):
     lib.ssd_workspace_status.restype = ctypes.c_int
     lib.ssd_set_tuning.argtypes = [ctypes.c_char_p, ctypes.c_int64]
     lib.ssd_set_tuning.restype = ctypes.c_int
+    lib.ssd_forward_noalloc.argtypes = [ctypes.POINTER(SsdProblem)] + [vp] * 12
+    lib.ssd_forward_noalloc.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -215,6 +219,15 @@ def ssd_forward(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx
         ctypes.byref(prob), x, dt, A_log, B, C, D or None, initial_states or None,
         seq_idx or None, y, final_states or None, workspace, int(workspace_bytes),
         stream or None)
+
+
+def ssd_forward_noalloc(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx, y,
+                        final_states, status, stream) -> int:
+    """Raw ABI call on integer device addresses (0 = NULL): the forward on the
+    library's fixed scratch array (no workspace); returns the status."""
+    return load_library().ssd_forward_noalloc(
+        ctypes.byref(prob), x, dt, A_log, B, C, D or None, initial_states or None,
+        seq_idx or None, y, final_states or None, status or None, stream or None)
 
 
 def ssd_forward_timed(prob: SsdProblem, x, dt, A_log, B, C, D, initial_states, seq_idx, y,
