@@ -418,10 +418,10 @@ struct MainSmem {
     u16 XS[2][kQ * kP];       // x of the current / next head (token-major, swizzled)
     float cs[2][kQ];          // chunk-local cumsum of dt A (log2 units) of the current / next head
     float dt[2][kQ];
-    float wtot[4];            // per-wavefront totals of the cumsum
+    float wtot[2][4];         // per-wavefront totals of the cumsum
     float wn[kP];             // normalisation weights of the current head
-    float vf[kQ];             // dt_s exp2(cs[tile end] - cs_s)
-    float w[kQ];              // dt_s exp2(cs[Q-1] - cs_s)
+    float vf[2][kQ];          // dt_s exp2(cs[tile end] - cs_s)
+    float w[2][kQ];           // dt_s exp2(cs[Q-1] - cs_s)
     int ticket;
 };
 
@@ -787,9 +787,11 @@ template <int N, bool PACKED, bool EARLY, bool Y32>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
                                           uint2 (&btf)[kQ / 32][2], uint4 (&cf)[2][N / 32],
-                                          u16& dtr, u16* __restrict__ xs, u16* __restrict__ xs_n,
+                                          u16& dtr, bool& ready, u16* __restrict__ xs, u16* __restrict__ xs_n,
                                           float* __restrict__ cs, float* __restrict__ dt,
                                           float* __restrict__ wt, float* __restrict__ vf, float* __restrict__ w,
+                                          float* __restrict__ cs_n, float* __restrict__ dt_n,
+                                          float* __restrict__ wt_n, float* __restrict__ vf_n, float* __restrict__ w_n,
                                           u16* __restrict__ gr, u16* __restrict__ hb, int* __restrict__ tk,
                                           const float* __restrict__ A_logp, const float* __restrict__ Dp,
                                           const float* __restrict__ biasp, float* __restrict__ wn)
@@ -828,49 +830,69 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // x (and this thread's dt) of the next head -- of this item, or of the next
     // item once known -- arrive while this head computes
     u16 dtr_next = 0;
+    int h_next = -1, L_next = 0;   // the next head of this workgroup, once known
     if (!last) {
         dma_head(p, it, h + 1, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, it, h + 1, tid);
+        h_next = h + 1;
+        L_next = L;
     } else if (hk > 0 && next < nwork) {
         const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
         dma_head(p, nit, nit.h0, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
+        h_next = nit.h0;
+        L_next = nit.L;
     }
 
     // ---- step 1: chunk-local inclusive cumsum of a = dt A (log2 units), one token
     // per thread (wavefront scans, then the wavefront totals through LDS), and the
-    // per-token weights of the diagonal block and the right factor
-    float d = 0.f, incl = 0.f;
-    if (tid < kQ) {
-        if (tid < L) {
-            d = bf(dtr);
-            if (p.dtx.active) {   // the block path's dt parameterisation
-                if (biasp) d += biasp[h];
-                if (p.dtx.softplus) d = softplus_f(d);
-                d = fminf(fmaxf(d, p.dtx.lo), p.dtx.hi);
+    // per-token weights of the diagonal block and the right factor.  The head
+    // before this one in the workgroup has normally done it already, in its
+    // output stage (`ready`); otherwise (a workgroup's first head) here.
+    // The scan for head hh of a chunk of Lh tokens: this thread's dt, its
+    // wavefront prefix, the wavefront totals to wtv.
+    const auto scan = [&](u16 raw, int hh, int Lh, float* wtv, float& dv, float& inc) {
+        dv = 0.f;
+        inc = 0.f;
+        if (tid < kQ) {
+            if (tid < Lh) {
+                dv = bf(raw);
+                if (p.dtx.active) {   // the block path's dt parameterisation
+                    if (biasp) dv += biasp[hh];
+                    if (p.dtx.softplus) dv = softplus_f(dv);
+                    dv = fminf(fmaxf(dv, p.dtx.lo), p.dtx.hi);
+                }
             }
+            inc = dv * (-expf(A_logp[hh]) * kLog2e);
+            inc = wave_inclusive_scan(inc);
+            if (lane == 63) wtv[wave] = inc;
         }
-        incl = d * (-expf(A_logp[h]) * kLog2e);
-        incl = wave_inclusive_scan(incl);
-        if (lane == 63) wt[wave] = incl;
-    }
-    lds_barrier();
-    if (tid < kQ) {
-        float pre = 0.f, tot = 0.f;
+    };
+    // ... and, after a barrier, the cumsum and the weights
+    const auto weights = [&](const float* wtv, float dv, float inc, float* csv, float* dtv, float* vfv, float* wv) {
+        if (tid < kQ) {
+            float pre = 0.f, tot = 0.f;
 #pragma unroll
-        for (int k = 0; k < kQ / 64; ++k) {
-            const float v = wt[k];
-            tot += v;
-            if (k < wave) pre += v;
+            for (int k = 0; k < kQ / 64; ++k) {
+                const float v = wtv[k];
+                tot += v;
+                if (k < wave) pre += v;
+            }
+            const float cst = inc + pre;
+            const float cend = row_last(cst, lane);   // end of this token's 16-token tile
+            csv[tid] = cst;
+            dtv[tid] = dv;
+            vfv[tid] = dv * exp2f(cend - cst);
+            wv[tid] = dv * exp2f(tot - cst);
         }
-        const float cst = incl + pre;
-        const float cend = row_last(cst, lane);   // end of this token's 16-token tile
-        cs[tid] = cst;
-        dt[tid] = d;
-        vf[tid] = d * exp2f(cend - cst);
-        w[tid] = d * exp2f(tot - cst);
+    };
+    if (!ready) {
+        float d, incl;
+        scan(dtr, h, L, wt, d, incl);
+        lds_barrier();
+        weights(wt, d, incl, cs, dt, vf, w);
+        lds_barrier();
     }
-    lds_barrier();
 
     // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
     f32x4_t y[2][4];
@@ -1113,23 +1135,17 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
                 }
             }
         }
-#pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4) {
-            const int t = 16 * strip[k4] + r;
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                uint2 packed;
-                packed.x = pack_bf16x2(y[k4][pt][0], y[k4][pt][1]);
-                packed.y = pack_bf16x2(y[k4][pt][2], y[k4][pt][3]);
-                *reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg)) = packed;   // cells this lane read
-            }
+        // step 1 of this workgroup's next head, while this head's y is written
+        if (last && hk == 0 && next < nwork) {   // one head per item: known since the state barrier
+            const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
+            h_next = nit.h0;
+            L_next = nit.L;
         }
-        lds_barrier();
-        if (!EARLY && tid == 0 && has_next)
-            __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        float d_next = 0.f, incl_next = 0.f;
+        if (h_next >= 0) scan(dtr_next, h_next, L_next, wt_n, d_next, incl_next);
         if constexpr (Y32) {
-            // lane: token 16 strip + r, features 16 pt + 4 lg .. + 3 (16 bytes)
+            // float32 y straight from the accumulators: lane = token 16 strip + r,
+            // features 16 pt + 4 lg .. + 3 (16 bytes)
             float* y32 = static_cast<float*>(p.y) + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
 #pragma unroll
             for (int k4 = 0; k4 < 2; ++k4) {
@@ -1140,28 +1156,45 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
                         *reinterpret_cast<float4*>(y32 + static_cast<unsigned>(t) * xrow + 16 * pt + 4 * lg) =
                             make_float4(y[k4][pt][0], y[k4][pt][1], y[k4][pt][2], y[k4][pt][3]);
             }
-            lds_barrier();
+            lds_barrier();   // (the next head's wavefront totals)
             if (!EARLY && tid == 0 && has_next)
                 __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (h_next >= 0) weights(wt_n, d_next, incl_next, cs_n, dt_n, vf_n, w_n);
             if (gram_ahead) wait_vmem();   // the next item's Gram tiles have landed
         } else {
-        u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
-        constexpr int kPieces = kQ * kP / 8 / kMainThreads;   // 16-byte pieces per thread
-        uint4 v[kPieces];
 #pragma unroll
-        for (int k = 0; k < kPieces; ++k) {
-            const int ci = tid + kMainThreads * k;      // piece: token ci/8, group ci%8
-            v[k] = *reinterpret_cast<const uint4*>(xw + xs_off(ci >> 3, 8 * (ci & 7)));
-        }
-        if (gram_ahead) wait_vmem();   // the next item's Gram tiles have landed
+            for (int k4 = 0; k4 < 2; ++k4) {
+                const int t = 16 * strip[k4] + r;
 #pragma unroll
-        for (int k = 0; k < kPieces; ++k) {
-            const int ci = tid + kMainThreads * k;
-            const int t = ci >> 3, grp = ci & 7;
-            // streaming (non-temporal) stores: y is not read again by this kernel
-            if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
-        }
+                for (int pt = 0; pt < 4; ++pt) {
+                    uint2 packed;
+                    packed.x = pack_bf16x2(y[k4][pt][0], y[k4][pt][1]);
+                    packed.y = pack_bf16x2(y[k4][pt][2], y[k4][pt][3]);
+                    *reinterpret_cast<uint2*>(xw + xs_off(t, 16 * pt + 4 * lg)) = packed;   // cells this lane read
+                }
+            }
+            lds_barrier();   // (y staged; the next head's wavefront totals)
+            if (!EARLY && tid == 0 && has_next)
+                __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (h_next >= 0) weights(wt_n, d_next, incl_next, cs_n, dt_n, vf_n, w_n);
+            u16* ychunk = yp + ((static_cast<int64_t>(b) * p.T + c0) * p.H + h) * kP;
+            constexpr int kPieces = kQ * kP / 8 / kMainThreads;   // 16-byte pieces per thread
+            uint4 v[kPieces];
+#pragma unroll
+            for (int k = 0; k < kPieces; ++k) {
+                const int ci = tid + kMainThreads * k;      // piece: token ci/8, group ci%8
+                v[k] = *reinterpret_cast<const uint4*>(xw + xs_off(ci >> 3, 8 * (ci & 7)));
+            }
+            if (gram_ahead) wait_vmem();   // the next item's Gram tiles have landed
+#pragma unroll
+            for (int k = 0; k < kPieces; ++k) {
+                const int ci = tid + kMainThreads * k;
+                const int t = ci >> 3, grp = ci & 7;
+                // streaming (non-temporal) stores: y is not read again by this kernel
+                if (t < L) __builtin_nontemporal_store(__builtin_bit_cast(uint4_t, v[k]), reinterpret_cast<uint4_t*>(ychunk + (static_cast<unsigned>(t) * xrow + 8u * grp)));
+            }
         }
     }
     // The next item's B^T and C fragments (their last uses in this item are
@@ -1172,8 +1205,9 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         load_bt<N>(p, nit, ntw, r, lg, btf);
         load_c<N>(p, nit, strip, r, lg, cf);
     }
-    lds_barrier();   // this head's LDS buffers may be refilled from here on
+    lds_barrier();   // this head's LDS buffers may be refilled from here on; the next head's weights are in place
     dtr = dtr_next;  // here, where the load has long completed (the epilogue waited for it)
+    ready = h_next >= 0;
 }
 
 // A_log, D and the dt bias come as separate read-only arguments so that their per-head values
@@ -1210,6 +1244,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     // by a running (or finished) workgroup.  The operands of the next item are
     // prefetched during the last head of the current one.
     u16 dtr = 0;    // this thread's dt of the current head (token tid), raw bf16
+    bool ready = false;   // the current head's step 1 done by the head before it
     if (tid == 0) sm.ticket = atomicAdd(p.ticket, 1);
     __syncthreads();
     int work = sm.ticket;
@@ -1238,9 +1273,9 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
     int next = nwork;
     for (int hk = 0; hk < p.HG; ++hk) {
-        head_step<N, PACKED, EARLY, Y32>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, sm.XS[q], sm.XS[q ^ 1],
-                     sm.cs[q], sm.dt[q], sm.wtot, sm.vf, sm.w, s_gr, s_hb, &sm.ticket, A_logp, Dp,
-                     biasp, sm.wn);
+        head_step<N, PACKED, EARLY, Y32>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, ready, sm.XS[q],
+                     sm.XS[q ^ 1], sm.cs[q], sm.dt[q], sm.wtot[q], sm.vf[q], sm.w[q], sm.cs[q ^ 1], sm.dt[q ^ 1],
+                     sm.wtot[q ^ 1], sm.vf[q ^ 1], sm.w[q ^ 1], s_gr, s_hb, &sm.ticket, A_logp, Dp, biasp, sm.wn);
         q ^= 1;
     }
     if (next >= nwork) break;

@@ -224,6 +224,8 @@ def test_packed_rows_both_device_paths(tune):
     (1, 256, 4, 128, 2),
     # many chunks, 4 heads per workgroup, several workgroups per (row, chunk)
     (3, 2000, 16, 128, 1),
+    # 10 heads per group: 5 heads per work item
+    (2, 1300, 10, 128, 1),
 ])
 def test_fused_shapes(shape):
     b, T, H, N, G = shape
@@ -231,13 +233,14 @@ def test_fused_shapes(shape):
     check(make_inputs(p, 11), tag="fused")
 
 
-@pytest.mark.parametrize("hg", ["1", "2", "4"])
+@pytest.mark.parametrize("hg", ["1", "2", "4", "5"])
 def test_fused_persistent_items(tune, hg):
     """Few persistent workgroups, so that each one runs many work items in a row
-    (prefetching the next item's operands); every head is checked."""
+    (prefetching the next item's operands and the next head's step 1); every
+    head is checked."""
     tune("max_workgroups", 3)
     tune("heads_per_item", int(hg))
-    p = Problem(2, 1500, 8, 64, 128, 1, 256, "bf16", init_states=True)
+    p = Problem(2, 1500, 10 if hg == "5" else 8, 64, 128, 1, 256, "bf16", init_states=True)
     check(make_inputs(p, 13), tag="persistent_hg" + hg)
 
 
