@@ -63,6 +63,7 @@ constexpr int kQ = 256;                       // chunk length
 constexpr int kNQ = kQ / 16;                  // 16-token strips per chunk
 constexpr int kTiles = kNQ * (kNQ + 1) / 2;   // causal 16x16 tiles (s-tile <= t-tile)
 constexpr int kP = 64;                        // head dimension
+constexpr int kNH = 128;                      // widest column block of the state the chunk kernel handles at once
 constexpr int kWaves = 8;
 constexpr int kMainThreads = kWaves * 64;
 constexpr int kPrepThreads = 512;
@@ -281,7 +282,7 @@ template <int N, bool PACKED>
 __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
 {
     constexpr int RS = N + 8;
-    __shared__ __attribute__((aligned(16))) PrepSmem<N> sm;
+    __shared__ __attribute__((aligned(16))) PrepSmem<(N > kNH ? kNH : N)> sm;
     const int c = blockIdx.x;
     const int b = static_cast<int>(blockIdx.y / p.G), g = static_cast<int>(blockIdx.y % p.G);
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
@@ -300,6 +301,97 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
         L = e.y;
     }
 
+    if constexpr (N > kNH) {
+        // The state's width (N = 256) is wider than LDS holds B for: the Gram
+        // contraction runs in passes over column blocks of B and C (NP
+        // columns each), the tiles accumulating in registers.
+        constexpr int NP = kNH, RSP = NP + 8;
+        const int64_t brow = p.G * N;
+        const u16* Bchunk = static_cast<const u16*>(p.B) + ((b * p.T + c0) * p.G + g) * N;
+        const u16* Cchunk = static_cast<const u16*>(p.C) + ((b * p.T + c0) * p.G + g) * N;
+        u16* gram = p.gram + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * kTiles * 256;
+        u16* bt = p.BT + ((static_cast<int64_t>(b) * p.G + g) * p.nC + c) * N * kQ;
+        for (int part = blockIdx.z; part < kGramParts; part += gridDim.z) {
+            if (part != static_cast<int>(blockIdx.z)) __syncthreads();   // the previous part's LDS reads are done
+            if (part == 0)
+                for (int hh = tid; hh < hpg; hh += kPrepThreads)
+                    p.flags[(static_cast<int64_t>(b) * p.H + g * hpg + hh) * p.nC + c] = 0;
+            const int rows[4] = {part, 7 - part, 8 + part, kNQ - 1 - part};
+            const int i = rows[wave >> 1];   // this wavefront's t-tile row; s-tiles (wave & 1) + 2 k
+            f32x4_t acc[kNQ / 2];
+#pragma unroll
+            for (int k = 0; k < kNQ / 2; ++k) acc[k] = zero4();
+#pragma unroll 1
+            for (int kp = 0; kp < N / NP; ++kp) {
+                if (kp > 0) __syncthreads();   // the previous block's LDS reads are done
+                constexpr int kBPer = kQ * NP / 8 / kPrepThreads, kCPer = 64 * NP / 8 / kPrepThreads;
+                static_assert(kBPer * kPrepThreads == kQ * NP / 8 && kCPer * kPrepThreads == 64 * NP / 8, "split");
+                uint4 vb[kBPer], vc[kCPer];
+#pragma unroll
+                for (int k = 0; k < kBPer; ++k) {
+                    const int e = tid + kPrepThreads * k;
+                    const int s = e / (NP / 8), col = 8 * (e % (NP / 8));
+                    vb[k] = *reinterpret_cast<const uint4*>(Bchunk + (s < L ? s : L - 1) * brow + kp * NP + col);
+                }
+#pragma unroll
+                for (int k = 0; k < kCPer; ++k) {
+                    const int e = tid + kPrepThreads * k;
+                    const int lr = e / (NP / 8), col = 8 * (e % (NP / 8));
+                    const int t = 16 * rows[lr >> 4] + (lr & 15);
+                    vc[k] = *reinterpret_cast<const uint4*>(Cchunk + (t < L ? t : L - 1) * brow + kp * NP + col);
+                }
+#pragma unroll
+                for (int k = 0; k < kBPer; ++k) {
+                    const int e = tid + kPrepThreads * k;
+                    const int s = e / (NP / 8), col = 8 * (e % (NP / 8));
+                    *reinterpret_cast<uint4*>(&sm.B[s * RSP + col]) = (s < L) ? vb[k] : make_uint4(0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int k = 0; k < kCPer; ++k) {
+                    const int e = tid + kPrepThreads * k;
+                    const int lr = e / (NP / 8), col = 8 * (e % (NP / 8));
+                    const int t = 16 * rows[lr >> 4] + (lr & 15);
+                    *reinterpret_cast<uint4*>(&sm.C[lr * RSP + col]) = (t < L) ? vc[k] : make_uint4(0, 0, 0, 0);
+                }
+                __syncthreads();
+                uint4 cfr[NP / 32];
+#pragma unroll
+                for (int k = 0; k < NP / 32; ++k)
+                    cfr[k] = *reinterpret_cast<const uint4*>(&sm.C[(16 * (wave >> 1) + r) * RSP + 32 * k + 8 * lg]);
+#pragma unroll
+                for (int kk = 0; kk < kNQ / 2; ++kk) {
+                    const int j = (wave & 1) + 2 * kk;
+                    if (j <= i)
+#pragma unroll
+                        for (int k = 0; k < NP / 32; ++k) {
+                            const uint4 va =
+                                *reinterpret_cast<const uint4*>(&sm.B[(16 * j + r) * RSP + 32 * k + 8 * lg]);
+                            acc[kk] = mfma(as_bf16x8(va), as_bf16x8(cfr[k]), acc[kk]);
+                        }
+                }
+                // this part's quarter of this block's B^T rows: item (n, 8 tokens), 16-byte stores along s
+                constexpr int kBtItems = NP * (kQ / 8) / kGramParts;
+                for (int e = part * kBtItems + tid; e < (part + 1) * kBtItems; e += kPrepThreads) {
+                    const int n = e % NP, so = e / NP;
+                    U16x8 v;
+#pragma unroll
+                    for (int q8 = 0; q8 < 8; ++q8) v.v[q8] = sm.B[(8 * so + q8) * RSP + n];
+                    *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(kp * NP + n) * kQ + 8 * so) =
+                        __builtin_bit_cast(uint4, v);
+                }
+            }
+#pragma unroll
+            for (int kk = 0; kk < kNQ / 2; ++kk) {
+                const int j = (wave & 1) + 2 * kk;
+                if (j <= i) {
+                    uint2 packed;
+                    packed.x = pack_bf16x2(acc[kk][0], acc[kk][1]);
+                    packed.y = pack_bf16x2(acc[kk][2], acc[kk][3]);
+                    *reinterpret_cast<uint2*>(gram + (static_cast<int64_t>(tile_index(i, j)) * 64 + lane) * 4) = packed;
+                }
+            }
+        }
+    } else {
     // A workgroup takes parts z, z + gridDim.z, ... of the chunk (fewer
     // workgroups per chunk when there are many chunks: the B rows stay in LDS).
     for (int part = blockIdx.z; part < kGramParts; part += gridDim.z) {
@@ -385,6 +477,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
             for (int e = 0; e < 8; ++e) v.v[e] = sm.B[(8 * so + e) * RS + n];
             *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
         }
+    }
     }
 }
 
@@ -744,15 +837,16 @@ __device__ __forceinline__ void dma_gram_rows(u16* gr, const FusedParams& p, con
     }
 }
 
-// B^T fragments of n-tile ntw for the right factor, in the diagonal block's
-// contraction order (slots 0-3: tokens 32m + 4 lg + e, slots 4-7:
-// 32m + 16 + 4 lg + e - 4), so that both share the x^T reads.
-template <int N>
-__device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, int ntw, int r, int lg,
-                                        uint2 (&btf)[kQ / 32][2])
+// B^T fragments of n-tile ntw of column block hf (NH columns) of the state
+// for the right factor, in the diagonal block's contraction order (slots 0-3:
+// tokens 32m + 4 lg + e, slots 4-7: 32m + 16 + 4 lg + e - 4), so that both
+// share the x^T reads.
+template <int N, int NH>
+__device__ __forceinline__ void load_bt_block(const FusedParams& p, const Item& it, int ntw, int r, int lg, int hf,
+                                              uint2 (&btf)[kQ / 32][2])
 {
     const u16* bt = p.BT + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * N * kQ;
-    const u16* btr = bt + (static_cast<unsigned>(16 * ntw + r) * kQ + 4u * lg);
+    const u16* btr = bt + (static_cast<unsigned>(hf * NH + 16 * ntw + r) * kQ + 4u * lg);
 #pragma unroll
     for (int m = 0; m < kQ / 32; ++m) {
         btf[m][0] = *reinterpret_cast<const uint2*>(btr + 32 * m);
@@ -760,11 +854,20 @@ __device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, in
     }
 }
 
-// C fragments of the two strips for the left factor (rows past a partial
-// chunk's end are clamped; they are never stored).
+// The item-level B^T fragments (one column block of the state: N <= 128; with
+// two blocks every head loads its own per block).
 template <int N>
-__device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, const int* strip, int r, int lg,
-                                       uint4 (&cf)[2][N / 32])
+__device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, int ntw, int r, int lg,
+                                        uint2 (&btf)[kQ / 32][2])
+{
+    if constexpr (N <= kNH) load_bt_block<N, N>(p, it, ntw, r, lg, 0, btf);
+}
+
+// C fragments of the two strips for the left factor, columns [hf NH, hf NH +
+// NH) of C (rows past a partial chunk's end are clamped; they are never stored).
+template <int N, int NH>
+__device__ __forceinline__ void load_c_block(const FusedParams& p, const Item& it, const int* strip, int r, int lg,
+                                             int hf, uint4 (&cf)[2][NH / 32])
 {
     const unsigned crow = static_cast<unsigned>(p.G * N);
 #pragma unroll
@@ -772,9 +875,18 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
         const int t = 16 * strip[k4] + r;
         const unsigned tc = static_cast<unsigned>(t < it.L ? t : it.L - 1);
 #pragma unroll
-        for (int k = 0; k < N / 32; ++k)
-            cf[k4][k] = *reinterpret_cast<const uint4*>(it.cchunk + (tc * crow + 32u * k + 8u * lg));
+        for (int k = 0; k < NH / 32; ++k)
+            cf[k4][k] = *reinterpret_cast<const uint4*>(it.cchunk + (tc * crow + hf * NH + 32u * k + 8u * lg));
     }
+}
+
+// The item-level C fragments (one column block of the state: N <= 128; with
+// two blocks every head loads its own per block).
+template <int N>
+__device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, const int* strip, int r, int lg,
+                                       uint4 (&cf)[2][(N < kNH ? N : kNH) / 32])
+{
+    if constexpr (N <= kNH) load_c_block<N, N>(p, it, strip, r, lg, 0, cf);
 }
 
 // One head of a work item.  Every LDS buffer is a separate __restrict__
@@ -786,7 +898,8 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
 template <int N, bool PACKED, bool EARLY, bool Y32>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
-                                          uint2 (&btf)[kQ / 32][2], uint4 (&cf)[2][N / 32],
+                                          uint2 (&btf)[kQ / 32][2],
+                                          uint4 (&cf)[2][(N < kNH ? N : kNH) / 32],
                                           u16& dtr, bool& ready, u16* __restrict__ xs, u16* __restrict__ xs_n,
                                           float* __restrict__ cs, float* __restrict__ dt,
                                           float* __restrict__ wt, float* __restrict__ vf, float* __restrict__ w,
@@ -796,10 +909,16 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
                                           const float* __restrict__ A_logp, const float* __restrict__ Dp,
                                           const float* __restrict__ biasp, float* __restrict__ wn)
 {
-    constexpr int NT = N / 16;
+    // The state (P x N) is processed in HALVES column blocks of NH <= 128
+    // (two for N = 256): right factor, state passing and left factor each
+    // per block, so that registers and the LDS copy of the state stay those of
+    // N = 128.
+    constexpr int NH = N < kNH ? N : kNH;
+    constexpr int HALVES = N / NH;
+    constexpr int NT = NH / 16;
     constexpr int PTW = 4 * NT / kWaves;
-    constexpr int KN = N / 32;
-    constexpr int HBS = N + 8;
+    constexpr int KN = NH / 32;
+    constexpr int HBS = NH + 8;
     // per-wavefront constants (loop-invariant; the compiler keeps them out of the loops)
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // provably uniform
@@ -843,6 +962,12 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         h_next = nit.h0;
         L_next = nit.L;
     }
+
+    // Two column blocks of the state: this head's B^T fragments of the first
+    // block now (they arrive during the diagonal block), of the second when the
+    // first block's right factor starts.
+    uint2 bth[HALVES > 1 ? 2 : 1][kQ / 32][2];
+    if constexpr (HALVES > 1) load_bt_block<N, NH>(p, it, ntw, r, lg, 0, bth[0]);
 
     // ---- step 1: chunk-local inclusive cumsum of a = dt A (log2 units), one token
     // per thread (wavefront scans, then the wavefront totals through LDS), and the
@@ -922,15 +1047,24 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
 
     // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
-    f32x4_t sacc[PTW];
+    // (per column block of the state)
+    f32x4_t sacc[HALVES][PTW];
 #pragma unroll
-    for (int i = 0; i < PTW; ++i) sacc[i] = zero4();
+    for (int hf = 0; hf < HALVES; ++hf)
+#pragma unroll
+        for (int i = 0; i < PTW; ++i) sacc[hf][i] = zero4();
     // Opaque to the optimiser, so that it does not hoist the unpacking of B^T out
     // of the head loop (64 more registers, and a wait for the loads at the start
     // of every item).
+    if constexpr (HALVES == 1) {
 #pragma unroll
-    for (int m = 0; m < kQ / 32; ++m) asm volatile("" : "+v"(btf[m][0]), "+v"(btf[m][1]));
-    {
+        for (int m = 0; m < kQ / 32; ++m) asm volatile("" : "+v"(btf[m][0]), "+v"(btf[m][1]));
+    }
+#pragma unroll
+    for (int hf = 0; hf < HALVES; ++hf) {
+        if (HALVES > 1) __builtin_amdgcn_sched_barrier(0);
+        if (HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth[hf + 1]);
+        const uint2 (&bsrc)[kQ / 32][2] = HALVES > 1 ? bth[hf] : btf;
         const char* xsb = reinterpret_cast<const char*>(xs);
         const float* wl = w + 4 * lg;
 #pragma unroll
@@ -938,7 +1072,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             const float4 w0 = *reinterpret_cast<const float4*>(wl + 32 * m);
             const float4 w1 = *reinterpret_cast<const float4*>(wl + 32 * m + 16);
             const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-            const u32 bw[4] = {btf[m][0].x, btf[m][0].y, btf[m][1].x, btf[m][1].y};
+            const u32 bw[4] = {bsrc[m][0].x, bsrc[m][0].y, bsrc[m][1].x, bsrc[m][1].y};
             float bf8[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -950,7 +1084,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             for (int i = 0; i < PTW; ++i) {
                 const char* xb = xsb + xa[pt0 + i] + 4096 * m;
                 const uint2 lo = tr_read(xb), hi = tr_read(xb + 2048);
-                sacc[i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[i]);
+                sacc[hf][i] = mfma(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), bop, sacc[hf][i]);
             }
         }
     }
@@ -960,7 +1094,8 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     float* ring_h = p.ring + (static_cast<int64_t>(it.ring) * p.H + h) * 2 * PN;
     const __amdgpu_buffer_rsrc_t ring_rs =
         __builtin_amdgcn_make_buffer_rsrc(ring_h, 0, static_cast<int>(2 * PN * sizeof(float)), 0x00020000);
-    const int frag_base = wave * PTW * 64 + lane;   // private ring layout: [wave][frag][lane][4]
+    // private ring layout: [column block][wave][frag][lane][4]
+    const int frag_base = wave * PTW * 64 + lane;
     // The first head reserves the next work item here: the wait for the atomic's
     // result merges with the state wait below, and the result is shared through
     // LDS at the state barrier.
@@ -982,112 +1117,129 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // wavefront copies the 32 rows of its own two strips, so its own wait
     // (in the output stage) suffices.
     if (gate) dma_z_strips(p, it, h, xs, strip, lane);
-    f32x4_t hprev[PTW];
-    if (has_prev) {
-        const int slot = (c + 1) & 1;
-#pragma unroll
-        for (int i = 0; i < PTW; ++i) {
-            const int off = static_cast<int>((slot * PN + (frag_base + i * 64) * 4) * sizeof(float));
-            hprev[i] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ring_rs, off, 0, 16));
-        }
-    } else if (p.init) {
-        // (P, N) layout of the caller's initial state: lane offset + uniform row offsets
-        const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<float*>(p.init + (static_cast<int64_t>(it.seq) * p.H + h) * PN), 0,
-            static_cast<int>(PN * sizeof(float)), 0x00020000);
-        const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
-#pragma unroll
-        for (int i = 0; i < PTW; ++i)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                hprev[i][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                    irs, lo, (16 * i + v) * N * static_cast<int>(sizeof(float)), 0));
-    } else {
-#pragma unroll
-        for (int i = 0; i < PTW; ++i) hprev[i] = zero4();
-    }
     const float decay = exp2f(cs[kQ - 1]);
+    // this lane's first element in the caller's (P, N) initial / final state
+    const int st_lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
+    bool gram_ahead = false;
+    f32x4_t tq[2][4];
 #pragma unroll
-    for (int i = 0; i < PTW; ++i) {
+    for (int k4 = 0; k4 < 2; ++k4)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            hb[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
-            sacc[i][v] = decay * hprev[i][v] + sacc[i][v];
+        for (int pt = 0; pt < 4; ++pt) tq[k4][pt] = zero4();
+#pragma unroll
+    for (int hf = 0; hf < HALVES; ++hf) {
+        // (the compiler keeps each block's loads in their block: hoisting the
+        // second block's would hold both blocks' operands in registers at once)
+        if (HALVES > 1) __builtin_amdgcn_sched_barrier(0);
+        if (hf > 0) lds_barrier();   // the previous block's left factor is done with the LDS state
+        const int hoff = hf * (PN / HALVES);   // this block's offset in a ring slot (floats)
+        const int coff = hf * NH * static_cast<int>(sizeof(float));   // ... and in a (P, N) state row (bytes)
+        f32x4_t hprev[PTW];
+        if (has_prev) {
+            const int slot = (c + 1) & 1;
+#pragma unroll
+            for (int i = 0; i < PTW; ++i) {
+                const int off = static_cast<int>((slot * PN + hoff + (frag_base + i * 64) * 4) * sizeof(float));
+                hprev[i] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ring_rs, off, 0, 16));
+            }
+        } else if (p.init) {
+            // (P, N) layout of the caller's initial state: lane offset + uniform row offsets
+            const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<float*>(p.init + (static_cast<int64_t>(it.seq) * p.H + h) * PN), 0,
+                static_cast<int>(PN * sizeof(float)), 0x00020000);
+#pragma unroll
+            for (int i = 0; i < PTW; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    hprev[i][v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                        irs, st_lo + coff, (16 * i + v) * N * static_cast<int>(sizeof(float)), 0));
+        } else {
+#pragma unroll
+            for (int i = 0; i < PTW; ++i) hprev[i] = zero4();
         }
-    }
-    if (has_next) {
-        const int slot = c & 1;
 #pragma unroll
         for (int i = 0; i < PTW; ++i) {
-            const int off = static_cast<int>((slot * PN + (frag_base + i * 64) * 4) * sizeof(float));
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(uint4_t, sacc[i]), ring_rs, off, 0, 16);
-        }
-    } else if (p.fin) {
-        const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
-            p.fin + (static_cast<int64_t>(it.seq) * p.H + h) * PN, 0,
-            static_cast<int>(PN * sizeof(float)), 0x00020000);
-        const int lo = ((16 * pt0 + 4 * lg) * N + 16 * ntw + r) * static_cast<int>(sizeof(float));
-#pragma unroll
-        for (int i = 0; i < PTW; ++i)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                // extract the element first: bit-casting a vector element in place is
-                // mis-lowered (component 0 stored for every v)
-                const float val = sacc[i][v];
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), frs, lo,
-                                                      (16 * i + v) * N * static_cast<int>(sizeof(float)), 0);
+                hb[(16 * (pt0 + i) + 4 * lg + v) * HBS + 16 * ntw + r] = to_bf16(hprev[i][v]);
+                sacc[hf][i][v] = decay * hprev[i][v] + sacc[hf][i][v];
             }
-    }
-    // The state stores drain while the left factor runs; the flag is set after
-    // the epilogue's barrier, once every wavefront has waited for its stores.
-    // Where the chain of chunks is what bounds the launch (early_flag), every
-    // wavefront waits for its stores here instead and the flag follows this
-    // barrier, so the next chunk need not wait for this one's left factor.
-    // (EARLY: a template parameter, so that the other launches carry none of it.)
-    if (norm && tid < kP) wn[tid] = wreg;
-    if constexpr (EARLY) wait_vmem();
-    lds_barrier();   // bf16 state in LDS complete; every wavefront is past the diagonal block
-    if (EARLY && tid == 0 && has_next)
-        __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (hk == 0) next = *tk;
-    // The next item's Gram tiles (and, with one head per item, its first head's
-    // x): only the bf16 state and z are read from here on.
-    // (With one head per item the next item is known only here: its Gram tiles
-    // and its first head's x follow now, by all wavefronts.)
-    const bool gram_ahead = last && hk == 0 && next < nwork;
-    if (gram_ahead) {
-        const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
-        dma_gram(gr, p, nit, wave, dmo);
-        dma_head(p, nit, nit.h0, xs_n, wave, dmo);
-        if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
-    }
+        }
+        if (has_next) {
+            const int slot = c & 1;
+#pragma unroll
+            for (int i = 0; i < PTW; ++i) {
+                const int off = static_cast<int>((slot * PN + hoff + (frag_base + i * 64) * 4) * sizeof(float));
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(uint4_t, sacc[hf][i]), ring_rs, off, 0, 16);
+            }
+        } else if (p.fin) {
+            const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
+                p.fin + (static_cast<int64_t>(it.seq) * p.H + h) * PN, 0,
+                static_cast<int>(PN * sizeof(float)), 0x00020000);
+#pragma unroll
+            for (int i = 0; i < PTW; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    // extract the element first: bit-casting a vector element in place is
+                    // mis-lowered (component 0 stored for every v)
+                    const float val = sacc[hf][i][v];
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), frs, st_lo + coff,
+                                                          (16 * i + v) * N * static_cast<int>(sizeof(float)), 0);
+                }
+        }
+        // The state stores drain while the left factor runs; the flag is set after
+        // the epilogue's barrier, once every wavefront has waited for its stores.
+        // Where the chain of chunks is what bounds the launch (early_flag), every
+        // wavefront waits for its stores here instead and the flag follows this
+        // barrier, so the next chunk need not wait for this one's left factor.
+        // (EARLY: a template parameter, so that the other launches carry none of it.)
+        if (hf + 1 == HALVES) {
+            if (norm && tid < kP) wn[tid] = wreg;
+            if constexpr (EARLY) wait_vmem();
+        }
+        // Two column blocks: this block's C fragments (the item-level ones
+        // hold the first block only when there is one block).
+        uint4 cfh[2][KN];
+        if constexpr (HALVES > 1) load_c_block<N, NH>(p, it, strip, r, lg, hf, cfh);
+        lds_barrier();   // bf16 state (block) in LDS complete; every wavefront is past the diagonal block
+        if (hf + 1 == HALVES && EARLY && tid == 0 && has_next)
+            __hip_atomic_store(p.flags + (static_cast<int64_t>(b) * p.H + h) * p.nC + c, 1,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (hf == 0) {
+            if (hk == 0) next = *tk;
+            // The next item's Gram tiles (and, with one head per item, its first head's
+            // x): only the bf16 state and z are read from here on.
+            // (With one head per item the next item is known only here: its Gram tiles
+            // and its first head's x follow now, by all wavefronts.)
+            gram_ahead = last && hk == 0 && next < nwork;
+            if (gram_ahead) {
+                const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
+                dma_gram(gr, p, nit, wave, dmo);
+                dma_head(p, nit, nit.h0, xs_n, wave, dmo);
+                if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
+            }
+        }
 
-    // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips ---------
-    {
-        f32x4_t tq[2][4];
-#pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4)
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) tq[k4][pt] = zero4();
+        // ---- left factor: Y^T += exp2(cs_t) * (h_{c-1} C_t^T) for both strips (this block's columns)
 #pragma unroll
         for (int k = 0; k < KN; ++k) {
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) {
                 const bf16x8_t aop = as_bf16x8(*reinterpret_cast<const uint4*>(&hb[(16 * pt + r) * HBS + 32 * k + 8 * lg]));
-                tq[0][pt] = mfma(aop, as_bf16x8(cf[0][k]), tq[0][pt]);
-                tq[1][pt] = mfma(aop, as_bf16x8(cf[1][k]), tq[1][pt]);
+                const uint4 c0v = HALVES > 1 ? cfh[0][k] : cf[0][k], c1v = HALVES > 1 ? cfh[1][k] : cf[1][k];
+                tq[0][pt] = mfma(aop, as_bf16x8(c0v), tq[0][pt]);
+                tq[1][pt] = mfma(aop, as_bf16x8(c1v), tq[1][pt]);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+    }
 #pragma unroll
-        for (int k4 = 0; k4 < 2; ++k4) {
-            const float ev = exp2f(cs[16 * strip[k4] + r]);
+    for (int k4 = 0; k4 < 2; ++k4) {
+        const float ev = exp2f(cs[16 * strip[k4] + r]);
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt)
+        for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) y[k4][pt][v] += ev * tq[k4][pt][v];
-        }
+            for (int v = 0; v < 4; ++v) y[k4][pt][v] += ev * tq[k4][pt][v];
     }
 
 
@@ -1217,11 +1369,12 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
                                                                 const float* __restrict__ Dp,
                                                                 const float* __restrict__ biasp)
 {
-    constexpr int NT = N / 16;            // n-tiles of the state
+    constexpr int NH = N < kNH ? N : kNH; // columns of the state per block (two blocks for N = 256)
+    constexpr int NT = NH / 16;           // n-tiles of a block
     constexpr int PTW = 4 * NT / kWaves;  // p-tiles per wavefront in the right factor (one n-tile each)
-    constexpr int KN = N / 32;            // K-steps over n
-    constexpr int HBS = N + 8;            // LDS row stride of the bf16 state
-    static_assert(PTW == 2 || PTW == 4, "N = 64 or 128");
+    constexpr int KN = NH / 32;           // K-steps over a block's columns
+    constexpr int HBS = NH + 8;           // LDS row stride of the bf16 state (one block)
+    static_assert(PTW == 2 || PTW == 4, "N = 64, 128 or 256");
     static_assert(kMainThreads >= kQ && kP == 64 && kQ * kP * 2 == 32 * 1024 * 1, "x buffer = 32 KiB");
     static_assert(kQ * kP / 512 == 4 * kWaves, "x DMA: 4 blocks of 8 tokens per wavefront");
     static_assert((kTiles * 256 * 2) % 1024 == 0, "Gram DMA in 1 KiB blocks");
@@ -1262,7 +1415,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     // register operands shared by an item's heads (see load_bt / load_c): loaded
     // here for the first item, and for every later item by the last head of the
     // item before it, right after their last use there
-    uint2 btf[kQ / 32][2];
+    uint2 btf[kQ / 32][2];   // (one column block of the state; with two, each head loads its own)
     uint4 cf[2][KN];   // raw bf16 (as a bf16 vector type the compiler merges lanes right at the loads)
     {
         const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
@@ -1366,7 +1519,7 @@ hipError_t launch_seq_table(const int32_t* seq_idx, const SeqStartsArg* arg_star
 
 bool fused_supported(int64_t P, int64_t N, int64_t Q, bool bf16)
 {
-    return bf16 && P == kP && Q == kQ && (N == 64 || N == 128);
+    return bf16 && P == kP && Q == kQ && (N == 64 || N == 128 || N == 256);
 }
 
 FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, int64_t nC, int64_t nseq)
@@ -1400,8 +1553,9 @@ FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, 
 hipError_t launch_fused(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begin,
                         hipEvent_t ev_end)
 {
-    return p.N == 64 ? launch_n<64>(p, stream, ev_begin, ev_end)
-                     : launch_n<128>(p, stream, ev_begin, ev_end);
+    return p.N == 64    ? launch_n<64>(p, stream, ev_begin, ev_end)
+           : p.N == 128 ? launch_n<128>(p, stream, ev_begin, ev_end)
+                        : launch_n<256>(p, stream, ev_begin, ev_end);
 }
 
 }  // namespace ssd

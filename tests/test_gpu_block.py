@@ -78,6 +78,8 @@ SHAPES = {
     # fused path: bf16, P 64, N 128 / 64, Q 256; ragged T, several chunks and items
     "fused_n128": Problem(2, 600, 8, 64, 128, 1, 256, "bf16", init_states=True),
     "fused_n64_g2": Problem(1, 700, 4, 64, 64, 2, 256, "bf16"),
+    # the state in two column blocks (N 256)
+    "fused_n256_g2": Problem(1, 900, 4, 64, 256, 2, 256, "bf16", init_states=True),
     # fused path on a packed row (the device chunk table), short and long sequences
     "fused_varlen": Problem(1, 1500, 8, 64, 128, 2, 256, "bf16", varlen=True, len_lo=1, len_hi=700,
                             init_states=True),

@@ -157,6 +157,7 @@ def _packed(lens, H, N, G, seed, init=True):
     # sequences inside one chunk, a sequence over three chunks
     ([1, 255, 256, 257, 1, 513, 2, 700, 3], 6, 64, 2),
     ([300, 1, 1, 1, 40, 600, 256], 4, 128, 1),
+    ([700, 1, 256, 300, 513], 4, 256, 2),
     # one sequence only, shorter than a chunk
     ([200], 2, 128, 1),
 ])
@@ -207,6 +208,18 @@ def test_fused_state_flag_placement(tune, early):
     check(_packed([300, 1, 700, 256, 90], 4, 64, 1, 41), tag="flag%s_packed" % early)
 
 
+@pytest.mark.parametrize("early", ["0", "1"])
+def test_fused_n256_few_workgroups(tune, early):
+    """N = 256 (two column blocks of the state per head) with few persistent
+    workgroups, both state-flag placements, 1 and 2 heads per item."""
+    tune("early_state_flag", 2 if early == "1" else 1)
+    tune("max_workgroups", 3)
+    for hg in (1, 2):
+        tune("heads_per_item", hg)
+        check(make_inputs(Problem(2, 1100, 4, 64, 256, 2, 256, "bf16", init_states=True), 81),
+              tag="n256_flag%s_hg%d" % (early, hg))
+
+
 def test_packed_rows_both_device_paths(tune):
     """The general kernels (forced) and the fused ones on one packed row, each
     against the oracle."""
@@ -226,6 +239,9 @@ def test_packed_rows_both_device_paths(tune):
     (3, 2000, 16, 128, 1),
     # 10 heads per group: 5 heads per work item
     (2, 1300, 10, 128, 1),
+    # the state in two column blocks (N 256): ragged, grouped, 5 heads per item
+    (2, 700, 6, 256, 2),
+    (1, 1300, 10, 256, 1),
 ])
 def test_fused_shapes(shape):
     b, T, H, N, G = shape
