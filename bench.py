@@ -64,7 +64,7 @@ def kernel_sources_digest(sources=FWD_SOURCES):
 
 
 def dominant_kernel_name(p):
-    fused = (p.dtype == "bf16" and p.headdim == 64 and p.chunk_size == 256 and p.dstate in (64, 128))
+    fused = (p.dtype == "bf16" and p.headdim == 64 and p.chunk_size == 256 and p.dstate in (64, 128, 256))
     return ("k_fused_main<%d>" % p.dstate) if fused else "k_chunk_output"
 
 
@@ -94,7 +94,7 @@ def cpu_baseline(inp, budget_s=20.0):
 
     p = inp.problem
     threads = oracle.default_threads()
-    # calibrate on one head
+    # calibrate on one head, one thread (also the 1-thread rate)
     t0 = time.perf_counter()
     oracle.forward_inputs(inp, heads=[0], nthreads=1)
     one = time.perf_counter() - t0
@@ -104,10 +104,23 @@ def cpu_baseline(inp, budget_s=20.0):
     oracle.forward_inputs(inp, heads=heads, nthreads=threads)
     el = time.perf_counter() - t0
     tok_per_s = p.batch * p.seqlen * (len(heads) / p.nheads) / el
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": tok_per_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": "all %d tokens x %d of %d heads (float64 sequential recurrence, "
                       "OpenMP over heads), %.1f s; rate scaled to all heads"
-                      % (p.batch * p.seqlen, len(heads), p.nheads, el)}
+                      % (p.batch * p.seqlen, len(heads), p.nheads, el),
+            "cpu_model": model,
+            "one_thread_value": p.batch * p.seqlen / p.nheads / one,
+            "one_thread_sample": "all %d tokens x 1 head on 1 thread, %.2f s; rate scaled to all heads"
+                                 % (p.batch * p.seqlen, one)}
 
 
 def decode_bench(args, torch, ssd):
@@ -595,6 +608,9 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--gemm-ceiling", action="store_true",
+                    help="time a large bf16 matrix product (torch.matmul, 8192^3) instead: the "
+                         "box's attainable bf16 matrix-core rate beside the datasheet peak")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: runs on one GPU only (--gpus 1); the sequence/head "
@@ -619,6 +635,27 @@ def main():
         ms = t0.elapsed_time(t1) / args.steps
         print(json.dumps({"copy_bytes_each_way": n, "ms": ms, "gbps_read_plus_write": 2 * n / ms / 1e6}),
               flush=True)
+        return
+
+    if args.gemm_ceiling:
+        n = 8192
+        g = torch.Generator(device="cuda:0").manual_seed(args.seed)
+        a = torch.randn(n, n, device="cuda:0", generator=g).to(torch.bfloat16)
+        b = torch.randn(n, n, device="cuda:0", generator=g).to(torch.bfloat16)
+        c = torch.empty(n, n, dtype=torch.bfloat16, device="cuda:0")
+        for _ in range(args.warmup):
+            torch.matmul(a, b, out=c)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(args.steps):
+            torch.matmul(a, b, out=c)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+        print(json.dumps({"gemm": "bf16 %dx%dx%d torch.matmul" % (n, n, n), "ms": ms, "tflops": tf,
+                          "pct_of_bf16_peak": 100.0 * tf * 1e12 / PEAK_BF16_FLOPS}), flush=True)
         return
 
     from paper_2405_21060_amd import ssd
@@ -693,22 +730,19 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    # whole-job time: plain calls, nothing recorded between them
+    # The timed region: K calls between two events on the launch stream (the
+    # whole-job time); inside each call the library records two more events
+    # on that stream right around the dominant (chunk) kernel, which time that
+    # kernel alone, live, in the same calls.
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
     for i in range(args.steps):
-        step(i)
+        step(i, None if args.no_kernel_events else kev[i])
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     kms = None
     if not args.no_kernel_events:
-        # the dominant kernel's own duration: a second pass of the same calls
-        # with events recorded on the launch stream right around it (the
-        # event records add their own cost, so this pass is not the job time)
-        for i in range(args.steps):
-            step(i, kev[i])
-        torch.cuda.synchronize()
         ks = sorted(a.elapsed_time(z) for a, z in kev)
         kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
                "p90": ks[(9 * len(ks)) // 10]}
