@@ -169,6 +169,16 @@ __device__ __forceinline__ void st_coherent(float* p, float v)
 // contiguous.
 __device__ __forceinline__ int swz(int p, int s) { return s ^ (((p >> 3) & 7) << 3); }
 
+// B^T rows (one per state column n, Q tokens) are stored in MFMA operand
+// order: within each 32-token block m, physical group g = 0..3 of 8 holds
+// tokens 32m + 4g .. + 3 and then 32m + 16 + 4g .. + 3, the eight
+// contraction slots one lane of a 16x16x32 MFMA operand takes (see
+// load_bt_block), so that it loads them with one 16-byte load.
+__device__ __forceinline__ int bt_token(int so, int e)
+{
+    return 32 * (so >> 2) + 4 * (so & 3) + (e < 4 ? e : 12 + e);
+}
+
 // Causal tile index of (s-tile j, t-tile i), j <= i.
 __device__ __forceinline__ int tile_index(int i, int j) { return i * (i + 1) / 2 + j; }
 
@@ -375,7 +385,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
                     const int n = e % NP, so = e / NP;
                     U16x8 v;
 #pragma unroll
-                    for (int q8 = 0; q8 < 8; ++q8) v.v[q8] = sm.B[(8 * so + q8) * RSP + n];
+                    for (int q8 = 0; q8 < 8; ++q8) v.v[q8] = sm.B[bt_token(so, q8) * RSP + n];
                     *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(kp * NP + n) * kQ + 8 * so) =
                         __builtin_bit_cast(uint4, v);
                 }
@@ -474,7 +484,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
             const int n = i % N, so = i / N;
             U16x8 v;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v.v[e] = sm.B[(8 * so + e) * RS + n];
+            for (int e = 0; e < 8; ++e) v.v[e] = sm.B[bt_token(so, e) * RS + n];
             *reinterpret_cast<uint4*>(bt + static_cast<int64_t>(n) * kQ + 8 * so) = __builtin_bit_cast(uint4, v);
         }
     }
@@ -843,22 +853,19 @@ __device__ __forceinline__ void dma_gram_rows(u16* gr, const FusedParams& p, con
 // share the x^T reads.
 template <int N, int NH>
 __device__ __forceinline__ void load_bt_block(const FusedParams& p, const Item& it, int ntw, int r, int lg, int hf,
-                                              uint2 (&btf)[kQ / 32][2])
+                                              uint4 (&btf)[kQ / 32])
 {
     const u16* bt = p.BT + ((static_cast<int64_t>(it.b) * p.G + it.g) * p.nC + it.c) * N * kQ;
-    const u16* btr = bt + (static_cast<unsigned>(hf * NH + 16 * ntw + r) * kQ + 4u * lg);
+    const u16* btr = bt + (static_cast<unsigned>(hf * NH + 16 * ntw + r) * kQ + 8u * lg);
 #pragma unroll
-    for (int m = 0; m < kQ / 32; ++m) {
-        btf[m][0] = *reinterpret_cast<const uint2*>(btr + 32 * m);
-        btf[m][1] = *reinterpret_cast<const uint2*>(btr + 32 * m + 16);
-    }
+    for (int m = 0; m < kQ / 32; ++m) btf[m] = *reinterpret_cast<const uint4*>(btr + 32 * m);
 }
 
 // The item-level B^T fragments (one column block of the state: N <= 128; with
 // two blocks every head loads its own per block).
 template <int N>
 __device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, int ntw, int r, int lg,
-                                        uint2 (&btf)[kQ / 32][2])
+                                        uint4 (&btf)[kQ / 32])
 {
     if constexpr (N <= kNH) load_bt_block<N, N>(p, it, ntw, r, lg, 0, btf);
 }
@@ -898,7 +905,7 @@ __device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, con
 template <int N, bool PACKED, bool EARLY, bool Y32>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
-                                          uint2 (&btf)[kQ / 32][2],
+                                          uint4 (&btf)[kQ / 32],
                                           uint4 (&cf)[2][(N < kNH ? N : kNH) / 32],
                                           u16& dtr, bool& ready, u16* __restrict__ xs, u16* __restrict__ xs_n,
                                           float* __restrict__ cs, float* __restrict__ dt,
@@ -951,13 +958,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     u16 dtr_next = 0;
     int h_next = -1, L_next = 0;   // the next head of this workgroup, once known
     if (!last) {
-        dma_head(p, it, h + 1, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, it, h + 1, tid);
         h_next = h + 1;
         L_next = L;
     } else if (hk > 0 && next < nwork) {
         const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
-        dma_head(p, nit, nit.h0, xs_n, wave, dmo);
         if (tid < kQ) dtr_next = load_dt(p, nit, nit.h0, tid);
         h_next = nit.h0;
         L_next = nit.L;
@@ -966,7 +971,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // Two column blocks of the state: this head's B^T fragments of the first
     // block now (they arrive during the diagonal block), of the second when the
     // first block's right factor starts.
-    uint2 bth[HALVES > 1 ? 2 : 1][kQ / 32][2];
+    uint4 bth[HALVES > 1 ? 2 : 1][kQ / 32];
     if constexpr (HALVES > 1) load_bt_block<N, NH>(p, it, ntw, r, lg, 0, bth[0]);
 
     // ---- step 1: chunk-local inclusive cumsum of a = dt A (log2 units), one token
@@ -1031,6 +1036,15 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // the next item, well ahead of that item's diagonal block.
     const bool gram_early = last && hk > 0 && next < nwork;
     if (gram_early) dma_gram_rows(gr, p, decode_item<PACKED>(p, next, per_c, nHG, N), wave, lane);
+    // x of the next head -- of this item, or of the next item once known --
+    // arrives while this head computes (issued here, not at the head's start,
+    // where the copies would queue behind the previous head's y stores)
+    if (!last)
+        dma_head(p, it, h + 1, xs_n, wave, dmo);
+    else if (hk > 0 && next < nwork) {
+        const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
+        dma_head(p, nit, nit.h0, xs_n, wave, dmo);
+    }
     // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
     // after the right factor)
 #pragma unroll
@@ -1058,13 +1072,17 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // of every item).
     if constexpr (HALVES == 1) {
 #pragma unroll
-        for (int m = 0; m < kQ / 32; ++m) asm volatile("" : "+v"(btf[m][0]), "+v"(btf[m][1]));
+        for (int m = 0; m < kQ / 32; ++m) {
+            uint4_t v = __builtin_bit_cast(uint4_t, btf[m]);
+            asm volatile("" : "+v"(v));
+            btf[m] = __builtin_bit_cast(uint4, v);
+        }
     }
 #pragma unroll
     for (int hf = 0; hf < HALVES; ++hf) {
         if (HALVES > 1) __builtin_amdgcn_sched_barrier(0);
         if (HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth[hf + 1]);
-        const uint2 (&bsrc)[kQ / 32][2] = HALVES > 1 ? bth[hf] : btf;
+        const uint4 (&bsrc)[kQ / 32] = HALVES > 1 ? bth[hf] : btf;
         const char* xsb = reinterpret_cast<const char*>(xs);
         const float* wl = w + 4 * lg;
 #pragma unroll
@@ -1072,7 +1090,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             const float4 w0 = *reinterpret_cast<const float4*>(wl + 32 * m);
             const float4 w1 = *reinterpret_cast<const float4*>(wl + 32 * m + 16);
             const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-            const u32 bw[4] = {bsrc[m][0].x, bsrc[m][0].y, bsrc[m][1].x, bsrc[m][1].y};
+            const u32 bw[4] = {bsrc[m].x, bsrc[m].y, bsrc[m].z, bsrc[m].w};
             float bf8[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -1415,7 +1433,7 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     // register operands shared by an item's heads (see load_bt / load_c): loaded
     // here for the first item, and for every later item by the last head of the
     // item before it, right after their last use there
-    uint2 btf[kQ / 32][2];   // (one column block of the state; with two, each head loads its own)
+    uint4 btf[kQ / 32];   // (one column block of the state; with two, each head loads its own)
     uint4 cf[2][KN];   // raw bf16 (as a bf16 vector type the compiler merges lanes right at the loads)
     {
         const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
