@@ -104,8 +104,13 @@ typedef struct {
 /* Workspace size in bytes for `prob` (Section 6 intermediates: chunk cumsums,
  * chunk states, the packed row's chunk table).  The size covers calls with and
  * without seq_idx; with batch 1 it depends on prob->nseq, so size it with the
- * nseq the call will pass.  Returns SSD_OK and writes *bytes, or a validation
- * error. */
+ * nseq the call will pass.  It is the size of the kernels the call will run:
+ * at the shapes of the fused kernels (bf16, headdim 64, dstate 64/128/256,
+ * chunk 256) a fraction of the general kernels' (which keep every chunk
+ * state), so a test setting that forces the general path (ssd_set_tuning)
+ * must be made before the size is asked.  A workspace too small for the path
+ * a call takes fails with SSD_ERR_WORKSPACE, never overruns.  Returns SSD_OK
+ * and writes *bytes, or a validation error. */
 int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes);
 
 /* The SSD forward (Section 6 algorithm; definition above).  `D`,

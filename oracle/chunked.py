@@ -11,9 +11,11 @@ valid).  Variable-length rows (Section 8.3) keep every quantity inside its own
 sequence; sequences that start inside a chunk restart from their own initial
 state.
 
-This module exists to expose per-step intermediates for comparison with the
-HIP kernels' workspace; it is pinned against the sequential oracle
-(``oracle.forward``) by the CPU tests.  It shares no code with the HIP path.
+This module writes the decomposition out step by step (returning its
+intermediates: chunk states, entering states) so that the CPU tests can show
+the block form equals the sequential oracle (``oracle.forward``) at every
+chunk length, including ragged last chunks and packed rows -- the identity
+the chunked kernels rely on.  It shares no code with the HIP path.
 """
 from __future__ import annotations
 

@@ -165,12 +165,19 @@ extern "C" int ssd_workspace_bytes(const ssd_problem* prob, size_t* bytes)
     ssd::Shape s;
     const int rc = ssd::validate(prob, /*has_seq_idx=*/false, &s);  // size does not depend on it
     if (rc != SSD_OK) return rc;
-    size_t need = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC).total;
-    if (ssd::fused_supported(s.P, s.N, s.Q, s.bf16)) {
-        size_t f = ssd::fused_layout(s.b, s.T, s.H, s.N, s.G, s.nC, 0).total;
+    // The size of the path the forward will take: the fused kernels' layout
+    // where they apply (a fraction of the general layout, which holds every
+    // chunk state), else the general one.  Forcing the general path through
+    // ssd_set_tuning changes the answer.
+    const size_t general = ssd::workspace_layout(s.b, s.H, s.P, s.N, s.G, s.Q, s.nC).total;
+    size_t need = general;
+    if (ssd::tuning(ssd::kTuneForceGeneral) != 1 && ssd::fused_supported(s.P, s.N, s.Q, s.bf16)) {
+        need = ssd::fused_layout(s.b, s.T, s.H, s.N, s.G, s.nC, 0).total;
         // a packed row of prob->nseq sequences (when seq_idx is passed) needs its chunk table
-        if (fused_packed_ok(prob)) f = std::max(f, ssd::fused_layout(1, s.T, s.H, s.N, s.G, s.nC, prob->nseq).total);
-        if (f > need) need = f;
+        if (fused_packed_ok(prob))
+            need = std::max(need, ssd::fused_layout(1, s.T, s.H, s.N, s.G, s.nC, prob->nseq).total);
+        else if (prob->batch == 1 && prob->nseq >= 1 && prob->nseq <= prob->seqlen)
+            need = std::max(need, general);   // a packed row the fused kernels cannot index
     }
     *bytes = need;
     return SSD_OK;

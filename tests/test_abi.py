@@ -95,6 +95,24 @@ def test_workspace_grows_with_problem(lib):
     assert ssd.ssd_workspace_bytes(prob(seqlen=4097)) > large  # partial chunk counted
 
 
+def test_workspace_is_that_of_the_path_taken(lib, tune):
+    # the fused kernels (bf16, P 64, N 128, chunk 256) keep two ring slots of
+    # states; the general kernels keep every chunk state: forcing the general
+    # path asks for more, and a fused-sized workspace is then refused
+    p = prob(dtype=ssd.SSD_DTYPE_BF16)
+    fused = ssd.ssd_workspace_bytes(p)
+    tune("force_general_path", 1)
+    general = ssd.ssd_workspace_bytes(p)
+    assert fused < general
+    assert fwd(p, ws_bytes=fused) == ssd.SSD_ERR_WORKSPACE
+    # f32 runs on the general kernels either way
+    tune("force_general_path", 0)
+    q = prob(dtype=ssd.SSD_DTYPE_F32)
+    f32 = ssd.ssd_workspace_bytes(q)
+    tune("force_general_path", 1)
+    assert ssd.ssd_workspace_bytes(q) == f32
+
+
 def test_timed_entry_validates_like_forward(lib):
     def timed(p, ws_bytes=1 << 40, seq_idx=0, x=FAKE):
         return ssd.ssd_forward_timed(p, x, FAKE, FAKE, FAKE, FAKE, 0, 0, seq_idx, FAKE, 0, FAKE,
