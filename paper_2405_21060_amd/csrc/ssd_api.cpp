@@ -90,8 +90,6 @@ int64_t tuning(Tuning k) { return g_tuning[k].load(std::memory_order_relaxed); }
 // then a divisor up to 6 that fills whole rounds where that is clearly cheaper
 // (below).  The heads_per_item tuning overrides it (ignored unless it divides
 // the heads per group).
-// chunks in flight from which a chunk's state flag is set early (see forward_impl)
-constexpr int64_t kEarlyFlagChunks = 8;
 
 int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int compute_units)
 {
@@ -108,15 +106,16 @@ int64_t heads_per_workgroup(int64_t heads_per_group, int64_t items_per_head, int
             }
         if (found) break;
     }
-    // A divisor up to 6 whose items fill whole rounds of the compute units
-    // replaces that choice when it is cheaper by rounds x (heads per item + 1/2
-    // of a head for the item's set-up): at the 130M layer shape, 6 heads give
-    // 256 items (one round) where 2 give 768 (three); at the 2.7B layer shape
-    // 5 heads give 1,024 items (four rounds, 0.197 ms) where 4 give 1,280
-    // (five, 0.200 ms).
+    // A divisor up to 6 replaces that choice when it is cheaper by rounds x
+    // (heads per item + 1/2 of a head for the item's set-up) + 1/4 of a head
+    // per head of an item (the longer an item, the longer a chunk's wait for
+    // the chunk before it carries into its later heads).  At the 2.7B layer
+    // shape 5 heads give 1,024 items (four rounds: 0.189 ms; 4 heads 0.188,
+    // 10 heads 0.193, 20 heads 0.209); at the 130M layer shape 3 heads give 512
+    // items (two rounds: 0.072 ms; 6 heads in one round 0.074-0.077).
     const auto cost = [&](int64_t h) {
         const int64_t items = items_per_head * (heads_per_group / h);
-        return static_cast<double>((items + compute_units - 1) / compute_units) * (h + 0.5);
+        return static_cast<double>((items + compute_units - 1) / compute_units) * (h + 0.5) + 0.25 * h;
     };
     double best = cost(hg);
     const double base = best;
@@ -266,11 +265,19 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
             return SSD_ERR_LAUNCH;
         f.HG = ssd::heads_per_workgroup(s.H / s.G, fw.nC * s.b * s.G, cus);
-        // Chunks of one chain the chip holds at once: with many of them the
-        // chain's latency bounds the launch, and each chunk publishes its state
-        // before its left factor.  The early_state_flag tuning overrides it.
-        const int64_t per_chunk = s.b * (s.H / f.HG);
-        f.early_flag = cus >= ssd::kEarlyFlagChunks * per_chunk ? 1 : 0;
+        // The chain of state passing takes about nC chunk steps one after the
+        // other (a step: a chunk's wait, state load, combine and publish), the
+        // work about rounds x heads per item head-times.  Where the chain is
+        // the longer (few heads and batch rows, many chunks: nC >= 2 x rounds
+        // x heads per item), each chunk publishes its state before its left
+        // factor, which shortens every chain step by the left factor and the
+        // output stage (the 2.7B layer split 8 ways by heads: 0.056 ms against
+        // 0.081); elsewhere it sets the flag after the output stage, which
+        // measures up to 2 % faster there.  The early_state_flag tuning
+        // overrides it.
+        const int64_t items = fw.nC * s.b * (s.H / f.HG);
+        const int64_t rounds = (items + cus - 1) / cus;
+        f.early_flag = fw.nC >= 2 * rounds * f.HG ? 1 : 0;
         if (const int64_t ef = ssd::tuning(ssd::kTuneEarlyFlag); ef == 1 || ef == 2) f.early_flag = ef == 2;
         f.status = status;
         f.reset_status = reset_status ? 1 : 0;
