@@ -861,13 +861,13 @@ __device__ __forceinline__ void load_bt_block(const FusedParams& p, const Item& 
     for (int m = 0; m < kQ / 32; ++m) btf[m] = *reinterpret_cast<const uint4*>(btr + 32 * m);
 }
 
-// The item-level B^T fragments (one column block of the state: N <= 128; with
-// two blocks every head loads its own per block).
+// The item-level B^T fragments: the first column block of the state (the
+// only one for N <= 128; with two, every head loads the second block's own).
 template <int N>
 __device__ __forceinline__ void load_bt(const FusedParams& p, const Item& it, int ntw, int r, int lg,
                                         uint4 (&btf)[kQ / 32])
 {
-    if constexpr (N <= kNH) load_bt_block<N, N>(p, it, ntw, r, lg, 0, btf);
+    load_bt_block<N, (N < kNH ? N : kNH)>(p, it, ntw, r, lg, 0, btf);
 }
 
 // C fragments of the two strips for the left factor, columns [hf NH, hf NH +
@@ -968,11 +968,10 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         L_next = nit.L;
     }
 
-    // Two column blocks of the state: this head's B^T fragments of the first
-    // block now (they arrive during the diagonal block), of the second when the
-    // first block's right factor starts.
-    uint4 bth[HALVES > 1 ? 2 : 1][kQ / 32];
-    if constexpr (HALVES > 1) load_bt_block<N, NH>(p, it, ntw, r, lg, 0, bth[0]);
+    // Two column blocks of the state: the first block's B^T fragments are the
+    // item's (btf, shared by its heads); the second block's are this head's own,
+    // requested when the first block's right factor starts.
+    uint4 bth[kQ / 32];
 
     // ---- step 1: chunk-local inclusive cumsum of a = dt A (log2 units), one token
     // per thread (wavefront scans, then the wavefront totals through LDS), and the
@@ -1070,7 +1069,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // Opaque to the optimiser, so that it does not hoist the unpacking of B^T out
     // of the head loop (64 more registers, and a wait for the loads at the start
     // of every item).
-    if constexpr (HALVES == 1) {
+    {
 #pragma unroll
         for (int m = 0; m < kQ / 32; ++m) {
             uint4_t v = __builtin_bit_cast(uint4_t, btf[m]);
@@ -1081,8 +1080,8 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 #pragma unroll
     for (int hf = 0; hf < HALVES; ++hf) {
         if (HALVES > 1) __builtin_amdgcn_sched_barrier(0);
-        if (HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth[hf + 1]);
-        const uint4 (&bsrc)[kQ / 32] = HALVES > 1 ? bth[hf] : btf;
+        if (HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth);
+        const uint4 (&bsrc)[kQ / 32] = hf > 0 ? bth : btf;
         const char* xsb = reinterpret_cast<const char*>(xs);
         const float* wl = w + 4 * lg;
 #pragma unroll
