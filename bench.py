@@ -63,8 +63,9 @@ def kernel_sources_digest(sources=FWD_SOURCES):
     return h.hexdigest()[:16]
 
 
-def dominant_kernel_name(p):
-    fused = (p.dtype == "bf16" and p.headdim == 64 and p.chunk_size == 256 and p.dstate in (64, 128, 256))
+def dominant_kernel_name(p, general=False):
+    fused = (not general and p.dtype == "bf16" and p.headdim == 64 and p.chunk_size == 256
+             and p.dstate in (64, 128, 256))
     return ("k_fused_main<%d>" % p.dstate) if fused else "k_chunk_output"
 
 
@@ -605,6 +606,9 @@ def main():
                     help="time the block's gradients (ssd_backward_block) instead")
     ap.add_argument("--cp-share", action="store_true",
                     help="time one rank's share of an 8-way sequence split instead")
+    ap.add_argument("--general-path", action="store_true",
+                    help="time the general (per-step) kernels at the workload's shape instead of the fused ones "
+                         "(the force_general_path setting of ssd_set_tuning)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 1 GiB device-to-device copy instead (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -661,6 +665,11 @@ def main():
     from paper_2405_21060_amd import ssd
     from paper_2405_21060_amd.inputs import WORKLOADS, make_inputs
     from paper_2405_21060_amd.device import to_device
+
+    if args.general_path:   # before any workspace is sized: the general kernels need the larger layout
+        rc = ssd.ssd_set_tuning("force_general_path", 1)
+        if rc != ssd.SSD_OK:
+            raise ssd.SsdError(rc, "ssd_set_tuning")
 
     if args.decode:
         return decode_bench(args, torch, ssd)
@@ -763,8 +772,9 @@ def main():
         roof = {"bound": "mfma", "achieved": f_full / ksec / 1e12, "peak": peak_flops / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(args.workload)
-    roof["kernel"] = dominant_kernel_name(p) + (" (whole forward: no kernel events)" if kms is None else "")
+    roof["traffic"] = None if args.general_path else measured_traffic(args.workload)
+    roof["kernel"] = dominant_kernel_name(p, args.general_path) + (
+        " (whole forward: no kernel events)" if kms is None else "")
     roof["kernel_ms"] = kms
     roof["algorithmic_bytes"] = byts
     line = {
@@ -784,7 +794,8 @@ def main():
         "config": {"workload": args.workload, "batch": p.batch, "seqlen": p.seqlen,
                    "nheads": p.nheads, "headdim": p.headdim, "dstate": p.dstate,
                    "ngroups": p.ngroups, "chunk_size": p.chunk_size,
-                   "nseq": inp.nseq if p.varlen else None},
+                   "nseq": inp.nseq if p.varlen else None,
+                   "path": "general" if args.general_path else "fused"},
         "tflops_full_block": f_full / sec / 1e12,
         "tflops_causal": f_causal / sec / 1e12,
         "pct_mfma_peak_full_block": 100.0 * f_full / sec / peak_flops,
