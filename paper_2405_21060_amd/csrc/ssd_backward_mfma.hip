@@ -65,6 +65,24 @@ __device__ __forceinline__ float load_dt(const void* dt, int64_t i)
         return bf(static_cast<const u16*>(dt)[i]);
 }
 
+// dt as raw bits (float32, or bf16 in the low half), widened where it is used:
+// a load whose value is converted at once makes the wavefront wait for every
+// memory operation issued before it (the prefetches and the state stores).
+template <bool H32>
+__device__ __forceinline__ uint32_t load_dt_raw(const void* dt, int64_t i)
+{
+    if constexpr (H32)
+        return __float_as_uint(static_cast<const float*>(dt)[i]);
+    else
+        return static_cast<const u16*>(dt)[i];
+}
+
+template <bool H32>
+__device__ __forceinline__ float dt_of_raw(uint32_t v)
+{
+    return H32 ? __uint_as_float(v) : __uint_as_float(v << 16);
+}
+
 __device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
@@ -210,7 +228,8 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     const int64_t bh = blockIdx.x;
     const int64_t b = bh / p.H, h = bh - b * p.H, g = h / (p.H / p.G);
     const int dir = static_cast<int>(blockIdx.y);
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // wavefront index, provably uniform (per-wavefront choices stay scalar)
+    const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, q = lane >> 4;
     const u16* src = static_cast<const u16*>(dir == 0 ? p.x : p.dy);
     const float* dyf = static_cast<const float*>(p.dy);   // H32, dir 1
@@ -235,7 +254,7 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     constexpr int kXK = kQ2 * kP2 / 8 / kPassT;   // 2
     constexpr int kYK = kQ2 * N / 8 / kPassT;     // N / 32
     struct Stage {
-        float dt;
+        uint32_t dt;   // raw bits (see load_dt_raw)
         uint4 x[kXK], y[kYK];
         float4 xf[H32 ? 2 * kXK : 1];   // H32, dir 1: dy in float32
     };
@@ -258,7 +277,7 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
             L = chunk_len2(p.T, c);
             t0 = b * p.T + c * kQ2;
         }
-        st.dt = lane < L ? load_dt<H32>(p.dt, (t0 + lane) * p.H + h) : 0.f;
+        st.dt = lane < L ? load_dt_raw<H32>(p.dt, (t0 + lane) * p.H + h) : 0u;
 #pragma unroll
         for (int kk = 0; kk < kXK; ++kk) {
             const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
@@ -283,9 +302,10 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         const int64_t c = chunk_at(k);
         const int L = PACKED ? p.vtab[c].y : chunk_len2(p.T, c);
         // token weights: cumsum with lane = token, then each piece's token's weight
-        const float cs = wave_scan(st.dt * A2);
+        const float dtv = dt_of_raw<H32>(st.dt);
+        const float cs = wave_scan(dtv * A2);
         const float csend = lane_value(cs, L - 1);
-        const float wt = dir == 0 ? exp2f(csend - cs) * st.dt : exp2f(cs);
+        const float wt = dir == 0 ? exp2f(csend - cs) * dtv : exp2f(cs);
         __syncthreads();   // the previous chunk's product is done with XS, YS
 #pragma unroll
         for (int kk = 0; kk < kXK; ++kk) {
@@ -390,7 +410,10 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 
     const int64_t c = blockIdx.x, b = blockIdx.y;
     const HeadRange hr = head_range(p);
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // wavefront index, provably uniform: the tile tables below are read with
+    // scalar loads, never vector loads whose wait would also wait for the
+    // next head's inputs in flight
+    const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, q = lane >> 4;
     int L0 = 0;
     int64_t t00 = 0;
@@ -465,11 +488,11 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
     // one head's inputs, fetched a head ahead: dt (wavefront 0, lane = token)
     // and one 8-wide piece of x and of dy per thread (token s_me = lane)
     const int s_me = lane, p0_me = 8 * w;   // token = lane, 8 p values per wavefront
-    float pdt = 0.f;
+    uint32_t pdt = 0;   // raw bits (see load_dt_raw)
     uint4 px = make_uint4(0, 0, 0, 0), pd = px;
     float4 pf0 = make_float4(0.f, 0.f, 0.f, 0.f), pf1 = pf0;   // H32: dy in float32
     const auto fetch = [&](int64_t h) {
-        if (w == 0) pdt = lane < L ? load_dt<H32>(p.dt, (t0 + lane) * p.H + h) : 0.f;
+        if (w == 0) pdt = lane < L ? load_dt_raw<H32>(p.dt, (t0 + lane) * p.H + h) : 0u;
         px = pd = make_uint4(0, 0, 0, 0);
         pf0 = pf1 = make_float4(0.f, 0.f, 0.f, 0.f);
         if (s_me < L) {
@@ -534,10 +557,11 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
         if (w == 0) {
             // cumsum of dt*A (log2 units) and the per-token factors
             const float A2 = Ah * kLog2e;
-            const float cs = wave_scan(pdt * A2);
+            const float dtv = dt_of_raw<H32>(pdt);
+            const float cs = wave_scan(dtv * A2);
             const float csend = lane_value(cs, L - 1);
             scs[lane] = cs;
-            sdt[lane] = pdt;
+            sdt[lane] = dtv;
             seend[lane] = lane < L ? exp2f(csend - cs) : 0.f;
             secs[lane] = lane < L ? exp2f(cs) : 0.f;
         }
