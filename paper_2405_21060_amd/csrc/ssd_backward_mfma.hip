@@ -265,8 +265,12 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     }
     const auto chunk_at = [&](int64_t k) { return first + (dir == 0 ? k : nch - 1 - k); };
     const auto fetch = [&](Stage& st, int64_t k) {
-        if (k >= nch) return;
-        const int64_t c = chunk_at(k);
+        // Branch-free: past the last chunk the last one is fetched again (never
+        // used), and rows past a partial chunk read as zeros through the buffer
+        // bounds, so that the compiler can count exactly which loads are still
+        // in flight when a stage is used (with branches around them it waits
+        // for all of them: the next stage's and the state stores included).
+        const int64_t c = chunk_at(k < nch ? k : nch - 1);
         int L;
         int64_t t0;
         if constexpr (PACKED) {
@@ -277,25 +281,43 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
             L = chunk_len2(p.T, c);
             t0 = b * p.T + c * kQ2;
         }
-        st.dt = lane < L ? load_dt_raw<H32>(p.dt, (t0 + lane) * p.H + h) : 0u;
+        constexpr int kDtBytes = H32 ? 4 : 2;
+        const __amdgpu_buffer_rsrc_t rdt = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(static_cast<const char*>(p.dt)) + (t0 * p.H + h) * kDtBytes, 0,
+            static_cast<int>(((L - 1) * p.H + 1) * kDtBytes), 0x00020000);
+        const int dtoff = lane * static_cast<int>(p.H) * kDtBytes;
+        if constexpr (H32)
+            st.dt = __builtin_amdgcn_raw_buffer_load_b32(rdt, dtoff, 0, 0);
+        else
+            st.dt = __builtin_amdgcn_raw_buffer_load_b16(rdt, dtoff, 0, 0);
+        const int xrow = static_cast<int>(p.H) * kP2;   // elements between tokens of x (dy)
 #pragma unroll
         for (int kk = 0; kk < kXK; ++kk) {
             const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
             if (src32) {
-                const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-                const float* a = dyf + ((t0 + s) * p.H + h) * kP2 + f;
-                st.xf[2 * kk] = s < L ? *reinterpret_cast<const float4*>(a) : z;
-                st.xf[2 * kk + 1] = s < L ? *reinterpret_cast<const float4*>(a + 4) : z;
+                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float*>(dyf) + (t0 * p.H + h) * kP2, 0,
+                    ((L - 1) * xrow + kP2) * static_cast<int>(sizeof(float)), 0x00020000);
+                const int off = (s * xrow + f) * static_cast<int>(sizeof(float));
+                st.xf[2 * kk] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+                st.xf[2 * kk + 1] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, 0));
             } else {
-                st.x[kk] = s < L ? *reinterpret_cast<const uint4*>(src + ((t0 + s) * p.H + h) * kP2 + f)
-                                 : make_uint4(0, 0, 0, 0);
+                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<u16*>(src) + (t0 * p.H + h) * kP2, 0,
+                    ((L - 1) * xrow + kP2) * static_cast<int>(sizeof(u16)), 0x00020000);
+                st.x[kk] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                         rs, (s * xrow + f) * static_cast<int>(sizeof(u16)), 0, 0));
             }
         }
+        const int yrow = static_cast<int>(p.G) * N;   // elements between tokens of B (C)
+        const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<u16*>(bc) + (t0 * p.G + g) * N, 0, ((L - 1) * yrow + N) * static_cast<int>(sizeof(u16)),
+            0x00020000);
 #pragma unroll
         for (int kk = 0; kk < kYK; ++kk) {
             const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
-            st.y[kk] = s < L ? *reinterpret_cast<const uint4*>(bc + ((t0 + s) * p.G + g) * N + f)
-                             : make_uint4(0, 0, 0, 0);
+            st.y[kk] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                     ry, (s * yrow + f) * static_cast<int>(sizeof(u16)), 0, 0));
         }
     };
     const auto step = [&](Stage& st, int64_t k) {
@@ -354,10 +376,13 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
     Stage s0st, s1st;
     fetch(s0st, 0);
     fetch(s1st, 1);
-    for (int64_t k = 0; k < nch; k += 2) {
+    // (pairs of steps, then an odd last one: no branch inside the loop body)
+    int64_t k = 0;
+    for (; k + 1 < nch; k += 2) {
         step(s0st, k);
-        if (k + 1 < nch) step(s1st, k + 1);
+        step(s1st, k + 1);
     }
+    if (k < nch) step(s0st, k);
     if (dir == 1 && p.dinit) {
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
