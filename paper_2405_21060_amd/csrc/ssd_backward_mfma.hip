@@ -25,6 +25,8 @@
 // + 7) as one 16-byte load, and the result tile D[4 q + v][r] lands in its
 // four accumulator registers.  Shared arrays are padded by 8 elements per
 // row so that the 16 rows of a fragment read fall in distinct banks.
+#include <type_traits>
+
 #include "ssd_bwd.h"
 #include "ssd_device.h"
 
@@ -220,7 +222,7 @@ __device__ __forceinline__ uint4 tr_frag(const u16* buf, int m, int f0, int lane
 // PACKED: a packed row; workgroup (sequence, head) walks that sequence's
 // chunks of the chunk table.
 template <int N, bool PACKED, bool H32>
-__global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
+__global__ __launch_bounds__(kPassT, H32 ? 2 : 1) void k_bwd2_pass(BwdParams p)
 {
     __shared__ __attribute__((aligned(16))) u16 XS[kQ2 * kP2];   // weighted x (or dy), token-major
     __shared__ __attribute__((aligned(16))) u16 YS[kQ2 * N];     // B (or C), token-major
@@ -248,141 +250,151 @@ __global__ __launch_bounds__(kPassT) void k_bwd2_pass(BwdParams p)
         for (int v = 0; v < 4; ++v)
             S[nt][v] = s0 ? s0[(bh * kP2 + 16 * w + 4 * q + v) * N + 16 * nt + r] : 0.f;
 
-    // One chunk's inputs: dt (lane = token), and 16-byte pieces of x (or dy)
-    // and of B (or C): piece i = tid + 256 k is row i / (F/8), group i % (F/8),
-    // so consecutive lanes read consecutive bytes of a row.
-    constexpr int kXK = kQ2 * kP2 / 8 / kPassT;   // 2
-    constexpr int kYK = kQ2 * N / 8 / kPassT;     // N / 32
-    struct Stage {
-        uint32_t dt;   // raw bits (see load_dt_raw)
-        uint4 x[kXK], y[kYK];
-        float4 xf[H32 ? 2 * kXK : 1];   // H32, dir 1: dy in float32
-    };
-    int64_t first = 0, nch = p.nC;   // this row's (or sequence's) chunks
-    if constexpr (PACKED) {
-        first = p.seq_first[b];
-        nch = p.seq_first[b + 1] - first;
-    }
-    const auto chunk_at = [&](int64_t k) { return first + (dir == 0 ? k : nch - 1 - k); };
-    const auto fetch = [&](Stage& st, int64_t k) {
-        // Branch-free: past the last chunk the last one is fetched again (never
-        // used), and rows past a partial chunk read as zeros through the buffer
-        // bounds, so that the compiler can count exactly which loads are still
-        // in flight when a stage is used (with branches around them it waits
-        // for all of them: the next stage's and the state stores included).
-        const int64_t c = chunk_at(k < nch ? k : nch - 1);
-        int L;
-        int64_t t0;
+    // The passes' loop, once per kind of source (the float32 dy of the block
+    // gradients' direction 1 is known per workgroup): no branch on it inside
+    // the loop, whose waits then count the loads in flight.
+    const auto run = [&](auto s32tag) {
+        constexpr bool S32 = decltype(s32tag)::value;
+        // One chunk's inputs: dt (lane = token), and 16-byte pieces of x (or dy)
+        // and of B (or C): piece i = tid + 256 k is row i / (F/8), group i % (F/8),
+        // so consecutive lanes read consecutive bytes of a row.
+        constexpr int kXK = kQ2 * kP2 / 8 / kPassT;   // 2
+        constexpr int kYK = kQ2 * N / 8 / kPassT;     // N / 32
+        struct Stage {
+            uint32_t dt;   // raw bits (see load_dt_raw)
+            uint4 x[kXK], y[kYK];
+            float4 xf[H32 ? 2 * kXK : 1];   // H32, dir 1: dy in float32
+        };
+        int64_t first = 0, nch = p.nC;   // this row's (or sequence's) chunks
         if constexpr (PACKED) {
-            const int4 e = p.vtab[c];
-            L = e.y;
-            t0 = e.x;
-        } else {
-            L = chunk_len2(p.T, c);
-            t0 = b * p.T + c * kQ2;
+            first = p.seq_first[b];
+            nch = p.seq_first[b + 1] - first;
         }
-        constexpr int kDtBytes = H32 ? 4 : 2;
-        const __amdgpu_buffer_rsrc_t rdt = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<char*>(static_cast<const char*>(p.dt)) + (t0 * p.H + h) * kDtBytes, 0,
-            static_cast<int>(((L - 1) * p.H + 1) * kDtBytes), 0x00020000);
-        const int dtoff = lane * static_cast<int>(p.H) * kDtBytes;
-        if constexpr (H32)
-            st.dt = __builtin_amdgcn_raw_buffer_load_b32(rdt, dtoff, 0, 0);
-        else
-            st.dt = __builtin_amdgcn_raw_buffer_load_b16(rdt, dtoff, 0, 0);
-        const int xrow = static_cast<int>(p.H) * kP2;   // elements between tokens of x (dy)
-#pragma unroll
-        for (int kk = 0; kk < kXK; ++kk) {
-            const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
-            if (src32) {
-                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                    const_cast<float*>(dyf) + (t0 * p.H + h) * kP2, 0,
-                    ((L - 1) * xrow + kP2) * static_cast<int>(sizeof(float)), 0x00020000);
-                const int off = (s * xrow + f) * static_cast<int>(sizeof(float));
-                st.xf[2 * kk] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-                st.xf[2 * kk + 1] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, 0));
+        const auto chunk_at = [&](int64_t k) { return first + (dir == 0 ? k : nch - 1 - k); };
+        const auto fetch = [&](Stage& st, int64_t k) {
+            // Branch-free: past the last chunk the last one is fetched again (never
+            // used), and rows past a partial chunk read as zeros through the buffer
+            // bounds, so that the compiler can count exactly which loads are still
+            // in flight when a stage is used (with branches around them it waits
+            // for all of them: the next stage's and the state stores included).
+            const int64_t c = chunk_at(k < nch ? k : nch - 1);
+            int L;
+            int64_t t0;
+            if constexpr (PACKED) {
+                const int4 e = p.vtab[c];
+                L = e.y;
+                t0 = e.x;
             } else {
-                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                    const_cast<u16*>(src) + (t0 * p.H + h) * kP2, 0,
-                    ((L - 1) * xrow + kP2) * static_cast<int>(sizeof(u16)), 0x00020000);
-                st.x[kk] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                         rs, (s * xrow + f) * static_cast<int>(sizeof(u16)), 0, 0));
+                L = chunk_len2(p.T, c);
+                t0 = b * p.T + c * kQ2;
             }
-        }
-        const int yrow = static_cast<int>(p.G) * N;   // elements between tokens of B (C)
-        const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<u16*>(bc) + (t0 * p.G + g) * N, 0, ((L - 1) * yrow + N) * static_cast<int>(sizeof(u16)),
-            0x00020000);
-#pragma unroll
-        for (int kk = 0; kk < kYK; ++kk) {
-            const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
-            st.y[kk] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                     ry, (s * yrow + f) * static_cast<int>(sizeof(u16)), 0, 0));
-        }
-    };
-    const auto step = [&](Stage& st, int64_t k) {
-        const int64_t c = chunk_at(k);
-        const int L = PACKED ? p.vtab[c].y : chunk_len2(p.T, c);
-        // token weights: cumsum with lane = token, then each piece's token's weight
-        const float dtv = dt_of_raw<H32>(st.dt);
-        const float cs = wave_scan(dtv * A2);
-        const float csend = lane_value(cs, L - 1);
-        const float wt = dir == 0 ? exp2f(csend - cs) * dtv : exp2f(cs);
-        __syncthreads();   // the previous chunk's product is done with XS, YS
-#pragma unroll
-        for (int kk = 0; kk < kXK; ++kk) {
-            const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
-            const float ws = __shfl(wt, s, 64);
-            uint32_t o[4];
-            if (src32) {
-                const float4 a = st.xf[2 * kk], c2 = st.xf[2 * kk + 1];
-                o[0] = pack2(ws * a.x, ws * a.y);
-                o[1] = pack2(ws * a.z, ws * a.w);
-                o[2] = pack2(ws * c2.x, ws * c2.y);
-                o[3] = pack2(ws * c2.z, ws * c2.w);
-            } else {
-                const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) o[e] = pack2(ws * lo_f(ex[e]), ws * hi_f(ex[e]));
+            constexpr int kDtBytes = H32 ? 4 : 2;
+            const __amdgpu_buffer_rsrc_t rdt = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<char*>(static_cast<const char*>(p.dt)) + (t0 * p.H + h) * kDtBytes, 0,
+                static_cast<int>(((L - 1) * p.H + 1) * kDtBytes), 0x00020000);
+            const int dtoff = lane * static_cast<int>(p.H) * kDtBytes;
+            if constexpr (H32)
+                st.dt = __builtin_amdgcn_raw_buffer_load_b32(rdt, dtoff, 0, 0);
+            else
+                st.dt = __builtin_amdgcn_raw_buffer_load_b16(rdt, dtoff, 0, 0);
+            const int xrow = static_cast<int>(p.H) * kP2;   // elements between tokens of x (dy)
+    #pragma unroll
+            for (int kk = 0; kk < kXK; ++kk) {
+                const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
+                if constexpr (S32) {
+                    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                        const_cast<float*>(dyf) + (t0 * p.H + h) * kP2, 0,
+                        ((L - 1) * xrow + kP2) * static_cast<int>(sizeof(float)), 0x00020000);
+                    const int off = (s * xrow + f) * static_cast<int>(sizeof(float));
+                    st.xf[2 * kk] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+                    st.xf[2 * kk + 1] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, 0));
+                } else {
+                    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                        const_cast<u16*>(src) + (t0 * p.H + h) * kP2, 0,
+                        ((L - 1) * xrow + kP2) * static_cast<int>(sizeof(u16)), 0x00020000);
+                    st.x[kk] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                             rs, (s * xrow + f) * static_cast<int>(sizeof(u16)), 0, 0));
+                }
             }
-            *reinterpret_cast<uint4*>(XS + tok_off<kP2>(s, f)) = make_uint4(o[0], o[1], o[2], o[3]);
-        }
-#pragma unroll
-        for (int kk = 0; kk < kYK; ++kk) {
-            const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
-            *reinterpret_cast<uint4*>(YS + tok_off<N>(s, f)) = st.y[kk];
-        }
-        fetch(st, k + 2);
+            const int yrow = static_cast<int>(p.G) * N;   // elements between tokens of B (C)
+            const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<u16*>(bc) + (t0 * p.G + g) * N, 0, ((L - 1) * yrow + N) * static_cast<int>(sizeof(u16)),
+                0x00020000);
+    #pragma unroll
+            for (int kk = 0; kk < kYK; ++kk) {
+                const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
+                st.y[kk] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                         ry, (s * yrow + f) * static_cast<int>(sizeof(u16)), 0, 0));
+            }
+        };
+        const auto step = [&](Stage& st, int64_t k) {
+            const int64_t c = chunk_at(k);
+            const int L = PACKED ? p.vtab[c].y : chunk_len2(p.T, c);
+            // token weights: cumsum with lane = token, then each piece's token's weight
+            const float dtv = dt_of_raw<H32>(st.dt);
+            const float cs = wave_scan(dtv * A2);
+            const float csend = lane_value(cs, L - 1);
+            const float wt = dir == 0 ? exp2f(csend - cs) * dtv : exp2f(cs);
+            __syncthreads();   // the previous chunk's product is done with XS, YS
+    #pragma unroll
+            for (int kk = 0; kk < kXK; ++kk) {
+                const int i = tid + kPassT * kk, s = i >> 3, f = 8 * (i & 7);
+                const float ws = __shfl(wt, s, 64);
+                uint32_t o[4];
+                if constexpr (S32) {
+                    const float4 a = st.xf[2 * kk], c2 = st.xf[2 * kk + 1];
+                    o[0] = pack2(ws * a.x, ws * a.y);
+                    o[1] = pack2(ws * a.z, ws * a.w);
+                    o[2] = pack2(ws * c2.x, ws * c2.y);
+                    o[3] = pack2(ws * c2.z, ws * c2.w);
+                } else {
+                    const uint32_t ex[4] = {st.x[kk].x, st.x[kk].y, st.x[kk].z, st.x[kk].w};
+    #pragma unroll
+                    for (int e = 0; e < 4; ++e) o[e] = pack2(ws * lo_f(ex[e]), ws * hi_f(ex[e]));
+                }
+                *reinterpret_cast<uint4*>(XS + tok_off<kP2>(s, f)) = make_uint4(o[0], o[1], o[2], o[3]);
+            }
+    #pragma unroll
+            for (int kk = 0; kk < kYK; ++kk) {
+                const int i = tid + kPassT * kk, s = i / (N / 8), f = 8 * (i % (N / 8));
+                *reinterpret_cast<uint4*>(YS + tok_off<N>(s, f)) = st.y[kk];
+            }
+            fetch(st, k + 2);
 
-        // S before this chunk's term -> out(c), bf16 (n x p)
-        u16* o = out + ((PACKED ? c : b * p.nC + c) * p.H + h) * kP2 * N;
-#pragma unroll
-        for (int nt = 0; nt < kNT; ++nt)
-            *reinterpret_cast<uint2*>(o + (16 * nt + r) * kP2 + 16 * w + 4 * q) =
-                make_uint2(pack2(S[nt][0], S[nt][1]), pack2(S[nt][2], S[nt][3]));
+            // S before this chunk's term -> out(c), bf16 (n x p)
+            u16* o = out + ((PACKED ? c : b * p.nC + c) * p.H + h) * kP2 * N;
+    #pragma unroll
+            for (int nt = 0; nt < kNT; ++nt)
+                *reinterpret_cast<uint2*>(o + (16 * nt + r) * kP2 + 16 * w + 4 * q) =
+                    make_uint2(pack2(S[nt][0], S[nt][1]), pack2(S[nt][2], S[nt][3]));
 
-        __syncthreads();   // this chunk's operands in place
-        const float a = exp2f(csend);
-        const uint4 xf0 = tr_frag<kP2>(XS, 0, 16 * w, lane), xf1 = tr_frag<kP2>(XS, 1, 16 * w, lane);
-#pragma unroll
-        for (int nt = 0; nt < kNT; ++nt) {
-            f32x4_t t = zero4();
-            t = mma(xf0, tr_frag<N>(YS, 0, 16 * nt, lane), t);
-            t = mma(xf1, tr_frag<N>(YS, 1, 16 * nt, lane), t);
-#pragma unroll
-            for (int v = 0; v < 4; ++v) S[nt][v] = fmaf(a, S[nt][v], t[v]);
+            __syncthreads();   // this chunk's operands in place
+            const float a = exp2f(csend);
+            const uint4 xf0 = tr_frag<kP2>(XS, 0, 16 * w, lane), xf1 = tr_frag<kP2>(XS, 1, 16 * w, lane);
+    #pragma unroll
+            for (int nt = 0; nt < kNT; ++nt) {
+                f32x4_t t = zero4();
+                t = mma(xf0, tr_frag<N>(YS, 0, 16 * nt, lane), t);
+                t = mma(xf1, tr_frag<N>(YS, 1, 16 * nt, lane), t);
+    #pragma unroll
+                for (int v = 0; v < 4; ++v) S[nt][v] = fmaf(a, S[nt][v], t[v]);
+            }
+        };
+        Stage s0st, s1st;
+        fetch(s0st, 0);
+        fetch(s1st, 1);
+        // (pairs of steps, then an odd last one: no branch inside the loop body)
+        int64_t k = 0;
+        for (; k + 1 < nch; k += 2) {
+            step(s0st, k);
+            step(s1st, k + 1);
         }
+        if (k < nch) step(s0st, k);
     };
-    Stage s0st, s1st;
-    fetch(s0st, 0);
-    fetch(s1st, 1);
-    // (pairs of steps, then an odd last one: no branch inside the loop body)
-    int64_t k = 0;
-    for (; k + 1 < nch; k += 2) {
-        step(s0st, k);
-        step(s1st, k + 1);
-    }
-    if (k < nch) step(s0st, k);
+    if (src32)
+        run(std::true_type{});
+    else
+        run(std::false_type{});
     if (dir == 1 && p.dinit) {
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt)
