@@ -200,10 +200,14 @@ class tuning:
         self.settings = settings
 
     def __enter__(self):
+        done = []
         for k, v in self.settings.items():
             rc = ssd_set_tuning(k, v)
             if rc != SSD_OK:
+                for d in done:   # nothing stays set when one setting is refused
+                    ssd_set_tuning(d, 0)
                 raise SsdError(rc, "ssd_set_tuning(%s)" % k)
+            done.append(k)
         return self
 
     def __exit__(self, *exc):

@@ -313,6 +313,15 @@ def test_tuning_hook_validates_names_and_values(lib):
         assert ssd.ssd_set_tuning(name, 0) == ssd.SSD_OK, name
 
 
+def test_tuning_context_leaves_nothing_set_on_a_refused_setting(lib):
+    p = prob(dtype=ssd.SSD_DTYPE_BF16)
+    fused = ssd.ssd_workspace_bytes(p)
+    with pytest.raises(ssd.SsdError):
+        with ssd.tuning(force_general_path=1, no_such_setting=1):
+            pass
+    assert ssd.ssd_workspace_bytes(p) == fused   # force_general_path was put back
+
+
 def test_workspace_status_null(lib):
     assert ssd.ssd_workspace_status(0, 0) == ssd.SSD_ERR_NULL_ARG
     assert "state" in ssd.ssd_error_string(ssd.SSD_ERR_STATE_TIMEOUT)
