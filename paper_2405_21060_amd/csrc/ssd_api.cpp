@@ -279,6 +279,15 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         const int64_t rounds = (items + cus - 1) / cus;
         f.early_flag = fw.nC >= 2 * rounds * f.HG ? 1 : 0;
         if (const int64_t ef = ssd::tuning(ssd::kTuneEarlyFlag); ef == 1 || ef == 2) f.early_flag = ef == 2;
+        // The right factor in the diagonal block's pass (x read from LDS once for
+        // both) shortens a head's matrix-product phase but holds more registers
+        // through it; measured faster with long items and the late flag (2.7B
+        // layer 0.1864 ms against 0.1908, the state-size sweep at N = 64 0.549
+        // against 0.597) and slower with items of 1-3 heads (130M layer, the
+        // 8-way head and sequence splits: 2-4 %) and with the early flag.
+        f.fuse_rf = !f.early_flag && f.HG >= 4 && s.N <= 128 && !y32 ? 1 : 0;
+        if (const int64_t fr = ssd::tuning(ssd::kTuneFusedRightFactor); fr == 1 || fr == 2)
+            f.fuse_rf = fr == 2 && !f.early_flag && s.N <= 128 && !y32;
         f.status = status;
         f.reset_status = reset_status ? 1 : 0;
         if (const int64_t sl = ssd::tuning(ssd::kTuneStateWaitLimit); sl >= 1) f.spin_limit = sl;
@@ -1240,6 +1249,7 @@ extern "C" int ssd_set_tuning(const char* name, int64_t value)
         {"bwd_heads_per_slice", ssd::kTuneBwdHeadsPerSlice, 0, 1 << 16},
         {"varlen_per_sequence", ssd::kTuneVarlenPerSequence, 0, 1},
         {"state_wait_limit", ssd::kTuneStateWaitLimit, 0, INT64_MAX},
+        {"fused_right_factor", ssd::kTuneFusedRightFactor, 0, 2},
     };
     for (const Entry& e : table)
         if (std::strcmp(name, e.name) == 0) {

@@ -612,6 +612,27 @@ __device__ __forceinline__ void strip_step(const uint4* af, const char* gbase, i
     for (int pt = 0; pt < 4; ++pt) yv[pt] = mfma(as_bf16x8(af[pt]), bop, yv[pt]);
 }
 
+// One K-step m of the right factor S[p][n] += sum_s x[s][p] w_s B[s][n] for this
+// wavefront's p-tiles PT0 .. PT0 + PTW - 1 (its n-tile's B^T fragment bt, scaled
+// by w here), from x^T fragments already in registers.
+template <int PTW, int PT0>
+__device__ __forceinline__ void rf_step(const uint4* af, uint4 bt, const float* wl, int m, f32x4_t* sacc)
+{
+    const float4 w0 = *reinterpret_cast<const float4*>(wl + 32 * m);
+    const float4 w1 = *reinterpret_cast<const float4*>(wl + 32 * m + 16);
+    const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+    const u32 bw[4] = {bt.x, bt.y, bt.z, bt.w};
+    float bf8[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        bf8[2 * e] = __uint_as_float(bw[e] << 16) * wv[2 * e];
+        bf8[2 * e + 1] = __uint_as_float(bw[e] & 0xFFFF0000u) * wv[2 * e + 1];
+    }
+    const bf16x8_t bop = pack8(bf8);
+#pragma unroll
+    for (int i = 0; i < PTW; ++i) sacc[i] = mfma(as_bf16x8(af[PT0 + i]), bop, sacc[i]);
+}
+
 // Diagonal block of wavefront W, whose strips (t-tiles) are W and 15 - W
 // (9 K-steps between them for every W).  K-step m covers s-tiles 2m, 2m+1; its
 // contraction index is permuted to the Gram accumulator layout (slot e<4 ->
@@ -619,10 +640,15 @@ __device__ __forceinline__ void strip_step(const uint4* af, const char* gbase, i
 // fragments and vf of a K-step are read once for both strips.  Everything
 // about the strips is a compile-time constant, so the body is straight-line
 // code with immediate LDS offsets.
-template <int W>
+// PTW > 0: the right factor (this wavefront's n-tile, PTW p-tiles) runs in the
+// same pass, on the x^T fragments the diagonal block has read (its first nB
+// K-steps; the rest read their own), so that x is read from LDS once for both.
+constexpr int kMidStep = 0;   // K-step after which `mid` runs (the next head's x copy)
+template <int W, int PTW, class Mid>
 __device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const float* cs,
-                                          const float* vf, const float* dt, const u16* GR, int r,
-                                          int lg, int lane, f32x4_t* yA, f32x4_t* yB)
+                                          const float* vf, const float* dt, const float* wrf, const uint4* btf,
+                                          const u16* GR, int r, int lg, int lane, f32x4_t* yA, f32x4_t* yB,
+                                          f32x4_t* sacc, const Mid& mid)
 {
     constexpr int sA = W, sB = 15 - W;
     constexpr int nA = sA / 2 + 1, nB = sB / 2 + 1;
@@ -635,6 +661,8 @@ __device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const 
     const char* x1 = xsb + xa[1];
     const char* x2 = xsb + xa[2];
     const char* x3 = xsb + xa[3];
+    constexpr int kPt0 = PTW == 4 ? 0 : 2 * (W >> 2);   // the right factor's first p-tile
+    const float* wrl = wrf + 4 * lg;
     // Software pipeline: the LDS operands of K-step m+1 are requested before
     // the masking and MFMAs of K-step m.
     struct Step {
@@ -666,25 +694,48 @@ __device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const 
             strip_step<sB, m>(cur.af, gB, tB, csB, cur.ce0, cur.ce1, cur.vf0, cur.vf1, cs, dt, lg, yB);
             if constexpr (m < nA)
                 strip_step<sA, m>(cur.af, gA, tA, csA, cur.ce0, cur.ce1, cur.vf0, cur.vf1, cs, dt, lg, yA);
+            if constexpr (PTW > 0) rf_step<PTW, kPt0>(cur.af, btf[m], wrl, m, sacc);
+            if constexpr (m == kMidStep) mid();
             if constexpr (m + 1 < nB) cur = nxt;
         }(), ...);
     }(std::make_integer_sequence<int, nB>{});
+    if constexpr (PTW > 0) {
+        // the right factor's remaining K-steps
+        const char* xp[4] = {x0, x1, x2, x3};
+        [&]<int... Ms>(std::integer_sequence<int, Ms...>) {
+            ([&] {
+                constexpr int m = nB + Ms;
+                uint4 af[4];
+#pragma unroll
+                for (int i = 0; i < PTW; ++i) {
+                    const uint2 lo = tr_read(xp[kPt0 + i] + 4096 * m), hi = tr_read(xp[kPt0 + i] + 4096 * m + 2048);
+                    af[kPt0 + i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                }
+                rf_step<PTW, kPt0>(af, btf[m], wrl, m, sacc);
+                if constexpr (m == kMidStep) mid();
+            }(), ...);
+        }(std::make_integer_sequence<int, kQ / 32 - nB>{});
+    }
 }
 
+template <int PTW, class Mid>
 __device__ __forceinline__ void diag_block(int wave, const char* xsb, const int* xa, const float* cs,
-                                           const float* vf, const float* dt, const u16* GR, int r,
-                                           int lg, int lane, f32x4_t* yA, f32x4_t* yB)
+                                           const float* vf, const float* dt, const float* wrf, const uint4* btf,
+                                           const u16* GR, int r, int lg, int lane, f32x4_t* yA, f32x4_t* yB,
+                                           f32x4_t* sacc, const Mid& mid)
 {
+#define SSD_DIAG_WAVE(W) diag_wave<W, PTW>(xsb, xa, cs, vf, dt, wrf, btf, GR, r, lg, lane, yA, yB, sacc, mid)
     switch (wave) {
-    case 0: diag_wave<0>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    case 1: diag_wave<1>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    case 2: diag_wave<2>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    case 3: diag_wave<3>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    case 4: diag_wave<4>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    case 5: diag_wave<5>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    case 6: diag_wave<6>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
-    default: diag_wave<7>(xsb, xa, cs, vf, dt, GR, r, lg, lane, yA, yB); break;
+    case 0: SSD_DIAG_WAVE(0); break;
+    case 1: SSD_DIAG_WAVE(1); break;
+    case 2: SSD_DIAG_WAVE(2); break;
+    case 3: SSD_DIAG_WAVE(3); break;
+    case 4: SSD_DIAG_WAVE(4); break;
+    case 5: SSD_DIAG_WAVE(5); break;
+    case 6: SSD_DIAG_WAVE(6); break;
+    default: SSD_DIAG_WAVE(7); break;
     }
+#undef SSD_DIAG_WAVE
 }
 
 // One work item of the chunk kernel: (chunk, batch row, group of HG heads).
@@ -887,26 +938,18 @@ __device__ __forceinline__ void load_c_block(const FusedParams& p, const Item& i
     }
 }
 
-// The item-level C fragments (one column block of the state: N <= 128; with
-// two blocks every head loads its own per block).
-template <int N>
-__device__ __forceinline__ void load_c(const FusedParams& p, const Item& it, const int* strip, int r, int lg,
-                                       uint4 (&cf)[2][(N < kNH ? N : kNH) / 32])
-{
-    if constexpr (N <= kNH) load_c_block<N, N>(p, it, strip, r, lg, 0, cf);
-}
-
 // One head of a work item.  Every LDS buffer is a separate __restrict__
 // parameter: the compiler then knows that the asynchronous copies into the
 // next head's buffers (and the next item's Gram tiles) never alias the buffers
 // read here, and does not make those reads wait for the copies.
 // Y32: y is written in float32 straight from the accumulators (the layer
 // recomputed for the block gradients, whose dy and dz need y before rounding).
-template <int N, bool PACKED, bool EARLY, bool Y32>
+// FUSE (one column block of the state only): the right factor runs in the
+// diagonal block's pass over x.
+template <int N, bool PACKED, bool EARLY, bool Y32, bool FUSE>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
-                                          uint4 (&btf)[kQ / 32],
-                                          uint4 (&cf)[2][(N < kNH ? N : kNH) / 32],
+                                          uint4 (&btf)[kQ / 32], uint4 (&cf)[2][(N < kNH ? N : kNH) / 32],
                                           u16& dtr, bool& ready, u16* __restrict__ xs, u16* __restrict__ xs_n,
                                           float* __restrict__ cs, float* __restrict__ dt,
                                           float* __restrict__ wt, float* __restrict__ vf, float* __restrict__ w,
@@ -926,6 +969,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     constexpr int PTW = 4 * NT / kWaves;
     constexpr int KN = NH / 32;
     constexpr int HBS = NH + 8;
+    static_assert(!FUSE || HALVES == 1, "the fused right factor takes one column block of the state");
     // per-wavefront constants (loop-invariant; the compiler keeps them out of the loops)
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // provably uniform
@@ -1024,26 +1068,58 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
 
     // ---- diagonal block: Y^T[p][t] for the two strips ------------------------
+    // (with one column block of the state, the right factor S[p][n] = sum_s
+    // x[s][p] w_s B[s][n] of this wavefront's tiles runs in the same pass: x is
+    // read from LDS once for both)
     f32x4_t y[2][4];
 #pragma unroll
     for (int k4 = 0; k4 < 2; ++k4)
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) y[k4][pt] = zero4();
-    diag_block(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, gr, r, lg, lane, y[0], y[1]);
+    f32x4_t sacc[HALVES][PTW];
+#pragma unroll
+    for (int hf = 0; hf < HALVES; ++hf)
+#pragma unroll
+        for (int i = 0; i < PTW; ++i) sacc[hf][i] = zero4();
+    // Opaque to the optimiser, so that it does not hoist the unpacking of B^T out
+    // of the head loop (64 more registers, and a wait for the loads at the start
+    // of every item).
+    const auto opaque_bt = [&] {
+#pragma unroll
+        for (int m = 0; m < kQ / 32; ++m) {
+            uint4_t v = __builtin_bit_cast(uint4_t, btf[m]);
+            asm volatile("" : "+v"(v));
+            btf[m] = __builtin_bit_cast(uint4, v);
+        }
+    };
+    // x of the next head -- of this item, or of the next item once known --
+    // arrives while this head computes.  It is requested after the diagonal
+    // block's first K-step (FUSE) or after the diagonal block, not at the head's
+    // start, where the copies queue behind the previous head's y stores; not
+    // much later either, since the state passing's own loads wait for it (the
+    // wait is in issue order).
+    const auto next_x = [&] {
+        if (!last)
+            dma_head(p, it, h + 1, xs_n, wave, dmo);
+        else if (hk > 0 && next < nwork) {
+            const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
+            dma_head(p, nit, nit.h0, xs_n, wave, dmo);
+        }
+    };
+    if constexpr (FUSE) {
+        opaque_bt();
+        diag_block<PTW>(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, w, btf, gr, r, lg, lane, y[0], y[1],
+                        sacc[0], next_x);
+    } else {
+        diag_block<0>(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, w, btf, gr, r, lg, lane, y[0], y[1],
+                      sacc[0], [] {});
+    }
     // Last head of an item with the next item known: this wavefront refills the
     // Gram rows it has just finished with (no other wavefront reads them) for
     // the next item, well ahead of that item's diagonal block.
     const bool gram_early = last && hk > 0 && next < nwork;
     if (gram_early) dma_gram_rows(gr, p, decode_item<PACKED>(p, next, per_c, nHG, N), wave, lane);
-    // x of the next head -- of this item, or of the next item once known --
-    // arrives while this head computes (issued here, not at the head's start,
-    // where the copies would queue behind the previous head's y stores)
-    if (!last)
-        dma_head(p, it, h + 1, xs_n, wave, dmo);
-    else if (hk > 0 && next < nwork) {
-        const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
-        dma_head(p, nit, nit.h0, xs_n, wave, dmo);
-    }
+    if constexpr (!FUSE) next_x();
     // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
     // after the right factor)
 #pragma unroll
@@ -1059,26 +1135,11 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         }
     }
 
-    // ---- right factor: S[p][n] = sum_s x[s][p] w_s B[s][n], this wavefront's tiles
-    // (per column block of the state)
-    f32x4_t sacc[HALVES][PTW];
+    // ---- right factor (unless fused above): S[p][n] = sum_s x[s][p] w_s B[s][n],
+    // this wavefront's tiles, per column block of the state
+    if constexpr (!FUSE) opaque_bt();
 #pragma unroll
-    for (int hf = 0; hf < HALVES; ++hf)
-#pragma unroll
-        for (int i = 0; i < PTW; ++i) sacc[hf][i] = zero4();
-    // Opaque to the optimiser, so that it does not hoist the unpacking of B^T out
-    // of the head loop (64 more registers, and a wait for the loads at the start
-    // of every item).
-    {
-#pragma unroll
-        for (int m = 0; m < kQ / 32; ++m) {
-            uint4_t v = __builtin_bit_cast(uint4_t, btf[m]);
-            asm volatile("" : "+v"(v));
-            btf[m] = __builtin_bit_cast(uint4, v);
-        }
-    }
-#pragma unroll
-    for (int hf = 0; hf < HALVES; ++hf) {
+    for (int hf = 0; hf < (FUSE ? 0 : HALVES); ++hf) {
         if (HALVES > 1) __builtin_amdgcn_sched_barrier(0);
         if (HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth);
         const uint4 (&bsrc)[kQ / 32] = hf > 0 ? bth : btf;
@@ -1214,8 +1275,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             if (norm && tid < kP) wn[tid] = wreg;
             if constexpr (EARLY) wait_vmem();
         }
-        // Two column blocks: this block's C fragments (the item-level ones
-        // hold the first block only when there is one block).
+        // Two column blocks: this block's C fragments.
         uint4 cfh[2][KN];
         if constexpr (HALVES > 1) load_c_block<N, NH>(p, it, strip, r, lg, hf, cfh);
         lds_barrier();   // bf16 state (block) in LDS complete; every wavefront is past the diagonal block
@@ -1366,13 +1426,12 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             }
         }
     }
-    // The next item's B^T and C fragments (their last uses in this item are
-    // behind us), requested after the waits above so that none of those waits
-    // for them.
+    // The next item's B^T fragments (their last use in this item is behind
+    // us), requested after the waits above so that none of those waits for them.
     if (last && next < nwork) {
         const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
         load_bt<N>(p, nit, ntw, r, lg, btf);
-        load_c<N>(p, nit, strip, r, lg, cf);
+        if constexpr (HALVES == 1) load_c_block<N, NH>(p, nit, strip, r, lg, 0, cf);
     }
     lds_barrier();   // this head's LDS buffers may be refilled from here on; the next head's weights are in place
     dtr = dtr_next;  // here, where the load has long completed (the epilogue waited for it)
@@ -1381,7 +1440,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
 
 // A_log, D and the dt bias come as separate read-only arguments so that their per-head values
 // are scalar loads (a vector load would wait behind the outstanding copies).
-template <int N, bool PACKED, bool EARLY, bool Y32>
+template <int N, bool PACKED, bool EARLY, bool Y32, bool FUSE>
 __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, const float* __restrict__ A_logp,
                                                                 const float* __restrict__ Dp,
                                                                 const float* __restrict__ biasp)
@@ -1433,17 +1492,17 @@ __global__ __launch_bounds__(kMainThreads, 1) void k_fused_main(FusedParams p, c
     // here for the first item, and for every later item by the last head of the
     // item before it, right after their last use there
     uint4 btf[kQ / 32];   // (one column block of the state; with two, each head loads its own)
-    uint4 cf[2][KN];   // raw bf16 (as a bf16 vector type the compiler merges lanes right at the loads)
+    uint4 cf[2][KN];      // C fragments of the left factor (one column block; with two, per head and block)
     {
         const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
         load_bt<N>(p, it, ntw, r, lg, btf);
-        load_c<N>(p, it, strip, r, lg, cf);
+        if constexpr (N <= kNH) load_c_block<N, N>(p, it, strip, r, lg, 0, cf);
     }
     for (;;) {
     const Item it = decode_item<PACKED>(p, work, per_c, nHG, N);
     int next = nwork;
     for (int hk = 0; hk < p.HG; ++hk) {
-        head_step<N, PACKED, EARLY, Y32>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, ready, sm.XS[q],
+        head_step<N, PACKED, EARLY, Y32, FUSE>(p, it, hk, next, nwork, per_c, nHG, btf, cf, dtr, ready, sm.XS[q],
                      sm.XS[q ^ 1], sm.cs[q], sm.dt[q], sm.wtot[q], sm.vf[q], sm.w[q], sm.cs[q ^ 1], sm.dt[q ^ 1],
                      sm.wtot[q ^ 1], sm.vf[q ^ 1], sm.w[q ^ 1], s_gr, s_hb, &sm.ticket, A_logp, Dp, biasp, sm.wn);
         q ^= 1;
@@ -1488,23 +1547,26 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     const float* Dp = p.D;
     const float* biasp = p.dtx.bias;
     if (p.y32 && p.early_flag)
-        hipLaunchKernelGGL((k_fused_main<N, false, true, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
+        hipLaunchKernelGGL((k_fused_main<N, false, true, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
                            biasp);
     else if (p.y32)
-        hipLaunchKernelGGL((k_fused_main<N, false, false, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+        hipLaunchKernelGGL((k_fused_main<N, false, false, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
                            Dp, biasp);
     else if (p.vtab && p.early_flag)
-        hipLaunchKernelGGL((k_fused_main<N, true, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
+        hipLaunchKernelGGL((k_fused_main<N, true, true, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
                            biasp);
     else if (p.vtab)
-        hipLaunchKernelGGL((k_fused_main<N, true, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+        hipLaunchKernelGGL((k_fused_main<N, true, false, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
                            Dp, biasp);
     else if (p.early_flag)
-        hipLaunchKernelGGL((k_fused_main<N, false, true, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+        hipLaunchKernelGGL((k_fused_main<N, false, true, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
                            Dp, biasp);
+    else if (N <= kNH && p.fuse_rf)
+        hipLaunchKernelGGL((k_fused_main<N, false, false, false, N <= kNH>), g_main, dim3(kMainThreads), 0, stream, p,
+                           A_logp, Dp, biasp);
     else
-        hipLaunchKernelGGL((k_fused_main<N, false, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
-                           Dp, biasp);
+        hipLaunchKernelGGL((k_fused_main<N, false, false, false, false>), g_main, dim3(kMainThreads), 0, stream, p,
+                           A_logp, Dp, biasp);
     err = hipGetLastError();
     if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, stream);
     return err;

@@ -19,6 +19,7 @@ enum Tuning {
     kTuneBwdHeadsPerSlice,   // heads per workgroup of the backward's chunk kernel
     kTuneVarlenPerSequence,  // 1: packed rows by host offsets run one call per sequence
     kTuneStateWaitLimit,     // polls before a chunk's wait for the state before it gives up
+    kTuneFusedRightFactor,   // 1: the chunk kernel's right factor in its own pass, 2: in the diagonal block's
     kTuneCount
 };
 int64_t tuning(Tuning k);
@@ -122,6 +123,9 @@ struct FusedParams {
     // nonzero: a chunk's state flag is set as soon as its state is stored
     // (before its left factor), for launches bound by the chain of chunks
     int early_flag = 0;
+    // nonzero: the right factor is computed in the diagonal block's pass over x
+    // (one column block of the state, plain rows, late flag)
+    int fuse_rf = 0;
     // gate / per-head normalisation in the output stage (null: none)
     const void* z = nullptr;             // (b, T, H, P) bf16
     const float* norm_weight = nullptr;  // (H * P), with norm_head

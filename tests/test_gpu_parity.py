@@ -220,6 +220,27 @@ def test_fused_n256_few_workgroups(tune, early):
               tag="n256_flag%s_hg%d" % (early, hg))
 
 
+@pytest.mark.parametrize("N", [64, 128])
+def test_fused_right_factor_both_passes(tune, N):
+    """The chunk kernel's right factor in a pass of its own and in the
+    diagonal block's pass (both forced; late state flag, few persistent
+    workgroups, 1 and 5 heads per item): each against the oracle, and the two
+    bit-identical (the same products in the same order)."""
+    import torch
+
+    tune("early_state_flag", 1)
+    tune("max_workgroups", 3)
+    inp = make_inputs(Problem(2, 1300, 10, 64, N, 1, 256, "bf16", init_states=True), 53)
+    for hg in (1, 5):
+        tune("heads_per_item", hg)
+        tune("fused_right_factor", 1)
+        y1, f1 = check(inp, tag="rf_own_pass_hg%d_n%d" % (hg, N))
+        tune("fused_right_factor", 2)
+        y2, f2 = check(inp, tag="rf_fused_hg%d_n%d" % (hg, N))
+        assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+        assert torch.equal(f1, f2)
+
+
 def test_packed_rows_both_device_paths(tune):
     """The general kernels (forced) and the fused ones on one packed row, each
     against the oracle."""
