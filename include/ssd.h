@@ -427,9 +427,8 @@ int ssd_workspace_status(const void* workspace, void* stream);
  *                          poll that finds the state missing)
  *   "fused_right_factor"   1: the fused chunk kernel computes the right
  *                          factor in a pass of its own, 2: in the diagonal
- *                          block's pass (plain rows with the late state flag
- *                          and a state of at most 128 columns; elsewhere 2
- *                          acts as 1)
+ *                          block's pass (plain rows with the late state flag;
+ *                          elsewhere 2 acts as 1)
  * Returns SSD_OK, SSD_ERR_NULL_ARG, or SSD_ERR_BAD_OPTION (unknown name, or a
  * value out of range).  The settings are process-wide and not ordered with
  * calls made concurrently on other host threads. */

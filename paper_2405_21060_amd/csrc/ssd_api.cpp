@@ -280,14 +280,15 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         f.early_flag = fw.nC >= 2 * rounds * f.HG ? 1 : 0;
         if (const int64_t ef = ssd::tuning(ssd::kTuneEarlyFlag); ef == 1 || ef == 2) f.early_flag = ef == 2;
         // The right factor in the diagonal block's pass (x read from LDS once for
-        // both) shortens a head's matrix-product phase but holds more registers
-        // through it; measured faster with long items and the late flag (2.7B
-        // layer 0.1864 ms against 0.1908, the state-size sweep at N = 64 0.549
-        // against 0.597) and slower with items of 1-3 heads (130M layer, the
-        // 8-way head and sequence splits: 2-4 %) and with the early flag.
-        f.fuse_rf = !f.early_flag && f.HG >= 4 && s.N <= 128 && !y32 ? 1 : 0;
+        // both; with N = 256 the first column block's) shortens a head's
+        // matrix-product phase but holds more registers through it; measured
+        // faster with long items and the late flag (2.7B layer 0.1864 ms against
+        // 0.1908, the state-size sweep at N = 64 0.549 against 0.597, at N = 256
+        // 1.256 against 1.295) and slower with items of 1-3 heads (130M layer,
+        // the 8-way head and sequence splits: 2-4 %) and with the early flag.
+        f.fuse_rf = !f.early_flag && f.HG >= 4 && !y32 ? 1 : 0;
         if (const int64_t fr = ssd::tuning(ssd::kTuneFusedRightFactor); fr == 1 || fr == 2)
-            f.fuse_rf = fr == 2 && !f.early_flag && s.N <= 128 && !y32;
+            f.fuse_rf = fr == 2 && !f.early_flag && !y32;
         f.status = status;
         f.reset_status = reset_status ? 1 : 0;
         if (const int64_t sl = ssd::tuning(ssd::kTuneStateWaitLimit); sl >= 1) f.spin_limit = sl;

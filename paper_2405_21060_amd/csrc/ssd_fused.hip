@@ -944,8 +944,8 @@ __device__ __forceinline__ void load_c_block(const FusedParams& p, const Item& i
 // read here, and does not make those reads wait for the copies.
 // Y32: y is written in float32 straight from the accumulators (the layer
 // recomputed for the block gradients, whose dy and dz need y before rounding).
-// FUSE (one column block of the state only): the right factor runs in the
-// diagonal block's pass over x.
+// FUSE: the right factor (of the first column block of the state, with two)
+// runs in the diagonal block's pass over x.
 template <int N, bool PACKED, bool EARLY, bool Y32, bool FUSE>
 __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, int hk, int& next, int nwork,
                                           int per_c, int nHG,
@@ -969,7 +969,6 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     constexpr int PTW = 4 * NT / kWaves;
     constexpr int KN = NH / 32;
     constexpr int HBS = NH + 8;
-    static_assert(!FUSE || HALVES == 1, "the fused right factor takes one column block of the state");
     // per-wavefront constants (loop-invariant; the compiler keeps them out of the loops)
     const int tid = threadIdx.x, lane = tid & 63, r = lane & 15, lg = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // provably uniform
@@ -1110,6 +1109,10 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         opaque_bt();
         diag_block<PTW>(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, w, btf, gr, r, lg, lane, y[0], y[1],
                         sacc[0], next_x);
+        // (two column blocks: the first block's right factor was fused; the
+        // second block's B^T fragments now -- requested during the diagonal
+        // block they would hold registers it needs)
+        if constexpr (HALVES > 1) load_bt_block<N, NH>(p, it, ntw, r, lg, 1, bth);
     } else {
         diag_block<0>(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, w, btf, gr, r, lg, lane, y[0], y[1],
                       sacc[0], [] {});
@@ -1135,13 +1138,13 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
         }
     }
 
-    // ---- right factor (unless fused above): S[p][n] = sum_s x[s][p] w_s B[s][n],
-    // this wavefront's tiles, per column block of the state
+    // ---- right factor (of the blocks not fused above): S[p][n] = sum_s x[s][p]
+    // w_s B[s][n], this wavefront's tiles, per column block of the state
     if constexpr (!FUSE) opaque_bt();
 #pragma unroll
-    for (int hf = 0; hf < (FUSE ? 0 : HALVES); ++hf) {
+    for (int hf = FUSE ? 1 : 0; hf < HALVES; ++hf) {
         if (HALVES > 1) __builtin_amdgcn_sched_barrier(0);
-        if (HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth);
+        if (!FUSE && HALVES > 1 && hf + 1 < HALVES) load_bt_block<N, NH>(p, it, ntw, r, lg, hf + 1, bth);
         const uint4 (&bsrc)[kQ / 32] = hf > 0 ? bth : btf;
         const char* xsb = reinterpret_cast<const char*>(xs);
         const float* wl = w + 4 * lg;
@@ -1561,8 +1564,8 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     else if (p.early_flag)
         hipLaunchKernelGGL((k_fused_main<N, false, true, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
                            Dp, biasp);
-    else if (N <= kNH && p.fuse_rf)
-        hipLaunchKernelGGL((k_fused_main<N, false, false, false, N <= kNH>), g_main, dim3(kMainThreads), 0, stream, p,
+    else if (p.fuse_rf)
+        hipLaunchKernelGGL((k_fused_main<N, false, false, false, true>), g_main, dim3(kMainThreads), 0, stream, p,
                            A_logp, Dp, biasp);
     else
         hipLaunchKernelGGL((k_fused_main<N, false, false, false, false>), g_main, dim3(kMainThreads), 0, stream, p,

@@ -123,8 +123,8 @@ struct FusedParams {
     // nonzero: a chunk's state flag is set as soon as its state is stored
     // (before its left factor), for launches bound by the chain of chunks
     int early_flag = 0;
-    // nonzero: the right factor is computed in the diagonal block's pass over x
-    // (one column block of the state, plain rows, late flag)
+    // nonzero: the right factor (the first column block's, with two) is
+    // computed in the diagonal block's pass over x (plain rows, late flag)
     int fuse_rf = 0;
     // gate / per-head normalisation in the output stage (null: none)
     const void* z = nullptr;             // (b, T, H, P) bf16

@@ -220,7 +220,7 @@ def test_fused_n256_few_workgroups(tune, early):
               tag="n256_flag%s_hg%d" % (early, hg))
 
 
-@pytest.mark.parametrize("N", [64, 128])
+@pytest.mark.parametrize("N", [64, 128, 256])
 def test_fused_right_factor_both_passes(tune, N):
     """The chunk kernel's right factor in a pass of its own and in the
     diagonal block's pass (both forced; late state flag, few persistent
