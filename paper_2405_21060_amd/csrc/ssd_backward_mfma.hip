@@ -226,6 +226,12 @@ __global__ __launch_bounds__(kPassT, H32 ? 2 : 1) void k_bwd2_pass(BwdParams p)
 {
     __shared__ __attribute__((aligned(16))) u16 XS[kQ2 * kP2];   // weighted x (or dy), token-major
     __shared__ __attribute__((aligned(16))) u16 YS[kQ2 * N];     // B (or C), token-major
+    // the chunk's state (bf16, n x p) on its way out: rows padded to 72
+    // elements so that the 16 n-rows of a wavefront's writes spread over the
+    // banks; read back as whole 128-byte rows, so that the global stores cover
+    // full rows (a wavefront's own fragments are 32-byte pieces of 16 rows)
+    constexpr int kOBld = kP2 + 8;
+    __shared__ __attribute__((aligned(16))) u16 OB[N * kOBld];
 
     const int64_t bh = blockIdx.x;
     const int64_t b = bh / p.H, h = bh - b * p.H, g = h / (p.H / p.G);
@@ -361,14 +367,23 @@ __global__ __launch_bounds__(kPassT, H32 ? 2 : 1) void k_bwd2_pass(BwdParams p)
             }
             fetch(st, k + 2);
 
-            // S before this chunk's term -> out(c), bf16 (n x p)
-            u16* o = out + ((PACKED ? c : b * p.nC + c) * p.H + h) * kP2 * N;
+            // S before this chunk's term -> out(c), bf16 (n x p), through OB
     #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
-                *reinterpret_cast<uint2*>(o + (16 * nt + r) * kP2 + 16 * w + 4 * q) =
+                *reinterpret_cast<uint2*>(OB + (16 * nt + r) * kOBld + 16 * w + 4 * q) =
                     make_uint2(pack2(S[nt][0], S[nt][1]), pack2(S[nt][2], S[nt][3]));
 
-            __syncthreads();   // this chunk's operands in place
+            __syncthreads();   // this chunk's operands and its state in place
+            {
+                u16* o = out + ((PACKED ? c : b * p.nC + c) * p.H + h) * kP2 * N;
+                constexpr int kOK = N * kP2 / 8 / kPassT;   // 16-byte pieces per thread
+    #pragma unroll
+                for (int kk = 0; kk < kOK; ++kk) {
+                    const int i = tid + kPassT * kk, row = i >> 3, c8 = 8 * (i & 7);
+                    *reinterpret_cast<uint4*>(o + row * kP2 + c8) =
+                        *reinterpret_cast<const uint4*>(OB + row * kOBld + c8);
+                }
+            }
             const float a = exp2f(csend);
             const uint4 xf0 = tr_frag<kP2>(XS, 0, 16 * w, lane), xf1 = tr_frag<kP2>(XS, 1, 16 * w, lane);
     #pragma unroll
