@@ -643,12 +643,14 @@ __device__ __forceinline__ void rf_step(const uint4* af, uint4 bt, const float* 
 // PTW > 0: the right factor (this wavefront's n-tile, PTW p-tiles) runs in the
 // same pass, on the x^T fragments the diagonal block has read (its first nB
 // K-steps; the rest read their own), so that x is read from LDS once for both.
+// `mid` runs after K-step kMidStep, `fin` once the Gram rows have been read for
+// the last time.
 constexpr int kMidStep = 0;   // K-step after which `mid` runs (the next head's x copy)
-template <int W, int PTW, class Mid>
+template <int W, int PTW, class Mid, class Fin>
 __device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const float* cs,
                                           const float* vf, const float* dt, const float* wrf, const uint4* btf,
                                           const u16* GR, int r, int lg, int lane, f32x4_t* yA, f32x4_t* yB,
-                                          f32x4_t* sacc, const Mid& mid)
+                                          f32x4_t* sacc, const Mid& mid, const Fin& fin)
 {
     constexpr int sA = W, sB = 15 - W;
     constexpr int nA = sA / 2 + 1, nB = sB / 2 + 1;
@@ -694,6 +696,7 @@ __device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const 
             strip_step<sB, m>(cur.af, gB, tB, csB, cur.ce0, cur.ce1, cur.vf0, cur.vf1, cs, dt, lg, yB);
             if constexpr (m < nA)
                 strip_step<sA, m>(cur.af, gA, tA, csA, cur.ce0, cur.ce1, cur.vf0, cur.vf1, cs, dt, lg, yA);
+            if constexpr (m + 1 == nB) fin();   // this wavefront's Gram rows are read for the last time
             if constexpr (PTW > 0) rf_step<PTW, kPt0>(cur.af, btf[m], wrl, m, sacc);
             if constexpr (m == kMidStep) mid();
             if constexpr (m + 1 < nB) cur = nxt;
@@ -718,13 +721,13 @@ __device__ __forceinline__ void diag_wave(const char* xsb, const int* xa, const 
     }
 }
 
-template <int PTW, class Mid>
+template <int PTW, class Mid, class Fin>
 __device__ __forceinline__ void diag_block(int wave, const char* xsb, const int* xa, const float* cs,
                                            const float* vf, const float* dt, const float* wrf, const uint4* btf,
                                            const u16* GR, int r, int lg, int lane, f32x4_t* yA, f32x4_t* yB,
-                                           f32x4_t* sacc, const Mid& mid)
+                                           f32x4_t* sacc, const Mid& mid, const Fin& fin)
 {
-#define SSD_DIAG_WAVE(W) diag_wave<W, PTW>(xsb, xa, cs, vf, dt, wrf, btf, GR, r, lg, lane, yA, yB, sacc, mid)
+#define SSD_DIAG_WAVE(W) diag_wave<W, PTW>(xsb, xa, cs, vf, dt, wrf, btf, GR, r, lg, lane, yA, yB, sacc, mid, fin)
     switch (wave) {
     case 0: SSD_DIAG_WAVE(0); break;
     case 1: SSD_DIAG_WAVE(1); break;
@@ -1105,23 +1108,34 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
             dma_head(p, nit, nit.h0, xs_n, wave, dmo);
         }
     };
+    // Last head of an item with the next item known: each wavefront refills the
+    // Gram rows of its own two strips for the next item (no other wavefront
+    // reads them), well ahead of that item's diagonal block: right after its
+    // diagonal block, or -- in the fused pass with N >= 128 -- as soon as the
+    // block has read them for the last time, before the right factor's
+    // remaining K-steps (2.7B layer 0.1878 -> 0.1856 ms; with N = 64, and
+    // outside the fused pass, that placement measured 0.5-2 % slower).
+    constexpr bool kGramInPass = FUSE && N >= kNH;
+    const bool gram_early = last && hk > 0 && next < nwork;
+    const auto gram_refill = [&] {
+        if (gram_early) dma_gram_rows(gr, p, decode_item<PACKED>(p, next, per_c, nHG, N), wave, lane);
+    };
+    const auto gram_fin = [&] {
+        if constexpr (kGramInPass) gram_refill();
+    };
     if constexpr (FUSE) {
         opaque_bt();
         diag_block<PTW>(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, w, btf, gr, r, lg, lane, y[0], y[1],
-                        sacc[0], next_x);
+                        sacc[0], next_x, gram_fin);
         // (two column blocks: the first block's right factor was fused; the
         // second block's B^T fragments now -- requested during the diagonal
         // block they would hold registers it needs)
         if constexpr (HALVES > 1) load_bt_block<N, NH>(p, it, ntw, r, lg, 1, bth);
     } else {
         diag_block<0>(wave, reinterpret_cast<const char*>(xs), xa, cs, vf, dt, w, btf, gr, r, lg, lane, y[0], y[1],
-                      sacc[0], [] {});
+                      sacc[0], [] {}, [] {});
     }
-    // Last head of an item with the next item known: this wavefront refills the
-    // Gram rows it has just finished with (no other wavefront reads them) for
-    // the next item, well ahead of that item's diagonal block.
-    const bool gram_early = last && hk > 0 && next < nwork;
-    if (gram_early) dma_gram_rows(gr, p, decode_item<PACKED>(p, next, per_c, nHG, N), wave, lane);
+    if constexpr (!kGramInPass) gram_refill();
     if constexpr (!FUSE) next_x();
     // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
     // after the right factor)
