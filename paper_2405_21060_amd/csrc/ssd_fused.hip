@@ -1116,6 +1116,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // remaining K-steps (2.7B layer 0.1878 -> 0.1856 ms; with N = 64, and
     // outside the fused pass, that placement measured 0.5-2 % slower).
     constexpr bool kGramInPass = FUSE && N >= kNH;
+    constexpr bool kBtInPass = FUSE && N == kNH;
     const bool gram_early = last && hk > 0 && next < nwork;
     const auto gram_refill = [&] {
         if (gram_early) dma_gram_rows(gr, p, decode_item<PACKED>(p, next, per_c, nHG, N), wave, lane);
@@ -1137,6 +1138,12 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     }
     if constexpr (!kGramInPass) gram_refill();
     if constexpr (!FUSE) next_x();
+    // The next item's B^T fragments, in an item's last head with the next item
+    // known: with the fused right factor and N = 128 as soon as the pass has used
+    // this item's (2.7B layer 0.1863 -> 0.1829 ms; with N = 64 it measured 1.6 %
+    // slower, so there, as everywhere else, they follow the y stores below).
+    if (kBtInPass && last && hk > 0 && next < nwork)
+        load_bt<N>(p, decode_item<PACKED>(p, next, per_c, nHG, N), ntw, r, lg, btf);
     // skip term D x, while x is in LDS (with the gate branch, its buffer takes z
     // after the right factor)
 #pragma unroll
@@ -1447,7 +1454,7 @@ __device__ __forceinline__ void head_step(const FusedParams& p, const Item& it, 
     // us), requested after the waits above so that none of those waits for them.
     if (last && next < nwork) {
         const Item nit = decode_item<PACKED>(p, next, per_c, nHG, N);
-        load_bt<N>(p, nit, ntw, r, lg, btf);
+        if (!(kBtInPass && hk > 0)) load_bt<N>(p, nit, ntw, r, lg, btf);
         if constexpr (HALVES == 1) load_c_block<N, NH>(p, nit, strip, r, lg, 0, cf);
     }
     lds_barrier();   // this head's LDS buffers may be refilled from here on; the next head's weights are in place
