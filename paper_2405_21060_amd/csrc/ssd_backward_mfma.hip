@@ -422,10 +422,17 @@ __global__ __launch_bounds__(kPassT, H32 ? 2 : 1) void k_bwd2_pass(BwdParams p)
 // Chunk gradients.
 template <int N, bool H32 = false>
 struct ChunkSmem {
-    static constexpr int kLdN = N + 8;
+    // Row strides (elements) of the shared tiles: N-wide rows (B, Gn) and
+    // 64-wide rows (the rest).  Padding spreads the 16 rows an operand read or
+    // a tile write touches over the banks; measured at the 2.7B shape (row
+    // strides 72 / N + 8 before): 80 / N + 16 0.885 ms per backward, 80 / N + 8
+    // 0.903, 88 / N + 8 0.935, 72 / N + 8 0.918.  With the float32 dy copy
+    // (H32) the 64-wide rows keep 72 elements so that it still fits.
+    static constexpr int kLdN = N + 16;
+    static constexpr int kLdC = H32 ? kLd : kLd + 8;
     static constexpr int kLdF = kP2 + 4;   // row stride (floats) of the float32 dy copy (H32)
     static constexpr size_t kBytes =
-        sizeof(u16) * (2 * static_cast<size_t>(kQ2) * kLdN + 2 * N * kLd + 6 * kQ2 * kLd) +
+        sizeof(u16) * (2 * static_cast<size_t>(kQ2) * kLdN + 2 * N * kLdC + 6 * kQ2 * kLdC) +
         (H32 ? sizeof(float) * kQ2 * kLdF : 0);
 };
 
@@ -440,6 +447,7 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
 {
     constexpr int kLdN = ChunkSmem<N>::kLdN;
     constexpr int kLdF = ChunkSmem<N, H32>::kLdF;
+    constexpr int kLd = ChunkSmem<N, H32>::kLdC;   // (this kernel's 64-wide row stride)
     constexpr int kNT = N / 16;             // n-tiles
     constexpr int kBW = N / 32;             // dB / dC tiles per wavefront
     extern __shared__ __attribute__((aligned(16))) u16 sm2[];
