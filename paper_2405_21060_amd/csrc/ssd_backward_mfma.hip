@@ -443,7 +443,13 @@ __constant__ int2 kLowerTile[10] = {{0, 0}, {1, 0}, {1, 1}, {2, 0}, {2, 1}, {2, 
 __constant__ int2 kUpperTile[6] = {{0, 1}, {0, 2}, {0, 3}, {1, 2}, {1, 3}, {2, 3}};
 
 template <int N, bool PACKED, bool H32>
-__global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
+// A_log and D come as separate read-only arguments so that their per-head
+// values are scalar loads: read through the parameter block (whose other
+// pointers the kernel writes through) they were vector loads, and the wait for
+// them at every head's start also waited for all the memory operations
+// before them, the previous head's gradient stores included.
+__global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p, const float* __restrict__ A_logp,
+                                                    const float* __restrict__ Dp)
 {
     constexpr int kLdN = ChunkSmem<N>::kLdN;
     constexpr int kLdF = ChunkSmem<N, H32>::kLdF;
@@ -573,8 +579,8 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p)
         const int64_t sbase = ((b * p.nC + c) * p.H + h) * kP2 * N;
         const u16* GnT = reinterpret_cast<const u16*>(p.gnT) + sbase;   // n x p
         const u16* HinT = reinterpret_cast<const u16*>(p.hin) + sbase;  // n x p
-        const float Ah = -expf(p.A_log[h]);
-        const float Dh = p.D ? p.D[h] : 0.f;
+        const float Ah = -expf(A_logp[h]);
+        const float Dh = Dp ? Dp[h] : 0.f;
         const int hb = static_cast<int>((h - hr.lo) & 1);
         float* const scs = scs2[hb];
         float* const sdt = sdt2[hb];
@@ -875,11 +881,11 @@ hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEv
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
     if (packed)
-        hipLaunchKernelGGL((k_bwd2_chunk<N, true, false>), grid, dim3(kT2), sm_chunk, st, p);
+        hipLaunchKernelGGL((k_bwd2_chunk<N, true, false>), grid, dim3(kT2), sm_chunk, st, p, p.A_log, p.D);
     else if (h32)
-        hipLaunchKernelGGL((k_bwd2_chunk<N, false, true>), grid, dim3(kT2), sm_chunk, st, p);
+        hipLaunchKernelGGL((k_bwd2_chunk<N, false, true>), grid, dim3(kT2), sm_chunk, st, p, p.A_log, p.D);
     else
-        hipLaunchKernelGGL((k_bwd2_chunk<N, false, false>), grid, dim3(kT2), sm_chunk, st, p);
+        hipLaunchKernelGGL((k_bwd2_chunk<N, false, false>), grid, dim3(kT2), sm_chunk, st, p, p.A_log, p.D);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
     return launch_backward_reduce(p, true, st);
