@@ -429,6 +429,10 @@ int ssd_workspace_status(const void* workspace, void* stream);
  *                          factor in a pass of its own, 2: in the diagonal
  *                          block's pass (plain rows with the late state flag;
  *                          elsewhere 2 acts as 1)
+ *   "packed_order"         1: the fused chunk kernel takes a packed row's
+ *                          chunks in token order, 2: by their index within
+ *                          their sequence (every sequence's first chunk,
+ *                          then every second chunk, ...)
  * Returns SSD_OK, SSD_ERR_NULL_ARG, or SSD_ERR_BAD_OPTION (unknown name, or a
  * value out of range).  The settings are process-wide and not ordered with
  * calls made concurrently on other host threads. */

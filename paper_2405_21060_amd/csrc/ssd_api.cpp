@@ -275,9 +275,15 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
         // 0.081); elsewhere it sets the flag after the output stage, which
         // measures up to 2 % faster there.  The early_state_flag tuning
         // overrides it.
+        // A packed row of several sequences, its chunks taken by their index
+        // within their sequence (below), has a chain per sequence: about
+        // table entries / sequences chunks long (the longest is unknown here
+        // when the boundaries are on the device).
+        const bool by_depth = nseq > 1 && ssd::tuning(ssd::kTunePackedOrder) != 1;
         const int64_t items = fw.nC * s.b * (s.H / f.HG);
         const int64_t rounds = (items + cus - 1) / cus;
-        f.early_flag = fw.nC >= 2 * rounds * f.HG ? 1 : 0;
+        const int64_t chain = by_depth ? (fw.nC + nseq - 1) / nseq : fw.nC;
+        f.early_flag = chain >= 2 * rounds * f.HG ? 1 : 0;
         if (const int64_t ef = ssd::tuning(ssd::kTuneEarlyFlag); ef == 1 || ef == 2) f.early_flag = ef == 2;
         // The right factor in the diagonal block's pass (x read from LDS once for
         // both; with N = 256 the first column block's) shortens a head's
@@ -317,6 +323,10 @@ int forward_impl(const ssd_problem* prob, const ssd_block_opts* opts, const void
             f.starts = reinterpret_cast<int*>(base + fw.starts);
             f.vtab = reinterpret_cast<int4*>(base + fw.vtab);
             f.vcount = f.ticket + 2;
+            // Several sequences: chunks taken by their index within their
+            // sequence rather than in table order (k_seq_order), so that the
+            // chunks in flight are mostly of different sequences.
+            if (by_depth) f.vorder = reinterpret_cast<int*>(base + fw.vorder);
         }
         f.dtx = dtx;
         // The chunk kernel gates, and normalises one-head groups, in its output
@@ -1251,6 +1261,7 @@ extern "C" int ssd_set_tuning(const char* name, int64_t value)
         {"varlen_per_sequence", ssd::kTuneVarlenPerSequence, 0, 1},
         {"state_wait_limit", ssd::kTuneStateWaitLimit, 0, INT64_MAX},
         {"fused_right_factor", ssd::kTuneFusedRightFactor, 0, 2},
+        {"packed_order", ssd::kTunePackedOrder, 0, 2},
     };
     for (const Entry& e : table)
         if (std::strcmp(name, e.name) == 0) {

@@ -287,6 +287,56 @@ __global__ __launch_bounds__(kTabThreads) void k_seq_chunks(const int* __restric
     }
 }
 
+// The order in which the chunk kernel takes a packed row's table entries:
+// by the entry's index within its sequence (every sequence's first chunk,
+// then every second chunk, ...; one workgroup).  In table order the items
+// taken together are consecutive chunks of one or two sequences, each
+// waiting for the one before it; in this order they are mostly of different
+// sequences, and a chunk's predecessor was taken about a round earlier.  Any
+// order that puts a chunk after the chunk before it in its sequence keeps the
+// chunk kernel deadlock-free, and the order of the entries of one index
+// (here the order of LDS atomics) changes no result.  Rows of more than
+// kOrderDepths chunks keep the table order.
+constexpr int kOrderDepths = 8192;
+
+template <int Q>
+__global__ __launch_bounds__(kTabThreads) void k_seq_order(const int4* __restrict__ vtab,
+                                                           const int* __restrict__ starts,
+                                                           const int* __restrict__ vcount, int T,
+                                                           int* __restrict__ vorder)
+{
+    __shared__ int pos[kOrderDepths];
+    __shared__ long long s_w[kTabThreads / 64];
+    const int n = *vcount;
+    const int depths = T / Q + (T % Q != 0 ? 1 : 0);   // no sequence has more chunks
+    if (depths > kOrderDepths) {
+        for (int e = threadIdx.x; e < n; e += kTabThreads) vorder[e] = e;
+        return;
+    }
+    // index of entry e within its sequence: its first token's distance from the
+    // sequence's first token (clamped as the table kernel clamps it), in chunks
+    const auto depth = [&](int e) {
+        const int4 v = vtab[e];
+        const int st = min(max(starts[v.z], 0), T);
+        return min(max((v.x - st) / Q, 0), depths - 1);
+    };
+    for (int k = threadIdx.x; k < depths; k += kTabThreads) pos[k] = 0;
+    __syncthreads();
+    for (int e = threadIdx.x; e < n; e += kTabThreads) atomicAdd(&pos[depth(e)], 1);
+    __syncthreads();
+    // entries per index -> first position of each index
+    long long base = 0;
+    for (int k0 = 0; k0 < depths; k0 += kTabThreads) {
+        const int k = k0 + static_cast<int>(threadIdx.x);
+        long long tot = 0;
+        const long long first = base + block_exclusive_sum(k < depths ? pos[k] : 0, s_w, &tot);
+        if (k < depths) pos[k] = static_cast<int>(first);   // only this thread reads pos[k] in this pass
+        base += tot;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < n; e += kTabThreads) vorder[atomicAdd(&pos[depth(e)], 1)] = e;
+}
+
 // PACKED: a packed row, chunk positions from the chunk table.
 template <int N, bool PACKED>
 __global__ __launch_bounds__(kPrepThreads) void k_fused_prep(FusedParams p)
@@ -757,6 +807,8 @@ __device__ __forceinline__ Item decode_item(const FusedParams& p, int work, int 
 {
     Item it;
     it.c = work / per_c;
+    if constexpr (PACKED)
+        if (p.vorder) it.c = p.vorder[it.c];   // the table entry taken in this place
     it.b = (work % per_c) / nHG;
     it.h0 = (work % nHG) * static_cast<int>(p.HG);
     it.g = it.h0 / static_cast<int>(p.H / p.G);
@@ -1541,8 +1593,13 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
 {
     if (p.y32 && (p.vtab || p.z || p.norm_head)) return hipErrorInvalidValue;   // plain rows, no gate/norm
     if (p.vtab) {   // packed row: the chunk table first
-        const hipError_t e = launch_seq_table(p.seq_idx, p.arg_starts, p.T, p.nseq, kQ, p.nC, p.ring_rows, p.starts,
-                                              p.vtab, nullptr, p.vcount, stream);
+        hipError_t e = launch_seq_table(p.seq_idx, p.arg_starts, p.T, p.nseq, kQ, p.nC, p.ring_rows, p.starts,
+                                        p.vtab, nullptr, p.vcount, stream);
+        if (e == hipSuccess && p.vorder) {
+            hipLaunchKernelGGL((k_seq_order<kQ>), dim3(1), dim3(kTabThreads), 0, stream, p.vtab, p.starts, p.vcount,
+                               static_cast<int>(p.T), p.vorder);
+            e = hipGetLastError();
+        }
         if (e != hipSuccess) return e;
     }
     int dev = 0, cus = 0;
@@ -1579,6 +1636,9 @@ hipError_t launch_n(const FusedParams& p, hipStream_t stream, hipEvent_t ev_begi
     else if (p.vtab && p.early_flag)
         hipLaunchKernelGGL((k_fused_main<N, true, true, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp, Dp,
                            biasp);
+    else if (p.vtab && p.fuse_rf)
+        hipLaunchKernelGGL((k_fused_main<N, true, false, false, true>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
+                           Dp, biasp);
     else if (p.vtab)
         hipLaunchKernelGGL((k_fused_main<N, true, false, false, false>), g_main, dim3(kMainThreads), 0, stream, p, A_logp,
                            Dp, biasp);
@@ -1649,6 +1709,8 @@ FusedLayout fused_layout(int64_t b, int64_t T, int64_t H, int64_t N, int64_t G, 
     off = al(off + sizeof(int) * static_cast<size_t>(nseq > 0 ? nseq + 1 : 0));
     w.vtab = off;
     off = al(off + sizeof(int4) * static_cast<size_t>(nseq > 0 ? w.nC : 0));
+    w.vorder = off;
+    off = al(off + sizeof(int) * static_cast<size_t>(nseq > 0 ? w.nC : 0));
     w.total = off;
     return w;
 }

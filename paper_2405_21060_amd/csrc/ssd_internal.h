@@ -20,6 +20,7 @@ enum Tuning {
     kTuneVarlenPerSequence,  // 1: packed rows by host offsets run one call per sequence
     kTuneStateWaitLimit,     // polls before a chunk's wait for the state before it gives up
     kTuneFusedRightFactor,   // 1: the chunk kernel's right factor in its own pass, 2: in the diagonal block's
+    kTunePackedOrder,        // 1: a packed row's chunks taken in table order, 2: by index within their sequence
     kTuneCount
 };
 int64_t tuning(Tuning k);
@@ -119,6 +120,9 @@ struct FusedParams {
     int4* vtab = nullptr;              // (nC) {first token, length, sequence, bit 0 first chunk of
                                        //  its sequence | bit 1 last | ring row << 2}
     int* vcount = nullptr;             // [0] table entries
+    // (nC) the order in which the chunk kernel takes the table's entries
+    // (null: table order); see k_seq_order
+    int* vorder = nullptr;
     int64_t ring_rows = 0;             // sequences of more than one chunk that the ring holds
     // nonzero: a chunk's state flag is set as soon as its state is stored
     // (before its left factor), for launches bound by the chain of chunks
@@ -136,7 +140,7 @@ struct FusedParams {
 };
 
 struct FusedLayout {
-    size_t gram, BT, ring, flags, ticket, starts, vtab, total;
+    size_t gram, BT, ring, flags, ticket, starts, vtab, vorder, total;
     int64_t nC;          // chunks the layout holds (table capacity for a packed row)
     int64_t ring_rows;   // rows of the state ring
 };

@@ -308,7 +308,7 @@ def test_tuning_hook_validates_names_and_values(lib):
     assert lib.ssd_set_tuning(None, 1) == ssd.SSD_ERR_NULL_ARG
     for name in ("force_general_path", "heads_per_item", "early_state_flag", "max_workgroups",
                  "separate_block_post", "bwd_heads_per_slice", "varlen_per_sequence",
-                 "state_wait_limit", "fused_right_factor"):
+                 "state_wait_limit", "fused_right_factor", "packed_order"):
         assert ssd.ssd_set_tuning(name, 1) == ssd.SSD_OK, name
         assert ssd.ssd_set_tuning(name, 0) == ssd.SSD_OK, name
 

@@ -182,6 +182,27 @@ def test_fused_packed_persistent_items(tune, hg):
     check(_packed([700, 30, 1, 900, 256, 513], 8, 128, 1, 19), tag="fused_packed_persistent_hg" + hg)
 
 
+@pytest.mark.parametrize("early", ["1", "2"])
+def test_fused_packed_work_order(tune, early):
+    """A packed row's chunks taken in table order and by their index within
+    their sequence (both forced; few persistent workgroups, 1 and 4 heads per
+    item, either state flag): each against the oracle, and the two
+    bit-identical (the order moves work between workgroups, not arithmetic)."""
+    import torch
+
+    tune("early_state_flag", int(early))
+    tune("max_workgroups", 3)
+    inp = _packed([700, 30, 1, 900, 256, 513, 1100, 2], 8, 128, 2, 37)
+    for hg in (1, 4):
+        tune("heads_per_item", hg)
+        tune("packed_order", 1)
+        y1, f1 = check(inp, tag="packed_table_order_hg%d_e%s" % (hg, early))
+        tune("packed_order", 2)
+        y2, f2 = check(inp, tag="packed_depth_order_hg%d_e%s" % (hg, early))
+        assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+        assert torch.equal(f1, f2)
+
+
 def test_fused_packed_one_sequence_equals_plain_row():
     """seq_idx all zero (one sequence) gives exactly the plain row's result:
     the same chunks, the same arithmetic."""
