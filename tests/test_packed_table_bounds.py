@@ -82,3 +82,30 @@ def test_workspace_covers_the_packed_layout():
     assert sizes[-1] > plain
     # nseq beyond T is invalid for a packed row and adds nothing
     assert ws(40000, T=32768) == plain
+
+
+def depth_order(lens):
+    """The order in which the chunk kernel takes the table's entries when a
+    row holds several sequences: by each entry's index within its sequence
+    (every sequence's first chunk, then every second chunk, ...)."""
+    tab = table(lens)
+    starts = np.concatenate([[0], np.cumsum(lens)])
+    depth = [(t0 - starts[s]) // Q for t0, _, s in tab]
+    return sorted(range(len(tab)), key=lambda e: depth[e]), tab
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_depth_order_follows_every_chain(seed):
+    """A permutation of the table in which every chunk comes after the chunk
+    before it in its sequence (what keeps the persistent kernel free of
+    deadlock), whatever the order among the entries of one index."""
+    rng = np.random.default_rng(100 + seed)
+    lens = rng.integers(1, [300, 2000, 5000][seed % 3], rng.integers(2, 60)).tolist()
+    order, tab = depth_order(lens)
+    assert sorted(order) == list(range(len(tab)))
+    pos = {e: i for i, e in enumerate(order)}
+    for e in range(1, len(tab)):
+        if tab[e][2] == tab[e - 1][2]:   # the same sequence: e - 1 is the chunk before e
+            assert pos[e - 1] < pos[e]
+    # the first entries taken are the sequences' first chunks, one per sequence
+    assert [tab[e][2] for e in order[:len(lens)]] == list(range(len(lens)))
