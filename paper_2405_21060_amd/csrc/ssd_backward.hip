@@ -467,13 +467,15 @@ hipError_t launch_all(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEve
 }
 
 template <typename T>
-hipError_t launch_reduce(const BwdParams& p, hipStream_t st)
+hipError_t launch_reduce(const BwdParams& p, hipStream_t st, bool with_bc)
 {
     const int64_t nbc = p.b * p.T * p.G * p.N;
-    hipLaunchKernelGGL(k_bwd_reduce_bc<T>, dim3(static_cast<unsigned>((nbc + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, st, p);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (with_bc) {
+        hipLaunchKernelGGL(k_bwd_reduce_bc<T>, dim3(static_cast<unsigned>((nbc + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, st, p);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(k_bwd_reduce_head, dim3(static_cast<unsigned>(p.H)), dim3(kThreads), 0, st, p);
     return hipGetLastError();
 }
@@ -542,9 +544,9 @@ hipError_t launch_sum_rows(const float* part, int64_t nrows, int64_t ncols, floa
     return hipGetLastError();
 }
 
-hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream)
+hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream, bool with_bc)
 {
-    return bf16 ? launch_reduce<uint16_t>(p, stream) : launch_reduce<float>(p, stream);
+    return bf16 ? launch_reduce<uint16_t>(p, stream, with_bc) : launch_reduce<float>(p, stream, with_bc);
 }
 
 hipError_t launch_backward(const BwdParams& p, bool bf16, hipStream_t stream, hipEvent_t ev_begin,

@@ -57,6 +57,16 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_bits
 
 __device__ __forceinline__ float bf(u16 v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
 
+// Two floats rounded to bf16 (nearest even; the inputs are finite), the first
+// in the low half.
+__device__ __forceinline__ uint32_t rne_pair(float a, float b)
+{
+    uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
+    ua += 0x7FFFu + ((ua >> 16) & 1u);
+    ub += 0x7FFFu + ((ub >> 16) & 1u);
+    return (ua >> 16) | (ub & 0xFFFF0000u);
+}
+
 // dt of token row i (bf16 bits, or float32 with H32).
 template <bool H32>
 __device__ __forceinline__ float load_dt(const void* dt, int64_t i)
@@ -442,7 +452,8 @@ struct ChunkSmem {
 __constant__ int2 kLowerTile[10] = {{0, 0}, {1, 0}, {1, 1}, {2, 0}, {2, 1}, {2, 2}, {3, 0}, {3, 1}, {3, 2}, {3, 3}};
 __constant__ int2 kUpperTile[6] = {{0, 1}, {0, 2}, {0, 3}, {1, 2}, {1, 3}, {2, 3}};
 
-template <int N, bool PACKED, bool H32>
+// DIRECT: one head slice per group; dB and dC stored by this kernel (bf16).
+template <int N, bool PACKED, bool H32, bool DIRECT>
 // A_log and D come as separate read-only arguments so that their per-head
 // values are scalar loads: read through the parameter block (whose other
 // pointers the kernel writes through) they were vector loads, and the wait for
@@ -842,32 +853,51 @@ __global__ __launch_bounds__(kT2) void k_bwd2_chunk(BwdParams p, const float* __
         }
     }
 
-    // this slice's dB and dC for the chunk: lane holds n = 16 nt + 4 q + v, t = 16 tt + r
+    // this slice's dB and dC for the chunk: lane holds n = 16 nt + 4 q + v, t = 16 tt + r.
+    // With one slice per group these sums are the gradients: rounded here to
+    // bf16 (nearest even, as the reduction over slices rounds them) and stored
+    // in place, and the launch skips that reduction (bc_direct).
 #pragma unroll
     for (int j = 0; j < kBW; ++j) {
         const int idx = w * kBW + j, nt = idx >> 2, tt = idx & 3;
         const int t = 16 * tt + r;
         if (t < L) {
-            const int64_t o = ((hr.slice * p.b * p.T + t0 + t) * p.G + hr.g) * N + 16 * nt + 4 * q;
-            *reinterpret_cast<float4*>(p.dBp + o) = make_float4(dBacc[j][0], dBacc[j][1], dBacc[j][2], dBacc[j][3]);
-            *reinterpret_cast<float4*>(p.dCp + o) = make_float4(dCacc[j][0], dCacc[j][1], dCacc[j][2], dCacc[j][3]);
+            if constexpr (DIRECT) {
+                const int64_t o = ((t0 + t) * p.G + hr.g) * N + 16 * nt + 4 * q;
+                *reinterpret_cast<uint2*>(static_cast<u16*>(p.dB) + o) =
+                    make_uint2(rne_pair(dBacc[j][0], dBacc[j][1]), rne_pair(dBacc[j][2], dBacc[j][3]));
+                *reinterpret_cast<uint2*>(static_cast<u16*>(p.dC) + o) =
+                    make_uint2(rne_pair(dCacc[j][0], dCacc[j][1]), rne_pair(dCacc[j][2], dCacc[j][3]));
+            } else {
+                const int64_t o = ((hr.slice * p.b * p.T + t0 + t) * p.G + hr.g) * N + 16 * nt + 4 * q;
+                *reinterpret_cast<float4*>(p.dBp + o) =
+                    make_float4(dBacc[j][0], dBacc[j][1], dBacc[j][2], dBacc[j][3]);
+                *reinterpret_cast<float4*>(p.dCp + o) =
+                    make_float4(dCacc[j][0], dCacc[j][1], dCacc[j][2], dCacc[j][3]);
+            }
         }
     }
 }
 
-template <int N>
-hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
+template <int N, bool PACKED, bool H32, bool DIRECT>
+hipError_t launch_chunk(const BwdParams& p, dim3 grid, size_t sm, hipStream_t st)
 {
-    const bool packed = p.vtab != nullptr, h32 = p.h32 != 0;
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_bwd2_chunk<N, PACKED, H32, DIRECT>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_bwd2_chunk<N, PACKED, H32, DIRECT>), grid, dim3(kT2), sm, st, p, p.A_log, p.D);
+    return hipGetLastError();
+}
+
+template <int N>
+hipError_t launch_fast(const BwdParams& params, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
+{
+    BwdParams p = params;
+    p.bc_direct = p.S == 1 && reinterpret_cast<uintptr_t>(p.dB) % 8 == 0 && reinterpret_cast<uintptr_t>(p.dC) % 8 == 0;
+    const bool packed = p.vtab != nullptr, h32 = p.h32 != 0, direct = p.bc_direct != 0;
     if (packed && h32) return hipErrorInvalidValue;   // float32 handoffs: plain rows only
     const size_t sm_chunk = h32 ? ChunkSmem<N, true>::kBytes : ChunkSmem<N>::kBytes;
     hipError_t e;
-    const void* chunk_fn = packed ? reinterpret_cast<const void*>(&k_bwd2_chunk<N, true, false>)
-                           : h32  ? reinterpret_cast<const void*>(&k_bwd2_chunk<N, false, true>)
-                                  : reinterpret_cast<const void*>(&k_bwd2_chunk<N, false, false>);
-    if ((e = hipFuncSetAttribute(chunk_fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(sm_chunk))) !=
-        hipSuccess)
-        return e;
     if (packed)   // one workgroup per (sequence, head) and direction
         hipLaunchKernelGGL((k_bwd2_pass<N, true, false>), dim3(static_cast<unsigned>(p.nseq * p.H), 2), dim3(kPassT),
                            0, st, p);
@@ -881,14 +911,17 @@ hipError_t launch_fast(const BwdParams& p, hipStream_t st, hipEvent_t ev0, hipEv
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess) return e;
     const dim3 grid(static_cast<unsigned>(p.nC), static_cast<unsigned>(p.b), static_cast<unsigned>(p.G * p.S));
     if (packed)
-        hipLaunchKernelGGL((k_bwd2_chunk<N, true, false>), grid, dim3(kT2), sm_chunk, st, p, p.A_log, p.D);
+        e = direct ? launch_chunk<N, true, false, true>(p, grid, sm_chunk, st)
+                   : launch_chunk<N, true, false, false>(p, grid, sm_chunk, st);
     else if (h32)
-        hipLaunchKernelGGL((k_bwd2_chunk<N, false, true>), grid, dim3(kT2), sm_chunk, st, p, p.A_log, p.D);
+        e = direct ? launch_chunk<N, false, true, true>(p, grid, sm_chunk, st)
+                   : launch_chunk<N, false, true, false>(p, grid, sm_chunk, st);
     else
-        hipLaunchKernelGGL((k_bwd2_chunk<N, false, false>), grid, dim3(kT2), sm_chunk, st, p, p.A_log, p.D);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+        e = direct ? launch_chunk<N, false, false, true>(p, grid, sm_chunk, st)
+                   : launch_chunk<N, false, false, false>(p, grid, sm_chunk, st);
+    if (e != hipSuccess) return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess) return e;
-    return launch_backward_reduce(p, true, st);
+    return launch_backward_reduce(p, true, st, !direct);
 }
 
 }  // namespace

@@ -55,6 +55,9 @@ struct BwdParams {
     // written in float32 (the block gradients' handoffs); x, B, C, dx, dB, dC
     // keep the bf16 activation dtype.
     int h32 = 0;
+    // matrix-core path, one head slice per group (S == 1) and dB, dC 8-byte
+    // aligned: the chunk kernel stores dB and dC (bf16) itself; set at launch
+    int bc_direct = 0;
 };
 
 struct BwdLayout {
@@ -72,8 +75,9 @@ bool bwd_fast_supported(bool bf16, int64_t P, int64_t N);
 hipError_t launch_backward_fast(const BwdParams& p, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_end);
 
 // The final sums over head slices (dB, dC) and over rows and chunks (dA_log,
-// dD), shared by both paths.
-hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream);
+// dD), shared by both paths; with with_bc false only the latter (the chunk
+// kernel stored dB and dC itself).
+hipError_t launch_backward_reduce(const BwdParams& p, bool bf16, hipStream_t stream, bool with_bc = true);
 
 // out[c] = sum over r of part[r * ncols + c], r in order (float32).
 hipError_t launch_sum_rows(const float* part, int64_t nrows, int64_t ncols, float* out, hipStream_t stream);
