@@ -389,7 +389,7 @@ def backward_bench(args, torch, ssd):
         ks = sorted(a.elapsed_time(z) for a, z in kev)
         kms = {"mean": sum(ks) / len(ks), "p10": ks[len(ks) // 10], "p50": ks[len(ks) // 2],
                "p90": ks[(9 * len(ks)) // 10]}
-    else:   # one call per sequence inside: no single chunk kernel to bracket; whole-call time
+    else:   # ssd_backward_varlen takes no events: the whole call's time
         kms = {"mean": ms, "p10": ms, "p50": ms, "p90": ms}
     flops, kbytes, state_bytes, Qb = backward_counts(p)
     compulsory = kbytes
@@ -403,7 +403,7 @@ def backward_bench(args, torch, ssd):
         else:
             roof = {"bound": "mfma", "achieved": flops / ksec / 1e12, "peak": PEAK_BF16_FLOPS / 1e12,
                     "unit": "TFLOP/s"}
-        kname = "k_bwd2_chunk<%d>" % p.dstate if starts is None else "whole call (one backward per sequence)"
+        kname = "k_bwd2_chunk<%d>" % p.dstate if starts is None else "whole call (packed row)"
     else:
         roof = {"bound": "alu", "achieved": flops / ksec / 1e12, "peak": PEAK_F32_VECTOR_FLOPS / 1e12,
                 "unit": "TFLOP/s"}
