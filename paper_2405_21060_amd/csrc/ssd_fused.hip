@@ -14,7 +14,8 @@
 //
 // k_fused_main, persistent workgroups (8 wavefronts, one per compute unit)
 // taking work items (chunk, batch, group of HG heads) from a ticket counter in
-// chunk-major order:
+// chunk-major order (a packed row's chunks by their index within their
+// sequence, k_seq_order):
 //   * per item: the chunk's Gram tiles (shared by the HG heads) are copied to
 //     LDS asynchronously, B^T and C fragments loaded into registers; per head,
 //     x (Q x P, token-major, swizzled) lands in a double-buffered LDS slot while
