@@ -1,11 +1,12 @@
 // Fused SSD forward for the Mamba-2 layer shapes: bf16 activations, head
-// dimension P = 64, state N in {64, 128}, chunk Q = 256; plain rows, or one
-// packed row of sequences (Section 8.3) through a chunk table built on the
-// device.
+// dimension P = 64, state N in {64, 128, 256} (256: two column blocks of
+// 128), chunk Q = 256; plain rows, or one packed row of sequences (Section
+// 8.3) through a chunk table built on the device.
 //
-// Two launches per call.
+// Two launches per call (a packed row adds the small kernels that build and
+// order its chunk table).
 //
-// k_fused_prep, four workgroups per (batch, chunk, group):
+// k_fused_prep, up to four workgroups per (batch, chunk, group):
 //   * B^T of the chunk (N x Q, bf16), the operand layout the chunk-state
 //     contraction needs (contraction over tokens);
 //   * the Gram matrix C B^T of the chunk (Section 5, eq. ssm-quad: G = C B^T),

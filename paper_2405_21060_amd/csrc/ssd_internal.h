@@ -78,7 +78,7 @@ WorkspaceLayout workspace_layout(int64_t b, int64_t H, int64_t P, int64_t N, int
 hipError_t launch_unfused(const Params& p, bool bf16, hipStream_t stream,
                           hipEvent_t ev_begin, hipEvent_t ev_end);
 
-// Fused path (bf16, P = 64, N in {64, 128}, Q = 256; plain rows or one packed row).
+// Fused path (bf16, P = 64, N in {64, 128, 256}, Q = 256; plain rows or one packed row).
 // Sequence starts of a packed row handed to the device by value (kernel
 // argument) when the caller gives them in host memory: n sequences, v[0..n].
 constexpr int kArgSeqs = 511;
